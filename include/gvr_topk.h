@@ -1,0 +1,153 @@
+/*
+ * gvr_topk.h -- exact per-row Top-K for decode-time sparse-attention indexer
+ * scores on AMD Instinct MI355X (gfx950).
+ *
+ * Problem (Sec. 4.1, "Core Idea"): for each row b, given the fp32 scores
+ * x[0..n) and a guessed index set P (the previous decode step's Top-K,
+ * Sec. 3.3), return the indices of the K largest scores.
+ *
+ * gvr_topk  -- Guess-Verify-Refine (Sec. 4): statistics of the guessed scores
+ *              (Phase 1), full-row threshold counting passes (Phase 2),
+ *              collection of the candidates at or above the accepted threshold
+ *              (Phase 3, Lemma 1 of Sec. 4.1 makes this set contain the answer),
+ *              exact on-chip selection among them (Phase 4).
+ * radix_topk -- distribution-agnostic radix select over the sortable key
+ *              (the baseline of Sec. 2.2), same signature, same result.
+ *
+ * Result definition, shared by both entry points:
+ *   - n = clamp(row_len[b], 0, ld); only scores[b*ld + 0 .. b*ld + n) are used.
+ *   - Order: each fp32 bit pattern u maps to the 32-bit key
+ *       (u & 0x80000000) ? ~u : (u | 0x80000000)
+ *     compared as unsigned, i.e. -NaN < -inf < ... < -0.0 < +0.0 < ... <
+ *     +inf < +NaN (NaNs ordered by payload; -0.0 below +0.0).
+ *   - Ties: among equal keys the lower index wins, so the answer is unique.
+ *   - out_idx[b*K + 0 .. K) receives the K selected indices in ascending
+ *     index order. If n <= K it receives 0, 1, ..., n-1 followed by -1.
+ *   - The result never depends on prev_topk (exactness): prev_topk only
+ *     changes how fast the answer is found.
+ *
+ * Memory and ownership:
+ *   - All array arguments are DEVICE pointers on the current HIP device;
+ *     the caller owns them; the library neither frees nor retains them.
+ *   - scores: [B][ld] fp32, row stride ld elements, 4-byte aligned.
+ *   - row_len: [B] int32 (device-resident, so values are clamped, not checked).
+ *   - prev_topk: [B][K] int32 or NULL. Entries outside [0, n) (e.g. -1
+ *     padding) are ignored; duplicates are tolerated.
+ *   - out_idx: [B][K] int32, written in full; must not overlap the inputs.
+ *   - stream: a hipStream_t passed as void* (NULL = the null stream).
+ *
+ * Errors and synchronisation:
+ *   - Argument problems detectable on the host are reported synchronously,
+ *     before any work is enqueued. B == 0 is a no-op returning GVR_OK.
+ *   - On GVR_OK the work is enqueued on `stream`; out_idx is complete when
+ *     the stream reaches that point. The call does not synchronise.
+ *   - gvr_topk / radix_topk use a workspace owned by the library (one per
+ *     device, grown on demand with hipMalloc, kept until process exit).
+ *     Calls that use it must not run concurrently on different streams of
+ *     one device, and must not be captured into a HIP graph (growing the
+ *     workspace allocates). gvr_topk_ex with a caller workspace has neither
+ *     restriction (each concurrent call needs its own workspace).
+ *   - Rows are processed by cooperatively launched kernels (all workgroups of
+ *     a launch co-resident); rows whose length exceeds what one launch can
+ *     keep on chip return GVR_ERR_TOO_LONG.
+ */
+#ifndef GVR_TOPK_H
+#define GVR_TOPK_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    GVR_OK = 0,
+    GVR_ERR_INVALID_ARG = -1,    /* B < 0, ld < 0, NULL required pointer, bad option */
+    GVR_ERR_UNSUPPORTED_K = -2,  /* K < 1 or K > GVR_MAX_K */
+    GVR_ERR_WORKSPACE = -3,      /* workspace too small / allocation failed */
+    GVR_ERR_HIP = -4,            /* a HIP runtime call or a launch failed */
+    GVR_ERR_TOO_LONG = -5        /* ld beyond what one launch keeps on chip */
+} gvr_status;
+
+/* Largest supported K (Sec. 5.5: K = M = 2048 in the deployed gate). */
+#define GVR_MAX_K 2048
+/* Default and largest refine capacity C (Sec. 4.1, Lemma 1: C = 6144). */
+#define GVR_MAX_CANDIDATES 6144
+
+/* Per-row outcome codes reported in gvr_row_stats.path. */
+enum {
+    GVR_PATH_TRIVIAL = 0,      /* n <= K: iota / -1 padding */
+    GVR_PATH_ALL = 1,          /* K < n <= C: every element is a candidate */
+    GVR_PATH_GUESS = 2,        /* threshold accepted from the guessed window */
+    GVR_PATH_NARROWED = 3,     /* threshold accepted after narrowing the window */
+    GVR_PATH_TIES = 4,         /* the K-th key isolated exactly (ties straddle
+                                  [K, C]); selection emitted without refine */
+    GVR_PATH_NO_GUESS = 5      /* prev_topk NULL or without a valid entry */
+};
+
+/* Optional knobs (NULL = defaults). Zero fields mean "default". */
+typedef struct gvr_options {
+    int32_t capacity;      /* refine capacity C, K <= C <= GVR_MAX_CANDIDATES (default 6144) */
+    int32_t max_passes;    /* cap on counting passes taken from the guess
+                              before the window falls back to the full key
+                              range (default 8; < 0 means 0: ignore the guess) */
+    int32_t flags;         /* bit 0: ignore prev_topk (run the radix schedule) */
+    int32_t reserved;
+} gvr_options;
+
+/* Optional per-row diagnostics, written when a device pointer is supplied. */
+typedef struct gvr_row_stats {
+    int32_t n;             /* clamped row length */
+    int32_t path;          /* GVR_PATH_* */
+    int32_t passes;        /* counting passes over the row (registers-resident) */
+    int32_t candidates;    /* candidates handed to the refine (0 if none) */
+    uint32_t threshold;    /* accepted threshold key T (K <= f(T) <= C) */
+    uint32_t kth_key;      /* key of the K-th largest score */
+    int32_t n_gt;          /* #{key > kth_key} */
+    int32_t guess_valid;   /* valid entries of prev_topk used by the guess */
+    int64_t t_start;       /* s_memtime stamps (shader clock) at phase ends: */
+    int64_t t_guess;       /*   guess statistics ready                         */
+    int64_t t_search;      /*   threshold accepted (after the last count pass) */
+    int64_t t_collect;     /*   candidates written                             */
+    int64_t t_refine;      /*   output written                                 */
+} gvr_row_stats;
+
+/* Guess-Verify-Refine Top-K (Sec. 4). See the file comment for semantics. */
+gvr_status gvr_topk(const float* scores, int64_t B, int64_t ld, const int32_t* row_len,
+                    const int32_t* prev_topk, int32_t K, int32_t* out_idx, void* stream);
+
+/* Distribution-agnostic radix-select Top-K (Sec. 2.2); prev_topk is accepted
+ * and ignored. Same result as gvr_topk. */
+gvr_status radix_topk(const float* scores, int64_t B, int64_t ld, const int32_t* row_len,
+                      const int32_t* prev_topk, int32_t K, int32_t* out_idx, void* stream);
+
+/* Bytes of caller workspace gvr_topk_ex / radix_topk_ex need for (B, ld, K)
+ * on the current device; 0 if the shape is unsupported. */
+size_t gvr_workspace_size(int64_t B, int64_t ld, int32_t K);
+
+/* As gvr_topk, with a caller-owned device workspace of ws_bytes bytes (at
+ * least gvr_workspace_size(B, ld, K)), options and per-row stats ([B] device
+ * array or NULL). The workspace must be zero-filled before its first use;
+ * every call leaves it zero-filled again. No allocation happens inside. */
+gvr_status gvr_topk_ex(const float* scores, int64_t B, int64_t ld, const int32_t* row_len,
+                       const int32_t* prev_topk, int32_t K, int32_t* out_idx, void* stream,
+                       void* workspace, size_t ws_bytes, const gvr_options* options,
+                       gvr_row_stats* stats);
+
+/* Radix-select counterpart of gvr_topk_ex. */
+gvr_status radix_topk_ex(const float* scores, int64_t B, int64_t ld, const int32_t* row_len,
+                         int32_t K, int32_t* out_idx, void* stream, void* workspace,
+                         size_t ws_bytes, const gvr_options* options, gvr_row_stats* stats);
+
+/* Human-readable name of a status code (static string). */
+const char* gvr_status_string(gvr_status status);
+
+/* Library version string (static). */
+const char* gvr_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GVR_TOPK_H */
