@@ -15,7 +15,8 @@
  *              (the baseline of Sec. 2.2), same signature, same result.
  *
  * Result definition, shared by both entry points:
- *   - n = clamp(row_len[b], 0, ld); only scores[b*ld + 0 .. b*ld + n) are used.
+ *   - n = clamp(row_len[b], 0, ld); only scores[b*ld + 0 .. b*ld + n) are used
+ *     (loads never leave the 16-byte-aligned blocks holding those elements).
  *   - Order: each fp32 bit pattern u maps to the 32-bit key
  *       (u & 0x80000000) ? ~u : (u | 0x80000000)
  *     compared as unsigned, i.e. -NaN < -inf < ... < -0.0 < +0.0 < ... <
@@ -129,7 +130,9 @@ size_t gvr_workspace_size(int64_t B, int64_t ld, int32_t K);
 /* As gvr_topk, with a caller-owned device workspace of ws_bytes bytes (at
  * least gvr_workspace_size(B, ld, K)), options and per-row stats ([B] device
  * array or NULL). The workspace must be zero-filled before its first use;
- * every call leaves it zero-filled again. No allocation happens inside. */
+ * every call leaves its control area (at its start, the same size for every
+ * shape on a device) zero-filled again, so one workspace serves any sequence
+ * of shapes on its device. No allocation happens inside. */
 gvr_status gvr_topk_ex(const float* scores, int64_t B, int64_t ld, const int32_t* row_len,
                        const int32_t* prev_topk, int32_t K, int32_t* out_idx, void* stream,
                        void* workspace, size_t ws_bytes, const gvr_options* options,

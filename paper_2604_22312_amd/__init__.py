@@ -1,0 +1,32 @@
+"""Exact decode-time Top-K for MI355X (gfx950): Guess-Verify-Refine and radix select.
+
+Thin Python binding over the C ABI of ``include/gvr_topk.h`` (library
+``libgvr_topk.so`` built in-tree by ``paper_2604_22312_amd.build``). This module
+only validates tensors and marshals pointers; every step of the Top-K runs in
+the HIP kernels of ``csrc/gvr_topk.hip``. There is no CPU fallback: if the
+library is missing, importing the functions raises.
+
+Functions mirror the C entry points:
+
+* ``gvr_topk(scores, row_len, prev_topk, K, out_idx=None, stream=None)``
+* ``radix_topk(scores, row_len, prev_topk, K, out_idx=None, stream=None)``
+* ``gvr_topk_ex`` / ``radix_topk_ex`` (caller workspace, options, stats)
+* ``workspace_size(B, ld, K)``
+"""
+from .binding import (  # noqa: F401
+    GVR_MAX_CANDIDATES,
+    GVR_MAX_K,
+    PATH_NAMES,
+    GvrError,
+    Options,
+    decode_stats,
+    gvr_topk,
+    gvr_topk_ex,
+    lib,
+    library_path,
+    radix_topk,
+    radix_topk_ex,
+    status_string,
+    version,
+    workspace_size,
+)

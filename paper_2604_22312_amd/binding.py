@@ -1,0 +1,183 @@
+"""ctypes marshalling for ``libgvr_topk.so`` (argument checks and pointers only)."""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+GVR_MAX_K = 2048
+GVR_MAX_CANDIDATES = 6144
+PATH_NAMES = {0: "trivial", 1: "all", 2: "guess", 3: "narrowed", 4: "ties", 5: "no_guess", -1: "error"}
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "libgvr_topk.so")
+_lib = None
+
+STATS_INTS = 18   # sizeof(gvr_row_stats) / 4
+
+
+class GvrError(RuntimeError):
+    def __init__(self, fn, status):
+        super().__init__("%s failed: %s (%d)" % (fn, status_string(status), status))
+        self.status = status
+
+
+class Options(ctypes.Structure):
+    """Mirror of ``gvr_options``: capacity C, max_passes, flags (bit 0: ignore guess)."""
+    _fields_ = [("capacity", ctypes.c_int32), ("max_passes", ctypes.c_int32),
+                ("flags", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
+def library_path() -> str:
+    return _LIB_PATH
+
+
+def lib():
+    """Load the HIP library; raise loudly if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            raise ImportError("libgvr_topk.so not built: run `python -m paper_2604_22312_amd.build` "
+                              "(or __graft_entry__.build())")
+        L = ctypes.CDLL(_LIB_PATH)
+        vp, i64, i32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
+        for name in ("gvr_topk", "radix_topk"):
+            f = getattr(L, name)
+            f.restype = ctypes.c_int
+            f.argtypes = [vp, i64, i64, vp, vp, i32, vp, vp]
+        L.gvr_topk_ex.restype = ctypes.c_int
+        L.gvr_topk_ex.argtypes = [vp, i64, i64, vp, vp, i32, vp, vp, vp, sz, ctypes.POINTER(Options), vp]
+        L.radix_topk_ex.restype = ctypes.c_int
+        L.radix_topk_ex.argtypes = [vp, i64, i64, vp, i32, vp, vp, vp, sz, ctypes.POINTER(Options), vp]
+        L.gvr_workspace_size.restype = sz
+        L.gvr_workspace_size.argtypes = [i64, i64, i32]
+        L.gvr_status_string.restype = ctypes.c_char_p
+        L.gvr_status_string.argtypes = [ctypes.c_int]
+        L.gvr_version.restype = ctypes.c_char_p
+        L.gvr_version.argtypes = []
+        _lib = L
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return lib().gvr_status_string(int(status)).decode()
+
+
+def version() -> str:
+    return lib().gvr_version().decode()
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream, device):
+    if stream is None:
+        stream = torch.cuda.current_stream(device)
+    return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+
+
+def _check(scores, row_len, prev_topk, K, out_idx):
+    if not isinstance(scores, torch.Tensor) or scores.dtype != torch.float32 or scores.dim() != 2:
+        raise ValueError("scores must be a float32 tensor [B][ld]")
+    if not scores.is_cuda:
+        raise ValueError("scores must be on a GPU (there is no CPU path)")
+    if not scores.is_contiguous():
+        raise ValueError("scores must be contiguous (row stride = ld)")
+    B, ld = scores.shape
+    dev = scores.device
+    K = int(K)
+    if row_len is not None:
+        if row_len.dtype != torch.int32 or row_len.shape != (B,) or row_len.device != dev or not row_len.is_contiguous():
+            raise ValueError("row_len must be a contiguous int32 tensor [B] on the scores' device")
+    if prev_topk is not None:
+        if (prev_topk.dtype != torch.int32 or prev_topk.shape != (B, K) or prev_topk.device != dev
+                or not prev_topk.is_contiguous()):
+            raise ValueError("prev_topk must be a contiguous int32 tensor [B][K] on the scores' device")
+    if out_idx is None:
+        out_idx = torch.empty((B, max(K, 0)), dtype=torch.int32, device=dev)
+    elif (out_idx.dtype != torch.int32 or out_idx.shape != (B, K) or out_idx.device != dev
+          or not out_idx.is_contiguous()):
+        raise ValueError("out_idx must be a contiguous int32 tensor [B][K] on the scores' device")
+    return B, ld, K, out_idx
+
+
+def _call(fn_name, scores, row_len, prev_topk, K, out_idx, stream):
+    B, ld, K, out_idx = _check(scores, row_len, prev_topk, K, out_idx)
+    with torch.cuda.device(scores.device):
+        st = getattr(lib(), fn_name)(_ptr(scores), B, ld, _ptr(row_len), _ptr(prev_topk), K,
+                                     _ptr(out_idx), _stream(stream, scores.device))
+    if st != 0:
+        raise GvrError(fn_name, st)
+    return out_idx
+
+
+def gvr_topk(scores, row_len, prev_topk, K, out_idx=None, stream=None):
+    """Guess-Verify-Refine Top-K; returns ``out_idx`` [B][K] int32 (ascending indices)."""
+    return _call("gvr_topk", scores, row_len, prev_topk, K, out_idx, stream)
+
+
+def radix_topk(scores, row_len, prev_topk, K, out_idx=None, stream=None):
+    """Radix-select Top-K (``prev_topk`` accepted and ignored); same result as ``gvr_topk``."""
+    return _call("radix_topk", scores, row_len, prev_topk, K, out_idx, stream)
+
+
+def workspace_size(B: int, ld: int, K: int) -> int:
+    return int(lib().gvr_workspace_size(int(B), int(ld), int(K)))
+
+
+def _call_ex(radix, scores, row_len, prev_topk, K, out_idx, stream, workspace, options, stats):
+    B, ld, K, out_idx = _check(scores, row_len, prev_topk, K, out_idx)
+    if workspace is None:
+        with torch.cuda.device(scores.device):
+            nbytes = workspace_size(B, ld, K)
+        workspace = torch.zeros(max(nbytes, 1), dtype=torch.uint8, device=scores.device)
+    if workspace.dtype != torch.uint8 or workspace.device != scores.device or not workspace.is_contiguous():
+        raise ValueError("workspace must be a contiguous uint8 tensor on the scores' device")
+    if stats is not None and (stats.dtype != torch.int32 or stats.shape != (B, STATS_INTS)
+                              or stats.device != scores.device or not stats.is_contiguous()):
+        raise ValueError("stats must be a contiguous int32 tensor [B][%d] on the scores' device" % STATS_INTS)
+    opt = None
+    if options is not None:
+        opt = Options(**options) if isinstance(options, dict) else options
+    optp = ctypes.byref(opt) if opt is not None else None
+    with torch.cuda.device(scores.device):
+        L = lib()
+        if radix:
+            st = L.radix_topk_ex(_ptr(scores), B, ld, _ptr(row_len), K, _ptr(out_idx),
+                                 _stream(stream, scores.device), _ptr(workspace), workspace.numel(),
+                                 optp, _ptr(stats))
+        else:
+            st = L.gvr_topk_ex(_ptr(scores), B, ld, _ptr(row_len), _ptr(prev_topk), K, _ptr(out_idx),
+                               _stream(stream, scores.device), _ptr(workspace), workspace.numel(),
+                               optp, _ptr(stats))
+    if st != 0:
+        raise GvrError("radix_topk_ex" if radix else "gvr_topk_ex", st)
+    return out_idx
+
+
+def gvr_topk_ex(scores, row_len, prev_topk, K, out_idx=None, stream=None, workspace=None,
+                options=None, stats=None):
+    """``gvr_topk`` with a caller workspace (uint8, zero-filled before first use),
+    options (dict or ``Options``) and optional stats tensor ([B][18] int32)."""
+    return _call_ex(False, scores, row_len, prev_topk, K, out_idx, stream, workspace, options, stats)
+
+
+def radix_topk_ex(scores, row_len, K, out_idx=None, stream=None, workspace=None, options=None, stats=None):
+    return _call_ex(True, scores, row_len, None, K, out_idx, stream, workspace, options, stats)
+
+
+def decode_stats(stats: torch.Tensor) -> dict:
+    """Split a [B][18] int32 stats tensor (``gvr_row_stats``) into named columns."""
+    s = stats.detach().cpu()
+    i32 = s[:, :8]
+    i64 = s[:, 8:18].contiguous().view(torch.int64)
+    u32 = lambda c: (i32[:, c].to(torch.int64) & 0xFFFFFFFF)  # noqa: E731
+    return {
+        "n": i32[:, 0].clone(), "path": i32[:, 1].clone(), "passes": i32[:, 2].clone(),
+        "candidates": i32[:, 3].clone(), "threshold": u32(4), "kth_key": u32(5),
+        "n_gt": i32[:, 6].clone(), "guess_valid": i32[:, 7].clone(),
+        "t_start": i64[:, 0].clone(), "t_guess": i64[:, 1].clone(), "t_search": i64[:, 2].clone(),
+        "t_collect": i64[:, 3].clone(), "t_refine": i64[:, 4].clone(),
+    }

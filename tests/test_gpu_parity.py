@@ -1,0 +1,326 @@
+"""GPU parity: gvr_topk / radix_topk through the C ABI vs the CPU oracle.
+
+Bar: bit-exact (same indices, same order -- ascending) on every row of every
+step. Inputs are the seeded decode workloads; the previous-step guess handed
+to the GPU is the oracle's answer of the previous step.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from tests.gpu_cases import K_TOPK, assert_rows_equal, note, run_decode, workload
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2604_22312_amd as g
+    g.lib()
+    oracle.build(force=False)
+
+
+def gvr(scores, row_len, prev, K, stats=None):
+    import paper_2604_22312_amd as g
+    if stats is None:
+        return g.gvr_topk(scores, row_len, prev, K)
+    return g.gvr_topk_ex(scores, row_len, prev, K, stats=stats)
+
+
+def radix(scores, row_len, prev, K, stats=None):
+    import paper_2604_22312_amd as g
+    if stats is None:
+        return g.radix_topk(scores, row_len, prev, K)
+    return g.radix_topk_ex(scores, row_len, K, stats=stats)
+
+
+FNS = [gvr, radix]
+
+# (config, steps, queries, sub) -- parity sizes that still span several
+# workgroups per row and ragged tails; full-size launches are further below.
+CASES = [
+    (0, 16, 1, None),
+    (1, 6, 4, None),
+    (2, 4, 4, None),
+    (3, 3, 8, "a"),
+    (3, 3, 8, "b"),
+    (3, 3, 8, "c"),
+    (3, 3, 8, "d"),
+    (4, 3, 2, None),
+]
+
+
+@pytest.mark.parametrize("fn", FNS, ids=lambda f: f.__name__)
+@pytest.mark.parametrize("case", CASES, ids=lambda c: "c%d%s" % (c[0], c[3] or ""))
+def test_decode_parity(fn, case):
+    cfg, nsteps, q, sub = case
+    run_decode(fn, cfg, nsteps, q, sub=sub, dev=DEV)
+
+
+@pytest.mark.parametrize("fn", FNS, ids=lambda f: f.__name__)
+def test_full_size_config2(fn):
+    """The benchmark's launch: 64 queries x 2 draft rows at ~102K (128 rows)."""
+    run_decode(fn, 2, 3, 64, dev=DEV)
+
+
+@pytest.mark.parametrize("fn", FNS, ids=lambda f: f.__name__)
+def test_full_size_config4(fn):
+    """16 queries x 3 draft rows, rows of 65K..262K keys (48 rows)."""
+    run_decode(fn, 4, 2, 16, dev=DEV)
+
+
+def test_stats_invariants_config2():
+    """Lemma 1 on the GPU's own threshold: K <= f(T) <= C and the candidate
+    count equals the oracle's f(T); the K-th key and #{key > T*} match."""
+    w, res = run_decode(gvr, 2, 3, 8, dev=DEV, stats_check=True)
+    for i, st, kth, ngt in res:
+        s_host = w.scores[i].numpy()
+        rl = w.row_len[i].numpy()
+        for r in range(w.rows):
+            path = int(st["path"][r])
+            assert path in (1, 2, 3, 5), path
+            if i > 0:
+                assert path in (2, 3), "step %d row %d: guess not used (path %d)" % (i, r, path)
+            T = int(st["threshold"][r])
+            f = oracle.count_ge(s_host[r], T, n=int(rl[r]))
+            assert int(st["candidates"][r]) == f
+            assert K_TOPK <= f <= 6144
+            assert int(st["kth_key"][r]) == int(kth[r])
+            assert int(st["n_gt"][r]) == int(ngt[r])
+            assert int(st["n"][r]) == int(rl[r])
+
+
+def test_guess_does_not_change_the_answer():
+    """Metamorphic: exact, random, reversed, -1, duplicated, out-of-range and
+    absent guesses all give the same output."""
+    import paper_2604_22312_amd as g
+    w = workload(2, 2, 4, None)
+    K = w.K
+    S = w.scores[1].to(DEV)
+    RL = w.row_len[1].to(DEV)
+    exp, _, _ = oracle.topk(w.scores[1].numpy(), K, row_len=w.row_len[1].numpy())
+    prev_exact, _, _ = oracle.topk(w.scores[0].numpy(), K, row_len=w.row_len[0].numpy())
+    n = int(w.row_len[1].min())
+    rng = np.random.default_rng(3)
+    variants = {
+        "exact": prev_exact,
+        "current": exp,
+        "random": rng.integers(0, n, size=exp.shape).astype(np.int32),
+        "reversed": prev_exact[:, ::-1].copy(),
+        "minus1": np.full(exp.shape, -1, np.int32),
+        "dup": np.repeat(prev_exact[:, :1], K, axis=1),
+        "oob": np.full(exp.shape, 1 << 30, np.int32),
+        "mixed_oob": np.where(rng.random(exp.shape) < 0.5, prev_exact, -7).astype(np.int32),
+    }
+    for name, pv in variants.items():
+        note("metamorphic prev=%s" % name)
+        out = g.gvr_topk(S, RL, torch.from_numpy(np.ascontiguousarray(pv)).to(DEV), K)
+        assert_rows_equal(out.cpu().numpy(), exp, "prev=%s" % name)
+    out = g.gvr_topk(S, RL, None, K)
+    assert_rows_equal(out.cpu().numpy(), exp, "prev=None")
+
+
+def test_options_force_other_paths():
+    """capacity = K and 'ignore guess' force narrowing / tie paths; same answer."""
+    import paper_2604_22312_amd as g
+    w = workload(2, 2, 4, None)
+    K = w.K
+    S = w.scores[1].to(DEV)
+    RL = w.row_len[1].to(DEV)
+    exp, _, _ = oracle.topk(w.scores[1].numpy(), K, row_len=w.row_len[1].numpy())
+    prev, _, _ = oracle.topk(w.scores[0].numpy(), K, row_len=w.row_len[0].numpy())
+    pd = torch.from_numpy(prev).to(DEV)
+    for opts in ({"capacity": K}, {"flags": 1}, {"capacity": K + 1}, {"capacity": 2500},
+                 {"max_passes": -1}):
+        note("options %s" % opts)
+        st = torch.zeros((w.rows, 18), dtype=torch.int32, device=DEV)
+        out = g.gvr_topk_ex(S, RL, pd, K, options=opts, stats=st)
+        assert_rows_equal(out.cpu().numpy(), exp, "options %s" % opts)
+        paths = set(g.decode_stats(st)["path"].tolist())
+        assert -1 not in paths
+        if opts.get("flags") == 1 or opts.get("max_passes") == -1:
+            assert paths <= {5}
+        out = g.radix_topk_ex(S, RL, K, options=opts)
+        assert_rows_equal(out.cpu().numpy(), exp, "radix options %s" % opts)
+
+
+def _special_rows(ld, K, rng):
+    rows = []
+    lens = []
+    base = rng.standard_normal(ld).astype(np.float32)
+    rows.append(np.full(ld, 1.5, np.float32)); lens.append(ld)                  # all equal
+    x = base.copy(); x[::7] = np.inf; rows.append(x); lens.append(ld)           # many +inf
+    x = base.copy(); x[::5] = -np.inf; rows.append(x); lens.append(ld)          # many -inf
+    x = base.copy(); xb = x.view(np.uint32); xb[::11] = 0x7FC00000; rows.append(x); lens.append(ld)  # +NaN
+    x = base.copy(); xb = x.view(np.uint32); xb[::3] = 0xFFC00000; rows.append(x); lens.append(ld)   # -NaN
+    x = np.where(rng.random(ld) < 0.5, np.float32(0.0), np.float32(-0.0)).astype(np.float32)
+    rows.append(x); lens.append(ld)                                              # +0 / -0 only
+    x = rng.integers(0, 3, ld).astype(np.float32); rows.append(x); lens.append(ld)  # 3 levels
+    x = np.arange(ld, dtype=np.float32); rows.append(x); lens.append(ld)        # increasing
+    x = -np.arange(ld, dtype=np.float32); rows.append(x); lens.append(ld)       # decreasing
+    for n in (0, 1, K - 1, K, K + 1, 6144, 6145, ld - 1):
+        rows.append(base.copy()); lens.append(n)
+    x = np.full(ld, 2.0, np.float32); x[: ld // 2] = 3.0; rows.append(x); lens.append(ld)  # 2 levels
+    x = rng.standard_normal(ld).astype(np.float16).astype(np.float32); rows.append(x); lens.append(ld)
+    return np.stack(rows), np.array(lens, np.int32)
+
+
+@pytest.mark.parametrize("fn", FNS, ids=lambda f: f.__name__)
+@pytest.mark.parametrize("ld,K", [(20001, 2048), (9999, 7), (70003, 1), (4097, 2048), (131071, 2000)])
+def test_special_rows(fn, ld, K):
+    rng = np.random.default_rng(ld + K)
+    rows, lens = _special_rows(ld, K, rng)
+    exp, _, _ = oracle.topk(rows, K, row_len=lens)
+    S = torch.from_numpy(rows).to(DEV)
+    RL = torch.from_numpy(lens).to(DEV)
+    prev = torch.from_numpy(np.ascontiguousarray(exp)).to(DEV)   # also try a guess
+    note("special rows %s ld=%d K=%d" % (fn.__name__, ld, K))
+    out = fn(S, RL, None, K)
+    assert_rows_equal(out.cpu().numpy(), exp, "special rows ld=%d K=%d" % (ld, K))
+    out = fn(S, RL, prev, K)
+    assert_rows_equal(out.cpu().numpy(), exp, "special rows with guess ld=%d K=%d" % (ld, K))
+
+
+@pytest.mark.parametrize("fn", FNS, ids=lambda f: f.__name__)
+def test_misaligned_row_starts(fn):
+    """Rows whose first element is not 16-byte aligned (ld % 4 != 0) and a
+    scores view offset by one float."""
+    rng = np.random.default_rng(9)
+    K = 2048
+    for ld in (30001, 30002, 30003):
+        big = rng.gamma(2.0, 1.0, size=(6 * ld + 1)).astype(np.float32)
+        rows = big[1:].reshape(6, ld)
+        lens = np.array([ld, ld - 1, ld - 2, ld - 3, 12345, 2049], np.int32)
+        exp, _, _ = oracle.topk(rows, K, row_len=lens)
+        t = torch.from_numpy(big).to(DEV)
+        S = t[1:].view(6, ld)
+        assert S.is_contiguous()
+        note("misaligned %s ld=%d" % (fn.__name__, ld))
+        out = fn(S, torch.from_numpy(lens).to(DEV), None, K)
+        assert_rows_equal(out.cpu().numpy(), exp, "misaligned ld=%d" % ld)
+
+
+@pytest.mark.parametrize("fn", FNS, ids=lambda f: f.__name__)
+def test_poison_beyond_row_len(fn):
+    """Values past row_len are NaN / +inf: they must never be used."""
+    w = workload(3, 1, 8, "c")
+    K = w.K
+    s = w.scores[0].numpy().copy()
+    rl = w.row_len[0].numpy()
+    exp, _, _ = oracle.topk(s, K, row_len=rl)
+    for poison in (np.float32(np.nan), np.float32(np.inf), np.float32(1e30)):
+        p = s.copy()
+        for r in range(p.shape[0]):
+            p[r, rl[r]:] = poison
+        note("poison %s %r" % (fn.__name__, float(poison)))
+        out = fn(torch.from_numpy(p).to(DEV), torch.from_numpy(rl).to(DEV), None, K)
+        assert_rows_equal(out.cpu().numpy(), exp, "poison %r" % float(poison))
+
+
+def test_determinism():
+    import paper_2604_22312_amd as g
+    w = workload(2, 2, 4, None)
+    K = w.K
+    S = w.scores[1].to(DEV)
+    RL = w.row_len[1].to(DEV)
+    prev, _, _ = oracle.topk(w.scores[0].numpy(), K, row_len=w.row_len[0].numpy())
+    pd = torch.from_numpy(prev).to(DEV)
+    note("determinism x30")
+    ref = g.gvr_topk(S, RL, pd, K).clone()
+    st0 = torch.zeros((w.rows, 18), dtype=torch.int32, device=DEV)
+    g.gvr_topk_ex(S, RL, pd, K, stats=st0)
+    for _ in range(30):
+        assert torch.equal(g.gvr_topk(S, RL, pd, K), ref)
+        assert torch.equal(g.radix_topk(S, RL, pd, K), ref)
+    st1 = torch.zeros_like(st0)
+    g.gvr_topk_ex(S, RL, pd, K, stats=st1)
+    a, b = g.decode_stats(st0), g.decode_stats(st1)
+    for key in ("path", "passes", "candidates", "threshold", "kth_key", "n_gt"):
+        assert torch.equal(a[key], b[key]), key
+
+
+def test_many_rows_several_launches():
+    """More rows than one co-resident launch holds: the host splits the batch."""
+    import paper_2604_22312_amd as g
+    rng = np.random.default_rng(21)
+    B, ld, K = 700, 60000, 2048
+    x = rng.standard_normal((B, ld)).astype(np.float32)
+    lens = rng.integers(K + 1, ld + 1, size=B).astype(np.int32)
+    exp, _, _ = oracle.topk(x, K, row_len=lens, threads=8)
+    note("many rows B=%d ld=%d" % (B, ld))
+    S = torch.from_numpy(x).to(DEV)
+    RL = torch.from_numpy(lens).to(DEV)
+    out = g.gvr_topk(S, RL, torch.from_numpy(exp).to(DEV), K)
+    assert_rows_equal(out.cpu().numpy(), exp, "many rows gvr")
+    out = g.radix_topk(S, RL, None, K)
+    assert_rows_equal(out.cpu().numpy(), exp, "many rows radix")
+
+
+def test_caller_workspace_matches():
+    import paper_2604_22312_amd as g
+    w = workload(1, 2, 4, None)
+    K = w.K
+    S = w.scores[1].to(DEV)
+    RL = w.row_len[1].to(DEV)
+    exp, _, _ = oracle.topk(w.scores[1].numpy(), K, row_len=w.row_len[1].numpy())
+    nbytes = g.workspace_size(w.rows, w.ld, K)
+    assert nbytes > 0
+    ws = torch.zeros(nbytes, dtype=torch.uint8, device=DEV)
+    note("caller workspace")
+    for _ in range(3):
+        out = g.gvr_topk_ex(S, RL, None, K, workspace=ws)
+        assert_rows_equal(out.cpu().numpy(), exp, "caller workspace")
+    with pytest.raises(g.GvrError):
+        g.gvr_topk_ex(S, RL, None, K, workspace=ws[: nbytes // 2])
+
+
+@pytest.mark.parametrize("dist", ["gamma", "lognormal", "beta", "logistic", "weibull", "uniform_ties"])
+def test_distribution_families(dist):
+    """Score families named in the paper's distribution analysis (Sec. 6.4)."""
+    import paper_2604_22312_amd as g
+    rng = np.random.default_rng(abs(hash(dist)) % 1000)
+    B, ld, K = 16, 70690, 2048
+    gen = {
+        "gamma": lambda: rng.gamma(2.0, 1.0, (B, ld)),
+        "lognormal": lambda: rng.lognormal(-1.0, 1.0, (B, ld)),
+        "beta": lambda: rng.beta(2.0, 5.0, (B, ld)) - 3.0,
+        "logistic": lambda: rng.logistic(-0.5, 1.0, (B, ld)),
+        "weibull": lambda: rng.weibull(1.5, (B, ld)) - 2.2,
+        "uniform_ties": lambda: rng.integers(0, 200, (B, ld)) * 0.25,
+    }[dist]
+    x = gen().astype(np.float32)
+    exp, _, _ = oracle.topk(x, K)
+    # guess: exact answer of a perturbed copy (temporal correlation)
+    y = (x + 0.05 * rng.standard_normal(x.shape)).astype(np.float32)
+    pv, _, _ = oracle.topk(y, K)
+    note("distribution %s" % dist)
+    S = torch.from_numpy(x).to(DEV)
+    out = g.gvr_topk(S, None, torch.from_numpy(pv).to(DEV), K)
+    assert_rows_equal(out.cpu().numpy(), exp, "gvr %s" % dist)
+    out = g.radix_topk(S, None, None, K)
+    assert_rows_equal(out.cpu().numpy(), exp, "radix %s" % dist)
+
+
+def test_alternating_shapes_share_the_library_workspace():
+    """Calls of different shapes (different launch plans) in a row on the
+    library-owned workspace: its barrier counters must stay clean."""
+    import paper_2604_22312_amd as g
+    rng = np.random.default_rng(5)
+    K = 2048
+    shapes = [(128, 102463), (4, 102463), (700, 60000), (32, 32831), (9, 262144), (128, 102463)]
+    for B, ld in shapes:
+        x = rng.gamma(2.0, 1.0, size=(B, ld)).astype(np.float32)
+        lens = rng.integers(K + 1, ld + 1, size=B).astype(np.int32)
+        exp, _, _ = oracle.topk(x, K, row_len=lens, threads=8)
+        note("shape B=%d ld=%d" % (B, ld))
+        S = torch.from_numpy(x).to(DEV)
+        RL = torch.from_numpy(lens).to(DEV)
+        out = g.gvr_topk(S, RL, torch.from_numpy(exp).to(DEV), K)
+        assert_rows_equal(out.cpu().numpy(), exp, "gvr B=%d ld=%d" % (B, ld))
+        out = g.radix_topk(S, RL, None, K)
+        assert_rows_equal(out.cpu().numpy(), exp, "radix B=%d ld=%d" % (B, ld))
