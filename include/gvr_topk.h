@@ -40,17 +40,11 @@
  * Errors and synchronisation:
  *   - Argument problems detectable on the host are reported synchronously,
  *     before any work is enqueued. B == 0 is a no-op returning GVR_OK.
- *   - On GVR_OK the work is enqueued on `stream`; out_idx is complete when
- *     the stream reaches that point. The call does not synchronise.
- *   - gvr_topk / radix_topk use a workspace owned by the library (one per
- *     device, grown on demand with hipMalloc, kept until process exit).
- *     Calls that use it must not run concurrently on different streams of
- *     one device, and must not be captured into a HIP graph (growing the
- *     workspace allocates). gvr_topk_ex with a caller workspace has neither
- *     restriction (each concurrent call needs its own workspace).
- *   - Rows are processed by cooperatively launched kernels (all workgroups of
- *     a launch co-resident); rows whose length exceeds what one launch can
- *     keep on chip return GVR_ERR_TOO_LONG.
+ *   - On GVR_OK the work is enqueued on `stream` as one kernel launch (one
+ *     workgroup per row); out_idx is complete when the stream reaches that
+ *     point. The call does not synchronise, allocates nothing and keeps no
+ *     state between calls, so calls on different streams may overlap and a
+ *     call may be captured into a HIP graph.
  */
 #ifndef GVR_TOPK_H
 #define GVR_TOPK_H
@@ -66,52 +60,57 @@ typedef enum {
     GVR_OK = 0,
     GVR_ERR_INVALID_ARG = -1,    /* B < 0, ld < 0, NULL required pointer, bad option */
     GVR_ERR_UNSUPPORTED_K = -2,  /* K < 1 or K > GVR_MAX_K */
-    GVR_ERR_WORKSPACE = -3,      /* workspace too small / allocation failed */
-    GVR_ERR_HIP = -4,            /* a HIP runtime call or a launch failed */
-    GVR_ERR_TOO_LONG = -5        /* ld beyond what one launch keeps on chip */
+    GVR_ERR_HIP = -4,            /* the kernel launch failed */
+    GVR_ERR_TOO_LONG = -5        /* ld > 2^31 - 16 */
 } gvr_status;
 
 /* Largest supported K (Sec. 5.5: K = M = 2048 in the deployed gate). */
 #define GVR_MAX_K 2048
-/* Default and largest refine capacity C (Sec. 4.1, Lemma 1: C = 6144). */
-#define GVR_MAX_CANDIDATES 6144
+/* Default and largest refine capacity C of Lemma 1 (Sec. 4.1): the number of
+ * (key, index) candidates one gfx950 workgroup keeps in LDS (128 KB). The
+ * paper's C = 6144 is sized for its B200 shared memory (Sec. 5.3). */
+#define GVR_MAX_CANDIDATES 16384
 
 /* Per-row outcome codes reported in gvr_row_stats.path. */
 enum {
     GVR_PATH_TRIVIAL = 0,      /* n <= K: iota / -1 padding */
     GVR_PATH_ALL = 1,          /* K < n <= C: every element is a candidate */
-    GVR_PATH_GUESS = 2,        /* threshold accepted from the guessed window */
-    GVR_PATH_NARROWED = 3,     /* threshold accepted after narrowing the window */
+    GVR_PATH_GUESS = 2,        /* the guessed threshold held the answer: one pass */
+    GVR_PATH_NARROWED = 3,     /* guess fell short; count passes narrowed the threshold */
     GVR_PATH_TIES = 4,         /* the K-th key isolated exactly (ties straddle
                                   [K, C]); selection emitted without refine */
-    GVR_PATH_NO_GUESS = 5      /* prev_topk NULL or without a valid entry */
+    GVR_PATH_NO_GUESS = 5      /* prev_topk NULL / without a valid entry, or radix */
 };
 
 /* Optional knobs (NULL = defaults). Zero fields mean "default". */
 typedef struct gvr_options {
-    int32_t capacity;      /* refine capacity C, K <= C <= GVR_MAX_CANDIDATES (default 6144) */
-    int32_t max_passes;    /* cap on counting passes taken from the guess
-                              before the window falls back to the full key
-                              range (default 8; < 0 means 0: ignore the guess) */
+    int32_t capacity;      /* refine capacity C, K <= C <= GVR_MAX_CANDIDATES
+                              (default GVR_MAX_CANDIDATES); a smaller C forces
+                              more narrowing passes, never another result */
     int32_t flags;         /* bit 0: ignore prev_topk (run the radix schedule) */
-    int32_t reserved;
+    int32_t reserved0;     /* must be 0 */
+    int32_t reserved1;     /* must be 0 */
 } gvr_options;
 
 /* Optional per-row diagnostics, written when a device pointer is supplied. */
 typedef struct gvr_row_stats {
     int32_t n;             /* clamped row length */
     int32_t path;          /* GVR_PATH_* */
-    int32_t passes;        /* counting passes over the row (registers-resident) */
-    int32_t candidates;    /* candidates handed to the refine (0 if none) */
+    int32_t passes;        /* full-row passes (1: the guess held the answer) */
+    int32_t candidates;    /* candidates handed to the refine = f(threshold) */
     uint32_t threshold;    /* accepted threshold key T (K <= f(T) <= C) */
     uint32_t kth_key;      /* key of the K-th largest score */
     int32_t n_gt;          /* #{key > kth_key} */
     int32_t guess_valid;   /* valid entries of prev_topk used by the guess */
-    int64_t t_start;       /* s_memtime stamps (shader clock) at phase ends: */
-    int64_t t_guess;       /*   guess statistics ready                         */
-    int64_t t_search;      /*   threshold accepted (after the last count pass) */
-    int64_t t_collect;     /*   candidates written                             */
-    int64_t t_refine;      /*   output written                                 */
+    uint32_t spec_threshold; /* T_spec derived from the guess (0xFFFFFFFF if none) */
+    int32_t spec_count;    /* f(T_spec) counted in the first pass */
+    float pmean;           /* mean of the guessed scores (T0 of Sec. 4.2.1) */
+    int32_t reserved;
+    int64_t t_start;       /* s_memtime stamps of the row's workgroup (shader */
+    int64_t t_guess;       /*   clock): start; guess ready;                    */
+    int64_t t_search;      /*   threshold accepted (last pass done);           */
+    int64_t t_collect;     /*   refine starts;                                 */
+    int64_t t_refine;      /*   output written.                                */
 } gvr_row_stats;
 
 /* Guess-Verify-Refine Top-K (Sec. 4). See the file comment for semantics. */
@@ -123,25 +122,16 @@ gvr_status gvr_topk(const float* scores, int64_t B, int64_t ld, const int32_t* r
 gvr_status radix_topk(const float* scores, int64_t B, int64_t ld, const int32_t* row_len,
                       const int32_t* prev_topk, int32_t K, int32_t* out_idx, void* stream);
 
-/* Bytes of caller workspace gvr_topk_ex / radix_topk_ex need for (B, ld, K)
- * on the current device; 0 if the shape is unsupported. */
-size_t gvr_workspace_size(int64_t B, int64_t ld, int32_t K);
-
-/* As gvr_topk, with a caller-owned device workspace of ws_bytes bytes (at
- * least gvr_workspace_size(B, ld, K)), options and per-row stats ([B] device
- * array or NULL). The workspace must be zero-filled before its first use;
- * every call leaves its control area (at its start, the same size for every
- * shape on a device) zero-filled again, so one workspace serves any sequence
- * of shapes on its device. No allocation happens inside. */
+/* As gvr_topk, with options (NULL = defaults) and per-row stats ([B] device
+ * array of gvr_row_stats, or NULL). */
 gvr_status gvr_topk_ex(const float* scores, int64_t B, int64_t ld, const int32_t* row_len,
                        const int32_t* prev_topk, int32_t K, int32_t* out_idx, void* stream,
-                       void* workspace, size_t ws_bytes, const gvr_options* options,
-                       gvr_row_stats* stats);
+                       const gvr_options* options, gvr_row_stats* stats);
 
 /* Radix-select counterpart of gvr_topk_ex. */
 gvr_status radix_topk_ex(const float* scores, int64_t B, int64_t ld, const int32_t* row_len,
-                         int32_t K, int32_t* out_idx, void* stream, void* workspace,
-                         size_t ws_bytes, const gvr_options* options, gvr_row_stats* stats);
+                         int32_t K, int32_t* out_idx, void* stream, const gvr_options* options,
+                         gvr_row_stats* stats);
 
 /* Human-readable name of a status code (static string). */
 const char* gvr_status_string(gvr_status status);

@@ -10,8 +10,7 @@ Functions mirror the C entry points:
 
 * ``gvr_topk(scores, row_len, prev_topk, K, out_idx=None, stream=None)``
 * ``radix_topk(scores, row_len, prev_topk, K, out_idx=None, stream=None)``
-* ``gvr_topk_ex`` / ``radix_topk_ex`` (caller workspace, options, stats)
-* ``workspace_size(B, ld, K)``
+* ``gvr_topk_ex`` / ``radix_topk_ex`` (options, per-row stats)
 """
 from .binding import (  # noqa: F401
     GVR_MAX_CANDIDATES,
@@ -24,9 +23,9 @@ from .binding import (  # noqa: F401
     gvr_topk_ex,
     lib,
     library_path,
+    new_stats,
     radix_topk,
     radix_topk_ex,
     status_string,
     version,
-    workspace_size,
 )

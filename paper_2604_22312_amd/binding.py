@@ -7,14 +7,14 @@ import os
 import torch
 
 GVR_MAX_K = 2048
-GVR_MAX_CANDIDATES = 6144
+GVR_MAX_CANDIDATES = 16384
 PATH_NAMES = {0: "trivial", 1: "all", 2: "guess", 3: "narrowed", 4: "ties", 5: "no_guess", -1: "error"}
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.path.join(_HERE, "libgvr_topk.so")
 _lib = None
 
-STATS_INTS = 18   # sizeof(gvr_row_stats) / 4
+STATS_INTS = 22   # sizeof(gvr_row_stats) / 4
 
 
 class GvrError(RuntimeError):
@@ -24,9 +24,9 @@ class GvrError(RuntimeError):
 
 
 class Options(ctypes.Structure):
-    """Mirror of ``gvr_options``: capacity C, max_passes, flags (bit 0: ignore guess)."""
-    _fields_ = [("capacity", ctypes.c_int32), ("max_passes", ctypes.c_int32),
-                ("flags", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+    """Mirror of ``gvr_options``: capacity C, flags (bit 0: ignore the guess)."""
+    _fields_ = [("capacity", ctypes.c_int32), ("flags", ctypes.c_int32),
+                ("reserved0", ctypes.c_int32), ("reserved1", ctypes.c_int32)]
 
 
 def library_path() -> str:
@@ -41,17 +41,15 @@ def lib():
             raise ImportError("libgvr_topk.so not built: run `python -m paper_2604_22312_amd.build` "
                               "(or __graft_entry__.build())")
         L = ctypes.CDLL(_LIB_PATH)
-        vp, i64, i32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
+        vp, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32
         for name in ("gvr_topk", "radix_topk"):
             f = getattr(L, name)
             f.restype = ctypes.c_int
             f.argtypes = [vp, i64, i64, vp, vp, i32, vp, vp]
         L.gvr_topk_ex.restype = ctypes.c_int
-        L.gvr_topk_ex.argtypes = [vp, i64, i64, vp, vp, i32, vp, vp, vp, sz, ctypes.POINTER(Options), vp]
+        L.gvr_topk_ex.argtypes = [vp, i64, i64, vp, vp, i32, vp, vp, ctypes.POINTER(Options), vp]
         L.radix_topk_ex.restype = ctypes.c_int
-        L.radix_topk_ex.argtypes = [vp, i64, i64, vp, i32, vp, vp, vp, sz, ctypes.POINTER(Options), vp]
-        L.gvr_workspace_size.restype = sz
-        L.gvr_workspace_size.argtypes = [i64, i64, i32]
+        L.radix_topk_ex.argtypes = [vp, i64, i64, vp, i32, vp, vp, ctypes.POINTER(Options), vp]
         L.gvr_status_string.restype = ctypes.c_char_p
         L.gvr_status_string.argtypes = [ctypes.c_int]
         L.gvr_version.restype = ctypes.c_char_p
@@ -123,18 +121,8 @@ def radix_topk(scores, row_len, prev_topk, K, out_idx=None, stream=None):
     return _call("radix_topk", scores, row_len, prev_topk, K, out_idx, stream)
 
 
-def workspace_size(B: int, ld: int, K: int) -> int:
-    return int(lib().gvr_workspace_size(int(B), int(ld), int(K)))
-
-
-def _call_ex(radix, scores, row_len, prev_topk, K, out_idx, stream, workspace, options, stats):
+def _call_ex(radix, scores, row_len, prev_topk, K, out_idx, stream, options, stats):
     B, ld, K, out_idx = _check(scores, row_len, prev_topk, K, out_idx)
-    if workspace is None:
-        with torch.cuda.device(scores.device):
-            nbytes = workspace_size(B, ld, K)
-        workspace = torch.zeros(max(nbytes, 1), dtype=torch.uint8, device=scores.device)
-    if workspace.dtype != torch.uint8 or workspace.device != scores.device or not workspace.is_contiguous():
-        raise ValueError("workspace must be a contiguous uint8 tensor on the scores' device")
     if stats is not None and (stats.dtype != torch.int32 or stats.shape != (B, STATS_INTS)
                               or stats.device != scores.device or not stats.is_contiguous()):
         raise ValueError("stats must be a contiguous int32 tensor [B][%d] on the scores' device" % STATS_INTS)
@@ -146,38 +134,42 @@ def _call_ex(radix, scores, row_len, prev_topk, K, out_idx, stream, workspace, o
         L = lib()
         if radix:
             st = L.radix_topk_ex(_ptr(scores), B, ld, _ptr(row_len), K, _ptr(out_idx),
-                                 _stream(stream, scores.device), _ptr(workspace), workspace.numel(),
-                                 optp, _ptr(stats))
+                                 _stream(stream, scores.device), optp, _ptr(stats))
         else:
             st = L.gvr_topk_ex(_ptr(scores), B, ld, _ptr(row_len), _ptr(prev_topk), K, _ptr(out_idx),
-                               _stream(stream, scores.device), _ptr(workspace), workspace.numel(),
-                               optp, _ptr(stats))
+                               _stream(stream, scores.device), optp, _ptr(stats))
     if st != 0:
         raise GvrError("radix_topk_ex" if radix else "gvr_topk_ex", st)
     return out_idx
 
 
-def gvr_topk_ex(scores, row_len, prev_topk, K, out_idx=None, stream=None, workspace=None,
-                options=None, stats=None):
-    """``gvr_topk`` with a caller workspace (uint8, zero-filled before first use),
-    options (dict or ``Options``) and optional stats tensor ([B][18] int32)."""
-    return _call_ex(False, scores, row_len, prev_topk, K, out_idx, stream, workspace, options, stats)
+def gvr_topk_ex(scores, row_len, prev_topk, K, out_idx=None, stream=None, options=None, stats=None):
+    """``gvr_topk`` with options (dict or ``Options``) and an optional stats
+    tensor ([B][22] int32, see ``decode_stats``)."""
+    return _call_ex(False, scores, row_len, prev_topk, K, out_idx, stream, options, stats)
 
 
-def radix_topk_ex(scores, row_len, K, out_idx=None, stream=None, workspace=None, options=None, stats=None):
-    return _call_ex(True, scores, row_len, None, K, out_idx, stream, workspace, options, stats)
+def radix_topk_ex(scores, row_len, K, out_idx=None, stream=None, options=None, stats=None):
+    return _call_ex(True, scores, row_len, None, K, out_idx, stream, options, stats)
+
+
+def new_stats(B, device):
+    """A zeroed stats tensor for ``*_ex`` calls."""
+    return torch.zeros((B, STATS_INTS), dtype=torch.int32, device=device)
 
 
 def decode_stats(stats: torch.Tensor) -> dict:
-    """Split a [B][18] int32 stats tensor (``gvr_row_stats``) into named columns."""
+    """Split a [B][22] int32 stats tensor (``gvr_row_stats``) into named columns."""
     s = stats.detach().cpu()
-    i32 = s[:, :8]
-    i64 = s[:, 8:18].contiguous().view(torch.int64)
+    i32 = s[:, :12]
+    i64 = s[:, 12:22].contiguous().view(torch.int64)
     u32 = lambda c: (i32[:, c].to(torch.int64) & 0xFFFFFFFF)  # noqa: E731
     return {
         "n": i32[:, 0].clone(), "path": i32[:, 1].clone(), "passes": i32[:, 2].clone(),
         "candidates": i32[:, 3].clone(), "threshold": u32(4), "kth_key": u32(5),
         "n_gt": i32[:, 6].clone(), "guess_valid": i32[:, 7].clone(),
+        "spec_threshold": u32(8), "spec_count": i32[:, 9].clone(),
+        "pmean": i32[:, 10].clone().view(torch.float32),
         "t_start": i64[:, 0].clone(), "t_guess": i64[:, 1].clone(), "t_search": i64[:, 2].clone(),
         "t_collect": i64[:, 3].clone(), "t_refine": i64[:, 4].clone(),
     }

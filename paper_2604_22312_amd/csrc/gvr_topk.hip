@@ -1,50 +1,49 @@
 // gvr_topk.hip -- Guess-Verify-Refine exact Top-K and radix-select Top-K for
 // MI355X (gfx950), behind the C ABI declared in include/gvr_topk.h.
 //
-// Design (one cooperative launch per group of rows; all workgroups of a
-// launch are co-resident):
-//   * A row is split into S contiguous chunks, one workgroup (WG) each. Every
-//     WG streams its chunk from HBM exactly once, converts it to sortable u32
-//     keys and KEEPS IT IN VGPRs for the rest of the kernel: every later pass
-//     over the row is on-chip ALU work, not HBM traffic.
-//   * Guess (Sec. 4.2.1, Phase 1): each WG gathers the row's scores at
-//     prev_topk and reduces them to pmin / pmax (and pmean for the stats).
-//   * Threshold search (Sec. 4.2.2, Phase 2): a counting pass evaluates the
-//     threshold count f(T) = #{key >= T} (Sec. 4.1) at every edge of a
-//     512-bin window of key space in one sweep (wave-private LDS histograms;
-//     the last bin holds everything at or above the window). The first window
-//     is [key(pmin), key(pmax)] from the guess; a failed window is replaced by
-//     the bin that brackets the K-th key (or by the key range below/above the
-//     window), so a pass multiplies the resolution by 512. Per-WG histograms
-//     are exchanged through the workspace with one per-row barrier per pass,
-//     and every WG takes the same decision from the same sums.
-//   * A threshold T is accepted when K <= f(T) <= C; by Lemma 1 (Sec. 4.1) the
-//     candidate set {key >= T} then holds the exact answer.
-//   * Collect (Sec. 4.2.3, Phase 3): each WG writes its candidates (key, index)
-//     at offsets known in advance (per-WG prefix from the exchanged
-//     histograms, per-wave counts from the wave-private histograms -- the
-//     count cache -- and in-wave ballot/mbcnt ranks), so no atomic and no
-//     second counting sweep is needed. Candidates land in ascending index
-//     order.
-//   * Refine (Sec. 4.2.4, Phase 4): the last WG of the row to finish its
-//     collect (one global atomic per WG) loads the <= C candidates into LDS,
-//     narrows a 2048-bin LDS histogram until the K-th key T* is isolated,
-//     then emits every key > T* and the first K - #{key > T*} keys equal to
-//     T* (lower index first) in ascending index order.
-//   * If the K-th key is isolated by the counting passes themselves while
-//     f(T*) > C (ties straddle [K, C]), the selection is emitted directly from
-//     the registers, again in index order.
-//   * radix_topk runs the same kernel without a guess: the first window is
-//     the whole key range (9 bits of key per pass from the top), i.e. a
-//     distribution-agnostic radix select (Sec. 2.2).
+// One workgroup (1024 threads, 16 wave64s) owns one row; rows never talk to
+// each other, so a call is a single ordinary launch with one workgroup per
+// row and no device workspace. Each wave streams a contiguous sub-range of
+// the row with a rolling window of dwordx4 loads (8 slabs of 1 KB in flight
+// per wave), so the candidates it keeps are in ascending index order.
+//
+//   Guess (Sec. 4.2.1, Phase 1). While the first slabs of the row are in
+//   flight, the workgroup gathers the row's scores at prev_topk and reduces
+//   them to pmin / pmax (and pmean, reported in the stats). A small LDS
+//   histogram of the gathered keys gives T_spec, the 65th-smallest gathered
+//   key: a threshold that the previous step's Top-K makes likely to hold a
+//   few thousand elements of the current row, i.e. inside [K, C].
+//
+//   Threshold search (Sec. 4.2.2, Phase 2). The first full-row pass counts
+//   f(T) = #{key >= T} (Sec. 4.1) at every edge of a 256-bin window over
+//   [pmin, pmax] of key space (wave-private LDS histograms: the count cache),
+//   and so evaluates 257 thresholds in one sweep instead of one.
+//
+//   Collect (Sec. 4.2.3, Phase 3). In the same sweep every element with
+//   key >= T_spec is appended to its wave's LDS list (ballot + mbcnt ranks,
+//   no atomics). If K <= f(T_spec) <= C, Lemma 1 (Sec. 4.1) says the lists
+//   hold the exact answer and the row is never read again.
+//
+//   Refine (Sec. 4.2.4, Phase 4). The window histogram names the bin that
+//   holds the K-th key; a 2048-bin LDS histogram over the listed keys in that
+//   bin narrows it to the exact K-th key T* (two levels for a ~3-binade
+//   window). Every key > T* and the first K - #{key > T*} keys equal to T*
+//   (lower index first) are written out in ascending index order.
+//
+//   When the guess does not deliver (no valid prev_topk, f(T_spec) < K, or a
+//   wave's list overflows) the row is streamed again: count passes narrow a
+//   256-bin window around the K-th key (8 bits of key per pass), then one
+//   collect pass gathers the <= C candidates at the accepted threshold with
+//   exact per-wave offsets from the count cache, or, when ties straddle
+//   [K, C], an emit pass writes the selection directly. radix_topk runs only
+//   this path, starting from the whole key range: a distribution-agnostic
+//   radix select (Sec. 2.2).
 
 #include <hip/hip_runtime.h>
 
 #include <stdint.h>
-#include <string.h>
 
-#include <mutex>
-#include <vector>
+#include <algorithm>
 
 #include "gvr_topk.h"
 
@@ -52,25 +51,21 @@
 
 namespace {
 
+constexpr int kBlock = 1024;
 constexpr int kWave = 64;
-constexpr int kBinsLog2 = 9;
-constexpr int kBins = 1 << kBinsLog2;         // bins of a counting pass
-constexpr int kBinsX = kBins + 1;             // + "at or above the window"
-constexpr int kXchStride = 528;               // ints per published histogram
-constexpr int kRefBinsLog2 = 11;
-constexpr int kRefBins = 1 << kRefBinsLog2;   // bins of a refine level
-constexpr int kCmax = GVR_MAX_CANDIDATES;
-constexpr int kMaxPasses = 12;                // safety cap; 5 always suffice
-constexpr uint32_t kSpinLimit = 1u << 20;   // ~1 s of polling at most
+constexpr int kNW = kBlock / kWave;            // 16 waves
+constexpr int kU = 8;                          // slabs in flight per wave
+constexpr int kBins = 256;                     // bins of a counting window
+constexpr int kBinsX = kBins + 1;              // + "at or above the window"
+constexpr int kCap = GVR_MAX_CANDIDATES;       // list capacity (LDS)
+constexpr int kCapW = kCap / kNW;              // per-wave list capacity, first pass
+constexpr int kRefBins = 4096;                 // bins of a refine level (12 bits of key)
+constexpr int kGuessBins = kBlock;             // bins of the gathered-key histogram (1 per thread)
+constexpr int kGuessPerThread = (GVR_MAX_K + kBlock - 1) / kBlock;
+constexpr int kSpecRank = 64;                  // T_spec = gathered key of this rank from the bottom
+constexpr int kMaxPasses = 8;                  // 2 + at most 4 narrowing passes + 1 final pass suffice
 
-// Per-row control block in the workspace (one 128-byte line per row).
-struct RowCtl {
-    unsigned arrive;   // barrier arrivals of the current generation
-    unsigned gen;      // barrier generation
-    unsigned ticket;   // collect completions (last one refines)
-    unsigned err;      // set if a barrier wait gave up
-    unsigned pad[28];
-};
+static_assert(GVR_MAX_CANDIDATES % kNW == 0, "per-wave capacity");
 
 struct Params {
     const float* scores;
@@ -79,16 +74,9 @@ struct Params {
     const int32_t* prev;
     int32_t* out;
     gvr_row_stats* stats;
-    RowCtl* ctl;
-    int* xch;
-    uint32_t* cand_key;   // [rows][kCmax] candidate keys
-    int32_t* cand_idx;    // [rows][kCmax] candidate indices
     int32_t K;
-    int32_t rows;       // rows in this launch
-    int32_t row0;       // first row of this launch
-    int32_t S;          // workgroups per row in this launch
-    int32_t capacity;   // C
-    int32_t use_guess;  // 0: radix schedule
+    int32_t capacity;    // C
+    int32_t use_guess;   // 0: radix schedule
 };
 
 // ------------------------------------------------------------------ helpers
@@ -96,266 +84,301 @@ struct Params {
 DEV uint32_t key_of_bits(uint32_t u) { return u ^ ((uint32_t)((int32_t)u >> 31) | 0x80000000u); }
 DEV uint32_t key_of(float v) { return key_of_bits(__float_as_uint(v)); }
 
+// Number of set bits of m below this lane, plus acc.
 DEV uint32_t lanes_below(uint64_t m, uint32_t acc) {
     return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, acc));
 }
 
+// Wave-wide reductions and scans with DPP (VALU lane moves, no LDS round
+// trip): quad_perm / row_half_mirror / row_mirror combine the 16 lanes of a
+// row, readlane combines the four rows; every lane gets the result.
+template <int CTRL, int ROW_MASK = 0xF>
+DEV int dpp_i(int old, int x) {
+    return __builtin_amdgcn_update_dpp(old, x, CTRL, ROW_MASK, 0xF, false);
+}
+constexpr int kQuadSwap1 = 0xB1;   // quad_perm [1,0,3,2]
+constexpr int kQuadSwap2 = 0x4E;   // quad_perm [2,3,0,1]
+constexpr int kRowHalfMirror = 0x141;
+constexpr int kRowMirror = 0x140;
+constexpr int kRowShr1 = 0x111;
+constexpr int kRowBcast15 = 0x142;
+constexpr int kRowBcast31 = 0x143;
+
 DEV int wave_sum(int v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
-    return v;
+    v += dpp_i<kQuadSwap1>(0, v);
+    v += dpp_i<kQuadSwap2>(0, v);
+    v += dpp_i<kRowHalfMirror>(0, v);
+    v += dpp_i<kRowMirror>(0, v);
+    return __builtin_amdgcn_readlane(v, 0) + __builtin_amdgcn_readlane(v, 16) + __builtin_amdgcn_readlane(v, 32) +
+           __builtin_amdgcn_readlane(v, 48);
 }
 DEV float wave_sum_f(float v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
-    return v;
+    // fixed combination order: pairs, quads, halves, rows, then rows 0..3
+    v += __int_as_float(dpp_i<kQuadSwap1>(0, __float_as_int(v)));
+    v += __int_as_float(dpp_i<kQuadSwap2>(0, __float_as_int(v)));
+    v += __int_as_float(dpp_i<kRowHalfMirror>(0, __float_as_int(v)));
+    v += __int_as_float(dpp_i<kRowMirror>(0, __float_as_int(v)));
+    return ((__int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0)) +
+             __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16))) +
+            __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32))) +
+           __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
 }
 DEV uint32_t wave_min_u(uint32_t v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v = min(v, (uint32_t)__shfl_xor((int)v, o, kWave));
-    return v;
+    v = min(v, (uint32_t)dpp_i<kQuadSwap1>(0, (int)v));
+    v = min(v, (uint32_t)dpp_i<kQuadSwap2>(0, (int)v));
+    v = min(v, (uint32_t)dpp_i<kRowHalfMirror>(0, (int)v));
+    v = min(v, (uint32_t)dpp_i<kRowMirror>(0, (int)v));
+    return min(min((uint32_t)__builtin_amdgcn_readlane((int)v, 0), (uint32_t)__builtin_amdgcn_readlane((int)v, 16)),
+               min((uint32_t)__builtin_amdgcn_readlane((int)v, 32), (uint32_t)__builtin_amdgcn_readlane((int)v, 48)));
 }
 DEV uint32_t wave_max_u(uint32_t v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v = max(v, (uint32_t)__shfl_xor((int)v, o, kWave));
+    v = max(v, (uint32_t)dpp_i<kQuadSwap1>(0, (int)v));
+    v = max(v, (uint32_t)dpp_i<kQuadSwap2>(0, (int)v));
+    v = max(v, (uint32_t)dpp_i<kRowHalfMirror>(0, (int)v));
+    v = max(v, (uint32_t)dpp_i<kRowMirror>(0, (int)v));
+    return max(max((uint32_t)__builtin_amdgcn_readlane((int)v, 0), (uint32_t)__builtin_amdgcn_readlane((int)v, 16)),
+               max((uint32_t)__builtin_amdgcn_readlane((int)v, 32), (uint32_t)__builtin_amdgcn_readlane((int)v, 48)));
+}
+// Inclusive prefix sum over the 64 lanes: Hillis-Steele shifts inside each
+// 16-lane row (lanes without a source add 0), then row_bcast:15 / :31 carry
+// the row totals into the rows above.
+DEV int wave_incl_scan(int v, int /*lane*/) {
+    v += dpp_i<kRowShr1>(0, v);
+    v += dpp_i<kRowShr1 + 1>(0, v);
+    v += dpp_i<kRowShr1 + 3>(0, v);
+    v += dpp_i<kRowShr1 + 7>(0, v);
+    v += dpp_i<kRowBcast15, 0xA>(0, v);
+    v += dpp_i<kRowBcast31, 0xC>(0, v);
     return v;
 }
-// Inclusive prefix sum over the lanes of a wave.
-DEV int wave_incl_scan(int v, int lane) {
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {
-        int t = __shfl_up(v, o, kWave);
-        if (lane >= o) v += t;
-    }
-    return v;
-}
+// Lane v of every wave reads wave v's value: one LDS read + one wave
+// reduction per cross-wave sum.
+DEV int sum_over_waves(const int* vals, int lane) { return wave_sum(lane < kNW ? vals[lane] : 0); }
+DEV int sum_over_waves_below(const int* vals, int lane, int wave) { return wave_sum(lane < wave ? vals[lane] : 0); }
+
+DEV int64_t stamp() { return (int64_t)__builtin_amdgcn_s_memtime(); }
 
 // A window of key space: bins j < kBins cover [lo + j<<shift, lo + (j+1)<<shift);
-// bin kBins holds every key >= lo + kBins<<shift. Keys below lo are not counted.
+// bin kBins holds every key >= lo + kBins<<shift; keys below lo are not counted.
 struct Window {
     uint32_t lo;
     uint32_t shift;
 };
-
-DEV Window make_window(uint32_t a, uint32_t b) {  // covers [a, b], b >= a
-    uint64_t width = (uint64_t)b - a + 1;
+DEV Window make_window(uint32_t a, uint32_t b) {   // covers [a, b], b >= a
+    const uint64_t width = (uint64_t)b - a + 1;
     uint32_t s = 0;
     while (((uint64_t)kBins << s) < width) ++s;
     return Window{a, s};
 }
 DEV uint64_t edge_of(const Window& w, int j) { return (uint64_t)w.lo + ((uint64_t)j << w.shift); }
 
-// Cross-workgroup communication. Data that another workgroup reads is written
-// with device-coherent stores (agent-scope relaxed atomics: sc1, written
-// through to the point of coherence) and read with device-coherent loads
-// (sc1, never served by a stale cache line). Every wave waits for its own
-// stores to complete (s_waitcnt) before the workgroup barrier that precedes
-// the signalling atomic, so a workgroup that observes the signal reads
-// complete data. No L2 write-back or invalidate is needed.
-DEV void st_dev(int* p, int v) { __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
-DEV void st_dev(uint32_t* p, uint32_t v) { __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
-DEV int ld_dev(const int* p) { return __hip_atomic_load(const_cast<int*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
-DEV uint32_t ld_dev(const uint32_t* p) {
-    return __hip_atomic_load(const_cast<uint32_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-DEV void wait_mem() { __builtin_amdgcn_s_waitcnt(0); }
+// ------------------------------------------------------------------ LDS
+struct Smem {
+    uint2 list[kCap];                   // candidates (key, index), per-wave segments
+    union {
+        int hist[kNW][kBinsX];          // wave-private counting histograms
+        int rhist[kRefBins];            // refine / guess histogram
+    } u;
+    int F[kBinsX + 1];                  // F[j] = f(edge j) over the row
+    uint2 dummy[kBlock];                // sink of the unconditional list stores
+    int seg_off[kNW];                   // list segment of each wave
+    int seg_cnt[kNW];
+    int wa[kNW];
+    int wb[kNW];
+    int red[4][kNW];
+    float redf[kNW];
+    int scal[8];
+};
 
-// Per-row barrier among the `parties` workgroups of a row. Called by one
-// thread per WG after every wave of its WG has completed the stores being
-// published. Gives up (flags err) after kSpinLimit polls so that every wave
-// always terminates.
-DEV void row_barrier(RowCtl* c, unsigned parties) {
-    const unsigned g0 = ld_dev(&c->gen);
-    wait_mem();   // read the generation before arriving
-    const unsigned old = __hip_atomic_fetch_add(&c->arrive, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (old == parties - 1) {
-        st_dev(&c->arrive, 0u);
-        wait_mem();
-        __hip_atomic_fetch_add(&c->gen, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    } else {
-        uint32_t spins = 0;
-        while (ld_dev(&c->gen) == g0) {
-            __builtin_amdgcn_s_sleep(1);
-            if (++spins > kSpinLimit) {
-                st_dev(&c->err, 1u);
-                break;
-            }
+// Block-wide exclusive scan of one int (all kBlock threads). Returns the total.
+DEV int block_excl_scan(int& a, Smem& sm, int tid) {
+    const int lane = tid & 63, wave = tid >> 6;
+    const int ia = wave_incl_scan(a, lane);
+    if (lane == kWave - 1) sm.wa[wave] = ia;
+    __syncthreads();
+    const int before = sum_over_waves_below(sm.wa, lane, wave);
+    const int tot = sum_over_waves(sm.wa, lane);
+    __syncthreads();
+    a = before + ia - a;
+    return tot;
+}
+
+// ------------------------------------------------------------------ streaming
+// One wave streams float4 blocks [qb, qe) of the row in slabs of 64 blocks
+// with kU slabs in flight; `body(v, q, qs)` gets each lane's block q, its data
+// and the slab's first block qs. Every block index is clamped to qlast, so no
+// load leaves the 16-byte blocks that hold the row (refills past the wave's
+// last slab re-read the row's last block and are never used); bodies mask
+// elements outside [0, n) themselves. `prologue()` runs once after the first
+// loads are issued. The refill of a buffer slot is issued after its slab is
+// consumed and unconditionally, so each slot keeps one register set and a
+// slab waits only for its own load (vmcnt(kU - 1)), not for all of them.
+template <typename Pro, typename Body>
+DEV void stream_wave(const float4* __restrict__ xa, int qb, int qe, int qlast, int lane, Pro&& prologue,
+                     Body&& body) {
+    const int nslab = qe > qb ? (qe - qb + 63) >> 6 : 0;
+    float4 buf[kU];
+#pragma unroll
+    for (int u = 0; u < kU; ++u) buf[u] = xa[min(qb + u * 64 + lane, qlast)];
+    prologue();
+    int s0 = 0;
+    for (; s0 + kU <= nslab; s0 += kU) {
+#pragma unroll
+        for (int u = 0; u < kU; ++u) {
+            const int s = s0 + u;
+            body(buf[u], qb + s * 64 + lane, qb + s * 64);
+            buf[u] = xa[min(qb + (s + kU) * 64 + lane, qlast)];
         }
     }
+#pragma unroll
+    for (int u = 0; u < kU; ++u)
+        if (s0 + u < nslab) body(buf[u], qb + (s0 + u) * 64 + lane, qb + (s0 + u) * 64);
 }
 
-// ------------------------------------------------------------------ LDS
-template <int NW>
-struct SmemCount {
-    int hist[NW][kBinsX];   // wave-private histograms (the per-wave count cache)
-    int G[kBinsX];          // row totals per bin
-    int pre[kBinsX];        // totals of the WGs before this one
-    int F[kBinsX + 1];      // F[j] = f(edge j) (suffix sums of G)
-};
-struct SmemRefine {
-    uint32_t key[kCmax];
-    int32_t idx[kCmax];
-    int hist[kRefBins];
-};
-template <int NW>
-struct Smem {
-    union {
-        SmemCount<NW> c;
-        SmemRefine r;
-    } u;
-    int red[4][NW];
-    float redf[NW];
-    int wtot[2][NW];
-    int scal[16];
-};
-
-// Cross-wave helpers: lane v of every wave reads wave v's value, so a
-// reduction over the NW waves costs one LDS read and one wave reduction
-// (few VGPRs) instead of NW unrolled LDS reads.
-template <int NW>
-DEV int sum_over_waves(const int* vals, int lane) {
-    return wave_sum(lane < NW ? vals[lane] : 0);
-}
-template <int NW>
-DEV int sum_over_waves_below(const int* vals, int lane, int wave) {
-    return wave_sum(lane < wave ? vals[lane] : 0);
-}
-
-// Block-wide exclusive scan of two ints (BLOCK threads). Returns totals.
-template <int NW>
-DEV void block_excl_scan2(int& a, int& b, int& tot_a, int& tot_b, int (&sa)[2][NW], int tid) {
-    const int lane = tid & 63, wave = tid >> 6;
-    int ia = wave_incl_scan(a, lane), ib = wave_incl_scan(b, lane);
-    if (lane == kWave - 1) {
-        sa[0][wave] = ia;
-        sa[1][wave] = ib;
+// Count key k (if `in`) into bin min((k - lo) >> sh, kBins) of a wave-private
+// histogram. With AGG, lanes sharing the first active lane's bin add in one
+// atomic: wide (radix) windows map most keys of a wave to a few bins, and
+// same-address LDS atomics serialise.
+template <bool AGG>
+DEV void hist_add(int* hw, uint32_t k, bool in, uint32_t lo, uint32_t sh) {
+    const uint32_t b = min((k - lo) >> sh, (uint32_t)kBins);
+    if (!AGG) {
+        if (in) __hip_atomic_fetch_add(&hw[b], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        return;
     }
-    __syncthreads();
-    const int ba = sum_over_waves_below<NW>(sa[0], lane, wave);
-    const int bb = sum_over_waves_below<NW>(sa[1], lane, wave);
-    tot_a = sum_over_waves<NW>(sa[0], lane);
-    tot_b = sum_over_waves<NW>(sa[1], lane);
-    __syncthreads();
-    a = ba + ia - a;
-    b = bb + ib - b;
+    const uint64_t act = __ballot(in);
+    if (!act) return;
+    const uint32_t lead = __builtin_amdgcn_readlane(b, (int)__builtin_ctzll(act));
+    const uint64_t same = __ballot(in && b == lead);
+    if (in && b == lead) {
+        if (lanes_below(same, 0) == 0)
+            __hip_atomic_fetch_add(&hw[lead], (int)__popcll(same), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    } else if (in) {
+        __hip_atomic_fetch_add(&hw[b], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    }
 }
 
-template <int NW>
-DEV int block_sum(int v, Smem<NW>& sm, int tid) {
-    v = wave_sum(v);
-    if ((tid & 63) == 0) sm.red[0][tid >> 6] = v;
-    __syncthreads();
-    const int s = sum_over_waves<NW>(sm.red[0], tid & 63);
-    __syncthreads();
-    return s;
+DEV void block_keys(const float4& v, uint32_t (&k)[4]) {
+    k[0] = key_of(v.x);
+    k[1] = key_of(v.y);
+    k[2] = key_of(v.z);
+    k[3] = key_of(v.w);
 }
-
-DEV int64_t stamp() { return (int64_t)__builtin_amdgcn_s_memtime(); }
 
 // ------------------------------------------------------------------ refine
-// Exact K-th selection among the c candidates (key, index) already staged in
-// LDS in ascending index order. The K-th key is known to lie in [wlo, whi];
-// `above` candidates lie above whi. Emits the K indices in ascending order.
-template <int BLOCK, int NW>
-DEV void refine_and_emit(Smem<NW>& sm, int c, uint32_t wlo, uint32_t whi, int above, int K,
-                         int32_t* out, int tid, uint32_t* kth_out, int* ngt_out) {
-    SmemRefine& r = sm.u.r;
+// Exact K-th key among the listed candidates. The K-th key lies in
+// [wlo, whi]; `above` listed candidates lie above whi. Wave w's list segment
+// is list[seg_off[w] .. + seg_cnt[w]).
+DEV uint32_t refine_kth(Smem& sm, uint32_t wlo, uint32_t whi, int above, int K, int tid) {
+    const int lane = tid & 63, wave = tid >> 6;
     int need = K - above;   // >= 1
-    for (int level = 0; level < 4; ++level) {
-        if (wlo == whi) break;
-        uint64_t width = (uint64_t)whi - wlo + 1;
+    for (int level = 0; level < 4 && wlo != whi; ++level) {
+        const uint64_t width = (uint64_t)whi - wlo + 1;
         uint32_t s = 0;
         while (((uint64_t)kRefBins << s) < width) ++s;
-        for (int i = tid; i < kRefBins; i += BLOCK) r.hist[i] = 0;
+        for (int i = tid; i < kRefBins; i += kBlock) sm.u.rhist[i] = 0;
         __syncthreads();
-        for (int i = tid; i < c; i += BLOCK) {
-            uint32_t k = r.key[i];
-            if (k >= wlo && k <= whi)
-                __hip_atomic_fetch_add(&r.hist[(k - wlo) >> s], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        {
+            const uint2* seg = sm.list + sm.seg_off[wave];
+            const int cnt = sm.seg_cnt[wave];
+            for (int i = lane; i < cnt; i += kWave) {
+                const uint32_t kk = seg[i].x;
+                if (kk >= wlo && kk <= whi)
+                    __hip_atomic_fetch_add(&sm.u.rhist[(kk - wlo) >> s], 1, __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_WORKGROUP);
+            }
         }
         __syncthreads();
-        // Suffix sums from the top bin: thread t owns bins [t*PER, (t+1)*PER).
-        constexpr int PER = kRefBins / BLOCK;
+        constexpr int PER = kRefBins / kBlock;   // 4 bins per thread
         int loc[PER];
-        int mysum = 0;
+        int mine = 0;
 #pragma unroll
         for (int q = 0; q < PER; ++q) {
-            loc[q] = r.hist[tid * PER + q];
-            mysum += loc[q];
+            loc[q] = sm.u.rhist[tid * PER + q];
+            mine += loc[q];
         }
-        // exclusive "sum of bins above my range" = total - inclusive prefix
-        int a = mysum, dummy = 0, tot = 0, tdummy = 0;
-        block_excl_scan2<NW>(a, dummy, tot, tdummy, sm.wtot, tid);
-        int above_me = tot - a - mysum;   // sum of bins with index > my range
-        // find the bin where the count from the top reaches `need`
-        int run = above_me;
-        int found = -1, found_above = 0;
+        int a = mine;
+        const int tot = block_excl_scan(a, sm, tid);
+        int run = tot - a - mine;   // bins above this thread's range
+        if (tid == 0) sm.scal[0] = -1;
+        __syncthreads();
 #pragma unroll
         for (int q = PER - 1; q >= 0; --q) {
-            int nr = run + loc[q];
-            if (found < 0 && run < need && nr >= need) {
-                found = tid * PER + q;
-                found_above = run;
+            const int nr = run + loc[q];
+            if (run < need && nr >= need) {
+                sm.scal[0] = tid * PER + q;
+                sm.scal[1] = run;
             }
             run = nr;
         }
-        if (found >= 0) {
-            sm.scal[0] = found;
-            sm.scal[1] = found_above;
-        }
         __syncthreads();
-        int b = sm.scal[0];
-        int ab = sm.scal[1];
+        const int b = sm.scal[0];
+        const int ab = sm.scal[1];
         __syncthreads();
+        if (b < 0) break;   // cannot happen for consistent counts; keeps every path finite
         need -= ab;
-        uint64_t nlo = (uint64_t)wlo + ((uint64_t)b << s);
+        const uint64_t nlo = (uint64_t)wlo + ((uint64_t)b << s);
         uint64_t nhi = nlo + ((uint64_t)1 << s) - 1;
         if (nhi > whi) nhi = whi;
         wlo = (uint32_t)nlo;
         whi = (uint32_t)nhi;
     }
-    const uint32_t T = wlo;   // the K-th key
-    // Ordered emission over the candidates in buffer (= index) order.
-    const int seg = (c + BLOCK - 1) / BLOCK;
-    const int i0 = min(tid * seg, c), i1 = min(i0 + seg, c);
+    return wlo;
+}
+
+// Write the selection from the lists: every key > T, then the first `take`
+// keys == T in list (= index) order; output in ascending index order.
+DEV void emit_from_lists(Smem& sm, uint32_t T, int K, int32_t* out, int tid, int* n_gt_out) {
+    const int lane = tid & 63, wave = tid >> 6;
+    const uint2* seg = sm.list + sm.seg_off[wave];
+    const int cnt = sm.seg_cnt[wave];
     int gt = 0, eq = 0;
-    for (int i = i0; i < i1; ++i) {
-        uint32_t k = r.key[i];
-        gt += (k > T);
-        eq += (k == T);
+    for (int i = lane; i < cnt; i += kWave) {
+        const uint32_t kk = seg[i].x;
+        gt += kk > T;
+        eq += kk == T;
     }
-    int gtb = gt, eqb = eq, gtt = 0, eqt = 0;
-    block_excl_scan2<NW>(gtb, eqb, gtt, eqt, sm.wtot, tid);
-    const int take = K - gtt;   // ties to take, lower index first
-    for (int i = i0; i < i1; ++i) {
-        uint32_t k = r.key[i];
-        if (k > T) {
-            const int o = gtb + min(eqb, take);
-            if (o >= 0 && o < K) out[o] = r.idx[i];
-            ++gtb;
-        } else if (k == T) {
-            const int o = gtb + eqb;
-            if (eqb < take && o >= 0 && o < K) out[o] = r.idx[i];
-            ++eqb;
+    gt = wave_sum(gt);
+    eq = wave_sum(eq);
+    if (lane == 0) {
+        sm.wa[wave] = gt;
+        sm.wb[wave] = eq;
+    }
+    __syncthreads();
+    int gb = sum_over_waves_below(sm.wa, lane, wave);
+    int eb = sum_over_waves_below(sm.wb, lane, wave);
+    const int gtot = sum_over_waves(sm.wa, lane);
+    const int take = K - gtot;
+    for (int i0 = 0; i0 < cnt; i0 += kWave) {
+        const int i = i0 + lane;
+        uint32_t kk = 0;
+        int idx = 0;
+        if (i < cnt) {
+            kk = seg[i].x;
+            idx = (int)seg[i].y;
         }
+        const bool fg = i < cnt && kk > T;
+        const bool fe = i < cnt && kk == T;
+        const uint64_t mg = __ballot(fg), me = __ballot(fe);
+        const int g = gb + (int)lanes_below(mg, 0), e = eb + (int)lanes_below(me, 0);
+        if (fg) {
+            const int o = g + min(e, take);
+            if (o >= 0 && o < K) out[o] = idx;
+        } else if (fe && e < take) {
+            const int o = g + e;
+            if (o >= 0 && o < K) out[o] = idx;
+        }
+        gb += __popcll(mg);
+        eb += __popcll(me);
     }
-    *kth_out = T;
-    *ngt_out = gtt;
+    *n_gt_out = gtot;
 }
 
 // ------------------------------------------------------------------ kernel
-template <int BLOCK, int R4, int MINW>
-__global__ __launch_bounds__(BLOCK, MINW) void topk_rows_kernel(Params p) {
-    constexpr int NW = BLOCK / kWave;
-    constexpr int WSPAN = R4 * 256;   // elements of one wave's sub-chunk
-    constexpr int CH = NW * WSPAN;    // elements of one WG's chunk
-    __shared__ Smem<NW> sm;
-
+__global__ __launch_bounds__(kBlock) void topk_row_kernel(Params p) {
+    __shared__ Smem sm;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int g = blockIdx.x;
-    const int rl = g / p.S, w = g % p.S;
-    if (rl >= p.rows) return;
-    const int64_t row = (int64_t)p.row0 + rl;
+    const int64_t row = blockIdx.x;
     const int64_t t0 = stamp();
 
     int64_t n64 = p.row_len ? (int64_t)p.row_len[row] : p.ld;
@@ -368,357 +391,411 @@ __global__ __launch_bounds__(BLOCK, MINW) void topk_rows_kernel(Params p) {
 
     // (a1) row classify: n <= K -> 0..n-1 then -1 padding.
     if (n <= K) {
-        if (w == 0) {
-            for (int i = tid; i < K; i += BLOCK) out[i] = (i < n) ? i : -1;
-            if (st && tid == 0) {
-                gvr_row_stats s = {};
-                s.n = n;
-                s.path = GVR_PATH_TRIVIAL;
-                s.t_start = t0;
-                s.t_refine = stamp();
-                *st = s;
-            }
+        for (int i = tid; i < K; i += kBlock) out[i] = (i < n) ? i : -1;
+        if (st && tid == 0) {
+            gvr_row_stats s = {};
+            s.n = n;
+            s.path = GVR_PATH_TRIVIAL;
+            s.t_start = t0;
+            s.t_refine = stamp();
+            *st = s;
         }
         return;
     }
-    const int aoff = (int)(((uintptr_t)x >> 2) & 3);   // x sits aoff floats into a 16-B block
-    const int s_row = (n + aoff + CH - 1) / CH;
-    if (w >= s_row) return;
-    RowCtl* ctl = p.ctl + rl;
-    int* xch = p.xch + (size_t)rl * 2 * p.S * kXchStride;
-    uint32_t* ckey = p.cand_key + (size_t)rl * kCmax;
-    int32_t* cidx = p.cand_idx + (size_t)rl * kCmax;
-    const int cap = p.capacity;
 
-    // ---------------- (a2) guess, overlapped with the chunk stream
-    // The guess indices are loaded first (8 KB per row); the scattered
-    // gathers x[prev] are issued right behind the chunk's loads, so both are
-    // in flight together and the gathers mostly hit lines the row's
-    // workgroups are streaming anyway.
-    constexpr int KPT = (GVR_MAX_K + BLOCK - 1) / BLOCK;
-    const bool have_prev = p.use_guess && p.prev;
-    int pq[KPT];
+    // Float4 blocks of the row (virtual index = element index + aoff, so a
+    // block is one aligned 16-byte load) and this wave's contiguous share.
+    const int aoff = (int)(((uintptr_t)x >> 2) & 3);
+    const float4* xa = reinterpret_cast<const float4*>(x - aoff);
+    const int nq = (n + aoff + 3) >> 2;
+    const int qlast = nq - 1;
+    const int per = ((nq + kNW - 1) / kNW + 63) & ~63;   // whole slabs per wave
+    const int qb = min(wave * per, nq), qe = min(qb + per, nq);
+    const int cap = p.capacity;
+    const bool all_mode = (n <= cap) && (per * 4 <= kCapW);   // every element is a candidate
+
+    // ---------------- pass 1 parameters and state
+    bool have_prev = p.use_guess && p.prev && !all_mode;
+    int gvalid = 0;
+    uint32_t gmin = 0xFFFFFFFFu, gmax = 0u, tspec = 0xFFFFFFFFu;
+    float gsum = 0.f;
+    Window win = make_window(0u, 0xFFFFFFFFu);
+    bool spec = all_mode || have_prev;   // pass 1 collects key >= tspec (else: counts)
+    int cnt_w = 0;              // this wave's elements >= tspec (counted past capacity)
+    int64_t t1 = t0;
+
+    // The guess indices are loaded before the first slabs (8 KB per row), so
+    // they return first; the gathers x[prev] go out right behind the slabs.
+    int pq[kGuessPerThread];
     if (have_prev) {
         const int32_t* pv = p.prev + row * (int64_t)K;
 #pragma unroll
-        for (int m = 0; m < KPT; ++m) {
-            const int j = tid + m * BLOCK;
+        for (int m = 0; m < kGuessPerThread; ++m) {
+            const int j = tid + m * kBlock;
             pq[m] = (j < K) ? pv[j] : -1;
         }
     }
-
-    // ---------------- load the chunk once; keep it as keys in VGPRs
-    // Virtual index v = element index + aoff, so that v % 4 == 0 is a 16-byte
-    // boundary; the wave's sub-chunk starts at vb. Every slab issues one
-    // unconditional dwordx4 load. Its block index is clamped to the last
-    // block that holds an element of the row, so no load leaves the 16-byte
-    // blocks that contain x[0..n); elements outside [0, n) are never used
-    // (their key is set to 0 and they are excluded from every count).
-    const int vb = w * CH + wave * WSPAN;
-    const float4* xa = reinterpret_cast<const float4*>(x - aoff);
-    const int qlast = (n - 1 + aoff) >> 2;
-    uint32_t k[R4][4];
-    float gv[KPT];
-    {
-        float4 raw[R4];
+    if (!spec)
+        for (int i = tid; i < kNW * kBinsX; i += kBlock) (&sm.u.hist[0][0])[i] = 0;
+    if (tid < kNW) sm.seg_off[tid] = tid * kCapW;
+    // Guess statistics (Phase 1), run while the first slabs are in flight.
+    auto prologue = [&]() {
+        if (all_mode) {
+            tspec = 0u;
+        } else if (have_prev) {
+            float gv[kGuessPerThread];
+            uint32_t gk[kGuessPerThread];
+            bool ok[kGuessPerThread];
 #pragma unroll
-        for (int i = 0; i < R4; ++i) {
-            const int q = min(((vb + i * 256) >> 2) + lane, qlast);
-            raw[i] = xa[q];
-        }
-        if (have_prev) {
+            for (int m = 0; m < kGuessPerThread; ++m) {
+                ok[m] = pq[m] >= 0 && pq[m] < n;
+                gv[m] = ok[m] ? x[pq[m]] : 0.f;
+            }
 #pragma unroll
-            for (int m = 0; m < KPT; ++m) gv[m] = (pq[m] >= 0 && pq[m] < n) ? x[pq[m]] : 0.f;
-        }
-#pragma unroll
-        for (int i = 0; i < R4; ++i) {
-            k[i][0] = key_of(raw[i].x);
-            k[i][1] = key_of(raw[i].y);
-            k[i][2] = key_of(raw[i].z);
-            k[i][3] = key_of(raw[i].w);
-            const int s0 = vb + i * 256 - aoff;   // element index of the slab's first slot
-            if (s0 < 0 || s0 + 255 >= n) {        // wave-uniform: an edge slab
-#pragma unroll
-                for (int c = 0; c < 4; ++c) {
-                    const int e = s0 + lane * 4 + c;
-                    if (e < 0 || e >= n) k[i][c] = 0u;
+            for (int m = 0; m < kGuessPerThread; ++m) {
+                gk[m] = key_of(gv[m]);
+                if (ok[m]) {
+                    gmin = min(gmin, gk[m]);
+                    gmax = max(gmax, gk[m]);
+                    gsum += gv[m];
+                    ++gvalid;
                 }
             }
-        }
-    }
-
-    // Guess statistics (Phase 1): pmin / pmax as keys, pmean for the stats.
-    int gvalid = 0;
-    uint32_t gmin = 0xFFFFFFFFu, gmax = 0u;
-    float gsum = 0.f;
-    if (have_prev) {
+            gvalid = wave_sum(gvalid);
+            gmin = wave_min_u(gmin);
+            gmax = wave_max_u(gmax);
+            gsum = wave_sum_f(gsum);
+            if (lane == 0) {
+                sm.red[0][wave] = gvalid;
+                sm.red[1][wave] = (int)gmin;
+                sm.red[2][wave] = (int)gmax;
+                sm.redf[wave] = gsum;
+            }
+            for (int i = tid; i < kGuessBins; i += kBlock) sm.u.rhist[i] = 0;
+            if (tid == 0) sm.scal[0] = 0;
+            __syncthreads();
+            gvalid = sum_over_waves(sm.red[0], lane);
+            gmin = wave_min_u(lane < kNW ? (uint32_t)sm.red[1][lane] : 0xFFFFFFFFu);
+            gmax = wave_max_u(lane < kNW ? (uint32_t)sm.red[2][lane] : 0u);
+            gsum = 0.f;
+            for (int v = 0; v < kNW; ++v) gsum += sm.redf[v];   // pmean: fixed order
+            if (gvalid > 0) {
+                // T_spec: lower edge of the histogram bin (over [pmin, pmax])
+                // holding the (kSpecRank + 1)-th smallest gathered key.
+                const uint64_t width = (uint64_t)gmax - gmin + 1;
+                uint32_t sh = 0;
+                while (((uint64_t)kGuessBins << sh) < width) ++sh;
 #pragma unroll
-        for (int m = 0; m < KPT; ++m) {
-            if (pq[m] >= 0 && pq[m] < n) {
-                const uint32_t kk = key_of(gv[m]);
-                gmin = min(gmin, kk);
-                gmax = max(gmax, kk);
-                gsum += gv[m];
-                ++gvalid;
+                for (int m = 0; m < kGuessPerThread; ++m)
+                    if (ok[m])
+                        __hip_atomic_fetch_add(&sm.u.rhist[(gk[m] - gmin) >> sh], 1, __ATOMIC_RELAXED,
+                                               __HIP_MEMORY_SCOPE_WORKGROUP);
+                __syncthreads();
+                // thread t owns bin t; a block scan finds the bin holding the target
+                const int cnt = sm.u.rhist[tid];
+                int below = cnt;
+                block_excl_scan(below, sm, tid);
+                const int target = min(kSpecRank + 1, gvalid);
+                if (below < target && below + cnt >= target) sm.scal[0] = tid;
+                __syncthreads();
+                tspec = gmin + ((uint32_t)sm.scal[0] << sh);
+            } else {
+                tspec = 0xFFFFFFFFu;   // no usable guess: pass 1 keeps nothing useful
+                have_prev = false;
             }
         }
-        gvalid = wave_sum(gvalid);
-        gmin = wave_min_u(gmin);
-        gmax = wave_max_u(gmax);
-        gsum = wave_sum_f(gsum);
-        if (lane == 0) {
-            sm.red[0][wave] = gvalid;
-            sm.red[1][wave] = (int)gmin;
-            sm.red[2][wave] = (int)gmax;
-            sm.redf[wave] = gsum;
-        }
         __syncthreads();
-        gvalid = sum_over_waves<NW>(sm.red[0], lane);
-        gmin = wave_min_u(lane < NW ? (uint32_t)sm.red[1][lane] : 0xFFFFFFFFu);
-        gmax = wave_max_u(lane < NW ? (uint32_t)sm.red[2][lane] : 0u);
-        // pmean: fixed summation order (wave partials in wave order).
-        gsum = 0.f;
-        for (int v = 0; v < NW; ++v) gsum += sm.redf[v];
-        __syncthreads();
-    }
-    const int64_t t1 = stamp();
-
-    // Slots of this wave / WG that hold no element (their key is 0).
-    auto valid_in = [&](int v0, int len) {   // #elements with virtual index in [v0, v0+len)
-        int a = max(v0, aoff), b = min(v0 + len, n + aoff);
-        return b > a ? b - a : 0;
+        t1 = stamp();
     };
-    const int inv_wave = WSPAN - valid_in(vb, WSPAN);
 
-    // Candidate set parameters decided below.
-    int path;
-    int passes = 0;
-    uint32_t T = 0;           // accepted threshold key
-    int FT = 0;               // f(T) = candidates of the row
-    int pre_ge = 0;           // candidates in the WGs before this one
-    int wave_ge = 0;          // candidates of this wave
-    uint32_t rlo = 0, rhi = 0xFFFFFFFFu;   // refine window for the K-th key
-    int above = 0;            // candidates known to be above rhi
-    bool ties = false;        // K-th key isolated by counting; emit directly
-    int gt_pre = 0, eq_pre = 0, gt_wave = 0, eq_wave = 0, n_gt_row = 0;
+    // ---------------- pass 1: speculative collect (or the first count pass)
+    int* hw = sm.u.hist[wave];
+    uint2* lw = sm.list + wave * kCapW;
+    // Append the listed elements of one lane's block (keys k, first index e0)
+    // whose key is >= tspec (and, in edge slabs, lies in [0, n)).
+    // Lanes whose element is not kept write to a private dummy slot, so the
+    // four stores of a slab need no exec-mask juggling; one capacity check per
+    // slab (wave-uniform) replaces per-element checks.
+    uint2* const dummy = sm.dummy + tid;
+    auto collect = [&](const uint32_t (&k)[4], int e0, bool edge) {
+        const bool v0 = !edge || (e0 >= 0 && e0 < n), v1 = !edge || (e0 + 1 >= 0 && e0 + 1 < n);
+        const bool v2 = !edge || (e0 + 2 >= 0 && e0 + 2 < n), v3 = !edge || (e0 + 3 >= 0 && e0 + 3 < n);
+        const bool f0 = v0 && k[0] >= tspec, f1 = v1 && k[1] >= tspec;
+        const bool f2 = v2 && k[2] >= tspec, f3 = v3 && k[3] >= tspec;
+        const uint64_t m0 = __ballot(f0), m1 = __ballot(f1), m2 = __ballot(f2), m3 = __ballot(f3);
+        const int total = __popcll(m0) + __popcll(m1) + __popcll(m2) + __popcll(m3);
+        cnt_w = __builtin_amdgcn_readfirstlane(cnt_w);   // wave-uniform: keep it scalar
+        if (cnt_w + total <= kCapW) {
+            int p = cnt_w + (int)lanes_below(m3, lanes_below(m2, lanes_below(m1, lanes_below(m0, 0))));
+            *(f0 ? lw + p : dummy) = make_uint2(k[0], (uint32_t)e0);
+            p += f0;
+            *(f1 ? lw + p : dummy) = make_uint2(k[1], (uint32_t)(e0 + 1));
+            p += f1;
+            *(f2 ? lw + p : dummy) = make_uint2(k[2], (uint32_t)(e0 + 2));
+            p += f2;
+            *(f3 ? lw + p : dummy) = make_uint2(k[3], (uint32_t)(e0 + 3));
+        }
+        cnt_w += total;   // counted past capacity: the overflow is detected later
+    };
+    stream_wave(xa, qb, qe, qlast, lane, prologue, [&](const float4& v, int q, int qs) {
+        uint32_t k[4];
+        block_keys(v, k);
+        const int e0 = 4 * q - aoff;
+        const bool edge = (4 * qs - aoff < 0 || 4 * qs + 255 - aoff >= n);   // wave-uniform
+        if (spec) {
+            if (edge) collect(k, e0, true);
+            else collect(k, e0, false);
+        } else {
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+                hist_add<true>(hw, k[c], !edge || (e0 + c >= 0 && e0 + c < n), 0u, win.shift);
+        }
+    });
+    int passes = 1;
+    int f_spec = 0;
+    bool overflow = false;
+    if (spec) {
+        if (lane == 0) {
+            sm.seg_cnt[wave] = min(cnt_w, kCapW);
+            sm.wa[wave] = cnt_w;
+        }
+        __syncthreads();
+        f_spec = sum_over_waves(sm.wa, lane);
+        overflow = wave_max_u(lane < kNW ? (uint32_t)sm.wa[lane] : 0u) > (uint32_t)kCapW;
+        __syncthreads();
+    }
 
-    if (n <= cap) {
-        // Every element is a candidate: counts are known without a pass.
-        path = GVR_PATH_ALL;
-        T = 0;
-        FT = n;
-        pre_ge = valid_in(0, w * CH);
-        wave_ge = WSPAN - inv_wave;
+    // Row totals per bin and F[j] = f(edge j) = sum_{b >= j} G[b].
+    auto compute_F = [&]() {
+        __syncthreads();   // every wave's histogram updates are done
+        int g = 0;
+        const int b = kBins - tid;   // thread t owns bin kBins - t (t < kBinsX)
+        if (b >= 0)
+            for (int v = 0; v < kNW; ++v) g += sm.u.hist[v][b];
+        int a = g;
+        block_excl_scan(a, sm, tid);
+        if (b >= 0) sm.F[b] = a + g;
+        if (tid == 0) sm.F[kBinsX] = 0;
+        __syncthreads();
+    };
+    // Largest bin j with F[j] >= K (-1 if F[0] < K).
+    auto crossing = [&]() {
+        if (tid == 0) sm.scal[2] = -1;
+        __syncthreads();
+        if (tid < kBinsX && sm.F[tid] >= K && sm.F[tid + 1] < K) sm.scal[2] = tid;
+        __syncthreads();
+        const int j = sm.scal[2];
+        __syncthreads();
+        return j;
+    };
+    // Count pass over window `win` (wave-private histograms, then F).
+    auto count_pass = [&]() {
+        __syncthreads();
+        for (int i = tid; i < kNW * kBinsX; i += kBlock) (&sm.u.hist[0][0])[i] = 0;
+        __syncthreads();
+        const uint32_t lo = win.lo, sh = win.shift;
+        stream_wave(xa, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
+            uint32_t k[4];
+            block_keys(v, k);
+            const int e0 = 4 * q - aoff;
+            const bool edge = (4 * qs - aoff < 0 || 4 * qs + 255 - aoff >= n);
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const bool ok = !edge || (e0 + c >= 0 && e0 + c < n);
+                hist_add<true>(hw, k[c], ok && k[c] >= lo, lo, sh);
+            }
+        });
+        ++passes;
+        __syncthreads();
+        compute_F();
+    };
+
+    int path = all_mode ? GVR_PATH_ALL : (have_prev ? GVR_PATH_GUESS : GVR_PATH_NO_GUESS);
+    uint32_t T = 0, rlo = 0, rhi = 0xFFFFFFFFu;
+    int above = 0, cands = 0;
+    bool done_lists = false;   // lists hold every key >= T
+    bool ties = false;
+    uint32_t tstar = 0;
+    int n_gt_row = 0;
+    int64_t t2 = t1, t3 = t1;
+
+    if (spec && !overflow && f_spec >= K && f_spec <= cap) {
+        // The speculative lists hold every key >= T_spec, hence the answer
+        // (Lemma 1); the refine window is the range of the listed keys.
+        T = tspec;
+        cands = f_spec;
+        done_lists = true;
+        uint32_t mn = 0xFFFFFFFFu, mx = 0u;
+        {
+            const uint2* seg = sm.list + sm.seg_off[wave];
+            const int cnt = sm.seg_cnt[wave];
+            for (int i = lane; i < cnt; i += kWave) {
+                mn = min(mn, seg[i].x);
+                mx = max(mx, seg[i].x);
+            }
+            mn = wave_min_u(mn);
+            mx = wave_max_u(mx);
+            if (lane == 0) {
+                sm.red[1][wave] = (int)mn;
+                sm.red[2][wave] = (int)mx;
+            }
+            __syncthreads();
+            mn = wave_min_u(lane < kNW ? (uint32_t)sm.red[1][lane] : 0xFFFFFFFFu);
+            mx = wave_max_u(lane < kNW ? (uint32_t)sm.red[2][lane] : 0u);
+        }
+        rlo = mn;
+        rhi = mx;
+        above = 0;
     } else {
-        const bool guess = p.use_guess && p.prev && gvalid > 0;
-        path = guess ? GVR_PATH_GUESS : GVR_PATH_NO_GUESS;
-        Window win = guess ? make_window(gmin, gmax) : make_window(0u, 0xFFFFFFFFu);
-        int parity = 0;
+        if (spec) {
+            // The guess fell short (or a wave's list overflowed): count passes
+            // around T_spec, whose f is known, then collect or emit.
+            if (path == GVR_PATH_GUESS) path = GVR_PATH_NARROWED;
+            win = (f_spec < K) ? make_window(0u, tspec - 1u) : make_window(tspec, 0xFFFFFFFFu);
+            count_pass();
+        } else {
+            compute_F();   // pass 1 was the first count pass (whole key range)
+        }
         for (;;) {
-            // Thread coordinates made opaque per iteration so that the many
-            // thread-dependent addresses below are recomputed here rather than
-            // hoisted out of the loop (where they would stay live next to the
-            // register-resident keys).
-            int tid_o = (int)threadIdx.x;
-            asm volatile("" : "+v"(tid_o));
-            const int tid = tid_o, lane = tid_o & 63, wave = tid_o >> 6;
-            // ---- (a3) counting pass over the register-resident keys
-            int* hw = sm.u.c.hist[wave];
-            for (int b = lane; b < kBinsX; b += kWave) hw[b] = 0;
-            // (LDS ops of one wave execute in order; no barrier needed here)
-            const uint32_t lo = win.lo, sh = win.shift;
-#pragma unroll
-            for (int i = 0; i < R4; ++i) {
-#pragma unroll
-                for (int c = 0; c < 4; ++c) {
-                    const uint32_t kk = k[i][c];
-                    if (kk >= lo) {
-                        const uint32_t b = min((kk - lo) >> sh, (uint32_t)kBins);
-                        __hip_atomic_fetch_add(&hw[b], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-                    }
-                }
-            }
-            if (lo == 0 && lane == 0 && inv_wave)
-                __hip_atomic_fetch_add(&hw[0], -inv_wave, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-            ++passes;
-            __syncthreads();
-            // WG totals, published for the other WGs of the row.
-            int* mine = xch + ((size_t)parity * p.S + w) * kXchStride;
-            for (int b = tid; b < kBinsX; b += BLOCK) {
-                int t = 0;
-#pragma unroll
-                for (int v = 0; v < NW; ++v) t += sm.u.c.hist[v][b];
-                st_dev(&mine[b], t);
-            }
-            wait_mem();
-            __syncthreads();
-            if (tid == 0) row_barrier(ctl, (unsigned)s_row);
-            __syncthreads();
-            const int* all = xch + (size_t)parity * p.S * kXchStride;
-            for (int b = tid; b < kBinsX; b += BLOCK) {
-                int tot = 0, pr = 0;
-                for (int v = 0; v < s_row; ++v) {
-                    int t = ld_dev(&all[(size_t)v * kXchStride + b]);
-                    tot += t;
-                    if (v < w) pr += t;
-                }
-                sm.u.c.G[b] = tot;
-                sm.u.c.pre[b] = pr;
-            }
-            __syncthreads();
-            // F[j] = sum_{b >= j} G[b]; block scan over bins in reverse order.
-            {
-                // thread t owns bin (kBins - t) and thread 0 also bin 0 at the end
-                int b0 = kBins - tid;          // kBins .. kBins-BLOCK+1
-                int v0 = (b0 >= 0) ? sm.u.c.G[b0] : 0;
-                // bins below kBins-BLOCK+1 (if BLOCK < kBinsX) handled by a tail loop
-                int a = v0, dz = 0, tot = 0, tz = 0;
-                block_excl_scan2<NW>(a, dz, tot, tz, sm.wtot, tid);
-                if (b0 >= 0) sm.u.c.F[b0] = a + v0;
-                // remaining bins b < kBins - BLOCK + 1 (serial by thread 0; at most one)
-                if (tid == 0) {
-                    int run = tot;
-                    for (int b = kBins - BLOCK; b >= 0; --b) {
-                        run += sm.u.c.G[b];
-                        sm.u.c.F[b] = run;
-                    }
-                    sm.u.c.F[kBinsX] = 0;
-                    sm.scal[0] = -1;
-                }
-            }
-            __syncthreads();
-            for (int b = tid; b < kBinsX; b += BLOCK) {
-                if (sm.u.c.F[b] >= K && sm.u.c.F[b + 1] < K) sm.scal[0] = b;
-            }
-            __syncthreads();
-            const int j = sm.scal[0];
-            const bool last_pass = passes >= kMaxPasses;
-            int decision;   // 0 accept, 1 ties, 2 narrow
+            const int j = crossing();
+            int decision = 2;   // 0 collect, 1 ties, 2 narrow
             Window nw = win;
             if (j < 0) {
-                // f(lo) < K: the K-th key lies below the window.
-                nw = make_window(0u, win.lo - 1u);
-                decision = 2;
+                nw = make_window(0u, win.lo - 1u);   // K-th key below the window
+            } else if (sm.F[j] <= cap) {
+                decision = 0;
+            } else if (j == kBins) {
+                nw = make_window((uint32_t)edge_of(win, kBins), 0xFFFFFFFFu);
+            } else if (win.shift == 0) {
+                decision = 1;
             } else {
                 const uint64_t e = edge_of(win, j);
-                const int fj = sm.u.c.F[j];
-                if (fj <= cap) {
-                    decision = 0;
-                } else if (j == kBins) {
-                    nw = make_window((uint32_t)e, 0xFFFFFFFFu);
-                    decision = 2;
-                } else if (win.shift == 0) {
-                    decision = 1;
-                } else {
-                    uint64_t hi = e + ((uint64_t)1 << win.shift) - 1;
-                    nw = make_window((uint32_t)e, (uint32_t)min(hi, (uint64_t)0xFFFFFFFFu));
-                    decision = 2;
-                }
+                nw = make_window((uint32_t)e,
+                                 (uint32_t)std::min<uint64_t>(e + ((uint64_t)1 << win.shift) - 1, 0xFFFFFFFFu));
             }
-            if (decision == 2 && last_pass) decision = -1;
-            if (decision == 0 || decision == 1) {
+            if (decision == 2 && passes >= kMaxPasses) decision = -1;
+            if (decision == 0) {
+                // Collect pass at T = edge j with exact per-wave offsets.
                 const uint64_t e = edge_of(win, j);
                 T = (uint32_t)e;
-                FT = sm.u.c.F[j];
-                if (decision == 0) {
-                    // Candidate counts at T: row prefix and this wave's share.
-                    int s1 = 0;
-                    for (int b = j + tid; b < kBinsX; b += BLOCK) s1 += sm.u.c.pre[b];
-                    int s2 = 0;
-                    for (int b = j + lane; b < kBinsX; b += kWave) s2 += sm.u.c.hist[wave][b];
-                    pre_ge = block_sum<NW>(s1, sm, tid);
-                    wave_ge = wave_sum(s2);
-                    if (j < kBins) {
-                        rlo = T;
-                        rhi = (uint32_t)min(e + ((uint64_t)1 << win.shift) - 1, (uint64_t)0xFFFFFFFFu);
-                        above = sm.u.c.F[j + 1];
-                    } else {
-                        rlo = T;
-                        rhi = 0xFFFFFFFFu;
-                        above = 0;
-                    }
-                } else {
-                    ties = true;
-                    n_gt_row = sm.u.c.F[j + 1];
-                    gt_pre = 0;
-                    eq_pre = 0;
-                    int a1 = 0, a2 = 0;
-                    for (int b = j + 1 + tid; b < kBinsX; b += BLOCK) a1 += sm.u.c.pre[b];
-                    gt_pre = block_sum<NW>(a1, sm, tid);
-                    eq_pre = sm.u.c.pre[j];
-                    for (int b = j + 1 + lane; b < kBinsX; b += kWave) a2 += sm.u.c.hist[wave][b];
-                    gt_wave = wave_sum(a2);
-                    eq_wave = sm.u.c.hist[wave][j];
+                cands = sm.F[j];
+                rlo = T;
+                rhi = (j < kBins) ? (uint32_t)std::min<uint64_t>(e + ((uint64_t)1 << win.shift) - 1, 0xFFFFFFFFu)
+                                  : 0xFFFFFFFFu;
+                above = (j < kBins) ? sm.F[j + 1] : 0;
+                int mine = 0;
+                for (int b = j + lane; b < kBinsX; b += kWave) mine += sm.u.hist[wave][b];
+                mine = wave_sum(mine);
+                if (lane == 0) sm.wa[wave] = mine;
+                __syncthreads();
+                const int off = sum_over_waves_below(sm.wa, lane, wave);
+                __syncthreads();
+                if (lane == 0) {
+                    sm.seg_off[wave] = off;
+                    sm.seg_cnt[wave] = mine;
                 }
+                __syncthreads();
+                uint2* lc = sm.list + off;
+                int run = 0;
+                stream_wave(xa, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
+                    uint32_t k[4];
+                    block_keys(v, k);
+                    const int e0 = 4 * q - aoff;
+                    bool f[4];
+                    uint64_t m[4];
+                    const bool edge = (4 * qs - aoff < 0 || 4 * qs + 255 - aoff >= n);
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) {
+                        f[c] = k[c] >= T && (!edge || (e0 + c >= 0 && e0 + c < n));
+                        m[c] = __ballot(f[c]);
+                    }
+                    int pos = run + (int)lanes_below(m[3], lanes_below(m[2], lanes_below(m[1], lanes_below(m[0], 0))));
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) {
+                        if (f[c]) {
+                            if (pos < mine) lc[pos] = make_uint2(k[c], (uint32_t)(e0 + c));
+                            ++pos;
+                        }
+                    }
+                    run += __popcll(m[0]) + __popcll(m[1]) + __popcll(m[2]) + __popcll(m[3]);
+                });
+                ++passes;
+                done_lists = true;
                 break;
             }
-            if (decision < 0) {
-                if (tid == 0) st_dev(&ctl->err, 2u);
-                T = 0xFFFFFFFFu;
-                FT = 0;
+            if (decision == 1) {
+                // The K-th key T* is isolated and f(T*) > C: emit directly.
+                ties = true;
+                tstar = (uint32_t)edge_of(win, j);
+                n_gt_row = sm.F[j + 1];
+                const int take = K - n_gt_row;
+                int g_mine = 0;
+                const int e_mine = sm.u.hist[wave][j];
+                for (int b = j + 1 + lane; b < kBinsX; b += kWave) g_mine += sm.u.hist[wave][b];
+                g_mine = wave_sum(g_mine);
+                if (lane == 0) {
+                    sm.wa[wave] = g_mine;
+                    sm.wb[wave] = e_mine;
+                }
+                __syncthreads();
+                int gb = sum_over_waves_below(sm.wa, lane, wave);
+                int eb = sum_over_waves_below(sm.wb, lane, wave);
+                stream_wave(xa, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
+                    uint32_t k[4];
+                    block_keys(v, k);
+                    const int e0 = 4 * q - aoff;
+                    const bool edge = (4 * qs - aoff < 0 || 4 * qs + 255 - aoff >= n);
+                    bool fg[4], fe[4];
+                    uint64_t mg[4], me[4];
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) {
+                        const bool ok = !edge || (e0 + c >= 0 && e0 + c < n);
+                        fg[c] = ok && k[c] > tstar;
+                        fe[c] = ok && k[c] == tstar;
+                        mg[c] = __ballot(fg[c]);
+                        me[c] = __ballot(fe[c]);
+                    }
+                    int g = gb + (int)lanes_below(mg[3], lanes_below(mg[2], lanes_below(mg[1], lanes_below(mg[0], 0))));
+                    int ee = eb + (int)lanes_below(me[3], lanes_below(me[2], lanes_below(me[1], lanes_below(me[0], 0))));
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) {
+                        if (fg[c]) {
+                            const int o = g + min(ee, take);
+                            if (o >= 0 && o < K) out[o] = e0 + c;
+                            ++g;
+                        } else if (fe[c]) {
+                            const int o = g + ee;
+                            if (ee < take && o >= 0 && o < K) out[o] = e0 + c;
+                            ++ee;
+                        }
+                    }
+                    gb += __popcll(mg[0]) + __popcll(mg[1]) + __popcll(mg[2]) + __popcll(mg[3]);
+                    eb += __popcll(me[0]) + __popcll(me[1]) + __popcll(me[2]) + __popcll(me[3]);
+                });
+                ++passes;
                 break;
             }
-            if (path == GVR_PATH_GUESS) path = GVR_PATH_NARROWED;
+            if (decision < 0) break;   // unreachable for 32-bit keys; keeps the loop finite
             win = nw;
-            parity ^= 1;
-            __syncthreads();
+            count_pass();
         }
     }
-    const int64_t t2 = stamp();
+    t2 = stamp();
 
     if (ties) {
-        // ---- K-th key T isolated with f(T) > C: emit the selection directly.
-        const int take = K - n_gt_row;
-        // wave prefixes of (gt, eq) inside the WG
-        if (lane == 0) {
-            sm.wtot[0][wave] = gt_wave;
-            sm.wtot[1][wave] = eq_wave;
-        }
-        __syncthreads();
-        int gb = gt_pre + sum_over_waves_below<NW>(sm.wtot[0], lane, wave);
-        int eb = eq_pre + sum_over_waves_below<NW>(sm.wtot[1], lane, wave);
-#pragma unroll
-        for (int i = 0; i < R4; ++i) {
-            bool fg[4], fe[4];
-            uint64_t mg[4], me[4];
-#pragma unroll
-            for (int c = 0; c < 4; ++c) {
-                const int e = vb + i * 256 + lane * 4 + c - aoff;
-                const bool valid = (e >= 0 && e < n);
-                fg[c] = valid && k[i][c] > T;
-                fe[c] = valid && k[i][c] == T;
-                mg[c] = __ballot(fg[c]);
-                me[c] = __ballot(fe[c]);
-            }
-            uint32_t g_before = lanes_below(mg[3], lanes_below(mg[2], lanes_below(mg[1], lanes_below(mg[0], 0))));
-            uint32_t e_before = lanes_below(me[3], lanes_below(me[2], lanes_below(me[1], lanes_below(me[0], 0))));
-            int gpos = gb + (int)g_before, epos = eb + (int)e_before;
-#pragma unroll
-            for (int c = 0; c < 4; ++c) {
-                const int e = vb + i * 256 + lane * 4 + c - aoff;
-                if (fg[c]) {
-                    const int o = gpos + min(epos, take);
-                    if (o >= 0 && o < K) out[o] = e;
-                    ++gpos;
-                } else if (fe[c]) {
-                    const int o = gpos + epos;
-                    if (epos < take && o >= 0 && o < K) out[o] = e;
-                    ++epos;
-                }
-            }
-            gb += __popcll(mg[0]) + __popcll(mg[1]) + __popcll(mg[2]) + __popcll(mg[3]);
-            eb += __popcll(me[0]) + __popcll(me[1]) + __popcll(me[2]) + __popcll(me[3]);
-        }
-        if (w == 0 && st && tid == 0) {
+        if (st && tid == 0) {
             gvr_row_stats s = {};
             s.n = n;
             s.path = GVR_PATH_TIES;
             s.passes = passes;
             s.candidates = 0;
-            s.threshold = T;
-            s.kth_key = T;
+            s.threshold = tstar;
+            s.kth_key = tstar;
             s.n_gt = n_gt_row;
             s.guess_valid = gvalid;
+            s.spec_threshold = tspec;
+            s.spec_count = f_spec;
+            s.pmean = gvalid ? gsum / (float)gvalid : 0.f;
             s.t_start = t0;
             s.t_guess = t1;
             s.t_search = t2;
@@ -728,11 +805,9 @@ __global__ __launch_bounds__(BLOCK, MINW) void topk_rows_kernel(Params p) {
         }
         return;
     }
-    if (FT == 0) {
-        // Search gave up (cannot happen for valid keys; kept so every path ends).
-        if (w == 0)
-            for (int i = tid; i < K; i += BLOCK) out[i] = -1;
-        if (w == 0 && st && tid == 0) {
+    if (!done_lists) {
+        for (int i = tid; i < K; i += kBlock) out[i] = -1;
+        if (st && tid == 0) {
             gvr_row_stats s = {};
             s.n = n;
             s.path = -1;
@@ -741,68 +816,25 @@ __global__ __launch_bounds__(BLOCK, MINW) void topk_rows_kernel(Params p) {
         }
         return;
     }
-
-    // ---------------- (a4) collect: candidates key >= T at precomputed offsets
-    if (lane == 0) sm.wtot[0][wave] = wave_ge;
     __syncthreads();
-    int base = pre_ge + sum_over_waves_below<NW>(sm.wtot[0], lane, wave);
-#pragma unroll
-    for (int i = 0; i < R4; ++i) {
-        bool f[4];
-        uint64_t m[4];
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-            f[c] = (path == GVR_PATH_ALL) ? (vb + i * 256 + lane * 4 + c - aoff >= 0 &&
-                                             vb + i * 256 + lane * 4 + c - aoff < n)
-                                          : (k[i][c] >= T);
-            m[c] = __ballot(f[c]);
-        }
-        int pos = base + (int)lanes_below(m[3], lanes_below(m[2], lanes_below(m[1], lanes_below(m[0], 0))));
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-            if (f[c]) {
-                if (pos >= 0 && pos < cap) {
-                    st_dev(&ckey[pos], k[i][c]);
-                    st_dev(&cidx[pos], vb + i * 256 + lane * 4 + c - aoff);
-                }
-                ++pos;
-            }
-        }
-        base += __popcll(m[0]) + __popcll(m[1]) + __popcll(m[2]) + __popcll(m[3]);
-    }
-    // Publish, then one atomic per WG; the last WG of the row refines.
-    wait_mem();
-    __syncthreads();
-    if (tid == 0) {
-        const unsigned old = __hip_atomic_fetch_add(&ctl->ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        const bool last = (old == (unsigned)s_row - 1);
-        if (last) st_dev(&ctl->ticket, 0u);
-        sm.scal[2] = last ? 1 : 0;
-    }
-    __syncthreads();
-    if (!sm.scal[2]) return;
-    const int64_t t3 = stamp();
-
-    // ---------------- (a5) refine the <= C candidates in LDS
-    const int c = min(FT, cap);
-    for (int i = tid; i < c; i += BLOCK) {
-        sm.u.r.key[i] = ld_dev(&ckey[i]);
-        sm.u.r.idx[i] = ld_dev(&cidx[i]);
-    }
-    __syncthreads();
-    uint32_t kth = 0;
+    t3 = stamp();
+    // ---------------- (a5) refine the listed candidates and emit
+    const uint32_t kth = refine_kth(sm, rlo, rhi, above, K, tid);
     int ngt = 0;
-    refine_and_emit<BLOCK, NW>(sm, c, rlo, rhi, above, K, out, tid, &kth, &ngt);
+    emit_from_lists(sm, kth, K, out, tid, &ngt);
     if (st && tid == 0) {
         gvr_row_stats s = {};
         s.n = n;
         s.path = path;
         s.passes = passes;
-        s.candidates = c;
+        s.candidates = cands;
         s.threshold = T;
         s.kth_key = kth;
         s.n_gt = ngt;
         s.guess_valid = gvalid;
+        s.spec_threshold = tspec;
+        s.spec_count = f_spec;
+        s.pmean = gvalid ? gsum / (float)gvalid : 0.f;
         s.t_start = t0;
         s.t_guess = t1;
         s.t_search = t2;
@@ -814,179 +846,47 @@ __global__ __launch_bounds__(BLOCK, MINW) void topk_rows_kernel(Params p) {
 
 // ------------------------------------------------------------------ host side
 
-struct Variant {
-    const void* fn;
-    int block;
-    int r4;
-    int occupancy;   // WGs per CU (filled per device)
-};
-
-template <int BLOCK, int R4, int MINW>
-const void* fn_ptr() {
-    return reinterpret_cast<const void*>(&topk_rows_kernel<BLOCK, R4, MINW>);
-}
-
-struct DeviceState {
-    bool init = false;
-    int cus = 0;
-    int max_rows = 0;   // most rows one launch can hold (sizes the control area)
-    std::vector<Variant> variants;
-    void* ws = nullptr;
-    size_t ws_bytes = 0;
-};
-
-std::mutex g_mu;
-std::vector<DeviceState> g_dev;
-
-// Workspace layout: [control blocks: max_rows x RowCtl][exchange: rows x 2 x S
-// histograms][candidates: rows x C keys][candidates: rows x C indices]. The
-// control area has a fixed size per device, so the self-cleaning barrier and
-// ticket counters always sit on the same (zero) bytes whatever the shape of
-// the call; the other areas are written before they are read.
-size_t row_ws_bytes(int S) {
-    return (size_t)2 * S * kXchStride * sizeof(int) + (size_t)kCmax * 2 * sizeof(uint32_t);
-}
-
-struct Plan {
-    const Variant* v;
-    int S;
-    int rows_per_launch;
-};
-
-size_t ws_bytes_for(const DeviceState& ds, const Plan& pl) {
-    return (size_t)ds.max_rows * sizeof(RowCtl) + (size_t)pl.rows_per_launch * row_ws_bytes(pl.S);
-}
-
-gvr_status init_device(int dev, DeviceState& ds) {
-    if (ds.init) return GVR_OK;
-    hipDeviceProp_t prop;
-    if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return GVR_ERR_HIP;
-    ds.cus = prop.multiProcessorCount;
-    ds.variants = {
-        {fn_ptr<512, 2, 4>(), 512, 2, 0},   {fn_ptr<512, 4, 4>(), 512, 4, 0},
-        {fn_ptr<512, 8, 4>(), 512, 8, 0},   {fn_ptr<512, 16, 4>(), 512, 16, 0},
-        {fn_ptr<512, 32, 2>(), 512, 32, 0},
-    };
-    for (auto& v : ds.variants) {
-        int occ = 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, v.fn, v.block, 0) != hipSuccess) return GVR_ERR_HIP;
-        v.occupancy = occ;
-        ds.max_rows = std::max(ds.max_rows, occ * ds.cus);
-    }
-    ds.init = true;
-    return GVR_OK;
-}
-
-// Smallest register chunk whose grid fits on the chip at once, with at most
-// kMaxS workgroups per row; else the largest chunk over several launches.
-bool make_plan(const DeviceState& ds, int64_t B, int64_t ld, Plan& pl) {
-    constexpr int kMaxS = 16;
-    const Variant* best = nullptr;
-    for (const auto& v : ds.variants) {
-        if (v.occupancy < 1) continue;
-        const int64_t ch = (int64_t)v.block * v.r4 * 4;
-        const int64_t S = (ld + 3 + ch - 1) / ch;
-        const int64_t cap = (int64_t)v.occupancy * ds.cus;
-        if (S <= kMaxS && B * S <= cap) {
-            pl.v = &v;
-            pl.S = (int)S;
-            pl.rows_per_launch = (int)B;
-            return true;
-        }
-        best = &v;
-    }
-    if (!best) return false;
-    const int64_t ch = (int64_t)best->block * best->r4 * 4;
-    const int64_t S = (ld + 3 + ch - 1) / ch;
-    const int64_t cap = (int64_t)best->occupancy * ds.cus;
-    if (S > cap) return false;
-    pl.v = best;
-    pl.S = (int)S;
-    pl.rows_per_launch = (int)std::min<int64_t>(B, cap / S);
-    return true;
-}
-
 gvr_status validate(const float* scores, int64_t B, int64_t ld, int32_t K, const int32_t* out,
                     const gvr_options* opt, int* capacity, int* use_guess) {
     if (K < 1 || K > GVR_MAX_K) return GVR_ERR_UNSUPPORTED_K;
     if (B < 0 || ld < 0) return GVR_ERR_INVALID_ARG;
     if (B > 0 && (!scores || !out)) return GVR_ERR_INVALID_ARG;
     if (ld > (int64_t)0x7FFFFFF0) return GVR_ERR_TOO_LONG;
-    if (B > (int64_t)0x7FFFFFFF) return GVR_ERR_INVALID_ARG;
     int cap = GVR_MAX_CANDIDATES;
     if (opt) {
         if (opt->capacity != 0) {
             if (opt->capacity < K || opt->capacity > GVR_MAX_CANDIDATES) return GVR_ERR_INVALID_ARG;
             cap = opt->capacity;
         }
-        if (opt->flags & ~1) return GVR_ERR_INVALID_ARG;
+        if ((opt->flags & ~1) || opt->reserved0 || opt->reserved1) return GVR_ERR_INVALID_ARG;
         if (opt->flags & 1) *use_guess = 0;
-        if (opt->max_passes < 0) *use_guess = 0;
     }
     *capacity = cap;
     return GVR_OK;
 }
 
 gvr_status run(const float* scores, int64_t B, int64_t ld, const int32_t* row_len, const int32_t* prev,
-               int32_t K, int32_t* out, void* stream, void* ws, size_t ws_bytes, const gvr_options* opt,
-               gvr_row_stats* stats, int use_guess, bool own_ws) {
+               int32_t K, int32_t* out, void* stream, const gvr_options* opt, gvr_row_stats* stats,
+               int use_guess) {
     int cap = 0;
     gvr_status st = validate(scores, B, ld, K, out, opt, &cap, &use_guess);
     if (st != GVR_OK) return st;
     if (B == 0) return GVR_OK;
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess) return GVR_ERR_HIP;
-    std::unique_lock<std::mutex> lk(g_mu);
-    if ((int)g_dev.size() <= dev) g_dev.resize(dev + 1);
-    DeviceState& ds = g_dev[dev];
-    if ((st = init_device(dev, ds)) != GVR_OK) return st;
-    Plan pl;
-    if (!make_plan(ds, B, ld, pl)) return GVR_ERR_TOO_LONG;
-    const size_t need = ws_bytes_for(ds, pl);
-    if (own_ws) {
-        if (ds.ws_bytes < need) {
-            if (ds.ws) {
-                if (hipStreamSynchronize((hipStream_t)stream) != hipSuccess) return GVR_ERR_HIP;
-                (void)hipFree(ds.ws);
-                ds.ws = nullptr;
-                ds.ws_bytes = 0;
-            }
-            if (hipMalloc(&ds.ws, need) != hipSuccess) return GVR_ERR_WORKSPACE;
-            if (hipMemsetAsync(ds.ws, 0, need, (hipStream_t)stream) != hipSuccess) return GVR_ERR_HIP;
-            ds.ws_bytes = need;
-        }
-        ws = ds.ws;
-    } else {
-        if (!ws || ws_bytes < need) return GVR_ERR_WORKSPACE;
-        lk.unlock();
-    }
-    const int rpl = pl.rows_per_launch;
-    char* base = (char*)ws;
-    Params prm;
-    prm.scores = scores;
-    prm.ld = ld;
-    prm.row_len = row_len;
-    prm.prev = prev;
-    prm.out = out;
-    prm.stats = stats;
-    prm.ctl = (RowCtl*)base;
-    char* xbase = base + (size_t)ds.max_rows * sizeof(RowCtl);
-    prm.xch = (int*)xbase;
-    char* cbase = xbase + (size_t)rpl * (size_t)2 * pl.S * kXchStride * sizeof(int);
-    prm.cand_key = (uint32_t*)cbase;
-    prm.cand_idx = (int32_t*)(cbase + (size_t)rpl * kCmax * sizeof(uint32_t));
-    prm.K = K;
-    prm.S = pl.S;
-    prm.capacity = cap;
-    prm.use_guess = use_guess;
-    for (int64_t r0 = 0; r0 < B; r0 += rpl) {
-        const int rows = (int)std::min<int64_t>(rpl, B - r0);
-        prm.rows = rows;
-        prm.row0 = (int)r0;
-        void* args[] = {&prm};
-        hipError_t e = hipLaunchCooperativeKernel(pl.v->fn, dim3((unsigned)(rows * pl.S)), dim3(pl.v->block), args, 0,
-                                                  (hipStream_t)stream);
-        if (e != hipSuccess) return GVR_ERR_HIP;
+    // One workgroup per row; the grid is split only past 2^31 - 1 rows.
+    for (int64_t r0 = 0; r0 < B; r0 += 0x7FFFFFFF) {
+        const int64_t rows = std::min<int64_t>(B - r0, 0x7FFFFFFF);
+        Params q;
+        q.scores = scores + r0 * ld;
+        q.ld = ld;
+        q.row_len = row_len ? row_len + r0 : nullptr;
+        q.prev = prev ? prev + r0 * K : nullptr;
+        q.out = out + r0 * K;
+        q.stats = stats ? stats + r0 : nullptr;
+        q.K = K;
+        q.capacity = cap;
+        q.use_guess = use_guess;
+        hipLaunchKernelGGL(topk_row_kernel, dim3((unsigned)rows), dim3(kBlock), 0, (hipStream_t)stream, q);
+        if (hipGetLastError() != hipSuccess) return GVR_ERR_HIP;
     }
     return GVR_OK;
 }
@@ -997,40 +897,24 @@ extern "C" {
 
 gvr_status gvr_topk(const float* scores, int64_t B, int64_t ld, const int32_t* row_len, const int32_t* prev_topk,
                     int32_t K, int32_t* out_idx, void* stream) {
-    return run(scores, B, ld, row_len, prev_topk, K, out_idx, stream, nullptr, 0, nullptr, nullptr, 1, true);
+    return run(scores, B, ld, row_len, prev_topk, K, out_idx, stream, nullptr, nullptr, 1);
 }
 
 gvr_status radix_topk(const float* scores, int64_t B, int64_t ld, const int32_t* row_len, const int32_t* prev_topk,
                       int32_t K, int32_t* out_idx, void* stream) {
     (void)prev_topk;
-    return run(scores, B, ld, row_len, nullptr, K, out_idx, stream, nullptr, 0, nullptr, nullptr, 0, true);
-}
-
-size_t gvr_workspace_size(int64_t B, int64_t ld, int32_t K) {
-    if (K < 1 || K > GVR_MAX_K || B < 0 || ld < 0 || ld > (int64_t)0x7FFFFFF0) return 0;
-    if (B == 0) return 0;
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess) return 0;
-    std::lock_guard<std::mutex> lk(g_mu);
-    if ((int)g_dev.size() <= dev) g_dev.resize(dev + 1);
-    DeviceState& ds = g_dev[dev];
-    if (init_device(dev, ds) != GVR_OK) return 0;
-    Plan pl;
-    if (!make_plan(ds, B, ld, pl)) return 0;
-    return ws_bytes_for(ds, pl);
+    return run(scores, B, ld, row_len, nullptr, K, out_idx, stream, nullptr, nullptr, 0);
 }
 
 gvr_status gvr_topk_ex(const float* scores, int64_t B, int64_t ld, const int32_t* row_len, const int32_t* prev_topk,
-                       int32_t K, int32_t* out_idx, void* stream, void* workspace, size_t ws_bytes,
-                       const gvr_options* options, gvr_row_stats* stats) {
-    return run(scores, B, ld, row_len, prev_topk, K, out_idx, stream, workspace, ws_bytes, options, stats, 1,
-               false);
+                       int32_t K, int32_t* out_idx, void* stream, const gvr_options* options,
+                       gvr_row_stats* stats) {
+    return run(scores, B, ld, row_len, prev_topk, K, out_idx, stream, options, stats, 1);
 }
 
 gvr_status radix_topk_ex(const float* scores, int64_t B, int64_t ld, const int32_t* row_len, int32_t K,
-                         int32_t* out_idx, void* stream, void* workspace, size_t ws_bytes,
-                         const gvr_options* options, gvr_row_stats* stats) {
-    return run(scores, B, ld, row_len, nullptr, K, out_idx, stream, workspace, ws_bytes, options, stats, 0, false);
+                         int32_t* out_idx, void* stream, const gvr_options* options, gvr_row_stats* stats) {
+    return run(scores, B, ld, row_len, nullptr, K, out_idx, stream, options, stats, 0);
 }
 
 const char* gvr_status_string(gvr_status s) {
@@ -1038,13 +922,12 @@ const char* gvr_status_string(gvr_status s) {
         case GVR_OK: return "ok";
         case GVR_ERR_INVALID_ARG: return "invalid argument";
         case GVR_ERR_UNSUPPORTED_K: return "unsupported K (1 <= K <= 2048)";
-        case GVR_ERR_WORKSPACE: return "workspace missing, too small or not allocatable";
         case GVR_ERR_HIP: return "HIP runtime error";
-        case GVR_ERR_TOO_LONG: return "row stride too long for one launch";
+        case GVR_ERR_TOO_LONG: return "row stride too long";
     }
     return "unknown status";
 }
 
-const char* gvr_version(void) { return "gvr_topk 0.1 (gfx950)"; }
+const char* gvr_version(void) { return "gvr_topk 0.2 (gfx950, one workgroup per row)"; }
 
 }  // extern "C"

@@ -63,7 +63,7 @@ def run_decode(fn, cfg, nsteps, queries, sub=None, dev="cuda", stats_check=False
             pd = None if prev is None else torch.from_numpy(prev).to(dev)
         note("%s cfg=%s sub=%s step=%d rows=%d ld=%d" % (fn.__name__, cfg, sub, t, w.rows, w.ld))
         if stats_check:
-            st = torch.zeros((w.rows, 18), dtype=torch.int32, device=dev)
+            st = gvr.new_stats(w.rows, dev)
             out = fn(S[i], RL[i], pd, K, stats=st)
         else:
             out = fn(S[i], RL[i], pd, K)

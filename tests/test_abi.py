@@ -31,7 +31,7 @@ def L():
 
 def test_header_declares_the_boundary():
     names = declared_functions()
-    for n in ("gvr_topk", "radix_topk", "gvr_topk_ex", "radix_topk_ex", "gvr_workspace_size",
+    for n in ("gvr_topk", "radix_topk", "gvr_topk_ex", "radix_topk_ex",
               "gvr_status_string", "gvr_version"):
         assert n in names, n
 
@@ -43,7 +43,7 @@ def test_every_declared_symbol_is_exported(L):
 
 def test_status_strings(L):
     import paper_2604_22312_amd as g
-    for code in (0, -1, -2, -3, -4, -5):
+    for code in (0, -1, -2, -4, -5):
         assert g.status_string(code) and "unknown" not in g.status_string(code)
     assert "unknown" in g.status_string(-99)
     assert "gfx950" in g.version()
@@ -75,21 +75,13 @@ def test_host_side_validation(L):
 def test_options_validation(L):
     import paper_2604_22312_amd as g
     vp = ctypes.c_void_p
-    opt = g.Options(capacity=100, max_passes=0, flags=0, reserved=0)   # capacity < K
-    st = L.gvr_topk_ex(vp(1), 2, 100, None, None, 128, vp(1), None, vp(1), 1 << 20, ctypes.byref(opt), None)
-    assert st == -1
-    opt = g.Options(capacity=0, max_passes=0, flags=4, reserved=0)     # unknown flag bit
-    st = L.gvr_topk_ex(vp(1), 2, 100, None, None, 128, vp(1), None, vp(1), 1 << 20, ctypes.byref(opt), None)
-    assert st == -1
-    opt = g.Options(capacity=7000, max_passes=0, flags=0, reserved=0)  # capacity > max
-    st = L.radix_topk_ex(vp(1), 2, 100, None, 128, vp(1), None, vp(1), 1 << 20, ctypes.byref(opt), None)
-    assert st == -1
-
-
-def test_workspace_size_rejects_bad_shapes(L):
-    assert L.gvr_workspace_size(4, 100, 0) == 0
-    assert L.gvr_workspace_size(-1, 100, 16) == 0
-    assert L.gvr_workspace_size(0, 100, 16) == 0
+    bad = [g.Options(capacity=100, flags=0, reserved0=0, reserved1=0),      # capacity < K
+           g.Options(capacity=0, flags=4, reserved0=0, reserved1=0),        # unknown flag bit
+           g.Options(capacity=0, flags=0, reserved0=1, reserved1=0),        # reserved field set
+           g.Options(capacity=20000, flags=0, reserved0=0, reserved1=0)]    # capacity > max
+    for opt in bad:
+        assert L.gvr_topk_ex(vp(1), 2, 100, None, None, 128, vp(1), None, ctypes.byref(opt), None) == -1
+        assert L.radix_topk_ex(vp(1), 2, 100, None, 128, vp(1), None, ctypes.byref(opt), None) == -1
 
 
 def test_python_binding_refuses_cpu_tensors():
