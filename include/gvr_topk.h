@@ -40,11 +40,22 @@
  * Errors and synchronisation:
  *   - Argument problems detectable on the host are reported synchronously,
  *     before any work is enqueued. B == 0 is a no-op returning GVR_OK.
- *   - On GVR_OK the work is enqueued on `stream` as one kernel launch (one
- *     workgroup per row); out_idx is complete when the stream reaches that
- *     point. The call does not synchronise, allocates nothing and keeps no
- *     state between calls, so calls on different streams may overlap and a
- *     call may be captured into a HIP graph.
+ *   - On GVR_OK the work is enqueued on `stream` as one kernel launch;
+ *     out_idx is complete when the stream reaches that point. The call does
+ *     not synchronise.
+ *
+ * Workspace:
+ *   - gvr_topk may split a long row over several workgroups (few rows, long
+ *     rows: see gvr_options.parts). The parts exchange their candidate lists
+ *     through a device workspace that the library allocates on the first
+ *     such call for each (device, stream) pair (hipMalloc, kept until the
+ *     process ends; arrival counters + 128 KB per row part) and reuses for
+ *     every later call on that stream. Calls on one stream run in order and
+ *     share it; calls on different streams use different workspaces and may
+ *     overlap. A call that has to allocate or grow the workspace synchronises
+ *     the stream and must not be captured into a HIP graph: issue one call of
+ *     the same shape before capturing. radix_topk and unsplit gvr_topk calls
+ *     use no workspace.
  */
 #ifndef GVR_TOPK_H
 #define GVR_TOPK_H
@@ -88,7 +99,9 @@ typedef struct gvr_options {
                               (default GVR_MAX_CANDIDATES); a smaller C forces
                               more narrowing passes, never another result */
     int32_t flags;         /* bit 0: ignore prev_topk (run the radix schedule) */
-    int32_t reserved0;     /* must be 0 */
+    int32_t parts;         /* workgroups per row, 1..16 (0 = chosen from B, ld
+                              and the device's compute units); never changes
+                              the result */
     int32_t reserved1;     /* must be 0 */
 } gvr_options;
 

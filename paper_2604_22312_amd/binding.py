@@ -24,9 +24,10 @@ class GvrError(RuntimeError):
 
 
 class Options(ctypes.Structure):
-    """Mirror of ``gvr_options``: capacity C, flags (bit 0: ignore the guess)."""
+    """Mirror of ``gvr_options``: capacity C, flags (bit 0: ignore the guess),
+    parts (workgroups per row, 0 = automatic)."""
     _fields_ = [("capacity", ctypes.c_int32), ("flags", ctypes.c_int32),
-                ("reserved0", ctypes.c_int32), ("reserved1", ctypes.c_int32)]
+                ("parts", ctypes.c_int32), ("reserved1", ctypes.c_int32)]
 
 
 def library_path() -> str:

@@ -1,49 +1,54 @@
 // gvr_topk.hip -- Guess-Verify-Refine exact Top-K and radix-select Top-K for
 // MI355X (gfx950), behind the C ABI declared in include/gvr_topk.h.
 //
-// One workgroup (1024 threads, 16 wave64s) owns one row; rows never talk to
-// each other, so a call is a single ordinary launch with one workgroup per
-// row and no device workspace. Each wave streams a contiguous sub-range of
-// the row with a rolling window of dwordx4 loads (8 slabs of 1 KB in flight
-// per wave), so the candidates it keeps are in ascending index order.
+// Workgroups of 1024 threads (16 wave64s). A row is handled by one
+// workgroup, or split over S of them ("parts", up to 16) when few long rows
+// would leave compute units idle and the streaming time saved outweighs the
+// merge; the parts of one row are placed on one XCD so they share its L2.
 //
-//   Guess (Sec. 4.2.1, Phase 1). While the first slabs of the row are in
-//   flight, the workgroup gathers the row's scores at prev_topk and reduces
-//   them to pmin / pmax (and pmean, reported in the stats). A small LDS
-//   histogram of the gathered keys gives T_spec, the 65th-smallest gathered
-//   key: a threshold that the previous step's Top-K makes likely to hold a
-//   few thousand elements of the current row, i.e. inside [K, C].
+//   Guess (Sec. 4.2.1, Phase 1). Wave 0 of every part gathers the scores at a
+//   strided sample of prev_topk (every 8th entry for K = 2048, 256 in all)
+//   and reduces them to pmin / pmax / pmean and T_spec, the lower edge of the
+//   histogram bin (over [pmin, pmax]) holding the sampled key of rank
+//   ceil(65 / 2048 * samples): a threshold the previous step's Top-K makes
+//   likely to leave a few thousand elements of the current row above it, so
+//   that K <= f(T_spec) <= C. Waves 1..15 have their first slabs (1 KB per
+//   wave: 64 lanes x one 16-byte load) in flight meanwhile and wait on an LDS
+//   flag, not a barrier, so a stalled load issue never delays T_spec.
 //
-//   Threshold search (Sec. 4.2.2, Phase 2). The first full-row pass counts
-//   f(T) = #{key >= T} (Sec. 4.1) at every edge of a 256-bin window over
-//   [pmin, pmax] of key space (wave-private LDS histograms: the count cache),
-//   and so evaluates 257 thresholds in one sweep instead of one.
+//   Verify / collect (Sec. 4.2.2-4.2.3, Phases 2-3). One pass over the
+//   part's slabs counts f(T_spec) and appends every element at or above it
+//   to per-wave LDS lists (ballot + mbcnt ranks, no atomics; each wave
+//   streams a contiguous range, so its list is in index order). The test
+//   runs on raw fp32 bits (one compare, see spec_keep). With S > 1 each part
+//   publishes its list and count to a workspace and the last part of the row
+//   to arrive (one agent-scope atomic per part) merges them. If
+//   K <= f(T_spec) <= C, Lemma 1 (Sec. 4.1) says the list holds the exact
+//   answer: the row was read once.
 //
-//   Collect (Sec. 4.2.3, Phase 3). In the same sweep every element with
-//   key >= T_spec is appended to its wave's LDS list (ballot + mbcnt ranks,
-//   no atomics). If K <= f(T_spec) <= C, Lemma 1 (Sec. 4.1) says the lists
-//   hold the exact answer and the row is never read again.
+//   Refine (Sec. 4.2.4, Phase 4). One LDS histogram level over the listed
+//   keys, a two-scan bin search by one wave, then that wave ranks the few
+//   keys of the K-th key's bin to get T* and the per-wave emission offsets;
+//   every key > T* and the first K - #{key > T*} keys equal to T* (lower
+//   index first) are written out in ascending index order.
 //
-//   Refine (Sec. 4.2.4, Phase 4). The window histogram names the bin that
-//   holds the K-th key; a 2048-bin LDS histogram over the listed keys in that
-//   bin narrows it to the exact K-th key T* (two levels for a ~3-binade
-//   window). Every key > T* and the first K - #{key > T*} keys equal to T*
-//   (lower index first) are written out in ascending index order.
-//
-//   When the guess does not deliver (no valid prev_topk, f(T_spec) < K, or a
-//   wave's list overflows) the row is streamed again: count passes narrow a
-//   256-bin window around the K-th key (8 bits of key per pass), then one
-//   collect pass gathers the <= C candidates at the accepted threshold with
-//   exact per-wave offsets from the count cache, or, when ties straddle
+//   When the guess does not deliver (no valid prev_topk, f(T_spec) outside
+//   [K, C], or a wave's list overflows) the last part reads the whole row
+//   again: count passes narrow a 256-bin window of key space around the K-th
+//   key (each pass evaluates f at 257 thresholds: the count cache of Phase 2
+//   generalised), then one collect pass gathers the <= C candidates at the
+//   accepted threshold with exact per-wave offsets, or, when ties straddle
 //   [K, C], an emit pass writes the selection directly. radix_topk runs only
-//   this path, starting from the whole key range: a distribution-agnostic
-//   radix select (Sec. 2.2).
+//   this schedule (one workgroup per row), starting from the whole key
+//   range: a distribution-agnostic radix select (Sec. 2.2).
 
 #include <hip/hip_runtime.h>
 
 #include <stdint.h>
 
 #include <algorithm>
+#include <mutex>
+#include <vector>
 
 #include "gvr_topk.h"
 
@@ -54,16 +59,22 @@ namespace {
 constexpr int kBlock = 1024;
 constexpr int kWave = 64;
 constexpr int kNW = kBlock / kWave;            // 16 waves
-constexpr int kU = 8;                          // slabs in flight per wave
+constexpr int kU = 8;                          // slabs in flight per wave (count / collect passes)
+constexpr int kSU = 8;                         // slabs in flight per wave (speculative pass)
+constexpr int kSW = kNW - 1;                   // streaming waves of the speculative pass (wave 0: guess)
 constexpr int kBins = 256;                     // bins of a counting window
 constexpr int kBinsX = kBins + 1;              // + "at or above the window"
 constexpr int kCap = GVR_MAX_CANDIDATES;       // list capacity (LDS)
-constexpr int kCapW = kCap / kNW;              // per-wave list capacity, first pass
+constexpr int kCapW = kCap / kNW;              // per-wave list capacity, speculative pass
 constexpr int kRefBins = 4096;                 // bins of a refine level (12 bits of key)
-constexpr int kGuessBins = kBlock;             // bins of the gathered-key histogram (1 per thread)
-constexpr int kGuessPerThread = (GVR_MAX_K + kBlock - 1) / kBlock;
-constexpr int kSpecRank = 64;                  // T_spec = gathered key of this rank from the bottom
+constexpr int kGuessSamples = 256;             // guessed indices gathered: a strided sample of prev_topk
+constexpr int kGuessBins = 1024;               // bins of the gathered-key histogram (16 per lane of wave 0)
+constexpr int kSpecQuantile = 65;              // T_spec: gathered key of rank ceil(65 / 2048 * sample size)
+constexpr int kSmall = 64;                     // refine: K-th key's bin resolved by one wave up to this size
 constexpr int kMaxPasses = 8;                  // 2 + at most 4 narrowing passes + 1 final pass suffice
+constexpr int kMaxParts = 16;                  // workgroups per row
+constexpr int kMinPartElems = 16384;           // a row is split only into parts at least this long
+constexpr int kXcds = 8;                       // gfx950 XCDs; workgroup i runs on XCD i % 8
 
 static_assert(GVR_MAX_CANDIDATES % kNW == 0, "per-wave capacity");
 
@@ -76,7 +87,12 @@ struct Params {
     gvr_row_stats* stats;
     int32_t K;
     int32_t capacity;    // C
-    int32_t use_guess;   // 0: radix schedule
+    int32_t rows;        // rows of this launch
+    int32_t parts;       // S: workgroups per row
+    int32_t chunk;       // gridDim.x / 8: consecutive (row, part) slots per XCD
+    uint32_t* arrivals;  // [rows] parts that finished the speculative pass (S > 1); 0 between calls
+    int32_t* part_count; // [rows][S] f(T_spec) of each part, bit 31 = a wave list overflowed
+    uint64_t* part_list; // [rows][S][kCap] (fp32 bits | index << 32) of each part
 };
 
 // ------------------------------------------------------------------ helpers
@@ -158,6 +174,15 @@ DEV int sum_over_waves_below(const int* vals, int lane, int wave) { return wave_
 
 DEV int64_t stamp() { return (int64_t)__builtin_amdgcn_s_memtime(); }
 
+// Workgroup barrier that orders LDS accesses only: unlike __syncthreads()
+// it does not wait for the wave's outstanding global loads, so prefetched
+// slabs stay in flight across it.
+DEV void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 // A window of key space: bins j < kBins cover [lo + j<<shift, lo + (j+1)<<shift);
 // bin kBins holds every key >= lo + kBins<<shift; keys below lo are not counted.
 struct Window {
@@ -175,7 +200,7 @@ DEV uint64_t edge_of(const Window& w, int j) { return (uint64_t)w.lo + ((uint64_
 // ------------------------------------------------------------------ LDS
 struct Smem {
     uint2 list[kCap];                   // candidates (key, index), per-wave segments
-    union {
+    union alignas(16) {
         int hist[kNW][kBinsX];          // wave-private counting histograms
         int rhist[kRefBins];            // refine / guess histogram
     } u;
@@ -188,6 +213,8 @@ struct Smem {
     int red[4][kNW];
     float redf[kNW];
     int scal[8];
+    uint4 small[kSmall];                // refine: (key, index, wave) of the K-th key's bin
+    int guess_ready;                    // set by wave 0 once T_spec is in scal[4..7]
 };
 
 // Block-wide exclusive scan of one int (all kBlock threads). Returns the total.
@@ -326,29 +353,12 @@ DEV uint32_t refine_kth(Smem& sm, uint32_t wlo, uint32_t whi, int above, int K, 
     return wlo;
 }
 
-// Write the selection from the lists: every key > T, then the first `take`
-// keys == T in list (= index) order; output in ascending index order.
-DEV void emit_from_lists(Smem& sm, uint32_t T, int K, int32_t* out, int tid, int* n_gt_out) {
-    const int lane = tid & 63, wave = tid >> 6;
+// Emission: this wave's list segment holds `gb` keys > T and `eb` keys == T
+// in the segments before it; write every key > T and the first `take` keys
+// == T (list order = index order) at their ranks: ascending index output.
+DEV void emit_segment(const Smem& sm, uint32_t T, int K, int take, int gb, int eb, int32_t* out, int lane, int wave) {
     const uint2* seg = sm.list + sm.seg_off[wave];
     const int cnt = sm.seg_cnt[wave];
-    int gt = 0, eq = 0;
-    for (int i = lane; i < cnt; i += kWave) {
-        const uint32_t kk = seg[i].x;
-        gt += kk > T;
-        eq += kk == T;
-    }
-    gt = wave_sum(gt);
-    eq = wave_sum(eq);
-    if (lane == 0) {
-        sm.wa[wave] = gt;
-        sm.wb[wave] = eq;
-    }
-    __syncthreads();
-    int gb = sum_over_waves_below(sm.wa, lane, wave);
-    int eb = sum_over_waves_below(sm.wb, lane, wave);
-    const int gtot = sum_over_waves(sm.wa, lane);
-    const int take = K - gtot;
     for (int i0 = 0; i0 < cnt; i0 += kWave) {
         const int i = i0 + lane;
         uint32_t kk = 0;
@@ -371,26 +381,242 @@ DEV void emit_from_lists(Smem& sm, uint32_t T, int K, int32_t* out, int tid, int
         gb += __popcll(mg);
         eb += __popcll(me);
     }
+}
+
+// Write the selection from the lists: every key > T, then the first `take`
+// keys == T in list (= index) order; output in ascending index order.
+DEV void emit_from_lists(Smem& sm, uint32_t T, int K, int32_t* out, int tid, int* n_gt_out) {
+    const int lane = tid & 63, wave = tid >> 6;
+    const uint2* seg = sm.list + sm.seg_off[wave];
+    const int cnt = sm.seg_cnt[wave];
+    int gt = 0, eq = 0;
+    for (int i = lane; i < cnt; i += kWave) {
+        const uint32_t kk = seg[i].x;
+        gt += kk > T;
+        eq += kk == T;
+    }
+    gt = wave_sum(gt);
+    eq = wave_sum(eq);
+    if (lane == 0) {
+        sm.wa[wave] = gt;
+        sm.wb[wave] = eq;
+    }
+    __syncthreads();
+    const int gb = sum_over_waves_below(sm.wa, lane, wave);
+    const int eb = sum_over_waves_below(sm.wb, lane, wave);
+    const int gtot = sum_over_waves(sm.wa, lane);
+    emit_segment(sm, T, K, K - gtot, gb, eb, out, lane, wave);
     *n_gt_out = gtot;
 }
 
+// Exact K-th key T* among the listed candidates and the emission. The K-th
+// key lies in [rlo, rhi]; `above` listed keys lie above rhi. One histogram
+// level of kRefBins bins over [rlo, bin_hi] (keys in (bin_hi, rhi] count in
+// the top bin) by all waves, then wave 0 finds the
+// bin b holding the K-th key with two wave scans. If b holds at most kSmall
+// candidates, the waves copy them (with their wave) to LDS and count the
+// keys above b; wave 0 ranks them to get T* and the per-wave emission
+// offsets, and every wave emits its segment. Otherwise histogram narrowing
+// (refine_kth) continues inside b.
+DEV uint32_t refine_emit(Smem& sm, uint32_t rlo, uint32_t rhi, uint32_t bin_hi, int above, int K, int32_t* out,
+                         int tid, int* n_gt_out, bool convert) {
+    const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    uint2* seg = sm.list + sm.seg_off[wave];
+    const int cnt = sm.seg_cnt[wave];
+    const uint64_t width = (uint64_t)bin_hi - rlo + 1;
+    uint32_t sh = 0;
+    while (((uint64_t)kRefBins << sh) < width) ++sh;
+    int* hb = sm.u.rhist;
+    for (int i = tid; i < kRefBins; i += kBlock) hb[i] = 0;
+    if (tid == 0) sm.scal[1] = 0;
+    __syncthreads();
+    for (int i = lane; i < cnt; i += kWave) {
+        uint32_t kk = seg[i].x;
+        if (convert) {   // lists of the speculative pass hold fp32 bit patterns
+            kk = key_of_bits(kk);
+            seg[i].x = kk;
+        }
+        if (kk >= rlo && kk <= rhi)
+            __hip_atomic_fetch_add(&hb[min((kk - rlo) >> sh, (uint32_t)kRefBins - 1)], 1, __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_WORKGROUP);
+    }
+    __syncthreads();
+    const int need0 = K - above;   // >= 1: rank of T* among the keys in [rlo, rhi], from the top
+    if (wave == 0) {
+        // lane l owns bins [64 l, 64 l + 64)
+        const int4* h4 = reinterpret_cast<const int4*>(hb) + lane * 16;
+        int s = 0;
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+            const int4 v = h4[j];
+            s += v.x + v.y + v.z + v.w;
+        }
+        const int incl = wave_incl_scan(s, lane);
+        const int total = __builtin_amdgcn_readlane(incl, 63);
+        const int abv = total - incl;   // keys in the bins of higher lanes
+        const uint64_t hit = __ballot(abv < need0 && abv + s >= need0);
+        const int L = hit ? (int)__builtin_ctzll(hit) : 0;
+        const int abv_l = __builtin_amdgcn_readlane(abv, L);
+        const int hj = hb[L * 64 + lane];
+        const int ij = wave_incl_scan(hj, lane);
+        const int s_l = __builtin_amdgcn_readlane(ij, 63);
+        const int abj = abv_l + s_l - ij;
+        const uint64_t hit2 = __ballot(abj < need0 && abj + hj >= need0);
+        const int J = hit2 ? (int)__builtin_ctzll(hit2) : 0;
+        if (lane == 0) {
+            sm.scal[0] = L * 64 + J;
+            sm.scal[2] = above + __builtin_amdgcn_readlane(abj, J);
+            sm.scal[3] = __builtin_amdgcn_readlane(hj, J);
+        }
+    }
+    __syncthreads();
+    const int b = sm.scal[0];
+    const int above_b = sm.scal[2];   // listed keys above bin b
+    const int cnt_b = sm.scal[3];
+    const uint64_t lo64 = (uint64_t)rlo + ((uint64_t)b << sh);
+    const uint32_t lo_b = (uint32_t)lo64;
+    const uint32_t hi_b =
+        b == kRefBins - 1 ? rhi : (uint32_t)std::min<uint64_t>(lo64 + ((uint64_t)1 << sh) - 1, rhi);
+    if (lo_b == hi_b) {   // the bin is one key: T* = lo_b
+        emit_from_lists(sm, lo_b, K, out, tid, n_gt_out);
+        return lo_b;
+    }
+    if (cnt_b > kSmall) {
+        __syncthreads();
+        const uint32_t kth = refine_kth(sm, lo_b, hi_b, above_b, K, tid);
+        emit_from_lists(sm, kth, K, out, tid, n_gt_out);
+        return kth;
+    }
+    // Copy bin b's candidates; count this segment's keys above the bin.
+    int gt_hi = 0;
+    for (int i0 = 0; i0 < cnt; i0 += kWave) {
+        const int i = i0 + lane;
+        const bool valid = i < cnt;
+        const uint2 e = valid ? seg[i] : make_uint2(0u, 0u);
+        gt_hi += valid && e.x > hi_b;
+        const bool inb = valid && e.x >= lo_b && e.x <= hi_b;
+        const uint64_t m = __ballot(inb);
+        if (m) {
+            const int first = (int)__builtin_ctzll(m);
+            int base = 0;
+            if (lane == first)
+                base = __hip_atomic_fetch_add(&sm.scal[1], (int)__popcll(m), __ATOMIC_RELAXED,
+                                              __HIP_MEMORY_SCOPE_WORKGROUP);
+            base = __builtin_amdgcn_readlane(base, first);
+            const int pos = base + (int)lanes_below(m, 0);
+            if (inb && pos < kSmall) sm.small[pos] = make_uint4(e.x, e.y, (uint32_t)wave, 0u);
+        }
+    }
+    gt_hi = wave_sum(gt_hi);
+    if (lane == 0) sm.wa[wave] = gt_hi;
+    __syncthreads();
+    if (wave == 0) {
+        const int need = K - above_b;   // rank of T* inside the bin, from the top
+        const uint4 mine = lane < cnt_b ? sm.small[lane] : make_uint4(0u, 0u, 0xFFFFFFFFu, 0u);
+        int gt = 0, ge = 0;
+        for (int t = 0; t < cnt_b; ++t) {
+            const uint32_t kt = (uint32_t)__builtin_amdgcn_readlane((int)mine.x, t);
+            gt += kt > mine.x;
+            ge += kt >= mine.x;
+        }
+        const uint64_t hit = __ballot(lane < cnt_b && gt < need && ge >= need);
+        const uint32_t kth = (uint32_t)__builtin_amdgcn_readlane((int)mine.x, hit ? (int)__builtin_ctzll(hit) : 0);
+        // Per-wave keys > T* and == T* (lane w < kNW counts for wave w).
+        int gw = 0, ew = 0;
+        for (int t = 0; t < cnt_b; ++t) {
+            const uint32_t kt = (uint32_t)__builtin_amdgcn_readlane((int)mine.x, t);
+            const int wt = __builtin_amdgcn_readlane((int)mine.z, t);
+            gw += (wt == lane) && kt > kth;
+            ew += (wt == lane) && kt == kth;
+        }
+        gw = lane < kNW ? gw + sm.wa[lane] : 0;
+        ew = lane < kNW ? ew : 0;
+        const int gi = wave_incl_scan(gw, lane), ei = wave_incl_scan(ew, lane);
+        const int gtot = __builtin_amdgcn_readlane(gi, 63);
+        if (lane < kNW) {
+            sm.red[0][lane] = gi - gw;
+            sm.red[1][lane] = ei - ew;
+        }
+        if (lane == 0) {
+            sm.scal[0] = (int)kth;
+            sm.scal[2] = gtot;
+        }
+    }
+    __syncthreads();
+    const uint32_t kth = (uint32_t)sm.scal[0];
+    const int gtot = sm.scal[2];
+    emit_segment(sm, kth, K, K - gtot, sm.red[0][wave], sm.red[1][wave], out, lane, wave);
+    *n_gt_out = gtot;
+    return kth;
+}
+
 // ------------------------------------------------------------------ kernel
-__global__ __launch_bounds__(kBlock) void topk_row_kernel(Params p) {
+
+// Threshold test of the speculative pass on raw fp32 bits u: key(u) >= tkey.
+// For tkey in the upper half (T >= +0) that is the signed compare
+// (int)u >= (int)(tkey ^ 0x80000000) (negative patterns are negative ints);
+// for tkey in the lower half (T <= -0) it is u <= ~tkey as unsigned (every
+// non-negative pattern passes; a negative one passes iff ~u >= tkey), which
+// is (int)(u ^ 0x7FFFFFFF) >= (int)(tkey ^ 0x80000000). Both cases: one xor
+// with a wave-uniform mask and one signed compare, no key transform.
+struct SpecTest {
+    uint32_t flip;   // 0 or 0x7FFFFFFF
+    int32_t bound;   // tkey ^ 0x80000000
+};
+DEV SpecTest make_spec_test(uint32_t tkey) {
+    return SpecTest{tkey >= 0x80000000u ? 0u : 0x7FFFFFFFu, (int32_t)(tkey ^ 0x80000000u)};
+}
+DEV bool spec_keep(uint32_t u, const SpecTest& t) { return (int32_t)(u ^ t.flip) >= t.bound; }
+// The fp32 pattern whose key is 0 (a NaN): it never passes a test with
+// tkey >= 1, so it stands in for elements outside the row.
+constexpr uint32_t kKeyZeroBits = 0xFFFFFFFFu;
+
+DEV uint64_t pack_entry(uint32_t bits, uint32_t idx) { return (uint64_t)bits | ((uint64_t)idx << 32); }
+
+template <bool GUESS>
+DEV void topk_body(const Params& p) {
     __shared__ Smem sm;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int64_t row = blockIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int S = p.parts;
+    const int slot = (int)(blockIdx.x % kXcds) * p.chunk + (int)(blockIdx.x / kXcds);
+    const int row_i = slot / S;
+    const int part = slot - row_i * S;
+    if (row_i >= p.rows) return;   // padding slot of the XCD-aligned grid
+    const int64_t row = row_i;
     const int64_t t0 = stamp();
 
-    int64_t n64 = p.row_len ? (int64_t)p.row_len[row] : p.ld;
+    // Wave 0 samples the guess: every st_g-th entry of prev_topk (at most
+    // kGuessSamples of them). The sample indices go out with the row length;
+    // the gathers that depend on them are the only serial memory latency
+    // before T_spec, and the part's first slabs are in flight meanwhile.
+    const int st_g = (p.K + kGuessSamples - 1) / kGuessSamples;
+    const int m_g = (p.K + st_g - 1) / st_g;
+    int pq[4] = {-1, -1, -1, -1};
+    if (GUESS && p.prev && wave == 0) {
+        const int32_t* pv = p.prev + row * (int64_t)p.K;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const int i = lane + 64 * c;
+            if (i < m_g) pq[c] = pv[i * st_g];
+        }
+    }
+    // Row length through the scalar cache (row is wave-uniform): it does not
+    // wait behind the vector loads above.
+    int64_t n64 = p.row_len ? (int64_t)__builtin_amdgcn_readfirstlane(
+                                  *(const __attribute__((address_space(4))) int32_t*)(p.row_len + row))
+                            : p.ld;
     n64 = n64 < 0 ? 0 : (n64 > p.ld ? p.ld : n64);
     const int n = (int)n64;
     const int K = p.K;
+    const int cap = p.capacity;
     const float* x = p.scores + row * p.ld;
     int32_t* out = p.out + row * (int64_t)K;
     gvr_row_stats* st = p.stats ? p.stats + row : nullptr;
 
-    // (a1) row classify: n <= K -> 0..n-1 then -1 padding.
+    // (a1) row classify: n <= K -> 0..n-1 then -1 padding (part 0 writes).
     if (n <= K) {
+        if (part != 0) return;
         for (int i = tid; i < K; i += kBlock) out[i] = (i < n) ? i : -1;
         if (st && tid == 0) {
             gvr_row_stats s = {};
@@ -404,168 +630,269 @@ __global__ __launch_bounds__(kBlock) void topk_row_kernel(Params p) {
     }
 
     // Float4 blocks of the row (virtual index = element index + aoff, so a
-    // block is one aligned 16-byte load) and this wave's contiguous share.
+    // block is one aligned 16-byte load); slabs of 64 blocks. Full-row share
+    // of each wave (count / collect passes): [qb, qe).
     const int aoff = (int)(((uintptr_t)x >> 2) & 3);
     const float4* xa = reinterpret_cast<const float4*>(x - aoff);
     const int nq = (n + aoff + 3) >> 2;
     const int qlast = nq - 1;
-    const int per = ((nq + kNW - 1) / kNW + 63) & ~63;   // whole slabs per wave
+    const int nslab_row = (nq + 63) >> 6;
+    const int per = ((nslab_row + kNW - 1) / kNW) * 64;   // whole slabs per wave
     const int qb = min(wave * per, nq), qe = min(qb + per, nq);
-    const int cap = p.capacity;
-    const bool all_mode = (n <= cap) && (per * 4 <= kCapW);   // every element is a candidate
+    // This part's slabs [ps0, ps1); waves 1..15 stream them in the
+    // speculative pass, wave 0 computes the guess meanwhile and streams
+    // nothing: this wave's float4 blocks [sqb, sqe).
+    const int ps = (nslab_row + S - 1) / S;
+    const int ps0 = min(part * ps, nslab_row), ps1 = min(ps0 + ps, nslab_row);
+    const int ws = (ps1 - ps0 + kSW - 1) / kSW;
+    const int sw = wave - 1;
+    const int sqb = wave == 0 ? 0 : min((ps0 + sw * ws) * 64, min(ps1 * 64, nq));
+    const int sqe = wave == 0 ? 0 : min((ps0 + min((sw + 1) * ws, ps1 - ps0)) * 64, nq);
+    const int nsl = sqe > sqb ? (sqe - sqb + 63) >> 6 : 0;
 
-    // ---------------- pass 1 parameters and state
-    bool have_prev = p.use_guess && p.prev && !all_mode;
+    // Every element is a candidate when the row fits the lists.
+    const bool all_mode = (n <= cap) && (ws * 256 <= kCapW);
+    bool have_prev = GUESS && p.prev && !all_mode;
+    const bool spec = all_mode || have_prev;
     int gvalid = 0;
     uint32_t gmin = 0xFFFFFFFFu, gmax = 0u, tspec = 0xFFFFFFFFu;
     float gsum = 0.f;
-    Window win = make_window(0u, 0xFFFFFFFFu);
-    bool spec = all_mode || have_prev;   // pass 1 collects key >= tspec (else: counts)
-    int cnt_w = 0;              // this wave's elements >= tspec (counted past capacity)
-    int64_t t1 = t0;
-
-    // The guess indices are loaded before the first slabs (8 KB per row), so
-    // they return first; the gathers x[prev] go out right behind the slabs.
-    int pq[kGuessPerThread];
-    if (have_prev) {
-        const int32_t* pv = p.prev + row * (int64_t)K;
-#pragma unroll
-        for (int m = 0; m < kGuessPerThread; ++m) {
-            const int j = tid + m * kBlock;
-            pq[m] = (j < K) ? pv[j] : -1;
-        }
-    }
-    if (!spec)
-        for (int i = tid; i < kNW * kBinsX; i += kBlock) (&sm.u.hist[0][0])[i] = 0;
-    if (tid < kNW) sm.seg_off[tid] = tid * kCapW;
-    // Guess statistics (Phase 1), run while the first slabs are in flight.
-    auto prologue = [&]() {
-        if (all_mode) {
-            tspec = 0u;
-        } else if (have_prev) {
-            float gv[kGuessPerThread];
-            uint32_t gk[kGuessPerThread];
-            bool ok[kGuessPerThread];
-#pragma unroll
-            for (int m = 0; m < kGuessPerThread; ++m) {
-                ok[m] = pq[m] >= 0 && pq[m] < n;
-                gv[m] = ok[m] ? x[pq[m]] : 0.f;
-            }
-#pragma unroll
-            for (int m = 0; m < kGuessPerThread; ++m) {
-                gk[m] = key_of(gv[m]);
-                if (ok[m]) {
-                    gmin = min(gmin, gk[m]);
-                    gmax = max(gmax, gk[m]);
-                    gsum += gv[m];
-                    ++gvalid;
-                }
-            }
-            gvalid = wave_sum(gvalid);
-            gmin = wave_min_u(gmin);
-            gmax = wave_max_u(gmax);
-            gsum = wave_sum_f(gsum);
-            if (lane == 0) {
-                sm.red[0][wave] = gvalid;
-                sm.red[1][wave] = (int)gmin;
-                sm.red[2][wave] = (int)gmax;
-                sm.redf[wave] = gsum;
-            }
-            for (int i = tid; i < kGuessBins; i += kBlock) sm.u.rhist[i] = 0;
-            if (tid == 0) sm.scal[0] = 0;
-            __syncthreads();
-            gvalid = sum_over_waves(sm.red[0], lane);
-            gmin = wave_min_u(lane < kNW ? (uint32_t)sm.red[1][lane] : 0xFFFFFFFFu);
-            gmax = wave_max_u(lane < kNW ? (uint32_t)sm.red[2][lane] : 0u);
-            gsum = 0.f;
-            for (int v = 0; v < kNW; ++v) gsum += sm.redf[v];   // pmean: fixed order
-            if (gvalid > 0) {
-                // T_spec: lower edge of the histogram bin (over [pmin, pmax])
-                // holding the (kSpecRank + 1)-th smallest gathered key.
-                const uint64_t width = (uint64_t)gmax - gmin + 1;
-                uint32_t sh = 0;
-                while (((uint64_t)kGuessBins << sh) < width) ++sh;
-#pragma unroll
-                for (int m = 0; m < kGuessPerThread; ++m)
-                    if (ok[m])
-                        __hip_atomic_fetch_add(&sm.u.rhist[(gk[m] - gmin) >> sh], 1, __ATOMIC_RELAXED,
-                                               __HIP_MEMORY_SCOPE_WORKGROUP);
-                __syncthreads();
-                // thread t owns bin t; a block scan finds the bin holding the target
-                const int cnt = sm.u.rhist[tid];
-                int below = cnt;
-                block_excl_scan(below, sm, tid);
-                const int target = min(kSpecRank + 1, gvalid);
-                if (below < target && below + cnt >= target) sm.scal[0] = tid;
-                __syncthreads();
-                tspec = gmin + ((uint32_t)sm.scal[0] << sh);
-            } else {
-                tspec = 0xFFFFFFFFu;   // no usable guess: pass 1 keeps nothing useful
-                have_prev = false;
-            }
-        }
-        __syncthreads();
-        t1 = stamp();
-    };
-
-    // ---------------- pass 1: speculative collect (or the first count pass)
-    int* hw = sm.u.hist[wave];
-    uint2* lw = sm.list + wave * kCapW;
-    // Append the listed elements of one lane's block (keys k, first index e0)
-    // whose key is >= tspec (and, in edge slabs, lies in [0, n)).
-    // Lanes whose element is not kept write to a private dummy slot, so the
-    // four stores of a slab need no exec-mask juggling; one capacity check per
-    // slab (wave-uniform) replaces per-element checks.
-    uint2* const dummy = sm.dummy + tid;
-    auto collect = [&](const uint32_t (&k)[4], int e0, bool edge) {
-        const bool v0 = !edge || (e0 >= 0 && e0 < n), v1 = !edge || (e0 + 1 >= 0 && e0 + 1 < n);
-        const bool v2 = !edge || (e0 + 2 >= 0 && e0 + 2 < n), v3 = !edge || (e0 + 3 >= 0 && e0 + 3 < n);
-        const bool f0 = v0 && k[0] >= tspec, f1 = v1 && k[1] >= tspec;
-        const bool f2 = v2 && k[2] >= tspec, f3 = v3 && k[3] >= tspec;
-        const uint64_t m0 = __ballot(f0), m1 = __ballot(f1), m2 = __ballot(f2), m3 = __ballot(f3);
-        const int total = __popcll(m0) + __popcll(m1) + __popcll(m2) + __popcll(m3);
-        cnt_w = __builtin_amdgcn_readfirstlane(cnt_w);   // wave-uniform: keep it scalar
-        if (cnt_w + total <= kCapW) {
-            int p = cnt_w + (int)lanes_below(m3, lanes_below(m2, lanes_below(m1, lanes_below(m0, 0))));
-            *(f0 ? lw + p : dummy) = make_uint2(k[0], (uint32_t)e0);
-            p += f0;
-            *(f1 ? lw + p : dummy) = make_uint2(k[1], (uint32_t)(e0 + 1));
-            p += f1;
-            *(f2 ? lw + p : dummy) = make_uint2(k[2], (uint32_t)(e0 + 2));
-            p += f2;
-            *(f3 ? lw + p : dummy) = make_uint2(k[3], (uint32_t)(e0 + 3));
-        }
-        cnt_w += total;   // counted past capacity: the overflow is detected later
-    };
-    stream_wave(xa, qb, qe, qlast, lane, prologue, [&](const float4& v, int q, int qs) {
-        uint32_t k[4];
-        block_keys(v, k);
-        const int e0 = 4 * q - aoff;
-        const bool edge = (4 * qs - aoff < 0 || 4 * qs + 255 - aoff >= n);   // wave-uniform
-        if (spec) {
-            if (edge) collect(k, e0, true);
-            else collect(k, e0, false);
-        } else {
-#pragma unroll
-            for (int c = 0; c < 4; ++c)
-                hist_add<true>(hw, k[c], !edge || (e0 + c >= 0 && e0 + c < n), 0u, win.shift);
-        }
-    });
-    int passes = 1;
+    int64_t t1 = t0, t2 = t0;
+    int passes = 0;
     int f_spec = 0;
     bool overflow = false;
+    if (tid < kNW) sm.seg_off[tid] = tid * kCapW;
+
     if (spec) {
+        if (!all_mode) {
+            if (tid == 0) sm.guess_ready = 0;
+            lds_barrier();
+        }
+        // The part's first slabs (refills past the wave's share re-read one
+        // 16-byte block of the row: qdup). Issuing them can stall on a full
+        // memory pipeline, so the streaming waves do not meet wave 0 at a
+        // barrier afterwards: they poll the guess_ready flag right before
+        // their first slab.
+        const int qdup = min(sqb, qlast);
+        float4 buf[kSU];
+#pragma unroll
+        for (int u = 0; u < kSU; ++u) buf[u] = xa[(u < nsl) ? min(sqb + u * 64 + lane, qlast) : qdup];
+
+        if (all_mode) {
+            tspec = 0u;
+        } else {
+            if (wave == 0) {
+                // ---------------- (a2) guess statistics (Sec. 4.2.1) over the
+                // sampled guessed scores: pmin, pmax, pmean, and T_spec = lower
+                // edge of the histogram bin (over [pmin, pmax]) holding the
+                // gathered key of rank ceil(65 * m / 2048) from the bottom.
+                bool ok[4];
+                float gv[4];
+                uint32_t gk[4];
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    ok[c] = pq[c] >= 0 && pq[c] < n;
+                    gv[c] = ok[c] ? x[pq[c]] : 0.f;
+                }
+                int cnt = 0;
+                uint32_t mn = 0xFFFFFFFFu, mx = 0u;
+                float sum = 0.f;
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    gk[c] = key_of(gv[c]);
+                    if (ok[c]) {
+                        mn = min(mn, gk[c]);
+                        mx = max(mx, gk[c]);
+                        sum += gv[c];
+                        ++cnt;
+                    }
+                }
+                cnt = wave_sum(cnt);
+                mn = wave_min_u(mn);
+                mx = wave_max_u(mx);
+                sum = wave_sum_f(sum);
+                uint32_t ts = 0xFFFFFFFFu;
+                if (cnt > 0) {
+                    const uint64_t width = (uint64_t)mx - mn + 1;
+                    uint32_t sh = 0;
+                    while (((uint64_t)kGuessBins << sh) < width) ++sh;
+                    int4* h4 = reinterpret_cast<int4*>(sm.u.rhist) + lane * 4;   // lane owns 16 bins
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) h4[j] = make_int4(0, 0, 0, 0);
+#pragma unroll
+                    for (int c = 0; c < 4; ++c)
+                        if (ok[c])
+                            __hip_atomic_fetch_add(&sm.u.rhist[(gk[c] - mn) >> sh], 1, __ATOMIC_RELAXED,
+                                                   __HIP_MEMORY_SCOPE_WORKGROUP);
+                    int h[16];
+                    int s16 = 0;
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const int4 v = h4[j];
+                        h[4 * j] = v.x;
+                        h[4 * j + 1] = v.y;
+                        h[4 * j + 2] = v.z;
+                        h[4 * j + 3] = v.w;
+                        s16 += v.x + v.y + v.z + v.w;
+                    }
+                    const int target = max(1, (kSpecQuantile * cnt + GVR_MAX_K - 1) / GVR_MAX_K);
+                    const int incl = wave_incl_scan(s16, lane);
+                    const int excl = incl - s16;
+                    const uint64_t hit = __ballot(excl < target && incl >= target);
+                    const int L = hit ? (int)__builtin_ctzll(hit) : 0;
+                    int jsel = 0, run = excl;
+#pragma unroll
+                    for (int j = 0; j < 16; ++j) {
+                        if (run < target && run + h[j] >= target) jsel = j;
+                        run += h[j];
+                    }
+                    jsel = __builtin_amdgcn_readlane(jsel, L);
+                    ts = mn + ((uint32_t)(L * 16 + jsel) << sh);
+                }
+                if (lane == 0) {
+                    sm.scal[4] = (int)ts;
+                    sm.scal[5] = cnt;
+                    sm.scal[6] = (int)mn;
+                    sm.scal[7] = (int)mx;
+                    sm.redf[0] = sum;
+                    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+                    __hip_atomic_store(&sm.guess_ready, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+                }
+            }
+            while (__hip_atomic_load(&sm.guess_ready, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) == 0)
+                __builtin_amdgcn_s_sleep(1);
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+            tspec = (uint32_t)sm.scal[4];
+            gvalid = sm.scal[5];
+            gmin = (uint32_t)sm.scal[6];
+            gmax = (uint32_t)sm.scal[7];
+            gsum = sm.redf[0];
+            if (gvalid == 0) have_prev = false;   // no usable guess: the pass keeps (almost) nothing
+        }
+        t1 = stamp();
+
+        // ---------------- (a3)+(a4) speculative pass over the part's slabs:
+        // count f(T_spec) and append every (key, index) with key >= T_spec.
+        int cnt_w = 0;
+        uint2* lw = sm.list + wave * kCapW;
+        // The pass keeps fp32 bit patterns (turned into keys by the refine)
+        // and tests them with one compare (one xor more when T_spec <= -0).
+        // T_spec >= key 1, so the key-0 pattern never passes: elements outside
+        // [0, n) in the row's two edge slabs are replaced by it (a wave-uniform
+        // branch; interior slabs carry no range test). Excluding key 0 keeps
+        // Lemma 1 exact: f is counted for keys >= max(T_spec, 1). Lanes whose
+        // element is not kept write to a private dummy slot, so the stores of
+        // a slab need no exec-mask changes; one capacity check per slab.
+        tspec = max(tspec, 1u);
+        const SpecTest test = make_spec_test(tspec);
+        uint2* const dummy = sm.dummy + tid;
+        for (int s0 = 0; s0 < nsl; s0 += kSU) {
+#pragma unroll
+            for (int u = 0; u < kSU; ++u) {
+                const int s = s0 + u;
+                if (s < nsl) {
+                    const int qs = sqb + s * 64;
+                    const int e0 = 4 * (qs + lane) - aoff;
+                    uint32_t k[4] = {__float_as_uint(buf[u].x), __float_as_uint(buf[u].y), __float_as_uint(buf[u].z),
+                                     __float_as_uint(buf[u].w)};
+                    if (4 * qs - aoff < 0 || 4 * qs + 255 - aoff >= n) {   // edge slab (wave-uniform)
+#pragma unroll
+                        for (int c = 0; c < 4; ++c)
+                            if ((uint32_t)(e0 + c) >= (uint32_t)n) k[c] = kKeyZeroBits;
+                    }
+                    bool f[4];
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) f[c] = spec_keep(k[c], test);
+                    const uint64_t m0 = __ballot(f[0]), m1 = __ballot(f[1]), m2 = __ballot(f[2]), m3 = __ballot(f[3]);
+                    const int total = __popcll(m0) + __popcll(m1) + __popcll(m2) + __popcll(m3);
+                    cnt_w = __builtin_amdgcn_readfirstlane(cnt_w);
+                    if (cnt_w + total <= kCapW) {
+                        int q = cnt_w + (int)lanes_below(m3, lanes_below(m2, lanes_below(m1, lanes_below(m0, 0))));
+#pragma unroll
+                        for (int c = 0; c < 4; ++c) {
+                            *(f[c] ? lw + q : dummy) = make_uint2(k[c], (uint32_t)(e0 + c));
+                            q += f[c];
+                        }
+                    }
+                    cnt_w += total;   // counted past capacity: the overflow is detected later
+                }
+                const int sr = s + kSU;
+                buf[u] = xa[(sr < nsl) ? min(sqb + sr * 64 + lane, qlast) : qdup];
+            }
+        }
+        passes = 1;
+        t2 = stamp();
         if (lane == 0) {
             sm.seg_cnt[wave] = min(cnt_w, kCapW);
             sm.wa[wave] = cnt_w;
         }
-        __syncthreads();
+        lds_barrier();
         f_spec = sum_over_waves(sm.wa, lane);
         overflow = wave_max_u(lane < kNW ? (uint32_t)sm.wa[lane] : 0u) > (uint32_t)kCapW;
-        __syncthreads();
+
+        if (S > 1) {
+            // ---------------- publish this part; the last part of the row goes on
+            uint64_t* plist = p.part_list + (row * S + part) * (int64_t)kCap;
+            const bool publish = !overflow && f_spec <= cap;
+            if (publish) {
+                const int off = sum_over_waves_below(sm.seg_cnt, lane, wave);
+                const uint2* seg = sm.list + wave * kCapW;
+                const int cnt = sm.seg_cnt[wave];
+                for (int i = lane; i < cnt; i += kWave)
+                    __hip_atomic_store(plist + off + i, pack_entry(seg[i].x, seg[i].y), __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+            }
+            if (tid == 0)
+                __hip_atomic_store(p.part_count + row * S + part,
+                                   (int32_t)((uint32_t)f_spec | (overflow ? 0x80000000u : 0u)), __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+            __builtin_amdgcn_s_waitcnt(0);   // this wave's stores have completed
+            __syncthreads();
+            if (tid == 0)
+                sm.scal[3] = (int)__hip_atomic_fetch_add(p.arrivals + row, 1u, __ATOMIC_ACQ_REL,
+                                                         __HIP_MEMORY_SCOPE_AGENT);
+            __syncthreads();
+            if (sm.scal[3] != S - 1) return;   // another part of this row finishes it
+            if (tid == 0) __hip_atomic_store(p.arrivals + row, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            // Row totals; part offsets of the merged list (parts in index order).
+            int c = 0;
+            if (lane < S)
+                c = __hip_atomic_load(p.part_count + row * S + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            const bool ovf = wave_max_u(lane < S && c < 0 ? 1u : 0u) != 0u;
+            const int cc = c & 0x7FFFFFFF;
+            f_spec = wave_sum(cc);
+            overflow = ovf;
+            const int coff = wave_incl_scan(cc, lane) - cc;
+            __syncthreads();   // everyone has read sm.wa / sm.seg_cnt of this part
+            if (wave == 0 && lane < S) {
+                sm.red[0][lane] = cc;
+                sm.red[1][lane] = coff;
+            }
+            __syncthreads();
+            if (!overflow && f_spec >= K && f_spec <= cap) {
+                // Merged list in LDS (keys now), split evenly over the waves.
+                for (int q = 0; q < S; ++q) {
+                    const uint64_t* src = p.part_list + (row * S + q) * (int64_t)kCap;
+                    const int cq = sm.red[0][q], oq = sm.red[1][q];
+                    for (int i = tid; i < cq; i += kBlock) {
+                        const uint64_t e = __hip_atomic_load(src + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        sm.list[oq + i] = make_uint2((uint32_t)e, (uint32_t)(e >> 32));
+                    }
+                }
+                const int chunk = (f_spec + kNW - 1) / kNW;
+                if (tid < kNW) {
+                    const int o = min(tid * chunk, f_spec);
+                    sm.seg_off[tid] = o;
+                    sm.seg_cnt[tid] = min(chunk, f_spec - o);
+                }
+                __syncthreads();
+            }
+        } else {
+            __syncthreads();
+        }
     }
 
-    // Row totals per bin and F[j] = f(edge j) = sum_{b >= j} G[b].
+    // Row-level decision (the single part, or the last part of the row).
     auto compute_F = [&]() {
         __syncthreads();   // every wave's histogram updates are done
         int g = 0;
@@ -588,6 +915,8 @@ __global__ __launch_bounds__(kBlock) void topk_row_kernel(Params p) {
         __syncthreads();
         return j;
     };
+    int* hw = sm.u.hist[wave];
+    Window win = make_window(0u, 0xFFFFFFFFu);
     // Count pass over window `win` (wave-private histograms, then F).
     auto count_pass = [&]() {
         __syncthreads();
@@ -601,8 +930,8 @@ __global__ __launch_bounds__(kBlock) void topk_row_kernel(Params p) {
             const bool edge = (4 * qs - aoff < 0 || 4 * qs + 255 - aoff >= n);
 #pragma unroll
             for (int c = 0; c < 4; ++c) {
-                const bool ok = !edge || (e0 + c >= 0 && e0 + c < n);
-                hist_add<true>(hw, k[c], ok && k[c] >= lo, lo, sh);
+                const bool okc = !edge || (e0 + c >= 0 && e0 + c < n);
+                hist_add<true>(hw, k[c], okc && k[c] >= lo, lo, sh);
             }
         });
         ++passes;
@@ -611,51 +940,55 @@ __global__ __launch_bounds__(kBlock) void topk_row_kernel(Params p) {
     };
 
     int path = all_mode ? GVR_PATH_ALL : (have_prev ? GVR_PATH_GUESS : GVR_PATH_NO_GUESS);
-    uint32_t T = 0, rlo = 0, rhi = 0xFFFFFFFFu;
+    uint32_t T = 0, rlo = 0, rhi = 0xFFFFFFFFu, bin_hi = 0xFFFFFFFFu;
+    bool convert = false;   // lists hold fp32 bits (speculative pass) rather than keys
     int above = 0, cands = 0;
     bool done_lists = false;   // lists hold every key >= T
     bool ties = false;
     uint32_t tstar = 0;
     int n_gt_row = 0;
-    int64_t t2 = t1, t3 = t1;
+    int64_t t3 = t1;
 
     if (spec && !overflow && f_spec >= K && f_spec <= cap) {
         // The speculative lists hold every key >= T_spec, hence the answer
-        // (Lemma 1); the refine window is the range of the listed keys.
+        // (Lemma 1). The refine bins [T_spec, pmax] and puts the (few) keys
+        // above pmax into its top bin.
         T = tspec;
         cands = f_spec;
         done_lists = true;
-        uint32_t mn = 0xFFFFFFFFu, mx = 0u;
-        {
-            const uint2* seg = sm.list + sm.seg_off[wave];
+        rlo = tspec;
+        rhi = 0xFFFFFFFFu;
+        bin_hi = max(gmax, tspec);
+        above = 0;
+        convert = !all_mode;
+        if (all_mode) {   // no guess range: bin [min, max] of the (few) listed keys
+            uint32_t mn = 0xFFFFFFFFu, mx = 0u;
+            uint2* seg = sm.list + sm.seg_off[wave];
             const int cnt = sm.seg_cnt[wave];
             for (int i = lane; i < cnt; i += kWave) {
-                mn = min(mn, seg[i].x);
-                mx = max(mx, seg[i].x);
+                const uint32_t kk = key_of_bits(seg[i].x);
+                seg[i].x = kk;
+                mn = min(mn, kk);
+                mx = max(mx, kk);
             }
             mn = wave_min_u(mn);
             mx = wave_max_u(mx);
             if (lane == 0) {
-                sm.red[1][wave] = (int)mn;
-                sm.red[2][wave] = (int)mx;
+                sm.red[2][wave] = (int)mn;
+                sm.red[3][wave] = (int)mx;
             }
             __syncthreads();
-            mn = wave_min_u(lane < kNW ? (uint32_t)sm.red[1][lane] : 0xFFFFFFFFu);
-            mx = wave_max_u(lane < kNW ? (uint32_t)sm.red[2][lane] : 0u);
+            rlo = wave_min_u(lane < kNW ? (uint32_t)sm.red[2][lane] : 0xFFFFFFFFu);
+            rhi = bin_hi = wave_max_u(lane < kNW ? (uint32_t)sm.red[3][lane] : 0u);
         }
-        rlo = mn;
-        rhi = mx;
-        above = 0;
     } else {
         if (spec) {
             // The guess fell short (or a wave's list overflowed): count passes
-            // around T_spec, whose f is known, then collect or emit.
+            // over the whole row around T_spec, whose f is known.
             if (path == GVR_PATH_GUESS) path = GVR_PATH_NARROWED;
             win = (f_spec < K) ? make_window(0u, tspec - 1u) : make_window(tspec, 0xFFFFFFFFu);
-            count_pass();
-        } else {
-            compute_F();   // pass 1 was the first count pass (whole key range)
         }
+        count_pass();
         for (;;) {
             const int j = crossing();
             int decision = 2;   // 0 collect, 1 ties, 2 narrow
@@ -682,6 +1015,7 @@ __global__ __launch_bounds__(kBlock) void topk_row_kernel(Params p) {
                 rlo = T;
                 rhi = (j < kBins) ? (uint32_t)std::min<uint64_t>(e + ((uint64_t)1 << win.shift) - 1, 0xFFFFFFFFu)
                                   : 0xFFFFFFFFu;
+                bin_hi = rhi;
                 above = (j < kBins) ? sm.F[j + 1] : 0;
                 int mine = 0;
                 for (int b = j + lane; b < kBinsX; b += kWave) mine += sm.u.hist[wave][b];
@@ -749,9 +1083,9 @@ __global__ __launch_bounds__(kBlock) void topk_row_kernel(Params p) {
                     uint64_t mg[4], me[4];
 #pragma unroll
                     for (int c = 0; c < 4; ++c) {
-                        const bool ok = !edge || (e0 + c >= 0 && e0 + c < n);
-                        fg[c] = ok && k[c] > tstar;
-                        fe[c] = ok && k[c] == tstar;
+                        const bool okc = !edge || (e0 + c >= 0 && e0 + c < n);
+                        fg[c] = okc && k[c] > tstar;
+                        fe[c] = okc && k[c] == tstar;
                         mg[c] = __ballot(fg[c]);
                         me[c] = __ballot(fe[c]);
                     }
@@ -779,8 +1113,8 @@ __global__ __launch_bounds__(kBlock) void topk_row_kernel(Params p) {
             win = nw;
             count_pass();
         }
+        t2 = stamp();
     }
-    t2 = stamp();
 
     if (ties) {
         if (st && tid == 0) {
@@ -819,9 +1153,8 @@ __global__ __launch_bounds__(kBlock) void topk_row_kernel(Params p) {
     __syncthreads();
     t3 = stamp();
     // ---------------- (a5) refine the listed candidates and emit
-    const uint32_t kth = refine_kth(sm, rlo, rhi, above, K, tid);
     int ngt = 0;
-    emit_from_lists(sm, kth, K, out, tid, &ngt);
+    const uint32_t kth = refine_emit(sm, rlo, rhi, bin_hi, above, K, out, tid, &ngt, convert);
     if (st && tid == 0) {
         gvr_row_stats s = {};
         s.n = n;
@@ -844,10 +1177,13 @@ __global__ __launch_bounds__(kBlock) void topk_row_kernel(Params p) {
     }
 }
 
+__global__ __launch_bounds__(kBlock) void gvr_topk_kernel(Params p) { topk_body<true>(p); }
+__global__ __launch_bounds__(kBlock) void radix_topk_kernel(Params p) { topk_body<false>(p); }
+
 // ------------------------------------------------------------------ host side
 
 gvr_status validate(const float* scores, int64_t B, int64_t ld, int32_t K, const int32_t* out,
-                    const gvr_options* opt, int* capacity, int* use_guess) {
+                    const gvr_options* opt, int* capacity, int* use_guess, int* parts) {
     if (K < 1 || K > GVR_MAX_K) return GVR_ERR_UNSUPPORTED_K;
     if (B < 0 || ld < 0) return GVR_ERR_INVALID_ARG;
     if (B > 0 && (!scores || !out)) return GVR_ERR_INVALID_ARG;
@@ -858,34 +1194,142 @@ gvr_status validate(const float* scores, int64_t B, int64_t ld, int32_t K, const
             if (opt->capacity < K || opt->capacity > GVR_MAX_CANDIDATES) return GVR_ERR_INVALID_ARG;
             cap = opt->capacity;
         }
-        if ((opt->flags & ~1) || opt->reserved0 || opt->reserved1) return GVR_ERR_INVALID_ARG;
+        if ((opt->flags & ~1) || opt->reserved1) return GVR_ERR_INVALID_ARG;
+        if (opt->parts < 0 || opt->parts > kMaxParts) return GVR_ERR_INVALID_ARG;
         if (opt->flags & 1) *use_guess = 0;
+        *parts = opt->parts;
     }
     *capacity = cap;
     return GVR_OK;
 }
 
+// Split-row workspace of one (device, stream): arrival counters, part counts
+// and part lists for up to `slots` (row, part) pairs of one launch. Calls on
+// one stream run in order, so they can share it; the counters are zeroed
+// when the buffer is made and every launch leaves them at zero.
+struct Workspace {
+    int device;
+    void* stream;
+    int slots;
+    uint32_t* arrivals;
+    int32_t* part_count;
+    uint64_t* part_list;
+    void* base;
+};
+
+std::mutex g_ws_mutex;
+std::vector<Workspace> g_ws;
+
+int cu_count(int device) {
+    static std::mutex m;
+    static std::vector<int> cache;
+    std::lock_guard<std::mutex> lk(m);
+    if ((int)cache.size() <= device) cache.resize(device + 1, 0);
+    if (cache[device] == 0) {
+        int v = 0;
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess || v <= 0) v = 256;
+        cache[device] = v;
+    }
+    return cache[device];
+}
+
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+gvr_status get_workspace(int device, void* stream, int rows, int parts, Workspace* out) {
+    std::lock_guard<std::mutex> lk(g_ws_mutex);
+    const int slots = rows * parts;
+    for (auto& w : g_ws)
+        if (w.device == device && w.stream == stream) {
+            if (w.slots >= slots) {
+                *out = w;
+                return GVR_OK;
+            }
+            // Grow: the old buffer may still be read by queued launches.
+            if (hipStreamSynchronize((hipStream_t)stream) != hipSuccess) return GVR_ERR_HIP;
+            (void)hipFree(w.base);
+            w = g_ws.back();
+            g_ws.pop_back();
+            break;
+        }
+    const size_t a_bytes = align_up((size_t)slots * sizeof(uint32_t), 256);
+    const size_t c_bytes = align_up((size_t)slots * sizeof(int32_t), 256);
+    const size_t l_bytes = (size_t)slots * kCap * sizeof(uint64_t);
+    void* base = nullptr;
+    if (hipMalloc(&base, a_bytes + c_bytes + l_bytes) != hipSuccess) return GVR_ERR_HIP;
+    if (hipMemset(base, 0, a_bytes) != hipSuccess) {
+        (void)hipFree(base);
+        return GVR_ERR_HIP;
+    }
+    Workspace w;
+    w.device = device;
+    w.stream = stream;
+    w.slots = slots;
+    w.base = base;
+    w.arrivals = static_cast<uint32_t*>(base);
+    w.part_count = reinterpret_cast<int32_t*>(static_cast<char*>(base) + a_bytes);
+    w.part_list = reinterpret_cast<uint64_t*>(static_cast<char*>(base) + a_bytes + c_bytes);
+    g_ws.push_back(w);
+    *out = w;
+    return GVR_OK;
+}
+
+// Parts per row. Splitting a row over S workgroups divides its streaming
+// time (one workgroup reads about 33 GB/s on MI355X) but costs the merge of
+// the parts' candidate lists, about 8 us of memory round trips; split only
+// when the time saved is larger, keep parts >= kMinPartElems long and stay
+// within the compute units.
+int choose_parts(int64_t rows, int64_t ld, int cus) {
+    if (rows <= 0 || rows >= cus) return 1;
+    int64_t s = cus / rows;
+    s = std::min<int64_t>(s, std::max<int64_t>(1, ld / kMinPartElems));
+    s = std::min<int64_t>(s, kMaxParts);
+    if (s <= 1) return 1;
+    const double stream_us = (double)ld * 4.0 / 33.0e3;   // one workgroup, whole row
+    const double saved_us = stream_us * (1.0 - 1.0 / (double)s);
+    return saved_us > 8.0 ? (int)s : 1;
+}
+
 gvr_status run(const float* scores, int64_t B, int64_t ld, const int32_t* row_len, const int32_t* prev,
                int32_t K, int32_t* out, void* stream, const gvr_options* opt, gvr_row_stats* stats,
                int use_guess) {
-    int cap = 0;
-    gvr_status st = validate(scores, B, ld, K, out, opt, &cap, &use_guess);
+    int cap = 0, parts_opt = 0;
+    gvr_status st = validate(scores, B, ld, K, out, opt, &cap, &use_guess, &parts_opt);
     if (st != GVR_OK) return st;
     if (B == 0) return GVR_OK;
-    // One workgroup per row; the grid is split only past 2^31 - 1 rows.
-    for (int64_t r0 = 0; r0 < B; r0 += 0x7FFFFFFF) {
-        const int64_t rows = std::min<int64_t>(B - r0, 0x7FFFFFFF);
+    const bool guess = use_guess && prev;
+    int device = 0;
+    if (hipGetDevice(&device) != hipSuccess) return GVR_ERR_HIP;
+    const int parts = !guess ? 1 : (parts_opt > 0 ? parts_opt : choose_parts(B, ld, cu_count(device)));
+    Workspace ws = {};
+    if (parts > 1) {
+        st = get_workspace(device, stream, (int)B, parts, &ws);
+        if (st != GVR_OK) return st;
+    }
+    // Rows in launches of at most 2^24 (the grid holds 8 * chunk slots).
+    const int64_t kRowsPerLaunch = (int64_t)1 << 24;
+    for (int64_t r0 = 0; r0 < B; r0 += kRowsPerLaunch) {
+        const int64_t rows = std::min<int64_t>(B - r0, kRowsPerLaunch);
+        const int64_t rows_pad = (rows + kXcds - 1) / kXcds * kXcds;
         Params q;
         q.scores = scores + r0 * ld;
         q.ld = ld;
         q.row_len = row_len ? row_len + r0 : nullptr;
-        q.prev = prev ? prev + r0 * K : nullptr;
+        q.prev = guess ? prev + r0 * K : nullptr;
         q.out = out + r0 * K;
         q.stats = stats ? stats + r0 : nullptr;
         q.K = K;
         q.capacity = cap;
-        q.use_guess = use_guess;
-        hipLaunchKernelGGL(topk_row_kernel, dim3((unsigned)rows), dim3(kBlock), 0, (hipStream_t)stream, q);
+        q.rows = (int32_t)rows;
+        q.parts = parts;
+        q.chunk = (int32_t)(rows_pad / kXcds * parts);
+        q.arrivals = ws.arrivals;
+        q.part_count = ws.part_count;
+        q.part_list = ws.part_list;
+        const dim3 grid((unsigned)(rows_pad * parts));
+        if (guess)
+            hipLaunchKernelGGL(gvr_topk_kernel, grid, dim3(kBlock), 0, (hipStream_t)stream, q);
+        else
+            hipLaunchKernelGGL(radix_topk_kernel, grid, dim3(kBlock), 0, (hipStream_t)stream, q);
         if (hipGetLastError() != hipSuccess) return GVR_ERR_HIP;
     }
     return GVR_OK;
@@ -928,6 +1372,6 @@ const char* gvr_status_string(gvr_status s) {
     return "unknown status";
 }
 
-const char* gvr_version(void) { return "gvr_topk 0.2 (gfx950, one workgroup per row)"; }
+const char* gvr_version(void) { return "gvr_topk 0.3 (gfx950, split rows, last-part merge)"; }
 
 }  // extern "C"

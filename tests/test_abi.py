@@ -75,10 +75,12 @@ def test_host_side_validation(L):
 def test_options_validation(L):
     import paper_2604_22312_amd as g
     vp = ctypes.c_void_p
-    bad = [g.Options(capacity=100, flags=0, reserved0=0, reserved1=0),      # capacity < K
-           g.Options(capacity=0, flags=4, reserved0=0, reserved1=0),        # unknown flag bit
-           g.Options(capacity=0, flags=0, reserved0=1, reserved1=0),        # reserved field set
-           g.Options(capacity=20000, flags=0, reserved0=0, reserved1=0)]    # capacity > max
+    bad = [g.Options(capacity=100, flags=0, parts=0, reserved1=0),      # capacity < K
+           g.Options(capacity=0, flags=4, parts=0, reserved1=0),        # unknown flag bit
+           g.Options(capacity=0, flags=0, parts=0, reserved1=1),        # reserved field set
+           g.Options(capacity=0, flags=0, parts=17, reserved1=0),       # too many parts
+           g.Options(capacity=0, flags=0, parts=-1, reserved1=0),       # negative parts
+           g.Options(capacity=20000, flags=0, parts=0, reserved1=0)]    # capacity > max
     for opt in bad:
         assert L.gvr_topk_ex(vp(1), 2, 100, None, None, 128, vp(1), None, ctypes.byref(opt), None) == -1
         assert L.radix_topk_ex(vp(1), 2, 100, None, 128, vp(1), None, ctypes.byref(opt), None) == -1

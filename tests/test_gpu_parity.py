@@ -310,3 +310,84 @@ def test_alternating_shapes():
         assert_rows_equal(out.cpu().numpy(), exp, "gvr B=%d ld=%d" % (B, ld))
         out = g.radix_topk(S, RL, None, K)
         assert_rows_equal(out.cpu().numpy(), exp, "radix B=%d ld=%d" % (B, ld))
+
+
+def _gvr_parts(S, RL, prev, K, parts):
+    import paper_2604_22312_amd as g
+    return g.gvr_topk_ex(S, RL, prev, K, options={"parts": parts})
+
+
+def test_parts_do_not_change_the_answer():
+    """The row split (1..16 workgroups per row, merged by the last part to
+    arrive) gives the oracle's answer for every split, with stats of one pass."""
+    import paper_2604_22312_amd as g
+    w = workload(2, 2, 4, None)
+    K = w.K
+    S = w.scores[1].to(DEV)
+    RL = w.row_len[1].to(DEV)
+    exp, _, _ = oracle.topk(w.scores[1].numpy(), K, row_len=w.row_len[1].numpy())
+    prev, _, _ = oracle.topk(w.scores[0].numpy(), K, row_len=w.row_len[0].numpy())
+    pd = torch.from_numpy(prev).to(DEV)
+    for parts in (1, 2, 3, 5, 7, 16):
+        note("parts=%d" % parts)
+        st = g.new_stats(w.rows, DEV)
+        out = g.gvr_topk_ex(S, RL, pd, K, options={"parts": parts}, stats=st)
+        assert_rows_equal(out.cpu().numpy(), exp, "parts=%d" % parts)
+        d = g.decode_stats(st)
+        assert set(d["path"].tolist()) <= {2, 3}, d["path"].tolist()
+        for r in range(w.rows):
+            if int(d["path"][r]) == 2:
+                assert int(d["passes"][r]) == 1
+                cnt = oracle.count_ge(w.scores[1].numpy()[r], int(d["threshold"][r]), n=int(w.row_len[1][r]))
+                assert int(d["candidates"][r]) == cnt
+
+
+@pytest.mark.parametrize("parts", [1, 4])
+@pytest.mark.parametrize("ld,K", [(20001, 2048), (131071, 2000), (9999, 7)])
+def test_special_rows_with_guess_and_parts(ld, K, parts):
+    rng = np.random.default_rng(ld + 7 * K)
+    rows, lens = _special_rows(ld, K, rng)
+    exp, _, _ = oracle.topk(rows, K, row_len=lens)
+    S = torch.from_numpy(rows).to(DEV)
+    RL = torch.from_numpy(lens).to(DEV)
+    guesses = {"exact": exp,
+               "random": rng.integers(0, ld, size=exp.shape).astype(np.int32)}
+    for name, pv in guesses.items():
+        note("special rows guess=%s ld=%d K=%d parts=%d" % (name, ld, K, parts))
+        out = _gvr_parts(S, RL, torch.from_numpy(np.ascontiguousarray(pv)).to(DEV), K, parts)
+        assert_rows_equal(out.cpu().numpy(), exp, "special rows guess=%s ld=%d K=%d parts=%d"
+                          % (name, ld, K, parts))
+
+
+@pytest.mark.parametrize("parts", [1, 3])
+def test_misaligned_rows_with_guess(parts):
+    rng = np.random.default_rng(19)
+    K = 2048
+    for ld in (30001, 30002, 30003):
+        big = rng.gamma(2.0, 1.0, size=(6 * ld + 1)).astype(np.float32)
+        rows = big[1:].reshape(6, ld)
+        lens = np.array([ld, ld - 1, ld - 2, ld - 3, 12345, 2049], np.int32)
+        exp, _, _ = oracle.topk(rows, K, row_len=lens)
+        t = torch.from_numpy(big).to(DEV)
+        S = t[1:].view(6, ld)
+        pv = torch.from_numpy(np.ascontiguousarray(exp)).to(DEV)
+        note("misaligned with guess ld=%d parts=%d" % (ld, parts))
+        out = _gvr_parts(S, torch.from_numpy(lens).to(DEV), pv, K, parts)
+        assert_rows_equal(out.cpu().numpy(), exp, "misaligned with guess ld=%d parts=%d" % (ld, parts))
+
+
+@pytest.mark.parametrize("parts", [1, 2])
+def test_poison_beyond_row_len_with_guess(parts):
+    w = workload(3, 1, 8, "c")
+    K = w.K
+    s = w.scores[0].numpy().copy()
+    rl = w.row_len[0].numpy()
+    exp, _, _ = oracle.topk(s, K, row_len=rl)
+    pv = torch.from_numpy(np.ascontiguousarray(exp)).to(DEV)
+    for poison in (np.float32(np.nan), np.float32(np.inf), np.float32(1e30)):
+        p = s.copy()
+        for r in range(p.shape[0]):
+            p[r, rl[r]:] = poison
+        note("poison with guess %r parts=%d" % (float(poison), parts))
+        out = _gvr_parts(torch.from_numpy(p).to(DEV), torch.from_numpy(rl).to(DEV), pv, K, parts)
+        assert_rows_equal(out.cpu().numpy(), exp, "poison with guess %r parts=%d" % (float(poison), parts))
