@@ -98,7 +98,10 @@ typedef struct gvr_options {
     int32_t capacity;      /* refine capacity C, K <= C <= GVR_MAX_CANDIDATES
                               (default GVR_MAX_CANDIDATES); a smaller C forces
                               more narrowing passes, never another result */
-    int32_t flags;         /* bit 0: ignore prev_topk (run the radix schedule) */
+    int32_t flags;         /* bit 0: ignore prev_topk (run the radix schedule);
+                              bit 1: place the parts of a row on different XCDs
+                              (a test of the path that does not rely on their
+                              shared L2; slower) */
     int32_t parts;         /* workgroups per row, 1..16 (0 = chosen from B, ld
                               and the device's compute units); never changes
                               the result */
@@ -116,7 +119,8 @@ typedef struct gvr_row_stats {
     int32_t n_gt;          /* #{key > kth_key} */
     int32_t guess_valid;   /* valid entries of prev_topk used by the guess */
     uint32_t spec_threshold; /* T_spec derived from the guess (0xFFFFFFFF if none) */
-    int32_t spec_count;    /* f(T_spec) counted in the first pass */
+    int32_t spec_count;    /* f(T_spec) counted in the first pass (-1 if a
+                              candidate list overflowed) */
     float pmean;           /* mean of the guessed scores (T0 of Sec. 4.2.1) */
     int32_t reserved;
     int64_t t_start;       /* s_memtime stamps of the row's workgroup (shader */

@@ -66,7 +66,8 @@ constexpr int kBins = 256;                     // bins of a counting window
 constexpr int kBinsX = kBins + 1;              // + "at or above the window"
 constexpr int kCap = GVR_MAX_CANDIDATES;       // list capacity (LDS)
 constexpr int kCapW = kCap / kNW;              // per-wave list capacity, speculative pass
-constexpr int kRefBins = 4096;                 // bins of a refine level (12 bits of key)
+constexpr int kRefBins = 4096;                 // bins of a narrowing refine level (12 bits of key)
+constexpr int kRefBins1 = 2048;                // bins of the first refine level (32 per lane of one wave)
 constexpr int kGuessSamples = 256;             // guessed indices gathered: a strided sample of prev_topk
 constexpr int kGuessBins = 1024;               // bins of the gathered-key histogram (16 per lane of wave 0)
 constexpr int kSpecQuantile = 65;              // T_spec: gathered key of rank ceil(65 / 2048 * sample size)
@@ -90,8 +91,11 @@ struct Params {
     int32_t rows;        // rows of this launch
     int32_t parts;       // S: workgroups per row
     int32_t chunk;       // gridDim.x / 8: consecutive (row, part) slots per XCD
-    uint32_t* arrivals;  // [rows] parts that finished the speculative pass (S > 1); 0 between calls
-    int32_t* part_count; // [rows][S] f(T_spec) of each part, bit 31 = a wave list overflowed
+    int32_t scatter;     // 1: slot = blockIdx.x (parts of a row on different XCDs)
+    uint64_t* arrivals;  // [rows] parts that finished the speculative pass (S > 1), per XCD above
+                         // bit 16; 0 between calls
+    int32_t* part_count; // [rows][S] f(threshold) of each part, bit 31 = a wave list overflowed
+    uint32_t* part_thresh; // [rows][S] threshold of each part's list (T_spec, the same in every part)
     uint64_t* part_list; // [rows][S][kCap] (fp32 bits | index << 32) of each part
 };
 
@@ -409,45 +413,52 @@ DEV void emit_from_lists(Smem& sm, uint32_t T, int K, int32_t* out, int tid, int
     *n_gt_out = gtot;
 }
 
+// First refine level: kRefBins1 bins of 2^sh keys from rlo; keys at or above
+// rlo + (kRefBins1 - 1) << sh share the top bin.
+DEV uint32_t ref_shift(uint32_t rlo, uint32_t bin_hi) {
+    const uint64_t width = (uint64_t)bin_hi - rlo + 1;
+    uint32_t sh = 0;
+    while (((uint64_t)kRefBins1 << sh) < width) ++sh;
+    return sh;
+}
+DEV int ref_bin(uint32_t kk, uint32_t rlo, uint32_t sh) { return (int)min((kk - rlo) >> sh, (uint32_t)kRefBins1 - 1); }
+DEV void ref_hist_add(Smem& sm, uint32_t kk, uint32_t rlo, uint32_t sh) {
+    __hip_atomic_fetch_add(&sm.u.rhist[ref_bin(kk, rlo, sh)], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
 // Exact K-th key T* among the listed candidates and the emission. The K-th
 // key lies in [rlo, rhi]; `above` listed keys lie above rhi. One histogram
-// level of kRefBins bins over [rlo, bin_hi] (keys in (bin_hi, rhi] count in
-// the top bin) by all waves, then wave 0 finds the
+// level of kRefBins1 bins over [rlo, bin_hi] (keys in (bin_hi, rhi] count in
+// the top bin; built here unless `hist_ready`), then wave 0 finds the
 // bin b holding the K-th key with two wave scans. If b holds at most kSmall
 // candidates, the waves copy them (with their wave) to LDS and count the
 // keys above b; wave 0 ranks them to get T* and the per-wave emission
 // offsets, and every wave emits its segment. Otherwise histogram narrowing
 // (refine_kth) continues inside b.
 DEV uint32_t refine_emit(Smem& sm, uint32_t rlo, uint32_t rhi, uint32_t bin_hi, int above, int K, int32_t* out,
-                         int tid, int* n_gt_out, bool convert) {
+                         int tid, int* n_gt_out, bool hist_ready) {
     const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    uint2* seg = sm.list + sm.seg_off[wave];
+    const uint2* seg = sm.list + sm.seg_off[wave];
     const int cnt = sm.seg_cnt[wave];
-    const uint64_t width = (uint64_t)bin_hi - rlo + 1;
-    uint32_t sh = 0;
-    while (((uint64_t)kRefBins << sh) < width) ++sh;
+    const uint32_t sh = ref_shift(rlo, bin_hi);
     int* hb = sm.u.rhist;
-    for (int i = tid; i < kRefBins; i += kBlock) hb[i] = 0;
     if (tid == 0) sm.scal[1] = 0;
-    __syncthreads();
-    for (int i = lane; i < cnt; i += kWave) {
-        uint32_t kk = seg[i].x;
-        if (convert) {   // lists of the speculative pass hold fp32 bit patterns
-            kk = key_of_bits(kk);
-            seg[i].x = kk;
+    if (!hist_ready) {
+        for (int i = tid; i < kRefBins1; i += kBlock) hb[i] = 0;
+        __syncthreads();
+        for (int i = lane; i < cnt; i += kWave) {
+            const uint32_t kk = seg[i].x;
+            if (kk >= rlo && kk <= rhi) ref_hist_add(sm, kk, rlo, sh);
         }
-        if (kk >= rlo && kk <= rhi)
-            __hip_atomic_fetch_add(&hb[min((kk - rlo) >> sh, (uint32_t)kRefBins - 1)], 1, __ATOMIC_RELAXED,
-                                   __HIP_MEMORY_SCOPE_WORKGROUP);
     }
     __syncthreads();
     const int need0 = K - above;   // >= 1: rank of T* among the keys in [rlo, rhi], from the top
     if (wave == 0) {
-        // lane l owns bins [64 l, 64 l + 64)
-        const int4* h4 = reinterpret_cast<const int4*>(hb) + lane * 16;
+        // lane l owns bins [32 l, 32 l + 32)
+        const int4* h4 = reinterpret_cast<const int4*>(hb) + lane * 8;
         int s = 0;
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
+        for (int j = 0; j < 8; ++j) {
             const int4 v = h4[j];
             s += v.x + v.y + v.z + v.w;
         }
@@ -457,14 +468,14 @@ DEV uint32_t refine_emit(Smem& sm, uint32_t rlo, uint32_t rhi, uint32_t bin_hi, 
         const uint64_t hit = __ballot(abv < need0 && abv + s >= need0);
         const int L = hit ? (int)__builtin_ctzll(hit) : 0;
         const int abv_l = __builtin_amdgcn_readlane(abv, L);
-        const int hj = hb[L * 64 + lane];
+        const int hj = lane < 32 ? hb[L * 32 + lane] : 0;
         const int ij = wave_incl_scan(hj, lane);
         const int s_l = __builtin_amdgcn_readlane(ij, 63);
         const int abj = abv_l + s_l - ij;
-        const uint64_t hit2 = __ballot(abj < need0 && abj + hj >= need0);
+        const uint64_t hit2 = __ballot(lane < 32 && abj < need0 && abj + hj >= need0);
         const int J = hit2 ? (int)__builtin_ctzll(hit2) : 0;
         if (lane == 0) {
-            sm.scal[0] = L * 64 + J;
+            sm.scal[0] = L * 32 + J;
             sm.scal[2] = above + __builtin_amdgcn_readlane(abj, J);
             sm.scal[3] = __builtin_amdgcn_readlane(hj, J);
         }
@@ -476,7 +487,7 @@ DEV uint32_t refine_emit(Smem& sm, uint32_t rlo, uint32_t rhi, uint32_t bin_hi, 
     const uint64_t lo64 = (uint64_t)rlo + ((uint64_t)b << sh);
     const uint32_t lo_b = (uint32_t)lo64;
     const uint32_t hi_b =
-        b == kRefBins - 1 ? rhi : (uint32_t)std::min<uint64_t>(lo64 + ((uint64_t)1 << sh) - 1, rhi);
+        b == kRefBins1 - 1 ? rhi : (uint32_t)std::min<uint64_t>(lo64 + ((uint64_t)1 << sh) - 1, rhi);
     if (lo_b == hi_b) {   // the bin is one key: T* = lo_b
         emit_from_lists(sm, lo_b, K, out, tid, n_gt_out);
         return lo_b;
@@ -579,7 +590,10 @@ DEV void topk_body(const Params& p) {
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int S = p.parts;
-    const int slot = (int)(blockIdx.x % kXcds) * p.chunk + (int)(blockIdx.x / kXcds);
+    // Slot (row, part) of this workgroup: consecutive slots on one XCD, so the
+    // parts of a row share an L2 (scatter: the plain order, for tests of the
+    // cross-XCD path).
+    const int slot = p.scatter ? (int)blockIdx.x : (int)(blockIdx.x % kXcds) * p.chunk + (int)(blockIdx.x / kXcds);
     const int row_i = slot / S;
     const int part = slot - row_i * S;
     if (row_i >= p.rows) return;   // padding slot of the XCD-aligned grid
@@ -659,7 +673,9 @@ DEV void topk_body(const Params& p) {
     float gsum = 0.f;
     int64_t t1 = t0, t2 = t0;
     int passes = 0;
-    int f_spec = 0;
+    int f_spec = 0;          // f(tthr), or -1 if unknown
+    bool hist_ready = false; // the refine's first histogram level is built (lists at tthr)
+    uint32_t tthr = 0u;      // threshold of the speculative lists
     bool overflow = false;
     if (tid < kNW) sm.seg_off[tid] = tid * kCapW;
 
@@ -759,6 +775,38 @@ DEV void topk_body(const Params& p) {
                     __hip_atomic_store(&sm.guess_ready, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
                 }
             }
+        }
+
+        // ---------------- (a3)+(a4) speculative pass over the part's slabs:
+        // count and append every (key, index) at or above T_spec.
+        //
+        // The pass keeps fp32 bit patterns (turned into keys afterwards) and
+        // tests them with one compare (one xor more for thresholds <= -0).
+        // Thresholds are >= key 1, so the key-0 pattern never passes: elements
+        // outside [0, n) in the row's two edge slabs are replaced by it (a
+        // wave-uniform branch; interior slabs carry no range test). Lanes
+        // whose element is not kept write to a private dummy slot, so the
+        // stores of a slab need no exec-mask changes; one capacity check per
+        // slab (wave-uniform).
+        int cnt_w = 0;
+        uint2* lw = sm.list + wave * kCapW;
+        uint2* const dummy = sm.dummy + tid;
+        auto slab_bits = [&](const float4& v, int qs, uint32_t (&k)[4]) {
+            const int e0 = 4 * (qs + lane) - aoff;
+            k[0] = __float_as_uint(v.x);
+            k[1] = __float_as_uint(v.y);
+            k[2] = __float_as_uint(v.z);
+            k[3] = __float_as_uint(v.w);
+            if (4 * qs - aoff < 0 || 4 * qs + 255 - aoff >= n) {   // edge slab (wave-uniform)
+#pragma unroll
+                for (int c = 0; c < 4; ++c)
+                    if ((uint32_t)(e0 + c) >= (uint32_t)n) k[c] = kKeyZeroBits;
+            }
+        };
+        // The streaming waves wait for T_spec here, with their first slabs in
+        // flight (polling an LDS flag, not a barrier: issuing those loads may
+        // stall a wave, which must not hold up wave 0).
+        if (!all_mode) {
             while (__hip_atomic_load(&sm.guess_ready, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) == 0)
                 __builtin_amdgcn_s_sleep(1);
             __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
@@ -770,22 +818,8 @@ DEV void topk_body(const Params& p) {
             if (gvalid == 0) have_prev = false;   // no usable guess: the pass keeps (almost) nothing
         }
         t1 = stamp();
-
-        // ---------------- (a3)+(a4) speculative pass over the part's slabs:
-        // count f(T_spec) and append every (key, index) with key >= T_spec.
-        int cnt_w = 0;
-        uint2* lw = sm.list + wave * kCapW;
-        // The pass keeps fp32 bit patterns (turned into keys by the refine)
-        // and tests them with one compare (one xor more when T_spec <= -0).
-        // T_spec >= key 1, so the key-0 pattern never passes: elements outside
-        // [0, n) in the row's two edge slabs are replaced by it (a wave-uniform
-        // branch; interior slabs carry no range test). Excluding key 0 keeps
-        // Lemma 1 exact: f is counted for keys >= max(T_spec, 1). Lanes whose
-        // element is not kept write to a private dummy slot, so the stores of
-        // a slab need no exec-mask changes; one capacity check per slab.
         tspec = max(tspec, 1u);
         const SpecTest test = make_spec_test(tspec);
-        uint2* const dummy = sm.dummy + tid;
         for (int s0 = 0; s0 < nsl; s0 += kSU) {
 #pragma unroll
             for (int u = 0; u < kSU; ++u) {
@@ -793,13 +827,8 @@ DEV void topk_body(const Params& p) {
                 if (s < nsl) {
                     const int qs = sqb + s * 64;
                     const int e0 = 4 * (qs + lane) - aoff;
-                    uint32_t k[4] = {__float_as_uint(buf[u].x), __float_as_uint(buf[u].y), __float_as_uint(buf[u].z),
-                                     __float_as_uint(buf[u].w)};
-                    if (4 * qs - aoff < 0 || 4 * qs + 255 - aoff >= n) {   // edge slab (wave-uniform)
-#pragma unroll
-                        for (int c = 0; c < 4; ++c)
-                            if ((uint32_t)(e0 + c) >= (uint32_t)n) k[c] = kKeyZeroBits;
-                    }
+                    uint32_t k[4];
+                    slab_bits(buf[u], qs, k);
                     bool f[4];
 #pragma unroll
                     for (int c = 0; c < 4; ++c) f[c] = spec_keep(k[c], test);
@@ -820,6 +849,9 @@ DEV void topk_body(const Params& p) {
                 buf[u] = xa[(sr < nsl) ? min(sqb + sr * 64 + lane, qlast) : qdup];
             }
         }
+        // Clear the refine's first histogram level (wave 0 is done with the
+        // guess histogram once its flag is set); filled by the count below.
+        for (int i = tid; i < kRefBins1; i += kBlock) sm.u.rhist[i] = 0;
         passes = 1;
         t2 = stamp();
         if (lane == 0) {
@@ -827,65 +859,130 @@ DEV void topk_body(const Params& p) {
             sm.wa[wave] = cnt_w;
         }
         lds_barrier();
-        f_spec = sum_over_waves(sm.wa, lane);
         overflow = wave_max_u(lane < kNW ? (uint32_t)sm.wa[lane] : 0u) > (uint32_t)kCapW;
+        // Every wave turns its list into keys and, for a whole row, adds them
+        // to the refine's first histogram level: f(T_spec) = the list sizes.
+        const uint32_t teff = tspec;
+        hist_ready = S == 1 && !all_mode && !overflow;
+        const uint32_t rsh = ref_shift(teff, max(gmax, teff));
+        int fw = 0;
+        if (!overflow) {
+            uint2* seg = sm.list + wave * kCapW;
+            const int cnt = sm.seg_cnt[wave];
+            for (int i0 = 0; i0 < cnt; i0 += kWave) {
+                const int i = i0 + lane;
+                uint2 e = i < cnt ? seg[i] : make_uint2(0u, 0u);
+                e.x = key_of_bits(e.x);
+                const bool keep = i < cnt && e.x >= teff;
+                const uint64_t m = __ballot(keep);
+                if (keep) {
+                    seg[fw + (int)lanes_below(m, 0)] = e;
+                    if (hist_ready) ref_hist_add(sm, e.x, teff, rsh);
+                }
+                fw += (int)__popcll(m);
+            }
+        }
+        lds_barrier();   // every wave has read sm.wa / sm.wb and added to the histogram
+        if (lane == 0) {
+            sm.wb[wave] = fw;
+            sm.seg_cnt[wave] = fw;
+        }
+        lds_barrier();
+        f_spec = overflow ? -1 : sum_over_waves(sm.wb, lane);
+        tthr = teff;
 
         if (S > 1) {
-            // ---------------- publish this part; the last part of the row goes on
+            // ---------------- publish this part; the last part of the row goes on.
+            // The parts of a row are launched on one XCD (the grid mapping),
+            // so they share its L2: a part's plain stores have reached that
+            // L2 once they complete (the vector L1 writes through), and the
+            // last part reads them back from it. The arrival word, updated by
+            // a device-scope atomic, also counts the parts per XCD (5 bits per
+            // XCD above 16 bits of arrivals): the last part uses the lists
+            // only if every part ran on its own XCD, and otherwise reads the
+            // whole row itself. A plain load by the last part cannot hit a
+            // stale vector-L1 line: this workgroup never read those lines
+            // before, and each launch starts with invalidated L1s.
             uint64_t* plist = p.part_list + (row * S + part) * (int64_t)kCap;
             const bool publish = !overflow && f_spec <= cap;
-            if (publish) {
-                const int off = sum_over_waves_below(sm.seg_cnt, lane, wave);
+            if (publish) {   // this part's entries, in index order
+                const int off = sum_over_waves_below(sm.wb, lane, wave);
                 const uint2* seg = sm.list + wave * kCapW;
                 const int cnt = sm.seg_cnt[wave];
-                for (int i = lane; i < cnt; i += kWave)
-                    __hip_atomic_store(plist + off + i, pack_entry(seg[i].x, seg[i].y), __ATOMIC_RELAXED,
-                                       __HIP_MEMORY_SCOPE_AGENT);
+                for (int i = lane; i < cnt; i += kWave) plist[off + i] = pack_entry(seg[i].x, seg[i].y);
             }
-            if (tid == 0)
-                __hip_atomic_store(p.part_count + row * S + part,
-                                   (int32_t)((uint32_t)f_spec | (overflow ? 0x80000000u : 0u)), __ATOMIC_RELAXED,
-                                   __HIP_MEMORY_SCOPE_AGENT);
-            __builtin_amdgcn_s_waitcnt(0);   // this wave's stores have completed
+            if (tid == 0) {
+                p.part_count[row * S + part] = (int32_t)((uint32_t)max(f_spec, 0) | (overflow ? 0x80000000u : 0u));
+                p.part_thresh[row * S + part] = tthr;
+            }
+            __builtin_amdgcn_s_waitcnt(0);   // this wave's stores have completed (reached L2)
             __syncthreads();
-            if (tid == 0)
-                sm.scal[3] = (int)__hip_atomic_fetch_add(p.arrivals + row, 1u, __ATOMIC_ACQ_REL,
-                                                         __HIP_MEMORY_SCOPE_AGENT);
+            if (tid == 0) {
+                const uint32_t xcc = (uint32_t)__builtin_amdgcn_s_getreg((31 << 11) | 20) & 7u;   // HW_REG_XCC_ID
+                const uint64_t add = 1ull + (1ull << (16 + 5 * xcc));
+                const uint64_t old =
+                    __hip_atomic_fetch_add(p.arrivals + row, add, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                const uint64_t now = old + add;
+                sm.scal[3] = (int)(old & 0xFFFFu);
+                sm.scal[2] = (int)((now >> (16 + 5 * xcc)) & 31u) == S;   // all parts on this XCD
+            }
             __syncthreads();
             if (sm.scal[3] != S - 1) return;   // another part of this row finishes it
-            if (tid == 0) __hip_atomic_store(p.arrivals + row, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            // Row totals; part offsets of the merged list (parts in index order).
-            int c = 0;
-            if (lane < S)
-                c = __hip_atomic_load(p.part_count + row * S + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            const bool ovf = wave_max_u(lane < S && c < 0 ? 1u : 0u) != 0u;
-            const int cc = c & 0x7FFFFFFF;
-            f_spec = wave_sum(cc);
-            overflow = ovf;
-            const int coff = wave_incl_scan(cc, lane) - cc;
-            __syncthreads();   // everyone has read sm.wa / sm.seg_cnt of this part
-            if (wave == 0 && lane < S) {
-                sm.red[0][lane] = cc;
-                sm.red[1][lane] = coff;
-            }
-            __syncthreads();
-            if (!overflow && f_spec >= K && f_spec <= cap) {
-                // Merged list in LDS (keys now), split evenly over the waves.
-                for (int q = 0; q < S; ++q) {
-                    const uint64_t* src = p.part_list + (row * S + q) * (int64_t)kCap;
-                    const int cq = sm.red[0][q], oq = sm.red[1][q];
-                    for (int i = tid; i < cq; i += kBlock) {
-                        const uint64_t e = __hip_atomic_load(src + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                        sm.list[oq + i] = make_uint2((uint32_t)e, (uint32_t)(e >> 32));
-                    }
-                }
-                const int chunk = (f_spec + kNW - 1) / kNW;
-                if (tid < kNW) {
-                    const int o = min(tid * chunk, f_spec);
-                    sm.seg_off[tid] = o;
-                    sm.seg_cnt[tid] = min(chunk, f_spec - o);
+            const bool same_xcd = sm.scal[2] != 0;
+            if (tid == 0) __hip_atomic_store(p.arrivals + row, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (!same_xcd) {
+                overflow = true;   // lists unusable: the fallback reads the whole row
+                f_spec = -1;
+            } else {
+                // Row threshold (the largest of the parts'), totals and part
+                // offsets of the merged list (parts in index order).
+                const int c = lane < S ? p.part_count[row * S + lane] : 0;
+                const uint32_t tp = lane < S ? p.part_thresh[row * S + lane] : 0u;
+                const bool ovf = wave_max_u(lane < S && c < 0 ? 1u : 0u) != 0u;
+                const uint32_t trow = wave_max_u(tp);
+                const bool mixed = wave_min_u(lane < S ? tp : 0xFFFFFFFFu) != trow;
+                const int cc = c & 0x7FFFFFFF;
+                f_spec = wave_sum(cc);
+                overflow = ovf;
+                tthr = trow;
+                const int coff = wave_incl_scan(cc, lane) - cc;
+                __syncthreads();   // everyone has read sm.wa / sm.wb / sm.seg_cnt of this part
+                if (wave == 0 && lane < S) {
+                    sm.red[0][lane] = cc;
+                    sm.red[1][lane] = coff;
                 }
                 __syncthreads();
+                if (!overflow && f_spec >= K && f_spec <= cap) {
+                    // Merged list in LDS, split evenly over the waves; the
+                    // refine's first histogram level is built on the way.
+                    const uint32_t msh = ref_shift(trow, max(gmax, trow));
+                    for (int q = 0; q < S; ++q) {
+                        const uint64_t* src = p.part_list + (row * S + q) * (int64_t)kCap;
+                        const int cq = sm.red[0][q], oq = sm.red[1][q];
+                        for (int i = tid; i < cq; i += kBlock) {
+                            const uint64_t e = src[i];
+                            sm.list[oq + i] = make_uint2((uint32_t)e, (uint32_t)(e >> 32));
+                            if ((uint32_t)e >= trow) ref_hist_add(sm, (uint32_t)e, trow, msh);
+                        }
+                    }
+                    hist_ready = true;
+                    const int chunk = (f_spec + kNW - 1) / kNW;
+                    if (tid < kNW) {
+                        const int o = min(tid * chunk, f_spec);
+                        sm.seg_off[tid] = o;
+                        sm.seg_cnt[tid] = min(chunk, f_spec - o);
+                    }
+                    __syncthreads();
+                    if (mixed) {   // parts kept different thresholds: count f(trow) itself
+                        int fw = 0;
+                        const uint2* seg = sm.list + sm.seg_off[wave];
+                        for (int i = lane; i < sm.seg_cnt[wave]; i += kWave) fw += seg[i].x >= trow;
+                        fw = wave_sum(fw);
+                        if (lane == 0) sm.wa[wave] = fw;
+                        __syncthreads();
+                        f_spec = sum_over_waves(sm.wa, lane);
+                    }
+                }
             }
         } else {
             __syncthreads();
@@ -941,7 +1038,7 @@ DEV void topk_body(const Params& p) {
 
     int path = all_mode ? GVR_PATH_ALL : (have_prev ? GVR_PATH_GUESS : GVR_PATH_NO_GUESS);
     uint32_t T = 0, rlo = 0, rhi = 0xFFFFFFFFu, bin_hi = 0xFFFFFFFFu;
-    bool convert = false;   // lists hold fp32 bits (speculative pass) rather than keys
+    bool use_hist = false;   // the refine's first level is already counted
     int above = 0, cands = 0;
     bool done_lists = false;   // lists hold every key >= T
     bool ties = false;
@@ -953,23 +1050,21 @@ DEV void topk_body(const Params& p) {
         // The speculative lists hold every key >= T_spec, hence the answer
         // (Lemma 1). The refine bins [T_spec, pmax] and puts the (few) keys
         // above pmax into its top bin.
-        T = tspec;
+        T = tthr;
         cands = f_spec;
         done_lists = true;
-        rlo = tspec;
+        use_hist = hist_ready && !all_mode;
+        rlo = tthr;
         rhi = 0xFFFFFFFFu;
-        bin_hi = max(gmax, tspec);
+        bin_hi = max(gmax, tthr);
         above = 0;
-        convert = !all_mode;
         if (all_mode) {   // no guess range: bin [min, max] of the (few) listed keys
             uint32_t mn = 0xFFFFFFFFu, mx = 0u;
             uint2* seg = sm.list + sm.seg_off[wave];
             const int cnt = sm.seg_cnt[wave];
             for (int i = lane; i < cnt; i += kWave) {
-                const uint32_t kk = key_of_bits(seg[i].x);
-                seg[i].x = kk;
-                mn = min(mn, kk);
-                mx = max(mx, kk);
+                mn = min(mn, seg[i].x);
+                mx = max(mx, seg[i].x);
             }
             mn = wave_min_u(mn);
             mx = wave_max_u(mx);
@@ -986,7 +1081,8 @@ DEV void topk_body(const Params& p) {
             // The guess fell short (or a wave's list overflowed): count passes
             // over the whole row around T_spec, whose f is known.
             if (path == GVR_PATH_GUESS) path = GVR_PATH_NARROWED;
-            win = (f_spec < K) ? make_window(0u, tspec - 1u) : make_window(tspec, 0xFFFFFFFFu);
+            if (f_spec >= 0)   // else: unknown (lists unusable or overflowed), count the whole key range
+                win = (f_spec < K) ? make_window(0u, tthr - 1u) : make_window(tthr, 0xFFFFFFFFu);
         }
         count_pass();
         for (;;) {
@@ -1154,7 +1250,7 @@ DEV void topk_body(const Params& p) {
     t3 = stamp();
     // ---------------- (a5) refine the listed candidates and emit
     int ngt = 0;
-    const uint32_t kth = refine_emit(sm, rlo, rhi, bin_hi, above, K, out, tid, &ngt, convert);
+    const uint32_t kth = refine_emit(sm, rlo, rhi, bin_hi, above, K, out, tid, &ngt, use_hist);
     if (st && tid == 0) {
         gvr_row_stats s = {};
         s.n = n;
@@ -1183,7 +1279,7 @@ __global__ __launch_bounds__(kBlock) void radix_topk_kernel(Params p) { topk_bod
 // ------------------------------------------------------------------ host side
 
 gvr_status validate(const float* scores, int64_t B, int64_t ld, int32_t K, const int32_t* out,
-                    const gvr_options* opt, int* capacity, int* use_guess, int* parts) {
+                    const gvr_options* opt, int* capacity, int* use_guess, int* parts, int* scatter) {
     if (K < 1 || K > GVR_MAX_K) return GVR_ERR_UNSUPPORTED_K;
     if (B < 0 || ld < 0) return GVR_ERR_INVALID_ARG;
     if (B > 0 && (!scores || !out)) return GVR_ERR_INVALID_ARG;
@@ -1194,9 +1290,10 @@ gvr_status validate(const float* scores, int64_t B, int64_t ld, int32_t K, const
             if (opt->capacity < K || opt->capacity > GVR_MAX_CANDIDATES) return GVR_ERR_INVALID_ARG;
             cap = opt->capacity;
         }
-        if ((opt->flags & ~1) || opt->reserved1) return GVR_ERR_INVALID_ARG;
+        if ((opt->flags & ~3) || opt->reserved1) return GVR_ERR_INVALID_ARG;
         if (opt->parts < 0 || opt->parts > kMaxParts) return GVR_ERR_INVALID_ARG;
         if (opt->flags & 1) *use_guess = 0;
+        *scatter = (opt->flags >> 1) & 1;
         *parts = opt->parts;
     }
     *capacity = cap;
@@ -1211,8 +1308,9 @@ struct Workspace {
     int device;
     void* stream;
     int slots;
-    uint32_t* arrivals;
+    uint64_t* arrivals;
     int32_t* part_count;
+    uint32_t* part_thresh;
     uint64_t* part_list;
     void* base;
 };
@@ -1251,11 +1349,12 @@ gvr_status get_workspace(int device, void* stream, int rows, int parts, Workspac
             g_ws.pop_back();
             break;
         }
-    const size_t a_bytes = align_up((size_t)slots * sizeof(uint32_t), 256);
+    const size_t a_bytes = align_up((size_t)slots * sizeof(uint64_t), 256);
     const size_t c_bytes = align_up((size_t)slots * sizeof(int32_t), 256);
+    const size_t t_bytes = align_up((size_t)slots * sizeof(uint32_t), 256);
     const size_t l_bytes = (size_t)slots * kCap * sizeof(uint64_t);
     void* base = nullptr;
-    if (hipMalloc(&base, a_bytes + c_bytes + l_bytes) != hipSuccess) return GVR_ERR_HIP;
+    if (hipMalloc(&base, a_bytes + c_bytes + t_bytes + l_bytes) != hipSuccess) return GVR_ERR_HIP;
     if (hipMemset(base, 0, a_bytes) != hipSuccess) {
         (void)hipFree(base);
         return GVR_ERR_HIP;
@@ -1265,9 +1364,10 @@ gvr_status get_workspace(int device, void* stream, int rows, int parts, Workspac
     w.stream = stream;
     w.slots = slots;
     w.base = base;
-    w.arrivals = static_cast<uint32_t*>(base);
+    w.arrivals = static_cast<uint64_t*>(base);
     w.part_count = reinterpret_cast<int32_t*>(static_cast<char*>(base) + a_bytes);
-    w.part_list = reinterpret_cast<uint64_t*>(static_cast<char*>(base) + a_bytes + c_bytes);
+    w.part_thresh = reinterpret_cast<uint32_t*>(static_cast<char*>(base) + a_bytes + c_bytes);
+    w.part_list = reinterpret_cast<uint64_t*>(static_cast<char*>(base) + a_bytes + c_bytes + t_bytes);
     g_ws.push_back(w);
     *out = w;
     return GVR_OK;
@@ -1292,8 +1392,8 @@ int choose_parts(int64_t rows, int64_t ld, int cus) {
 gvr_status run(const float* scores, int64_t B, int64_t ld, const int32_t* row_len, const int32_t* prev,
                int32_t K, int32_t* out, void* stream, const gvr_options* opt, gvr_row_stats* stats,
                int use_guess) {
-    int cap = 0, parts_opt = 0;
-    gvr_status st = validate(scores, B, ld, K, out, opt, &cap, &use_guess, &parts_opt);
+    int cap = 0, parts_opt = 0, scatter = 0;
+    gvr_status st = validate(scores, B, ld, K, out, opt, &cap, &use_guess, &parts_opt, &scatter);
     if (st != GVR_OK) return st;
     if (B == 0) return GVR_OK;
     const bool guess = use_guess && prev;
@@ -1322,8 +1422,10 @@ gvr_status run(const float* scores, int64_t B, int64_t ld, const int32_t* row_le
         q.rows = (int32_t)rows;
         q.parts = parts;
         q.chunk = (int32_t)(rows_pad / kXcds * parts);
+        q.scatter = scatter;
         q.arrivals = ws.arrivals;
         q.part_count = ws.part_count;
+        q.part_thresh = ws.part_thresh;
         q.part_list = ws.part_list;
         const dim3 grid((unsigned)(rows_pad * parts));
         if (guess)
