@@ -519,29 +519,37 @@ DEV uint32_t refine_emit(Smem& sm, uint32_t rlo, uint32_t rhi, uint32_t bin_hi, 
         }
     }
     gt_hi = wave_sum(gt_hi);
-    if (lane == 0) sm.wa[wave] = gt_hi;
+    if (lane == 0) {
+        sm.wa[wave] = gt_hi;
+        sm.wb[wave] = 0;
+    }
     __syncthreads();
     if (wave == 0) {
+        // One lane per candidate of bin b: T* is the need-th largest of
+        // them, found by a radix select over the offsets key - lo_b (MSB
+        // first, one ballot per bit).
         const int need = K - above_b;   // rank of T* inside the bin, from the top
-        const uint4 mine = lane < cnt_b ? sm.small[lane] : make_uint4(0u, 0u, 0xFFFFFFFFu, 0u);
-        int gt = 0, ge = 0;
-        for (int t = 0; t < cnt_b; ++t) {
-            const uint32_t kt = (uint32_t)__builtin_amdgcn_readlane((int)mine.x, t);
-            gt += kt > mine.x;
-            ge += kt >= mine.x;
+        const bool v = lane < cnt_b;
+        const uint4 mine = v ? sm.small[lane] : make_uint4(0u, 0u, 0u, 0u);
+        const uint32_t off = mine.x - lo_b;
+        const int nbits = 32 - __builtin_clz(hi_b - lo_b);   // hi_b > lo_b here
+        uint32_t prefix = 0u;
+        int r = need;
+        for (int bit = nbits - 1; bit >= 0; --bit) {
+            const uint32_t cand = prefix | (1u << bit);
+            const int c1 = (int)__popcll(__ballot(v && (off >> bit) == (cand >> bit)));
+            if (c1 >= r) prefix = cand;
+            else r -= c1;
         }
-        const uint64_t hit = __ballot(lane < cnt_b && gt < need && ge >= need);
-        const uint32_t kth = (uint32_t)__builtin_amdgcn_readlane((int)mine.x, hit ? (int)__builtin_ctzll(hit) : 0);
-        // Per-wave keys > T* and == T* (lane w < kNW counts for wave w).
-        int gw = 0, ew = 0;
-        for (int t = 0; t < cnt_b; ++t) {
-            const uint32_t kt = (uint32_t)__builtin_amdgcn_readlane((int)mine.x, t);
-            const int wt = __builtin_amdgcn_readlane((int)mine.z, t);
-            gw += (wt == lane) && kt > kth;
-            ew += (wt == lane) && kt == kth;
-        }
-        gw = lane < kNW ? gw + sm.wa[lane] : 0;
-        ew = lane < kNW ? ew : 0;
+        const uint32_t kth = lo_b + prefix;
+        // Per-wave keys > T* and == T*: the bin's candidates add themselves
+        // to their wave's counts (keys above the bin are in sm.wa already).
+        if (v && mine.x > kth)
+            __hip_atomic_fetch_add(&sm.wa[mine.z], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        if (v && mine.x == kth)
+            __hip_atomic_fetch_add(&sm.wb[mine.z], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        const int gw = lane < kNW ? sm.wa[lane] : 0;
+        const int ew = lane < kNW ? sm.wb[lane] : 0;
         const int gi = wave_incl_scan(gw, lane), ei = wave_incl_scan(ew, lane);
         const int gtot = __builtin_amdgcn_readlane(gi, 63);
         if (lane < kNW) {
