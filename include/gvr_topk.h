@@ -103,7 +103,8 @@ typedef struct gvr_options {
                               (a test of the path that does not rely on their
                               shared L2; slower) */
     int32_t parts;         /* workgroups per row, 1..16 (0 = chosen from B, ld
-                              and the device's compute units); never changes
+                              and the device's compute units; a forced value is
+                              lowered so that B * parts <= 2048); never changes
                               the result */
     int32_t reserved1;     /* must be 0 */
 } gvr_options;

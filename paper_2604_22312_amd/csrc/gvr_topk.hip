@@ -75,6 +75,7 @@ constexpr int kSmall = 64;                     // refine: K-th key's bin resolve
 constexpr int kMaxPasses = 8;                  // 2 + at most 4 narrowing passes + 1 final pass suffice
 constexpr int kMaxParts = 16;                  // workgroups per row
 constexpr int kMinPartElems = 16384;           // a row is split only into parts at least this long
+constexpr int kMaxSlots = 2048;                // (row, part) pairs of one split call: 256 MB of workspace
 constexpr int kXcds = 8;                       // gfx950 XCDs; workgroup i runs on XCD i % 8
 
 static_assert(GVR_MAX_CANDIDATES % kNW == 0, "per-wave capacity");
@@ -1407,7 +1408,10 @@ gvr_status run(const float* scores, int64_t B, int64_t ld, const int32_t* row_le
     const bool guess = use_guess && prev;
     int device = 0;
     if (hipGetDevice(&device) != hipSuccess) return GVR_ERR_HIP;
-    const int parts = !guess ? 1 : (parts_opt > 0 ? parts_opt : choose_parts(B, ld, cu_count(device)));
+    int parts = !guess ? 1 : (parts_opt > 0 ? parts_opt : choose_parts(B, ld, cu_count(device)));
+    // A forced split is capped at kMaxSlots (row, part) pairs per call, which
+    // bounds the workspace (128 KB of list per pair).
+    if (parts > 1 && (int64_t)parts * B > kMaxSlots) parts = (int)std::max<int64_t>(1, kMaxSlots / B);
     Workspace ws = {};
     if (parts > 1) {
         st = get_workspace(device, stream, (int)B, parts, &ws);
