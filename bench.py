@@ -99,7 +99,7 @@ def time_calls(fn, w, prevs, steps, warmup, out):
     return e0.elapsed_time(e1) / 1e3   # seconds
 
 
-def pass_stats(fn_ex, w, prevs, radix):
+def pass_stats(fn_ex, w, prevs, radix, options=None):
     import numpy as np
     import paper_2604_22312_amd as g
 
@@ -109,7 +109,7 @@ def pass_stats(fn_ex, w, prevs, radix):
         if radix:
             fn_ex(w.scores[t], w.row_len[t], K_TOPK, stats=st)
         else:
-            fn_ex(w.scores[t], w.row_len[t], prevs[t], K_TOPK, stats=st)
+            fn_ex(w.scores[t], w.row_len[t], prevs[t], K_TOPK, stats=st, options=options)
         d = g.decode_stats(st)
         passes.append(d["passes"].numpy())
         cands.append(d["candidates"].numpy())
@@ -165,6 +165,8 @@ def main():
     ap.add_argument("--mode", choices=["bench", "copy"], default="bench")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--no-radix", action="store_true", help="skip timing radix_topk")
+    ap.add_argument("--no-secant", action="store_true",
+                    help="skip timing the paper's own threshold schedule (gvr_topk_ex flag bit 2)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py: this build runs on one GPU; rows of a decode step shard across GPUs with no "
@@ -227,6 +229,20 @@ def main():
                              "achieved_GBs": round(alg_bytes / rper / 1e9, 1),
                              "passes_per_row": pass_stats(g.radix_topk_ex, w, prevs, radix=True)}
         res["speedup_vs_radix"] = round(rper / per, 3)
+    if not args.no_secant:
+        # The paper's schedule (T0 = pmean, secant counting passes, collect
+        # pass) on the same rows: same answers, reported for comparison.
+        opts = {"flags": 4}
+
+        def secant(scores, row_len, prev, K, out_idx=None, stream=None):
+            return g.gvr_topk_ex(scores, row_len, prev, K, out_idx=out_idx, stream=stream, options=opts)
+        ssecs = time_calls(secant, w, prevs, args.steps, args.warmup, out)
+        sper = ssecs / args.steps
+        res["gvr_topk_paper_schedule"] = {"value": round(rows * args.steps / ssecs, 1), "unit": "rows/s",
+                                          "ms_per_step": round(sper * 1e3, 5),
+                                          "achieved_GBs": round(alg_bytes / sper / 1e9, 1),
+                                          "passes_per_row": pass_stats(g.gvr_topk_ex, w, prevs, radix=False,
+                                                                       options=opts)}
     if not args.no_cpu:
         res["cpu_baseline"] = cpu_baseline(w)
     print(json.dumps(res))

@@ -90,7 +90,9 @@ enum {
     GVR_PATH_NARROWED = 3,     /* guess fell short; count passes narrowed the threshold */
     GVR_PATH_TIES = 4,         /* the K-th key isolated exactly (ties straddle
                                   [K, C]); selection emitted without refine */
-    GVR_PATH_NO_GUESS = 5      /* prev_topk NULL / without a valid entry, or radix */
+    GVR_PATH_NO_GUESS = 5,     /* prev_topk NULL / without a valid entry, or radix */
+    GVR_PATH_SECANT = 6        /* flag bit 2: the secant threshold search accepted a
+                                  threshold and one collect pass gathered the list */
 };
 
 /* Optional knobs (NULL = defaults). Zero fields mean "default". */
@@ -101,7 +103,11 @@ typedef struct gvr_options {
     int32_t flags;         /* bit 0: ignore prev_topk (run the radix schedule);
                               bit 1: place the parts of a row on different XCDs
                               (a test of the path that does not rely on their
-                              shared L2; slower) */
+                              shared L2; slower);
+                              bit 2: the paper's own threshold search -- every
+                              guessed score, T0 = pmean, secant counting passes,
+                              a collect pass (one workgroup per row) -- instead
+                              of the speculative first pass */
     int32_t parts;         /* workgroups per row, 1..16 (0 = chosen from B, ld
                               and the device's compute units; a forced value is
                               lowered so that B * parts <= 2048); never changes

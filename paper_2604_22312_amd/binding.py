@@ -8,7 +8,7 @@ import torch
 
 GVR_MAX_K = 2048
 GVR_MAX_CANDIDATES = 16384
-PATH_NAMES = {0: "trivial", 1: "all", 2: "guess", 3: "narrowed", 4: "ties", 5: "no_guess", -1: "error"}
+PATH_NAMES = {0: "trivial", 1: "all", 2: "guess", 3: "narrowed", 4: "ties", 5: "no_guess", 6: "secant", -1: "error"}
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.path.join(_HERE, "libgvr_topk.so")
@@ -24,8 +24,9 @@ class GvrError(RuntimeError):
 
 
 class Options(ctypes.Structure):
-    """Mirror of ``gvr_options``: capacity C, flags (bit 0: ignore the guess),
-    parts (workgroups per row, 0 = automatic)."""
+    """Mirror of ``gvr_options``: capacity C, flags (bit 0: ignore the guess;
+    bit 1: scatter a row's parts over XCDs; bit 2: the paper's secant
+    threshold search), parts (workgroups per row, 0 = automatic)."""
     _fields_ = [("capacity", ctypes.c_int32), ("flags", ctypes.c_int32),
                 ("parts", ctypes.c_int32), ("reserved1", ctypes.c_int32)]
 

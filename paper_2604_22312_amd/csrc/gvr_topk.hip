@@ -73,6 +73,7 @@ constexpr int kGuessBins = 1024;               // bins of the gathered-key histo
 constexpr int kSpecQuantile = 65;              // T_spec: gathered key of rank ceil(65 / 2048 * sample size)
 constexpr int kSmall = 64;                     // refine: K-th key's bin resolved by one wave up to this size
 constexpr int kMaxPasses = 8;                  // 2 + at most 4 narrowing passes + 1 final pass suffice
+constexpr int kMaxSecant = 8;                  // probes of the secant search after T0 (I_max)
 constexpr int kMaxParts = 16;                  // workgroups per row
 constexpr int kMinPartElems = 16384;           // a row is split only into parts at least this long
 constexpr int kMaxSlots = 2048;                // (row, part) pairs of one split call: 256 MB of workspace
@@ -93,6 +94,7 @@ struct Params {
     int32_t parts;       // S: workgroups per row
     int32_t chunk;       // gridDim.x / 8: consecutive (row, part) slots per XCD
     int32_t scatter;     // 1: slot = blockIdx.x (parts of a row on different XCDs)
+    int32_t secant;      // 1: the paper's Phase 2 (secant counting passes) instead of the speculative pass
     uint64_t* arrivals;  // [rows] parts that finished the speculative pass (S > 1), per XCD above
                          // bit 16; 0 between calls
     int32_t* part_count; // [rows][S] f(threshold) of each part, bit 31 = a wave list overflowed
@@ -104,6 +106,7 @@ struct Params {
 
 DEV uint32_t key_of_bits(uint32_t u) { return u ^ ((uint32_t)((int32_t)u >> 31) | 0x80000000u); }
 DEV uint32_t key_of(float v) { return key_of_bits(__float_as_uint(v)); }
+DEV float float_of_key(uint32_t k) { return __uint_as_float((k & 0x80000000u) ? (k ^ 0x80000000u) : ~k); }
 
 // Number of set bits of m below this lane, plus acc.
 DEV uint32_t lanes_below(uint64_t m, uint32_t acc) {
@@ -676,7 +679,9 @@ DEV void topk_body(const Params& p) {
     // Every element is a candidate when the row fits the lists.
     const bool all_mode = (n <= cap) && (ws * 256 <= kCapW);
     bool have_prev = GUESS && p.prev && !all_mode;
-    const bool spec = all_mode || have_prev;
+    // The paper's Phase 2 schedule (secant counting passes), when asked for.
+    const bool secant = GUESS && p.secant && have_prev;
+    const bool spec = (all_mode || have_prev) && !secant;
     int gvalid = 0;
     uint32_t gmin = 0xFFFFFFFFu, gmax = 0u, tspec = 0xFFFFFFFFu;
     float gsum = 0.f;
@@ -1055,7 +1060,192 @@ DEV void topk_body(const Params& p) {
     int n_gt_row = 0;
     int64_t t3 = t1;
 
-    if (spec && !overflow && f_spec >= K && f_spec <= cap) {
+    // ---------------- the paper's schedule (Sec. 4.2.1-4.2.3), as an option:
+    // Phase 1 over every valid guessed score, Phase 2 probes one threshold per
+    // full-row counting pass (T0 = pmean, then secant steps toward f_target
+    // inside the counted bracket, the first step damped to half the bracket,
+    // bisection in key space when a step leaves it, at most kMaxSecant probes),
+    // Phase 3 one collect pass at the accepted threshold.
+    bool sec_ok = false;
+    uint32_t sec_lo = 0u, sec_hi = 0xFFFFFFFFu;   // f(sec_lo) > C, f(sec_hi) < K (bracket, keys)
+    uint32_t row_max = 0xFFFFFFFFu;
+    if (secant) {
+        if (tid < kNW) sm.seg_off[tid] = 0;
+        // Phase 1: all K guessed scores, 2 per thread.
+        const int32_t* pv = p.prev + row * (int64_t)K;
+        uint32_t mn = 0xFFFFFFFFu, mx = 0u;
+        float sum = 0.f;
+        int cnt = 0;
+#pragma unroll
+        for (int m = 0; m < (GVR_MAX_K + kBlock - 1) / kBlock; ++m) {
+            const int j = tid + m * kBlock;
+            const int idx = j < K ? pv[j] : -1;
+            if (idx >= 0 && idx < n) {
+                const float v = x[idx];
+                const uint32_t kk = key_of(v);
+                mn = min(mn, kk);
+                mx = max(mx, kk);
+                sum += v;
+                ++cnt;
+            }
+        }
+        cnt = wave_sum(cnt);
+        mn = wave_min_u(mn);
+        mx = wave_max_u(mx);
+        sum = wave_sum_f(sum);
+        if (lane == 0) {
+            sm.red[0][wave] = cnt;
+            sm.red[1][wave] = (int)mn;
+            sm.red[2][wave] = (int)mx;
+            sm.redf[wave] = sum;
+        }
+        __syncthreads();
+        gvalid = sum_over_waves(sm.red[0], lane);
+        gmin = wave_min_u(lane < kNW ? (uint32_t)sm.red[1][lane] : 0xFFFFFFFFu);
+        gmax = wave_max_u(lane < kNW ? (uint32_t)sm.red[2][lane] : 0u);
+        gsum = 0.f;
+        for (int v = 0; v < kNW; ++v) gsum += sm.redf[v];   // fixed order
+        __syncthreads();
+        t1 = stamp();
+        // f(T) over the row (per-wave counts kept in sm.wa for the collect);
+        // the first pass also finds the row's smallest and largest key.
+        auto count_ge = [&](uint32_t tk, bool minmax) {
+            int c = 0;
+            uint32_t lo = 0xFFFFFFFFu, hi = 0u;
+            stream_wave(xa, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
+                uint32_t k[4];
+                block_keys(v, k);
+                const int e0 = 4 * q - aoff;
+                const bool edge = (4 * qs - aoff < 0 || 4 * qs + 255 - aoff >= n);
+#pragma unroll
+                for (int cc = 0; cc < 4; ++cc) {
+                    const bool okc = !edge || (e0 + cc >= 0 && e0 + cc < n);
+                    c += (int)__popcll(__ballot(okc && k[cc] >= tk));
+                    if (minmax && okc) {
+                        lo = min(lo, k[cc]);
+                        hi = max(hi, k[cc]);
+                    }
+                }
+            });
+            ++passes;
+            if (minmax) {
+                lo = wave_min_u(lo);
+                hi = wave_max_u(hi);
+            }
+            if (lane == 0) {
+                sm.wa[wave] = c;
+                sm.red[1][wave] = (int)lo;
+                sm.red[2][wave] = (int)hi;
+            }
+            __syncthreads();
+            const int f = sum_over_waves(sm.wa, lane);
+            if (minmax) {
+                sec_lo = wave_min_u(lane < kNW ? (uint32_t)sm.red[1][lane] : 0xFFFFFFFFu);
+                row_max = wave_max_u(lane < kNW ? (uint32_t)sm.red[2][lane] : 0u);
+            }
+            __syncthreads();
+            return f;
+        };
+        const int f_target = min(K + K / 2, (K + cap) / 2);
+        uint32_t ka = gvalid > 0 ? key_of(gvalid > 0 ? gsum / (float)gvalid : 0.f) : 0x80000000u;   // T0 = pmean
+        tspec = ka;
+        int fa = count_ge(ka, true);
+        f_spec = fa;
+        // Bracket from the first pass: f(row min) = n > C, f(above row max) = 0 < K.
+        int fl = n, fh = 0;
+        sec_hi = row_max == 0xFFFFFFFFu ? 0xFFFFFFFFu : row_max + 1u;
+        uint32_t kb = sec_hi;   // the other interpolation point
+        int fb = 0;
+        if (fa >= K && fa <= cap) {
+            sec_ok = true;
+        } else {
+            if (fa > cap) {
+                sec_lo = ka;
+                fl = fa;
+            } else {
+                sec_hi = ka;
+                fh = fa;
+                kb = sec_lo;
+                fb = fl;
+            }
+            for (int it = 0; it < kMaxSecant && !sec_ok; ++it) {
+                if (sec_hi - sec_lo <= 1u) break;   // no admissible threshold: ties straddle [K, C]
+                const float ta = float_of_key(ka), tb = float_of_key(kb);
+                float t = ta + (float)(fa - f_target) * (tb - ta) / (float)(fa - fb);
+                if (it == 0) {   // damping: at most half the bracket away from the last probe
+                    const float half = 0.5f * (float_of_key(sec_hi) - float_of_key(sec_lo));
+                    t = fminf(fmaxf(t, ta - half), ta + half);
+                }
+                uint32_t kn = key_of(t);
+                if (!(t == t) || kn <= sec_lo || kn >= sec_hi) kn = sec_lo + (sec_hi - sec_lo) / 2u;   // bisect
+                const int fn = count_ge(kn, false);
+                kb = ka;
+                fb = fa;
+                ka = kn;
+                fa = fn;
+                if (fn >= K && fn <= cap) {
+                    sec_ok = true;
+                } else if (fn > cap) {
+                    sec_lo = kn;
+                    fl = fn;
+                } else {
+                    sec_hi = kn;
+                    fh = fn;
+                }
+            }
+        }
+        (void)fl;
+        (void)fh;
+        if (sec_ok) {
+            // Phase 3: collect every key >= T at per-wave offsets from the
+            // last pass's per-wave counts (sm.wa), in index order.
+            T = ka;
+            cands = fa;
+            const int off = sum_over_waves_below(sm.wa, lane, wave);
+            const int mine = sm.wa[wave];
+            __syncthreads();
+            if (lane == 0) {
+                sm.seg_off[wave] = off;
+                sm.seg_cnt[wave] = mine;
+            }
+            uint2* lc = sm.list + off;
+            int run = 0;
+            stream_wave(xa, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
+                uint32_t k[4];
+                block_keys(v, k);
+                const int e0 = 4 * q - aoff;
+                bool f[4];
+                uint64_t m[4];
+                const bool edge = (4 * qs - aoff < 0 || 4 * qs + 255 - aoff >= n);
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    f[c] = k[c] >= T && (!edge || (e0 + c >= 0 && e0 + c < n));
+                    m[c] = __ballot(f[c]);
+                }
+                int pos = run + (int)lanes_below(m[3], lanes_below(m[2], lanes_below(m[1], lanes_below(m[0], 0))));
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    if (f[c]) {
+                        if (pos < mine) lc[pos] = make_uint2(k[c], (uint32_t)(e0 + c));
+                        ++pos;
+                    }
+                }
+                run += __popcll(m[0]) + __popcll(m[1]) + __popcll(m[2]) + __popcll(m[3]);
+            });
+            ++passes;
+            __syncthreads();
+        }
+    }
+
+    if (secant && sec_ok) {
+        // The collected lists hold every key >= T with K <= f(T) <= C (Lemma 1).
+        path = GVR_PATH_SECANT;
+        done_lists = true;
+        rlo = T;
+        rhi = 0xFFFFFFFFu;
+        bin_hi = max(row_max, T);
+        above = 0;
+    } else if (spec && !overflow && f_spec >= K && f_spec <= cap) {
         // The speculative lists hold every key >= T_spec, hence the answer
         // (Lemma 1). The refine bins [T_spec, pmax] and puts the (few) keys
         // above pmax into its top bin.
@@ -1086,6 +1276,11 @@ DEV void topk_body(const Params& p) {
             rhi = bin_hi = wave_max_u(lane < kNW ? (uint32_t)sm.red[3][lane] : 0u);
         }
     } else {
+        if (secant) {
+            // The secant search gave up: narrow inside its counted bracket.
+            path = GVR_PATH_NARROWED;
+            win = make_window(sec_lo, sec_hi - 1u);
+        }
         if (spec) {
             // The guess fell short (or a wave's list overflowed): count passes
             // over the whole row around T_spec, whose f is known.
@@ -1288,7 +1483,7 @@ __global__ __launch_bounds__(kBlock) void radix_topk_kernel(Params p) { topk_bod
 // ------------------------------------------------------------------ host side
 
 gvr_status validate(const float* scores, int64_t B, int64_t ld, int32_t K, const int32_t* out,
-                    const gvr_options* opt, int* capacity, int* use_guess, int* parts, int* scatter) {
+                    const gvr_options* opt, int* capacity, int* use_guess, int* parts, int* scatter, int* secant) {
     if (K < 1 || K > GVR_MAX_K) return GVR_ERR_UNSUPPORTED_K;
     if (B < 0 || ld < 0) return GVR_ERR_INVALID_ARG;
     if (B > 0 && (!scores || !out)) return GVR_ERR_INVALID_ARG;
@@ -1299,10 +1494,11 @@ gvr_status validate(const float* scores, int64_t B, int64_t ld, int32_t K, const
             if (opt->capacity < K || opt->capacity > GVR_MAX_CANDIDATES) return GVR_ERR_INVALID_ARG;
             cap = opt->capacity;
         }
-        if ((opt->flags & ~3) || opt->reserved1) return GVR_ERR_INVALID_ARG;
+        if ((opt->flags & ~7) || opt->reserved1) return GVR_ERR_INVALID_ARG;
         if (opt->parts < 0 || opt->parts > kMaxParts) return GVR_ERR_INVALID_ARG;
         if (opt->flags & 1) *use_guess = 0;
         *scatter = (opt->flags >> 1) & 1;
+        *secant = (opt->flags >> 2) & 1;
         *parts = opt->parts;
     }
     *capacity = cap;
@@ -1401,8 +1597,8 @@ int choose_parts(int64_t rows, int64_t ld, int cus) {
 gvr_status run(const float* scores, int64_t B, int64_t ld, const int32_t* row_len, const int32_t* prev,
                int32_t K, int32_t* out, void* stream, const gvr_options* opt, gvr_row_stats* stats,
                int use_guess) {
-    int cap = 0, parts_opt = 0, scatter = 0;
-    gvr_status st = validate(scores, B, ld, K, out, opt, &cap, &use_guess, &parts_opt, &scatter);
+    int cap = 0, parts_opt = 0, scatter = 0, secant = 0;
+    gvr_status st = validate(scores, B, ld, K, out, opt, &cap, &use_guess, &parts_opt, &scatter, &secant);
     if (st != GVR_OK) return st;
     if (B == 0) return GVR_OK;
     const bool guess = use_guess && prev;
@@ -1412,6 +1608,7 @@ gvr_status run(const float* scores, int64_t B, int64_t ld, const int32_t* row_le
     // A forced split is capped at kMaxSlots (row, part) pairs per call, which
     // bounds the workspace (128 KB of list per pair).
     if (parts > 1 && (int64_t)parts * B > kMaxSlots) parts = (int)std::max<int64_t>(1, kMaxSlots / B);
+    if (secant) parts = 1;   // the secant search reads whole rows
     Workspace ws = {};
     if (parts > 1) {
         st = get_workspace(device, stream, (int)B, parts, &ws);
@@ -1435,6 +1632,7 @@ gvr_status run(const float* scores, int64_t B, int64_t ld, const int32_t* row_le
         q.parts = parts;
         q.chunk = (int32_t)(rows_pad / kXcds * parts);
         q.scatter = scatter;
+        q.secant = secant;
         q.arrivals = ws.arrivals;
         q.part_count = ws.part_count;
         q.part_thresh = ws.part_thresh;

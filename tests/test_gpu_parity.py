@@ -413,3 +413,31 @@ def test_poison_beyond_row_len_with_guess(parts):
         note("poison with guess %r parts=%d" % (float(poison), parts))
         out = _gvr_parts(torch.from_numpy(p).to(DEV), torch.from_numpy(rl).to(DEV), pv, K, parts)
         assert_rows_equal(out.cpu().numpy(), exp, "poison with guess %r parts=%d" % (float(poison), parts))
+
+
+@pytest.mark.parametrize("case", [(1, 4, 4, None), (2, 3, 4, None), (3, 2, 8, "a"), (3, 2, 8, "b"),
+                                  (3, 2, 8, "c"), (4, 2, 2, None)], ids=lambda c: "c%d%s" % (c[0], c[3] or ""))
+def test_secant_schedule_parity(case):
+    """The paper's own schedule (flag bit 2: T0 = pmean, secant counting
+    passes, a collect pass) gives the oracle's answer; when it accepts, the
+    threshold satisfies Lemma 1."""
+    import paper_2604_22312_amd as g
+
+    def secant(scores, row_len, prev, K, stats=None):
+        return g.gvr_topk_ex(scores, row_len, prev, K, options={"flags": 4}, stats=stats)
+    secant.__name__ = "gvr_secant"
+    cfg, steps, queries, sub = case
+    w, res = run_decode(secant, cfg, steps, queries, sub, dev=DEV, stats_check=True)
+    for i, st, kth, ngt in res:
+        s_host = w.scores[i].numpy()
+        rl = w.row_len[i].numpy()
+        for r in range(w.rows):
+            path = int(st["path"][r])
+            assert path != -1
+            if path == 6:
+                T = int(st["threshold"][r])
+                f = oracle.count_ge(s_host[r], T, n=int(rl[r]))
+                assert int(st["candidates"][r]) == f
+                assert K_TOPK <= f <= 16384
+            if int(rl[r]) > K_TOPK:
+                assert int(st["kth_key"][r]) == int(kth[r])
