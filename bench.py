@@ -42,13 +42,13 @@ def kernel_source_hash() -> str:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def build_inputs(dev):
+def build_inputs(dev, config=CONFIG, sub=None, steps=None):
     import torch
     import workloads
     import paper_2604_22312_amd as g
 
     t0 = time.time()
-    w = workloads.generate(CONFIG, device=dev)
+    w = workloads.generate(config, device=dev, sub=sub, steps=steps)
     torch.cuda.synchronize()
     log("generated %s: scores %s in %.1f s" % (w.name, tuple(w.scores.shape), time.time() - t0))
     rows, B, nn = w.rows, w.B, w.next_n
@@ -59,8 +59,11 @@ def build_inputs(dev):
     prevs = torch.empty((T, rows, K_TOPK), dtype=torch.int32, device=dev)
     g.gvr_topk(w.scores[0], w.row_len[0], None, K_TOPK, out_idx=outs[0])
     for t in range(1, T):
-        last = outs[t - 1].view(B, nn, K_TOPK)[:, nn - 1:nn, :]
-        prevs[t].copy_(last.expand(B, nn, K_TOPK).reshape(rows, K_TOPK))
+        if w.random_prev is not None:
+            prevs[t].copy_(w.random_prev[t])
+        else:
+            last = outs[t - 1].view(B, nn, K_TOPK)[:, nn - 1:nn, :]
+            prevs[t].copy_(last.expand(B, nn, K_TOPK).reshape(rows, K_TOPK))
         g.gvr_topk(w.scores[t], w.row_len[t], prevs[t], K_TOPK, out_idx=outs[t])
     torch.cuda.synchronize()
     return w, outs, prevs
@@ -145,6 +148,70 @@ def cpu_baseline(w, min_seconds=15.0, max_steps=8):
                       % (calls, len(host), w.rows, rows_done, threads, dt)}
 
 
+def time_graph(fn, w, prevs, reps, out):
+    """GPU time per call without host launch overhead: the calls for steps
+    1..T-1 are captured once into a HIP graph (after an eager warm-up call per
+    step, which also sets up any workspace) and the graph is replayed."""
+    import torch
+
+    T = w.scores.shape[0]
+    stream = torch.cuda.Stream()
+    with torch.cuda.stream(stream):
+        for t in range(1, T):
+            fn(w.scores[t], w.row_len[t], prevs[t], K_TOPK, out_idx=out, stream=stream)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=stream):
+        for t in range(1, T):
+            fn(w.scores[t], w.row_len[t], prevs[t], K_TOPK, out_idx=out, stream=stream)
+    graph.replay()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        graph.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / 1e3 / (reps * (T - 1))
+
+
+def run_configs(args, dev):
+    """One JSON line per decode workload (configs 0-4, sub-cases of 3):
+    GPU us per call of gvr_topk, radix_topk and the paper's schedule, from a
+    replayed HIP graph of the calls for the workload's steps (at most 32
+    steps are generated), plus full-row passes per row."""
+    import torch
+    import workloads
+    import paper_2604_22312_amd as g
+
+    cases = [(0, None), (1, None), (2, None), (3, "a"), (3, "b"), (3, "c"), (3, "d"), (4, None)]
+    for cfg, sub in cases:
+        nsteps = min(workloads.CONFIGS[cfg]["steps"], 32)
+        w, outs, prevs = build_inputs(dev, cfg, sub, list(range(nsteps)))
+        T = w.scores.shape[0]
+        out = torch.empty((w.rows, K_TOPK), dtype=torch.int32, device=dev)
+        rl = w.row_len[1:].to(torch.int64).clamp(min=0)
+        alg = int((4 * rl + 12 * K_TOPK * (rl > K_TOPK)).sum()) // (T - 1)   # per call, averaged
+        opts = {"flags": 4}
+
+        def secant(scores, row_len, prev, K, out_idx=None, stream=None):
+            return g.gvr_topk_ex(scores, row_len, prev, K, out_idx=out_idx, stream=stream, options=opts)
+        line = {"workload": w.name, "rows": w.rows, "ld": w.ld, "steps": T - 1}
+        for name, fn in (("gvr_topk", g.gvr_topk), ("radix_topk", g.radix_topk), ("paper_schedule", secant)):
+            us = time_graph(fn, w, prevs, max(1, args.steps // (T - 1)), out) * 1e6
+            line[name + "_us"] = round(us, 3)
+            line[name + "_GBs"] = round(alg / (us * 1e-6) / 1e9, 1)
+        line["gvr_passes"] = pass_stats(g.gvr_topk_ex, w, prevs, radix=False)
+        line["paper_schedule_passes"] = pass_stats(g.gvr_topk_ex, w, prevs, radix=False, options=opts)
+        line["radix_passes"] = pass_stats(g.radix_topk_ex, w, prevs, radix=True)
+        line["speedup_vs_radix"] = round(line["radix_topk_us"] / line["gvr_topk_us"], 3)
+        print(json.dumps(line))
+        sys.stdout.flush()
+        del w, outs, prevs
+        torch.cuda.empty_cache()
+
+
 def read_traffic(n_launch_bytes):
     if not os.path.exists(TRAFFIC_FILE):
         return None
@@ -162,7 +229,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--mode", choices=["bench", "copy"], default="bench")
+    ap.add_argument("--mode", choices=["bench", "copy", "configs"], default="bench")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--no-radix", action="store_true", help="skip timing radix_topk")
     ap.add_argument("--no-secant", action="store_true",
@@ -187,6 +254,10 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"mode": "copy", "bytes_read_per_launch": 4 * n, "bytes_written_per_launch": 4 * n,
                           "launches": args.warmup + args.steps}))
+        return
+
+    if args.mode == "configs":
+        run_configs(args, dev)
         return
 
     w, outs, prevs = build_inputs(dev)
