@@ -70,6 +70,7 @@ constexpr int kRefBins = 4096;                 // bins of a narrowing refine lev
 constexpr int kRefBins1 = 2048;                // bins of the first refine level (32 per lane of one wave)
 constexpr int kGuessSamples = 256;             // guessed indices gathered: a strided sample of prev_topk
 constexpr int kGuessBins = 1024;               // bins of the gathered-key histogram (16 per lane of wave 0)
+static_assert(kRefBins1 + kGuessBins <= kRefBins, "guess histogram above the first refine level");
 constexpr int kSpecQuantile = 65;              // T_spec: gathered key of rank ceil(65 / 2048 * sample size)
 constexpr int kSmall = 64;                     // refine: K-th key's bin resolved by one wave up to this size
 constexpr int kMaxPasses = 8;                  // 2 + at most 4 narrowing passes + 1 final pass suffice
@@ -80,6 +81,9 @@ constexpr int kMaxSlots = 2048;                // (row, part) pairs of one split
 constexpr int kXcds = 8;                       // gfx950 XCDs; workgroup i runs on XCD i % 8
 
 static_assert(GVR_MAX_CANDIDATES % kNW == 0, "per-wave capacity");
+static_assert((kBins & (kBins - 1)) == 0 && (kRefBins & (kRefBins - 1)) == 0 && (kRefBins1 & (kRefBins1 - 1)) == 0 &&
+                  (kGuessBins & (kGuessBins - 1)) == 0, "bin counts are powers of two");
+static_assert(kNW * kSmall * 2 <= kRefBins, "refine slots over the histogram");
 
 struct Params {
     const float* scores;
@@ -191,6 +195,14 @@ DEV void lds_barrier() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
+// Smallest s with (2^lg_bins << s) >= width, for 1 <= width <= 2^32: bins of
+// 2^s keys from the window's low edge cover `width` keys.
+DEV uint32_t bin_shift(uint64_t width, int lg_bins) {
+    const int bits = 64 - __builtin_clzll(width - 1 | 1);   // bit length of width - 1 (>= 1)
+    return (uint32_t)max(0, (width <= 1 ? 0 : bits) - lg_bins);
+}
+constexpr int log2i(int v) { return v <= 1 ? 0 : 1 + log2i(v / 2); }
+
 // A window of key space: bins j < kBins cover [lo + j<<shift, lo + (j+1)<<shift);
 // bin kBins holds every key >= lo + kBins<<shift; keys below lo are not counted.
 struct Window {
@@ -199,8 +211,7 @@ struct Window {
 };
 DEV Window make_window(uint32_t a, uint32_t b) {   // covers [a, b], b >= a
     const uint64_t width = (uint64_t)b - a + 1;
-    uint32_t s = 0;
-    while (((uint64_t)kBins << s) < width) ++s;
+    const uint32_t s = bin_shift(width, log2i(kBins));
     return Window{a, s};
 }
 DEV uint64_t edge_of(const Window& w, int j) { return (uint64_t)w.lo + ((uint64_t)j << w.shift); }
@@ -213,7 +224,6 @@ struct Smem {
         int rhist[kRefBins];            // refine / guess histogram
     } u;
     int F[kBinsX + 1];                  // F[j] = f(edge j) over the row
-    uint2 dummy[kBlock];                // sink of the unconditional list stores
     int seg_off[kNW];                   // list segment of each wave
     int seg_cnt[kNW];
     int wa[kNW];
@@ -221,7 +231,6 @@ struct Smem {
     int red[4][kNW];
     float redf[kNW];
     int scal[8];
-    uint4 small[kSmall];                // refine: (key, index, wave) of the K-th key's bin
     int guess_ready;                    // set by wave 0 once T_spec is in scal[4..7]
 };
 
@@ -309,10 +318,9 @@ DEV uint32_t refine_kth(Smem& sm, uint32_t wlo, uint32_t whi, int above, int K, 
     int need = K - above;   // >= 1
     for (int level = 0; level < 4 && wlo != whi; ++level) {
         const uint64_t width = (uint64_t)whi - wlo + 1;
-        uint32_t s = 0;
-        while (((uint64_t)kRefBins << s) < width) ++s;
+        const uint32_t s = bin_shift(width, log2i(kRefBins));
         for (int i = tid; i < kRefBins; i += kBlock) sm.u.rhist[i] = 0;
-        __syncthreads();
+        lds_barrier();
         {
             const uint2* seg = sm.list + sm.seg_off[wave];
             const int cnt = sm.seg_cnt[wave];
@@ -323,7 +331,7 @@ DEV uint32_t refine_kth(Smem& sm, uint32_t wlo, uint32_t whi, int above, int K, 
                                            __HIP_MEMORY_SCOPE_WORKGROUP);
             }
         }
-        __syncthreads();
+        lds_barrier();
         constexpr int PER = kRefBins / kBlock;   // 4 bins per thread
         int loc[PER];
         int mine = 0;
@@ -336,7 +344,7 @@ DEV uint32_t refine_kth(Smem& sm, uint32_t wlo, uint32_t whi, int above, int K, 
         const int tot = block_excl_scan(a, sm, tid);
         int run = tot - a - mine;   // bins above this thread's range
         if (tid == 0) sm.scal[0] = -1;
-        __syncthreads();
+        lds_barrier();
 #pragma unroll
         for (int q = PER - 1; q >= 0; --q) {
             const int nr = run + loc[q];
@@ -346,10 +354,10 @@ DEV uint32_t refine_kth(Smem& sm, uint32_t wlo, uint32_t whi, int above, int K, 
             }
             run = nr;
         }
-        __syncthreads();
+        lds_barrier();
         const int b = sm.scal[0];
         const int ab = sm.scal[1];
-        __syncthreads();
+        lds_barrier();
         if (b < 0) break;   // cannot happen for consistent counts; keeps every path finite
         need -= ab;
         const uint64_t nlo = (uint64_t)wlo + ((uint64_t)b << s);
@@ -367,27 +375,32 @@ DEV uint32_t refine_kth(Smem& sm, uint32_t wlo, uint32_t whi, int above, int K, 
 DEV void emit_segment(const Smem& sm, uint32_t T, int K, int take, int gb, int eb, int32_t* out, int lane, int wave) {
     const uint2* seg = sm.list + sm.seg_off[wave];
     const int cnt = sm.seg_cnt[wave];
-    for (int i0 = 0; i0 < cnt; i0 += kWave) {
-        const int i = i0 + lane;
-        uint32_t kk = 0;
-        int idx = 0;
-        if (i < cnt) {
-            kk = seg[i].x;
-            idx = (int)seg[i].y;
+    for (int i0 = 0; i0 < cnt; i0 += 4 * kWave) {
+        uint2 en[4];   // four entries per lane read before any is written out
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int i = i0 + j * kWave + lane;
+            en[j] = i < cnt ? seg[i] : make_uint2(0u, 0u);
         }
-        const bool fg = i < cnt && kk > T;
-        const bool fe = i < cnt && kk == T;
-        const uint64_t mg = __ballot(fg), me = __ballot(fe);
-        const int g = gb + (int)lanes_below(mg, 0), e = eb + (int)lanes_below(me, 0);
-        if (fg) {
-            const int o = g + min(e, take);
-            if (o >= 0 && o < K) out[o] = idx;
-        } else if (fe && e < take) {
-            const int o = g + e;
-            if (o >= 0 && o < K) out[o] = idx;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int i = i0 + j * kWave + lane;
+            const uint32_t kk = en[j].x;
+            const int idx = (int)en[j].y;
+            const bool fg = i < cnt && kk > T;
+            const bool fe = i < cnt && kk == T;
+            const uint64_t mg = __ballot(fg), me = __ballot(fe);
+            const int g = gb + (int)lanes_below(mg, 0), e = eb + (int)lanes_below(me, 0);
+            if (fg) {
+                const int o = g + min(e, take);
+                if (o >= 0 && o < K) out[o] = idx;
+            } else if (fe && e < take) {
+                const int o = g + e;
+                if (o >= 0 && o < K) out[o] = idx;
+            }
+            gb += __popcll(mg);
+            eb += __popcll(me);
         }
-        gb += __popcll(mg);
-        eb += __popcll(me);
     }
 }
 
@@ -409,7 +422,7 @@ DEV void emit_from_lists(Smem& sm, uint32_t T, int K, int32_t* out, int tid, int
         sm.wa[wave] = gt;
         sm.wb[wave] = eq;
     }
-    __syncthreads();
+    lds_barrier();
     const int gb = sum_over_waves_below(sm.wa, lane, wave);
     const int eb = sum_over_waves_below(sm.wb, lane, wave);
     const int gtot = sum_over_waves(sm.wa, lane);
@@ -421,8 +434,7 @@ DEV void emit_from_lists(Smem& sm, uint32_t T, int K, int32_t* out, int tid, int
 // rlo + (kRefBins1 - 1) << sh share the top bin.
 DEV uint32_t ref_shift(uint32_t rlo, uint32_t bin_hi) {
     const uint64_t width = (uint64_t)bin_hi - rlo + 1;
-    uint32_t sh = 0;
-    while (((uint64_t)kRefBins1 << sh) < width) ++sh;
+    const uint32_t sh = bin_shift(width, log2i(kRefBins1));
     return sh;
 }
 DEV int ref_bin(uint32_t kk, uint32_t rlo, uint32_t sh) { return (int)min((kk - rlo) >> sh, (uint32_t)kRefBins1 - 1); }
@@ -430,15 +442,38 @@ DEV void ref_hist_add(Smem& sm, uint32_t kk, uint32_t rlo, uint32_t sh) {
     __hip_atomic_fetch_add(&sm.u.rhist[ref_bin(kk, rlo, sh)], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 
+// One wave: turn the fp32 bit patterns of its list segment seg[0, cnt) into
+// keys in place and, if `hist`, add them to the first refine level from rlo.
+// Four entries per lane are read before any is written back.
+DEV void keys_in_place(Smem& sm, uint2* seg, int cnt, bool hist, uint32_t rlo, uint32_t sh, int lane) {
+    for (int i0 = 0; i0 < cnt; i0 += 4 * kWave) {
+        uint32_t b[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int i = i0 + j * kWave + lane;
+            b[j] = i < cnt ? seg[i].x : 0u;
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int i = i0 + j * kWave + lane;
+            if (i < cnt) {
+                const uint32_t kk = key_of_bits(b[j]);
+                seg[i].x = kk;
+                if (hist) ref_hist_add(sm, kk, rlo, sh);
+            }
+        }
+    }
+}
+
 // Exact K-th key T* among the listed candidates and the emission. The K-th
 // key lies in [rlo, rhi]; `above` listed keys lie above rhi. One histogram
 // level of kRefBins1 bins over [rlo, bin_hi] (keys in (bin_hi, rhi] count in
 // the top bin; built here unless `hist_ready`), then wave 0 finds the
 // bin b holding the K-th key with two wave scans. If b holds at most kSmall
-// candidates, the waves copy them (with their wave) to LDS and count the
-// keys above b; wave 0 ranks them to get T* and the per-wave emission
-// offsets, and every wave emits its segment. Otherwise histogram narrowing
-// (refine_kth) continues inside b.
+// candidates, each wave copies its share to its own LDS slots and counts its
+// keys above b; wave 0 takes one candidate per lane, selects T* among them
+// and the per-wave emission offsets, and every wave emits its segment.
+// Otherwise histogram narrowing (refine_kth) continues inside b.
 DEV uint32_t refine_emit(Smem& sm, uint32_t rlo, uint32_t rhi, uint32_t bin_hi, int above, int K, int32_t* out,
                          int tid, int* n_gt_out, bool hist_ready) {
     const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -449,13 +484,13 @@ DEV uint32_t refine_emit(Smem& sm, uint32_t rlo, uint32_t rhi, uint32_t bin_hi, 
     if (tid == 0) sm.scal[1] = 0;
     if (!hist_ready) {
         for (int i = tid; i < kRefBins1; i += kBlock) hb[i] = 0;
-        __syncthreads();
+        lds_barrier();
         for (int i = lane; i < cnt; i += kWave) {
             const uint32_t kk = seg[i].x;
             if (kk >= rlo && kk <= rhi) ref_hist_add(sm, kk, rlo, sh);
         }
     }
-    __syncthreads();
+    lds_barrier();
     const int need0 = K - above;   // >= 1: rank of T* among the keys in [rlo, rhi], from the top
     if (wave == 0) {
         // lane l owns bins [32 l, 32 l + 32)
@@ -484,7 +519,7 @@ DEV uint32_t refine_emit(Smem& sm, uint32_t rlo, uint32_t rhi, uint32_t bin_hi, 
             sm.scal[3] = __builtin_amdgcn_readlane(hj, J);
         }
     }
-    __syncthreads();
+    lds_barrier();
     const int b = sm.scal[0];
     const int above_b = sm.scal[2];   // listed keys above bin b
     const int cnt_b = sm.scal[3];
@@ -497,63 +532,69 @@ DEV uint32_t refine_emit(Smem& sm, uint32_t rlo, uint32_t rhi, uint32_t bin_hi, 
         return lo_b;
     }
     if (cnt_b > kSmall) {
-        __syncthreads();
+        lds_barrier();
         const uint32_t kth = refine_kth(sm, lo_b, hi_b, above_b, K, tid);
         emit_from_lists(sm, kth, K, out, tid, n_gt_out);
         return kth;
     }
-    // Copy bin b's candidates; count this segment's keys above the bin.
-    int gt_hi = 0;
-    for (int i0 = 0; i0 < cnt; i0 += kWave) {
-        const int i = i0 + lane;
-        const bool valid = i < cnt;
-        const uint2 e = valid ? seg[i] : make_uint2(0u, 0u);
-        gt_hi += valid && e.x > hi_b;
-        const bool inb = valid && e.x >= lo_b && e.x <= hi_b;
-        const uint64_t m = __ballot(inb);
-        if (m) {
-            const int first = (int)__builtin_ctzll(m);
-            int base = 0;
-            if (lane == first)
-                base = __hip_atomic_fetch_add(&sm.scal[1], (int)__popcll(m), __ATOMIC_RELAXED,
-                                              __HIP_MEMORY_SCOPE_WORKGROUP);
-            base = __builtin_amdgcn_readlane(base, first);
-            const int pos = base + (int)lanes_below(m, 0);
-            if (inb && pos < kSmall) sm.small[pos] = make_uint4(e.x, e.y, (uint32_t)wave, 0u);
+    // Copy bin b's candidates to this wave's slots (over the histogram, no
+    // longer needed: at most kSmall candidates in all, so at most kSmall per
+    // wave) in list order, and count this segment's keys above the bin.
+    uint2* const slots = reinterpret_cast<uint2*>(sm.u.rhist);   // [kNW][kSmall]
+    int gt_hi = 0, nin = 0;
+    for (int i0 = 0; i0 < cnt; i0 += 4 * kWave) {
+        uint2 en[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int i = i0 + j * kWave + lane;
+            en[j] = i < cnt ? seg[i] : make_uint2(0u, 0u);
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const bool valid = i0 + j * kWave + lane < cnt;
+            gt_hi += valid && en[j].x > hi_b;
+            const bool inb = valid && en[j].x >= lo_b && en[j].x <= hi_b;
+            const uint64_t m = __ballot(inb);
+            const int pos = nin + (int)lanes_below(m, 0);
+            if (inb && pos < kSmall) slots[wave * kSmall + pos] = en[j];
+            nin += (int)__popcll(m);
         }
     }
     gt_hi = wave_sum(gt_hi);
     if (lane == 0) {
         sm.wa[wave] = gt_hi;
-        sm.wb[wave] = 0;
+        sm.wb[wave] = min(nin, kSmall);
     }
-    __syncthreads();
+    lds_barrier();
     if (wave == 0) {
-        // One lane per candidate of bin b: T* is the need-th largest of
-        // them, found by a radix select over the offsets key - lo_b (MSB
-        // first, one ballot per bit).
-        const int need = K - above_b;   // rank of T* inside the bin, from the top
+        // Lane l takes the l-th candidate of bin b (wave order = list order).
+        const int nw = lane < kNW ? sm.wb[lane] : 0;
+        const int pin = wave_incl_scan(nw, lane);   // candidates of waves <= lane
+        const int pex = pin - nw;
+        int wv = 0;
+#pragma unroll
+        for (int v = 0; v < kNW - 1; ++v) wv += lane >= __builtin_amdgcn_readlane(pin, v);
+        const int wbase = __shfl(pex, wv);
         const bool v = lane < cnt_b;
-        const uint4 mine = v ? sm.small[lane] : make_uint4(0u, 0u, 0u, 0u);
-        const uint32_t off = mine.x - lo_b;
-        const int nbits = 32 - __builtin_clz(hi_b - lo_b);   // hi_b > lo_b here
-        uint32_t prefix = 0u;
-        int r = need;
-        for (int bit = nbits - 1; bit >= 0; --bit) {
-            const uint32_t cand = prefix | (1u << bit);
-            const int c1 = (int)__popcll(__ballot(v && (off >> bit) == (cand >> bit)));
-            if (c1 >= r) prefix = cand;
-            else r -= c1;
+        const uint2 mine = v ? slots[wv * kSmall + (lane - wbase)] : make_uint2(0u, 0u);
+        // T* is the need-th largest of them: the key of a lane with fewer
+        // than `need` keys above it and at least `need` at or above it
+        // (every lane compares its key with each candidate's).
+        const int need = K - above_b;   // rank of T* inside the bin, from the top
+        int gt = 0, ge = 0;
+        for (int j = 0; j < cnt_b; ++j) {
+            const uint32_t kj = __builtin_amdgcn_readlane(mine.x, j);
+            gt += kj > mine.x;
+            ge += kj >= mine.x;
         }
-        const uint32_t kth = lo_b + prefix;
-        // Per-wave keys > T* and == T*: the bin's candidates add themselves
-        // to their wave's counts (keys above the bin are in sm.wa already).
-        if (v && mine.x > kth)
-            __hip_atomic_fetch_add(&sm.wa[mine.z], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-        if (v && mine.x == kth)
-            __hip_atomic_fetch_add(&sm.wb[mine.z], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-        const int gw = lane < kNW ? sm.wa[lane] : 0;
-        const int ew = lane < kNW ? sm.wb[lane] : 0;
+        const uint64_t hitk = __ballot(v && gt < need && ge >= need);
+        const uint32_t kth = __builtin_amdgcn_readlane(mine.x, hitk ? (int)__builtin_ctzll(hitk) : 0);
+        // Per wave: keys > T* (above the bin, plus the bin's) and == T*;
+        // lane w < kNW owns wave w, whose candidates are lanes [pex, pin).
+        const uint64_t mgt = __ballot(v && mine.x > kth), meq = __ballot(v && mine.x == kth);
+        const uint64_t rng = (nw == 0) ? 0ull : ((nw >= 64 ? ~0ull : ((1ull << nw) - 1ull)) << pex);
+        const int gw = lane < kNW ? sm.wa[lane] + (int)__popcll(mgt & rng) : 0;
+        const int ew = lane < kNW ? (int)__popcll(meq & rng) : 0;
         const int gi = wave_incl_scan(gw, lane), ei = wave_incl_scan(ew, lane);
         const int gtot = __builtin_amdgcn_readlane(gi, 63);
         if (lane < kNW) {
@@ -565,7 +606,7 @@ DEV uint32_t refine_emit(Smem& sm, uint32_t rlo, uint32_t rhi, uint32_t bin_hi, 
             sm.scal[2] = gtot;
         }
     }
-    __syncthreads();
+    lds_barrier();
     const uint32_t kth = (uint32_t)sm.scal[0];
     const int gtot = sm.scal[2];
     emit_segment(sm, kth, K, K - gtot, sm.red[0][wave], sm.red[1][wave], out, lane, wave);
@@ -698,15 +739,17 @@ DEV void topk_body(const Params& p) {
             if (tid == 0) sm.guess_ready = 0;
             lds_barrier();
         }
-        // The part's first slabs (refills past the wave's share re-read one
-        // 16-byte block of the row: qdup). Issuing them can stall on a full
+        // The part's first slabs (refills past the wave's share re-read its
+        // last slab, just fetched: qtail). Issuing them can stall on a full
         // memory pipeline, so the streaming waves do not meet wave 0 at a
         // barrier afterwards: they poll the guess_ready flag right before
         // their first slab.
-        const int qdup = min(sqb, qlast);
+        const int qtail = min(sqb + max(nsl - 1, 0) * 64 + lane, qlast);
         float4 buf[kSU];
+        if (nsl > 0) {
 #pragma unroll
-        for (int u = 0; u < kSU; ++u) buf[u] = xa[(u < nsl) ? min(sqb + u * 64 + lane, qlast) : qdup];
+            for (int u = 0; u < kSU; ++u) buf[u] = xa[(u < nsl) ? min(sqb + u * 64 + lane, qlast) : qtail];
+        }
 
         if (all_mode) {
             tspec = 0u;
@@ -740,19 +783,20 @@ DEV void topk_body(const Params& p) {
                 cnt = wave_sum(cnt);
                 mn = wave_min_u(mn);
                 mx = wave_max_u(mx);
-                sum = wave_sum_f(sum);
+                if (p.stats) sum = wave_sum_f(sum);   // pmean is only reported
                 uint32_t ts = 0xFFFFFFFFu;
                 if (cnt > 0) {
                     const uint64_t width = (uint64_t)mx - mn + 1;
-                    uint32_t sh = 0;
-                    while (((uint64_t)kGuessBins << sh) < width) ++sh;
-                    int4* h4 = reinterpret_cast<int4*>(sm.u.rhist) + lane * 4;   // lane owns 16 bins
+                    const uint32_t sh = bin_shift(width, log2i(kGuessBins));
+                    // (above the refine's first level, which stays free)
+                    int* gh = sm.u.rhist + kRefBins1;
+                    int4* h4 = reinterpret_cast<int4*>(gh) + lane * 4;   // lane owns 16 bins
 #pragma unroll
                     for (int j = 0; j < 4; ++j) h4[j] = make_int4(0, 0, 0, 0);
 #pragma unroll
                     for (int c = 0; c < 4; ++c)
                         if (ok[c])
-                            __hip_atomic_fetch_add(&sm.u.rhist[(gk[c] - mn) >> sh], 1, __ATOMIC_RELAXED,
+                            __hip_atomic_fetch_add(&gh[(gk[c] - mn) >> sh], 1, __ATOMIC_RELAXED,
                                                    __HIP_MEMORY_SCOPE_WORKGROUP);
                     int h[16];
                     int s16 = 0;
@@ -779,6 +823,11 @@ DEV void topk_body(const Params& p) {
                     jsel = __builtin_amdgcn_readlane(jsel, L);
                     ts = mn + ((uint32_t)(L * 16 + jsel) << sh);
                 }
+                if (S == 1) {   // the refine's first level, filled after the pass
+                    int4* r4 = reinterpret_cast<int4*>(sm.u.rhist) + lane * (kRefBins1 / 4 / kWave);
+#pragma unroll
+                    for (int j = 0; j < kRefBins1 / 4 / kWave; ++j) r4[j] = make_int4(0, 0, 0, 0);
+                }
                 if (lane == 0) {
                     sm.scal[4] = (int)ts;
                     sm.scal[5] = cnt;
@@ -792,31 +841,20 @@ DEV void topk_body(const Params& p) {
         }
 
         // ---------------- (a3)+(a4) speculative pass over the part's slabs:
-        // count and append every (key, index) at or above T_spec.
+        // count and append every (fp32 bits, index) at or above T_spec.
         //
-        // The pass keeps fp32 bit patterns (turned into keys afterwards) and
-        // tests them with one compare (one xor more for thresholds <= -0).
-        // Thresholds are >= key 1, so the key-0 pattern never passes: elements
-        // outside [0, n) in the row's two edge slabs are replaced by it (a
-        // wave-uniform branch; interior slabs carry no range test). Lanes
-        // whose element is not kept write to a private dummy slot, so the
-        // stores of a slab need no exec-mask changes; one capacity check per
-        // slab (wave-uniform).
+        // The test runs on the raw bits (spec_keep): one signed compare, plus
+        // one xor for thresholds <= -0; the two forms are two copies of the
+        // loop, chosen once. Thresholds are >= key 1, so the key-0 pattern
+        // never passes: elements outside [0, n) in the row's two edge slabs
+        // are replaced by it (a wave-uniform branch; interior slabs carry no
+        // range test). A slab whose elements all fail costs the compares and
+        // one branch. Otherwise each lane appends its kept elements at its
+        // rank (kept elements of the lanes below, then its own in order), so
+        // every list stays in index order; one capacity check per slab
+        // (wave-uniform), and a wave whose list would overflow keeps counting.
         int cnt_w = 0;
         uint2* lw = sm.list + wave * kCapW;
-        uint2* const dummy = sm.dummy + tid;
-        auto slab_bits = [&](const float4& v, int qs, uint32_t (&k)[4]) {
-            const int e0 = 4 * (qs + lane) - aoff;
-            k[0] = __float_as_uint(v.x);
-            k[1] = __float_as_uint(v.y);
-            k[2] = __float_as_uint(v.z);
-            k[3] = __float_as_uint(v.w);
-            if (4 * qs - aoff < 0 || 4 * qs + 255 - aoff >= n) {   // edge slab (wave-uniform)
-#pragma unroll
-                for (int c = 0; c < 4; ++c)
-                    if ((uint32_t)(e0 + c) >= (uint32_t)n) k[c] = kKeyZeroBits;
-            }
-        };
         // The streaming waves wait for T_spec here, with their first slabs in
         // flight (polling an LDS flag, not a barrier: issuing those loads may
         // stall a wave, which must not hold up wave 0).
@@ -834,76 +872,66 @@ DEV void topk_body(const Params& p) {
         t1 = stamp();
         tspec = max(tspec, 1u);
         const SpecTest test = make_spec_test(tspec);
-        for (int s0 = 0; s0 < nsl; s0 += kSU) {
+        auto spec_pass = [&](auto flip_tag) {
+            constexpr uint32_t kFlip = decltype(flip_tag)::value ? 0x7FFFFFFFu : 0u;
+            for (int s0 = 0; s0 < nsl; s0 += kSU) {
 #pragma unroll
-            for (int u = 0; u < kSU; ++u) {
-                const int s = s0 + u;
-                if (s < nsl) {
-                    const int qs = sqb + s * 64;
-                    const int e0 = 4 * (qs + lane) - aoff;
-                    uint32_t k[4];
-                    slab_bits(buf[u], qs, k);
-                    bool f[4];
+                for (int u = 0; u < kSU; ++u) {
+                    const int s = s0 + u;
+                    if (s < nsl) {
+                        const int qs = sqb + s * 64;
+                        uint32_t k[4] = {__float_as_uint(buf[u].x), __float_as_uint(buf[u].y),
+                                         __float_as_uint(buf[u].z), __float_as_uint(buf[u].w)};
+                        const int e0 = 4 * (qs + lane) - aoff;
+                        if (4 * qs - aoff < 0 || 4 * qs + 255 - aoff >= n) {   // edge slab (wave-uniform)
 #pragma unroll
-                    for (int c = 0; c < 4; ++c) f[c] = spec_keep(k[c], test);
-                    const uint64_t m0 = __ballot(f[0]), m1 = __ballot(f[1]), m2 = __ballot(f[2]), m3 = __ballot(f[3]);
-                    const int total = __popcll(m0) + __popcll(m1) + __popcll(m2) + __popcll(m3);
-                    cnt_w = __builtin_amdgcn_readfirstlane(cnt_w);
-                    if (cnt_w + total <= kCapW) {
-                        int q = cnt_w + (int)lanes_below(m3, lanes_below(m2, lanes_below(m1, lanes_below(m0, 0))));
-#pragma unroll
-                        for (int c = 0; c < 4; ++c) {
-                            *(f[c] ? lw + q : dummy) = make_uint2(k[c], (uint32_t)(e0 + c));
-                            q += f[c];
+                            for (int c = 0; c < 4; ++c)
+                                if ((uint32_t)(e0 + c) >= (uint32_t)n) k[c] = kKeyZeroBits;
                         }
+                        bool f[4];
+#pragma unroll
+                        for (int c = 0; c < 4; ++c) f[c] = (int32_t)(k[c] ^ kFlip) >= test.bound;
+                        const uint64_t m0 = __ballot(f[0]), m1 = __ballot(f[1]), m2 = __ballot(f[2]),
+                                       m3 = __ballot(f[3]);
+                        const int total = __popcll(m0) + __popcll(m1) + __popcll(m2) + __popcll(m3);
+                        cnt_w = __builtin_amdgcn_readfirstlane(cnt_w);
+                        if (total != 0 && cnt_w + total <= kCapW) {
+                            int q = cnt_w + (int)lanes_below(m3, lanes_below(m2, lanes_below(m1, lanes_below(m0, 0))));
+#pragma unroll
+                            for (int c = 0; c < 4; ++c) {
+                                if (f[c]) lw[q] = make_uint2(k[c], (uint32_t)(e0 + c));
+                                q += f[c];
+                            }
+                        }
+                        cnt_w += total;   // counted past capacity: the overflow is detected below
                     }
-                    cnt_w += total;   // counted past capacity: the overflow is detected later
+                    const int sr = s + kSU;
+                    buf[u] = xa[(sr < nsl) ? min(sqb + sr * 64 + lane, qlast) : qtail];
                 }
-                const int sr = s + kSU;
-                buf[u] = xa[(sr < nsl) ? min(sqb + sr * 64 + lane, qlast) : qdup];
             }
+        };
+        if (test.flip)
+            spec_pass(std::true_type{});
+        else
+            spec_pass(std::false_type{});
+
+        // Every wave turns its list into keys in place and, for a whole row,
+        // adds them to the refine's first histogram level over
+        // [T_spec, max(pmax, T_spec)] (cleared by wave 0 before its flag):
+        // waves done with their slabs do this while the others still stream.
+        const bool own_hist = S == 1 && !all_mode;
+        if (cnt_w <= kCapW) keys_in_place(sm, lw, cnt_w, own_hist, tspec, ref_shift(tspec, max(gmax, tspec)), lane);
+        if (lane == 0) {
+            sm.wa[wave] = cnt_w;
+            sm.seg_cnt[wave] = min(cnt_w, kCapW);
         }
-        // Clear the refine's first histogram level (wave 0 is done with the
-        // guess histogram once its flag is set); filled by the count below.
-        for (int i = tid; i < kRefBins1; i += kBlock) sm.u.rhist[i] = 0;
         passes = 1;
         t2 = stamp();
-        if (lane == 0) {
-            sm.seg_cnt[wave] = min(cnt_w, kCapW);
-            sm.wa[wave] = cnt_w;
-        }
         lds_barrier();
         overflow = wave_max_u(lane < kNW ? (uint32_t)sm.wa[lane] : 0u) > (uint32_t)kCapW;
-        // Every wave turns its list into keys and, for a whole row, adds them
-        // to the refine's first histogram level: f(T_spec) = the list sizes.
-        const uint32_t teff = tspec;
-        hist_ready = S == 1 && !all_mode && !overflow;
-        const uint32_t rsh = ref_shift(teff, max(gmax, teff));
-        int fw = 0;
-        if (!overflow) {
-            uint2* seg = sm.list + wave * kCapW;
-            const int cnt = sm.seg_cnt[wave];
-            for (int i0 = 0; i0 < cnt; i0 += kWave) {
-                const int i = i0 + lane;
-                uint2 e = i < cnt ? seg[i] : make_uint2(0u, 0u);
-                e.x = key_of_bits(e.x);
-                const bool keep = i < cnt && e.x >= teff;
-                const uint64_t m = __ballot(keep);
-                if (keep) {
-                    seg[fw + (int)lanes_below(m, 0)] = e;
-                    if (hist_ready) ref_hist_add(sm, e.x, teff, rsh);
-                }
-                fw += (int)__popcll(m);
-            }
-        }
-        lds_barrier();   // every wave has read sm.wa / sm.wb and added to the histogram
-        if (lane == 0) {
-            sm.wb[wave] = fw;
-            sm.seg_cnt[wave] = fw;
-        }
-        lds_barrier();
-        f_spec = overflow ? -1 : sum_over_waves(sm.wb, lane);
-        tthr = teff;
+        f_spec = overflow ? -1 : sum_over_waves(sm.wa, lane);
+        hist_ready = own_hist && !overflow;
+        tthr = tspec;
 
         if (S > 1) {
             // ---------------- publish this part; the last part of the row goes on.
@@ -913,17 +941,29 @@ DEV void topk_body(const Params& p) {
             // last part reads them back from it. The arrival word, updated by
             // a device-scope atomic, also counts the parts per XCD (5 bits per
             // XCD above 16 bits of arrivals): the last part uses the lists
-            // only if every part ran on its own XCD, and otherwise reads the
+            // only if every part ran on its XCD, and otherwise reads the
             // whole row itself. A plain load by the last part cannot hit a
             // stale vector-L1 line: this workgroup never read those lines
             // before, and each launch starts with invalidated L1s.
             uint64_t* plist = p.part_list + (row * S + part) * (int64_t)kCap;
             const bool publish = !overflow && f_spec <= cap;
             if (publish) {   // this part's entries, in index order
-                const int off = sum_over_waves_below(sm.wb, lane, wave);
+                const int off = sum_over_waves_below(sm.wa, lane, wave);
                 const uint2* seg = sm.list + wave * kCapW;
                 const int cnt = sm.seg_cnt[wave];
-                for (int i = lane; i < cnt; i += kWave) plist[off + i] = pack_entry(seg[i].x, seg[i].y);
+                for (int i0 = 0; i0 < cnt; i0 += 4 * kWave) {
+                    uint2 e[4];
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const int i = i0 + j * kWave + lane;
+                        e[j] = i < cnt ? seg[i] : make_uint2(0u, 0u);
+                    }
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const int i = i0 + j * kWave + lane;
+                        if (i < cnt) plist[off + i] = pack_entry(e[j].x, e[j].y);
+                    }
+                }
             }
             if (tid == 0) {
                 p.part_count[row * S + part] = (int32_t)((uint32_t)max(f_spec, 0) | (overflow ? 0x80000000u : 0u));
@@ -948,8 +988,10 @@ DEV void topk_body(const Params& p) {
                 overflow = true;   // lists unusable: the fallback reads the whole row
                 f_spec = -1;
             } else {
-                // Row threshold (the largest of the parts'), totals and part
-                // offsets of the merged list (parts in index order).
+                // Totals and part offsets of the merged list (parts in index
+                // order). Every part computes the same T_spec from the same
+                // data; a part that kept another threshold (or overflowed)
+                // sends the row to the fallback.
                 const int c = lane < S ? p.part_count[row * S + lane] : 0;
                 const uint32_t tp = lane < S ? p.part_thresh[row * S + lane] : 0u;
                 const bool ovf = wave_max_u(lane < S && c < 0 ? 1u : 0u) != 0u;
@@ -957,26 +999,43 @@ DEV void topk_body(const Params& p) {
                 const bool mixed = wave_min_u(lane < S ? tp : 0xFFFFFFFFu) != trow;
                 const int cc = c & 0x7FFFFFFF;
                 f_spec = wave_sum(cc);
-                overflow = ovf;
+                overflow = ovf || mixed;
                 tthr = trow;
                 const int coff = wave_incl_scan(cc, lane) - cc;
-                __syncthreads();   // everyone has read sm.wa / sm.wb / sm.seg_cnt of this part
-                if (wave == 0 && lane < S) {
-                    sm.red[0][lane] = cc;
-                    sm.red[1][lane] = coff;
-                }
-                __syncthreads();
                 if (!overflow && f_spec >= K && f_spec <= cap) {
                     // Merged list in LDS, split evenly over the waves; the
                     // refine's first histogram level is built on the way.
+                    // Each thread owns merged positions tid + j * kBlock and
+                    // loads four of them (from their parts' lists) before it
+                    // stores any.
                     const uint32_t msh = ref_shift(trow, max(gmax, trow));
-                    for (int q = 0; q < S; ++q) {
-                        const uint64_t* src = p.part_list + (row * S + q) * (int64_t)kCap;
-                        const int cq = sm.red[0][q], oq = sm.red[1][q];
-                        for (int i = tid; i < cq; i += kBlock) {
-                            const uint64_t e = src[i];
-                            sm.list[oq + i] = make_uint2((uint32_t)e, (uint32_t)(e >> 32));
-                            if ((uint32_t)e >= trow) ref_hist_add(sm, (uint32_t)e, trow, msh);
+                    for (int i = tid; i < kRefBins1; i += kBlock) sm.u.rhist[i] = 0;
+                    const int jn = (f_spec + kBlock - 1) / kBlock;
+                    for (int j0 = 0; j0 < jn; j0 += 4) {
+                        int qj[4] = {0, 0, 0, 0}, oj[4] = {0, 0, 0, 0};
+                        for (int q = 1; q < S; ++q) {
+                            const int bq = __builtin_amdgcn_readlane(coff, q);
+#pragma unroll
+                            for (int jj = 0; jj < 4; ++jj) {
+                                const bool past = tid + (j0 + jj) * kBlock >= bq;
+                                qj[jj] += past;
+                                oj[jj] = past ? bq : oj[jj];
+                            }
+                        }
+                        uint64_t e[4];
+#pragma unroll
+                        for (int jj = 0; jj < 4; ++jj) {
+                            const int P = tid + (j0 + jj) * kBlock;
+                            e[jj] = P < f_spec ? p.part_list[(row * S + qj[jj]) * (int64_t)kCap + (P - oj[jj])] : 0ull;
+                        }
+                        if (j0 == 0) lds_barrier();   // the histogram is cleared; the loads stay in flight
+#pragma unroll
+                        for (int jj = 0; jj < 4; ++jj) {
+                            const int P = tid + (j0 + jj) * kBlock;
+                            if (P < f_spec) {
+                                sm.list[P] = make_uint2((uint32_t)e[jj], (uint32_t)(e[jj] >> 32));
+                                ref_hist_add(sm, (uint32_t)e[jj], trow, msh);
+                            }
                         }
                     }
                     hist_ready = true;
@@ -986,20 +1045,8 @@ DEV void topk_body(const Params& p) {
                         sm.seg_off[tid] = o;
                         sm.seg_cnt[tid] = min(chunk, f_spec - o);
                     }
-                    __syncthreads();
-                    if (mixed) {   // parts kept different thresholds: count f(trow) itself
-                        int fw = 0;
-                        const uint2* seg = sm.list + sm.seg_off[wave];
-                        for (int i = lane; i < sm.seg_cnt[wave]; i += kWave) fw += seg[i].x >= trow;
-                        fw = wave_sum(fw);
-                        if (lane == 0) sm.wa[wave] = fw;
-                        __syncthreads();
-                        f_spec = sum_over_waves(sm.wa, lane);
-                    }
                 }
             }
-        } else {
-            __syncthreads();
         }
     }
 
@@ -1450,7 +1497,7 @@ DEV void topk_body(const Params& p) {
         }
         return;
     }
-    __syncthreads();
+    lds_barrier();
     t3 = stamp();
     // ---------------- (a5) refine the listed candidates and emit
     int ngt = 0;
