@@ -216,6 +216,33 @@ DEV Window make_window(uint32_t a, uint32_t b) {   // covers [a, b], b >= a
 }
 DEV uint64_t edge_of(const Window& w, int j) { return (uint64_t)w.lo + ((uint64_t)j << w.shift); }
 
+// Raw buffer resource over [base, base + bytes): 32-bit per-lane offsets.
+typedef __attribute__((ext_vector_type(4))) unsigned u32x4;
+constexpr int kBufWord3 = 0x00020000;   // 32-bit data format, no swizzle
+DEV __amdgpu_buffer_rsrc_t row_rsrc(const void* base, int bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, kBufWord3);
+}
+DEV float4 buf_load16(__amdgpu_buffer_rsrc_t r, int off) {
+    const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+    return make_float4(__uint_as_float(v.x), __uint_as_float(v.y), __uint_as_float(v.z), __uint_as_float(v.w));
+}
+// Byte offset of an LDS object (its address in the LDS aperture).
+DEV uint32_t lds_addr(const void* p) {
+    return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)p;
+}
+// Two dwords to LDS at a byte address: the pair's registers need not be
+// adjacent (no copies into a register pair).
+DEV void lds_store_pair(uint32_t addr, uint32_t a, uint32_t b) {
+    asm volatile("ds_write2_b32 %0, %1, %2 offset1:1" : : "v"(addr), "v"(a), "v"(b) : "memory");
+}
+// q + (this lane's bit of m): one add-with-carry taking the lane mask as carry-in.
+DEV int add_lane_bit(int q, uint64_t m) {
+    int r;
+    uint64_t carry_out;
+    asm volatile("v_addc_co_u32_e64 %0, %1, 0, %2, %3" : "=v"(r), "=&s"(carry_out) : "v"(q), "s"(m));
+    return r;
+}
+
 // ------------------------------------------------------------------ LDS
 struct Smem {
     uint2 list[kCap];                   // candidates (key, index), per-wave segments
@@ -376,27 +403,30 @@ DEV void emit_segment(const Smem& sm, uint32_t T, int K, int take, int gb, int e
     const uint2* seg = sm.list + sm.seg_off[wave];
     const int cnt = sm.seg_cnt[wave];
     for (int i0 = 0; i0 < cnt; i0 += 4 * kWave) {
+        const int rem = cnt - i0;
         uint2 en[4];   // four entries per lane read before any is written out
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int i = i0 + j * kWave + lane;
-            en[j] = i < cnt ? seg[i] : make_uint2(0u, 0u);
-        }
+        for (int j = 0; j < 4; ++j) en[j] = j * kWave + lane < rem ? seg[i0 + j * kWave + lane] : make_uint2(0u, 0u);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const int i = i0 + j * kWave + lane;
+            const bool valid = j * kWave + lane < rem;
             const uint32_t kk = en[j].x;
-            const int idx = (int)en[j].y;
-            const bool fg = i < cnt && kk > T;
-            const bool fe = i < cnt && kk == T;
+            const bool fg = valid && kk > T;
+            const bool fe = valid && kk == T;
             const uint64_t mg = __ballot(fg), me = __ballot(fe);
-            const int g = gb + (int)lanes_below(mg, 0), e = eb + (int)lanes_below(me, 0);
-            if (fg) {
-                const int o = g + min(e, take);
-                if (o >= 0 && o < K) out[o] = idx;
-            } else if (fe && e < take) {
-                const int o = g + e;
-                if (o >= 0 && o < K) out[o] = idx;
+            const int g = gb + (int)lanes_below(mg, 0);
+            if (me == 0) {   // no key == T here (wave-uniform): keys > T go after min(eb, take) ties
+                const int o = g + min(eb, take);
+                if (fg && o < K) out[o] = (int)en[j].y;
+            } else {
+                const int e = eb + (int)lanes_below(me, 0);
+                if (fg) {
+                    const int o = g + min(e, take);
+                    if (o >= 0 && o < K) out[o] = (int)en[j].y;
+                } else if (fe && e < take) {
+                    const int o = g + e;
+                    if (o >= 0 && o < K) out[o] = (int)en[j].y;
+                }
             }
             gb += __popcll(mg);
             eb += __popcll(me);
@@ -541,42 +571,47 @@ DEV uint32_t refine_emit(Smem& sm, uint32_t rlo, uint32_t rhi, uint32_t bin_hi, 
     // longer needed: at most kSmall candidates in all, so at most kSmall per
     // wave) in list order, and count this segment's keys above the bin.
     uint2* const slots = reinterpret_cast<uint2*>(sm.u.rhist);   // [kNW][kSmall]
-    int gt_hi = 0, nin = 0;
+    const uint32_t wid = hi_b - lo_b;
+    int gtl = 0, nin = 0;
     for (int i0 = 0; i0 < cnt; i0 += 4 * kWave) {
+        const int rem = cnt - i0;
         uint2 en[4];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int i = i0 + j * kWave + lane;
-            en[j] = i < cnt ? seg[i] : make_uint2(0u, 0u);
-        }
+        for (int j = 0; j < 4; ++j) en[j] = j * kWave + lane < rem ? seg[i0 + j * kWave + lane] : make_uint2(0u, 0u);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const bool valid = i0 + j * kWave + lane < cnt;
-            gt_hi += valid && en[j].x > hi_b;
-            const bool inb = valid && en[j].x >= lo_b && en[j].x <= hi_b;
+            const bool valid = j * kWave + lane < rem;
+            gtl = add_lane_bit(gtl, __ballot(valid && en[j].x > hi_b));
+            const bool inb = valid && en[j].x - lo_b <= wid;
             const uint64_t m = __ballot(inb);
-            const int pos = nin + (int)lanes_below(m, 0);
-            if (inb && pos < kSmall) slots[wave * kSmall + pos] = en[j];
-            nin += (int)__popcll(m);
+            if (m) {   // rare (wave-uniform)
+                const int pos = nin + (int)lanes_below(m, 0);
+                if (inb && pos < kSmall) slots[wave * kSmall + pos] = en[j];
+                nin += (int)__popcll(m);
+            }
         }
     }
-    gt_hi = wave_sum(gt_hi);
+    const int gt_hi = wave_sum(gtl);
     if (lane == 0) {
         sm.wa[wave] = gt_hi;
         sm.wb[wave] = min(nin, kSmall);
     }
     lds_barrier();
     if (wave == 0) {
-        // Lane l takes the l-th candidate of bin b (wave order = list order).
+        // Lane l takes the l-th candidate of bin b (wave order = list order):
+        // one masked read per wave that holds any.
         const int nw = lane < kNW ? sm.wb[lane] : 0;
         const int pin = wave_incl_scan(nw, lane);   // candidates of waves <= lane
         const int pex = pin - nw;
-        int wv = 0;
-#pragma unroll
-        for (int v = 0; v < kNW - 1; ++v) wv += lane >= __builtin_amdgcn_readlane(pin, v);
-        const int wbase = __shfl(pex, wv);
+        uint64_t nz = __ballot(nw > 0);
+        uint2 mine = make_uint2(0u, 0u);
+        while (nz) {
+            const int wv = (int)__builtin_ctzll(nz);
+            nz &= nz - 1;
+            const int base = __builtin_amdgcn_readlane(pex, wv), cw = __builtin_amdgcn_readlane(nw, wv);
+            if (lane >= base && lane < base + cw) mine = slots[wv * kSmall + (lane - base)];
+        }
         const bool v = lane < cnt_b;
-        const uint2 mine = v ? slots[wv * kSmall + (lane - wbase)] : make_uint2(0u, 0u);
         // T* is the need-th largest of them: the key of a lane with fewer
         // than `need` keys above it and at least `need` at or above it
         // (every lane compares its key with each candidate's).
@@ -739,16 +774,20 @@ DEV void topk_body(const Params& p) {
             if (tid == 0) sm.guess_ready = 0;
             lds_barrier();
         }
-        // The part's first slabs (refills past the wave's share re-read its
-        // last slab, just fetched: qtail). Issuing them can stall on a full
-        // memory pipeline, so the streaming waves do not meet wave 0 at a
-        // barrier afterwards: they poll the guess_ready flag right before
-        // their first slab.
-        const int qtail = min(sqb + max(nsl - 1, 0) * 64 + lane, qlast);
+        // The part's first slabs, by buffer loads over the row's float4
+        // blocks (lane offset clamped to the last block; refills past the
+        // wave's share re-read its last slab, just fetched). Issuing them can
+        // stall on a full memory pipeline, so the streaming waves do not meet
+        // wave 0 at a barrier afterwards: they poll the guess_ready flag right
+        // before their first slab.
+        const __amdgpu_buffer_rsrc_t rrow = row_rsrc(xa, nq * 16);
+        const int lane16 = lane * 16, qlast16 = qlast * 16;
+        const int off_last = (sqb + max(nsl - 1, 0) * 64) * 16;   // the wave's last slab
+        auto slab_load = [&](int s) { return buf_load16(rrow, min(lane16 + min((sqb + s * 64) * 16, off_last), qlast16)); };
         float4 buf[kSU];
         if (nsl > 0) {
 #pragma unroll
-            for (int u = 0; u < kSU; ++u) buf[u] = xa[(u < nsl) ? min(sqb + u * 64 + lane, qlast) : qtail];
+            for (int u = 0; u < kSU; ++u) buf[u] = slab_load(u);
         }
 
         if (all_mode) {
@@ -872,43 +911,75 @@ DEV void topk_body(const Params& p) {
         t1 = stamp();
         tspec = max(tspec, 1u);
         const SpecTest test = make_spec_test(tspec);
+        // Slab s of this wave is the row's slab sg = sqb / 64 + s; slabs
+        // [in_lo, in_hi) hold no element outside [0, n).
+        const int in_lo = aoff > 0 ? 1 : 0, in_hi = (n + aoff) >> 8;
+        const uint32_t lw_addr = lds_addr(lw);
+        const uint32_t dummy = lds_addr(sm.list) + 8 * lane;   // wave 0's segment: never streamed into
         auto spec_pass = [&](auto flip_tag) {
             constexpr uint32_t kFlip = decltype(flip_tag)::value ? 0x7FFFFFFFu : 0u;
-            for (int s0 = 0; s0 < nsl; s0 += kSU) {
+            // One slab. `room`: the list has room for a whole slab, so every
+            // lane stores each element (kept ones at their rank, the others
+            // to a private dummy slot) and the new count comes from the rank
+            // of lane 63; otherwise the exact count decides (the overflow is
+            // detected after the pass).
+            auto slab = [&](const float4& v, int s, bool room) {
+                const int sg = (sqb >> 6) + s;
+                const int e0 = 4 * lane - aoff + 256 * sg;
+                uint32_t k[4] = {__float_as_uint(v.x), __float_as_uint(v.y), __float_as_uint(v.z), __float_as_uint(v.w)};
+                if ((unsigned)(sg - in_lo) >= (unsigned)(in_hi - in_lo)) {   // edge slab (wave-uniform)
+#pragma unroll
+                    for (int c = 0; c < 4; ++c)
+                        if ((uint32_t)(e0 + c) >= (uint32_t)n) k[c] = kKeyZeroBits;
+                }
+                bool f[4];
+#pragma unroll
+                for (int c = 0; c < 4; ++c) f[c] = (int32_t)(k[c] ^ kFlip) >= test.bound;
+                const uint64_t m[4] = {__ballot(f[0]), __ballot(f[1]), __ballot(f[2]), __ballot(f[3])};
+                const int below = (int)lanes_below(m[3], lanes_below(m[2], lanes_below(m[1], lanes_below(m[0], (uint32_t)cnt_w))));
+                if (room) {
+                    int q = below;
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) {
+                        lds_store_pair(f[c] ? lw_addr + 8 * q : dummy, k[c], (uint32_t)(e0 + c));
+                        q = add_lane_bit(q, m[c]);
+                    }
+                    cnt_w = __builtin_amdgcn_readlane(q, kWave - 1);
+                } else {
+                    const int total = __popcll(m[0]) + __popcll(m[1]) + __popcll(m[2]) + __popcll(m[3]);
+                    if (cnt_w + total <= kCapW) {
+                        int q = below;
+#pragma unroll
+                        for (int c = 0; c < 4; ++c) {
+                            if (f[c]) lds_store_pair(lw_addr + 8 * q, k[c], (uint32_t)(e0 + c));
+                            q = add_lane_bit(q, m[c]);
+                        }
+                    }
+                    cnt_w += total;   // counted past capacity: the overflow is detected below
+                }
+            };
+            // Whole windows with their refills (no per-slab bounds), the last
+            // whole window refilling only what remains, then the rest: no
+            // load is left in flight after the pass.
+            int s0 = 0;
+            for (; s0 + 2 * kSU <= nsl; s0 += kSU) {
 #pragma unroll
                 for (int u = 0; u < kSU; ++u) {
-                    const int s = s0 + u;
-                    if (s < nsl) {
-                        const int qs = sqb + s * 64;
-                        uint32_t k[4] = {__float_as_uint(buf[u].x), __float_as_uint(buf[u].y),
-                                         __float_as_uint(buf[u].z), __float_as_uint(buf[u].w)};
-                        const int e0 = 4 * (qs + lane) - aoff;
-                        if (4 * qs - aoff < 0 || 4 * qs + 255 - aoff >= n) {   // edge slab (wave-uniform)
-#pragma unroll
-                            for (int c = 0; c < 4; ++c)
-                                if ((uint32_t)(e0 + c) >= (uint32_t)n) k[c] = kKeyZeroBits;
-                        }
-                        bool f[4];
-#pragma unroll
-                        for (int c = 0; c < 4; ++c) f[c] = (int32_t)(k[c] ^ kFlip) >= test.bound;
-                        const uint64_t m0 = __ballot(f[0]), m1 = __ballot(f[1]), m2 = __ballot(f[2]),
-                                       m3 = __ballot(f[3]);
-                        const int total = __popcll(m0) + __popcll(m1) + __popcll(m2) + __popcll(m3);
-                        cnt_w = __builtin_amdgcn_readfirstlane(cnt_w);
-                        if (total != 0 && cnt_w + total <= kCapW) {
-                            int q = cnt_w + (int)lanes_below(m3, lanes_below(m2, lanes_below(m1, lanes_below(m0, 0))));
-#pragma unroll
-                            for (int c = 0; c < 4; ++c) {
-                                if (f[c]) lw[q] = make_uint2(k[c], (uint32_t)(e0 + c));
-                                q += f[c];
-                            }
-                        }
-                        cnt_w += total;   // counted past capacity: the overflow is detected below
-                    }
-                    const int sr = s + kSU;
-                    buf[u] = xa[(sr < nsl) ? min(sqb + sr * 64 + lane, qlast) : qtail];
+                    slab(buf[u], s0 + u, cnt_w <= kCapW - 256);
+                    buf[u] = slab_load(s0 + u + kSU);
                 }
             }
+            if (s0 + kSU <= nsl) {
+#pragma unroll
+                for (int u = 0; u < kSU; ++u) {
+                    slab(buf[u], s0 + u, cnt_w <= kCapW - 256);
+                    if (s0 + u + kSU < nsl) buf[u] = slab_load(s0 + u + kSU);
+                }
+                s0 += kSU;
+            }
+#pragma unroll
+            for (int u = 0; u < kSU; ++u)
+                if (s0 + u < nsl) slab(buf[u], s0 + u, false);
         };
         if (test.flip)
             spec_pass(std::true_type{});
@@ -983,11 +1054,24 @@ DEV void topk_body(const Params& p) {
             __syncthreads();
             if (sm.scal[3] != S - 1) return;   // another part of this row finishes it
             const bool same_xcd = sm.scal[2] != 0;
-            if (tid == 0) __hip_atomic_store(p.arrivals + row, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             if (!same_xcd) {
                 overflow = true;   // lists unusable: the fallback reads the whole row
                 f_spec = -1;
             } else {
+                // Up to four parts: each thread loads the first entries of
+                // every part's list (positions tid + j * kBlock, j < kSpecJ)
+                // together with the counts, before it knows which of them
+                // exist: one round trip for the usual lists.
+                const int kSpecJ = S <= 2 ? 2 : 1;
+                const bool spec_ld = S <= 4;
+                uint64_t ev[4] = {0ull, 0ull, 0ull, 0ull};
+                if (spec_ld) {
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) {
+                        const int q = kSpecJ == 2 ? k >> 1 : k, j = kSpecJ == 2 ? k & 1 : 0;
+                        if (q < S) ev[k] = p.part_list[(row * S + q) * (int64_t)kCap + tid + j * kBlock];
+                    }
+                }
                 // Totals and part offsets of the merged list (parts in index
                 // order). Every part computes the same T_spec from the same
                 // data; a part that kept another threshold (or overflowed)
@@ -1005,36 +1089,53 @@ DEV void topk_body(const Params& p) {
                 if (!overflow && f_spec >= K && f_spec <= cap) {
                     // Merged list in LDS, split evenly over the waves; the
                     // refine's first histogram level is built on the way.
-                    // Each thread owns merged positions tid + j * kBlock and
-                    // loads four of them (from their parts' lists) before it
-                    // stores any.
                     const uint32_t msh = ref_shift(trow, max(gmax, trow));
                     for (int i = tid; i < kRefBins1; i += kBlock) sm.u.rhist[i] = 0;
-                    const int jn = (f_spec + kBlock - 1) / kBlock;
-                    for (int j0 = 0; j0 < jn; j0 += 4) {
-                        int qj[4] = {0, 0, 0, 0}, oj[4] = {0, 0, 0, 0};
-                        for (int q = 1; q < S; ++q) {
-                            const int bq = __builtin_amdgcn_readlane(coff, q);
+                    lds_barrier();   // the histogram is cleared; the loads stay in flight
+                    auto put = [&](int P, uint64_t e) {
+                        sm.list[P] = make_uint2((uint32_t)e, (uint32_t)(e >> 32));
+                        ref_hist_add(sm, (uint32_t)e, trow, msh);
+                    };
+                    if (spec_ld) {
+#pragma unroll
+                        for (int k = 0; k < 4; ++k) {
+                            const int q = kSpecJ == 2 ? k >> 1 : k, j = kSpecJ == 2 ? k & 1 : 0;
+                            const int cq = __builtin_amdgcn_readlane(cc, min(q, S - 1)), oq = __builtin_amdgcn_readlane(coff, min(q, S - 1));
+                            const int i = tid + j * kBlock;
+                            if (q < S && i < cq) put(oq + i, ev[k]);
+                        }
+                        // entries past the first kSpecJ * kBlock of a part (rare)
+                        for (int q = 0; q < S; ++q) {
+                            const int cq = __builtin_amdgcn_readlane(cc, q), oq = __builtin_amdgcn_readlane(coff, q);
+                            const uint64_t* src = p.part_list + (row * S + q) * (int64_t)kCap;
+                            for (int i = kSpecJ * kBlock + tid; i < cq; i += kBlock) put(oq + i, src[i]);
+                        }
+                    } else {
+                        // Each thread owns merged positions tid + j * kBlock
+                        // and loads four of them (from their parts' lists)
+                        // before it stores any.
+                        const int jn = (f_spec + kBlock - 1) / kBlock;
+                        for (int j0 = 0; j0 < jn; j0 += 4) {
+                            int qj[4] = {0, 0, 0, 0}, oj[4] = {0, 0, 0, 0};
+                            for (int q = 1; q < S; ++q) {
+                                const int bq = __builtin_amdgcn_readlane(coff, q);
+#pragma unroll
+                                for (int jj = 0; jj < 4; ++jj) {
+                                    const bool past = tid + (j0 + jj) * kBlock >= bq;
+                                    qj[jj] += past;
+                                    oj[jj] = past ? bq : oj[jj];
+                                }
+                            }
+                            uint64_t e[4];
 #pragma unroll
                             for (int jj = 0; jj < 4; ++jj) {
-                                const bool past = tid + (j0 + jj) * kBlock >= bq;
-                                qj[jj] += past;
-                                oj[jj] = past ? bq : oj[jj];
+                                const int P = tid + (j0 + jj) * kBlock;
+                                e[jj] = P < f_spec ? p.part_list[(row * S + qj[jj]) * (int64_t)kCap + (P - oj[jj])] : 0ull;
                             }
-                        }
-                        uint64_t e[4];
 #pragma unroll
-                        for (int jj = 0; jj < 4; ++jj) {
-                            const int P = tid + (j0 + jj) * kBlock;
-                            e[jj] = P < f_spec ? p.part_list[(row * S + qj[jj]) * (int64_t)kCap + (P - oj[jj])] : 0ull;
-                        }
-                        if (j0 == 0) lds_barrier();   // the histogram is cleared; the loads stay in flight
-#pragma unroll
-                        for (int jj = 0; jj < 4; ++jj) {
-                            const int P = tid + (j0 + jj) * kBlock;
-                            if (P < f_spec) {
-                                sm.list[P] = make_uint2((uint32_t)e[jj], (uint32_t)(e[jj] >> 32));
-                                ref_hist_add(sm, (uint32_t)e[jj], trow, msh);
+                            for (int jj = 0; jj < 4; ++jj) {
+                                const int P = tid + (j0 + jj) * kBlock;
+                                if (P < f_spec) put(P, e[jj]);
                             }
                         }
                     }
@@ -1045,8 +1146,11 @@ DEV void topk_body(const Params& p) {
                         sm.seg_off[tid] = o;
                         sm.seg_cnt[tid] = min(chunk, f_spec - o);
                     }
+                    lds_barrier();   // every wave reads its new segment bounds after this
                 }
             }
+            // Ready for the next call (issued after the loads above).
+            if (tid == 0) __hip_atomic_store(p.arrivals + row, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
     }
 
