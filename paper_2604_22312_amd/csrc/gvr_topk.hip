@@ -752,8 +752,9 @@ DEV void topk_body(const Params& p) {
     const int sqe = wave == 0 ? 0 : min((ps0 + min((sw + 1) * ws, ps1 - ps0)) * 64, nq);
     const int nsl = sqe > sqb ? (sqe - sqb + 63) >> 6 : 0;
 
-    // Every element is a candidate when the row fits the lists.
-    const bool all_mode = (n <= cap) && (ws * 256 <= kCapW);
+    // Without a guess, every element is a candidate when the row fits the
+    // lists (a guess, when given, also cuts a short row's candidates).
+    const bool all_mode = !(GUESS && p.prev) && (n <= cap) && (ws * 256 <= kCapW);
     bool have_prev = GUESS && p.prev && !all_mode;
     // The paper's Phase 2 schedule (secant counting passes), when asked for.
     const bool secant = GUESS && p.secant && have_prev;

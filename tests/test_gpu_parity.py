@@ -91,9 +91,8 @@ def test_stats_invariants_config2():
             assert int(st["candidates"][r]) == f
             assert K_TOPK <= f <= 16384
             if i > 0 and path == 2:
-                # one pass: the lists at T >= T_spec (the guessed threshold,
-                # raised by the streaming waves' provisional thresholds) held
-                # the answer
+                # one pass: the lists at T = T_spec (the guessed threshold)
+                # held the answer
                 assert int(st["passes"][r]) == 1
                 assert T >= int(st["spec_threshold"][r])
                 assert int(st["spec_count"][r]) == f
