@@ -20,7 +20,9 @@
 //   part's slabs counts f(T_spec) and appends every element at or above it
 //   to per-wave LDS lists (ballot + mbcnt ranks, no atomics; each wave
 //   streams a contiguous range, so its list is in index order). The test
-//   runs on raw fp32 bits (one compare, see spec_keep). With S > 1 each part
+//   runs on raw fp32 bits (one compare, see spec_keep), and every lane stores
+//   each element, kept ones at their rank and the others to a dummy slot, so
+//   a slab costs a few scalar instructions. With S > 1 each part
 //   publishes its list and count to a workspace and the last part of the row
 //   to arrive (one agent-scope atomic per part) merges them. If
 //   K <= f(T_spec) <= C, Lemma 1 (Sec. 4.1) says the list holds the exact
@@ -41,6 +43,11 @@
 //   [K, C], an emit pass writes the selection directly. radix_topk runs only
 //   this schedule (one workgroup per row), starting from the whole key
 //   range: a distribution-agnostic radix select (Sec. 2.2).
+//
+//   On request (option flag 4) the paper's own Phase 2 schedule runs instead
+//   of the speculative pass: T0 = pmean of all guessed scores, one threshold
+//   counted per full-row pass, damped secant steps with a bisection fallback,
+//   then one collect pass at the accepted threshold.
 
 #include <hip/hip_runtime.h>
 
