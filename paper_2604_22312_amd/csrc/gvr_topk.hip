@@ -90,7 +90,7 @@ constexpr int kXcds = 8;                       // gfx950 XCDs; workgroup i runs 
 static_assert(GVR_MAX_CANDIDATES % kNW == 0, "per-wave capacity");
 static_assert((kBins & (kBins - 1)) == 0 && (kRefBins & (kRefBins - 1)) == 0 && (kRefBins1 & (kRefBins1 - 1)) == 0 &&
                   (kGuessBins & (kGuessBins - 1)) == 0, "bin counts are powers of two");
-static_assert(kNW * kSmall * 2 <= kRefBins, "refine slots over the histogram");
+static_assert(kSmall * 4 <= kRefBins, "refine candidates over the histogram");
 
 struct Params {
     const float* scores;
@@ -416,11 +416,10 @@ DEV void emit_segment(const Smem& sm, uint32_t T, int K, int take, int gb, int e
         for (int j = 0; j < 4; ++j) en[j] = j * kWave + lane < rem ? seg[i0 + j * kWave + lane] : make_uint2(0u, 0u);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const bool valid = j * kWave + lane < rem;
+            const uint64_t vm = __ballot(j * kWave + lane < rem);   // valid lanes
             const uint32_t kk = en[j].x;
-            const bool fg = valid && kk > T;
-            const bool fe = valid && kk == T;
-            const uint64_t mg = __ballot(fg), me = __ballot(fe);
+            const uint64_t mg = __ballot(kk > T) & vm, me = __ballot(kk == T) & vm;
+            const bool fg = (mg >> lane) & 1, fe = (me >> lane) & 1;
             const int g = gb + (int)lanes_below(mg, 0);
             if (me == 0) {   // no key == T here (wave-uniform): keys > T go after min(eb, take) ties
                 const int o = g + min(eb, take);
@@ -507,9 +506,10 @@ DEV void keys_in_place(Smem& sm, uint2* seg, int cnt, bool hist, uint32_t rlo, u
 // level of kRefBins1 bins over [rlo, bin_hi] (keys in (bin_hi, rhi] count in
 // the top bin; built here unless `hist_ready`), then wave 0 finds the
 // bin b holding the K-th key with two wave scans. If b holds at most kSmall
-// candidates, each wave copies its share to its own LDS slots and counts its
-// keys above b; wave 0 takes one candidate per lane, selects T* among them
-// and the per-wave emission offsets, and every wave emits its segment.
+// candidates, the waves copy them (with their wave) to a small LDS array and
+// count their keys above b; wave 0 takes one candidate per lane, selects T*
+// among them and the per-wave emission offsets, and every wave emits its
+// segment.
 // Otherwise histogram narrowing (refine_kth) continues inside b.
 DEV uint32_t refine_emit(Smem& sm, uint32_t rlo, uint32_t rhi, uint32_t bin_hi, int above, int K, int32_t* out,
                          int tid, int* n_gt_out, bool hist_ready) {
@@ -574,12 +574,13 @@ DEV uint32_t refine_emit(Smem& sm, uint32_t rlo, uint32_t rhi, uint32_t bin_hi, 
         emit_from_lists(sm, kth, K, out, tid, n_gt_out);
         return kth;
     }
-    // Copy bin b's candidates to this wave's slots (over the histogram, no
-    // longer needed: at most kSmall candidates in all, so at most kSmall per
-    // wave) in list order, and count this segment's keys above the bin.
-    uint2* const slots = reinterpret_cast<uint2*>(sm.u.rhist);   // [kNW][kSmall]
+    // Copy bin b's candidates, with their wave, to one small LDS array over
+    // the histogram (no longer needed; at most kSmall of them): a chunk that
+    // holds some (rare) reserves room with one LDS atomic. Each wave counts
+    // its keys above the bin.
+    uint4* const small = reinterpret_cast<uint4*>(sm.u.rhist);
     const uint32_t wid = hi_b - lo_b;
-    int gtl = 0, nin = 0;
+    int gtl = 0;
     for (int i0 = 0; i0 < cnt; i0 += 4 * kWave) {
         const int rem = cnt - i0;
         uint2 en[4];
@@ -587,56 +588,53 @@ DEV uint32_t refine_emit(Smem& sm, uint32_t rlo, uint32_t rhi, uint32_t bin_hi, 
         for (int j = 0; j < 4; ++j) en[j] = j * kWave + lane < rem ? seg[i0 + j * kWave + lane] : make_uint2(0u, 0u);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const bool valid = j * kWave + lane < rem;
-            gtl = add_lane_bit(gtl, __ballot(valid && en[j].x > hi_b));
-            const bool inb = valid && en[j].x - lo_b <= wid;
-            const uint64_t m = __ballot(inb);
+            const uint64_t vm = __ballot(j * kWave + lane < rem);   // valid lanes
+            gtl = add_lane_bit(gtl, __ballot(en[j].x > hi_b) & vm);
+            const uint64_t m = __ballot(en[j].x - lo_b <= wid) & vm;
             if (m) {   // rare (wave-uniform)
-                const int pos = nin + (int)lanes_below(m, 0);
-                if (inb && pos < kSmall) slots[wave * kSmall + pos] = en[j];
-                nin += (int)__popcll(m);
+                int base = 0;
+                if (lane == 0)
+                    base = __hip_atomic_fetch_add(&sm.scal[1], (int)__popcll(m), __ATOMIC_RELAXED,
+                                                  __HIP_MEMORY_SCOPE_WORKGROUP);
+                base = __builtin_amdgcn_readfirstlane(base);
+                const int pos = base + (int)lanes_below(m, 0);
+                if (((m >> lane) & 1) && pos < kSmall) small[pos] = make_uint4(en[j].x, en[j].y, (uint32_t)wave, 0u);
             }
         }
     }
     const int gt_hi = wave_sum(gtl);
     if (lane == 0) {
         sm.wa[wave] = gt_hi;
-        sm.wb[wave] = min(nin, kSmall);
+        sm.wb[wave] = 0;
     }
     lds_barrier();
     if (wave == 0) {
-        // Lane l takes the l-th candidate of bin b (wave order = list order):
-        // one masked read per wave that holds any.
-        const int nw = lane < kNW ? sm.wb[lane] : 0;
-        const int pin = wave_incl_scan(nw, lane);   // candidates of waves <= lane
-        const int pex = pin - nw;
-        uint64_t nz = __ballot(nw > 0);
-        uint2 mine = make_uint2(0u, 0u);
-        while (nz) {
-            const int wv = (int)__builtin_ctzll(nz);
-            nz &= nz - 1;
-            const int base = __builtin_amdgcn_readlane(pex, wv), cw = __builtin_amdgcn_readlane(nw, wv);
-            if (lane >= base && lane < base + cw) mine = slots[wv * kSmall + (lane - base)];
-        }
+        // Lane l takes the l-th copied candidate (any order).
         const bool v = lane < cnt_b;
+        const uint4 mine = v ? small[lane] : make_uint4(0u, 0u, 0u, 0u);
         // T* is the need-th largest of them: the key of a lane with fewer
         // than `need` keys above it and at least `need` at or above it
         // (every lane compares its key with each candidate's).
         const int need = K - above_b;   // rank of T* inside the bin, from the top
         int gt = 0, ge = 0;
-        for (int j = 0; j < cnt_b; ++j) {
-            const uint32_t kj = __builtin_amdgcn_readlane(mine.x, j);
-            gt += kj > mine.x;
-            ge += kj >= mine.x;
+        for (int j0 = 0; j0 < cnt_b; j0 += 4) {
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) {
+                const int j = min(j0 + jj, cnt_b - 1);
+                const uint32_t kj = __builtin_amdgcn_readlane(mine.x, j);
+                const bool in = j0 + jj < cnt_b;
+                gt += in && kj > mine.x;
+                ge += in && kj >= mine.x;
+            }
         }
         const uint64_t hitk = __ballot(v && gt < need && ge >= need);
         const uint32_t kth = __builtin_amdgcn_readlane(mine.x, hitk ? (int)__builtin_ctzll(hitk) : 0);
         // Per wave: keys > T* (above the bin, plus the bin's) and == T*;
-        // lane w < kNW owns wave w, whose candidates are lanes [pex, pin).
-        const uint64_t mgt = __ballot(v && mine.x > kth), meq = __ballot(v && mine.x == kth);
-        const uint64_t rng = (nw == 0) ? 0ull : ((nw >= 64 ? ~0ull : ((1ull << nw) - 1ull)) << pex);
-        const int gw = lane < kNW ? sm.wa[lane] + (int)__popcll(mgt & rng) : 0;
-        const int ew = lane < kNW ? (int)__popcll(meq & rng) : 0;
+        // each candidate adds itself to its wave's counts.
+        if (v && mine.x > kth) __hip_atomic_fetch_add(&sm.wa[mine.z], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        if (v && mine.x == kth) __hip_atomic_fetch_add(&sm.wb[mine.z], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        const int gw = lane < kNW ? sm.wa[lane] : 0;
+        const int ew = lane < kNW ? sm.wb[lane] : 0;
         const int gi = wave_incl_scan(gw, lane), ei = wave_incl_scan(ew, lane);
         const int gtot = __builtin_amdgcn_readlane(gi, 63);
         if (lane < kNW) {
@@ -1160,6 +1158,35 @@ DEV void topk_body(const Params& p) {
             // Ready for the next call (issued after the loads above).
             if (tid == 0) __hip_atomic_store(p.arrivals + row, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
+    }
+
+    // The guess delivered (the usual case): refine the lists right away.
+    if (spec && !all_mode && !overflow && f_spec >= K && f_spec <= cap) {
+        lds_barrier();
+        const int64_t t3f = stamp();
+        int ngt = 0;
+        const uint32_t kth = refine_emit(sm, tthr, 0xFFFFFFFFu, max(gmax, tthr), 0, K, out, tid, &ngt, hist_ready);
+        if (st && tid == 0) {
+            gvr_row_stats s = {};
+            s.n = n;
+            s.path = GVR_PATH_GUESS;
+            s.passes = passes;
+            s.candidates = f_spec;
+            s.threshold = tthr;
+            s.kth_key = kth;
+            s.n_gt = ngt;
+            s.guess_valid = gvalid;
+            s.spec_threshold = tspec;
+            s.spec_count = f_spec;
+            s.pmean = gvalid ? gsum / (float)gvalid : 0.f;
+            s.t_start = t0;
+            s.t_guess = t1;
+            s.t_search = t2;
+            s.t_collect = t3f;
+            s.t_refine = stamp();
+            *st = s;
+        }
+        return;
     }
 
     // Row-level decision (the single part, or the last part of the row).
