@@ -51,6 +51,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <stddef.h>
 #include <stdint.h>
 
 #include <algorithm>
@@ -120,6 +121,9 @@ DEV uint32_t key_of(float v) { return key_of_bits(__float_as_uint(v)); }
 DEV float float_of_key(uint32_t k) { return __uint_as_float((k & 0x80000000u) ? (k ^ 0x80000000u) : ~k); }
 
 // Number of set bits of m below this lane, plus acc.
+// Mask of lanes [0, r) for any r (wave-uniform): scalar instructions only.
+DEV uint64_t first_lanes(int r) { return r >= kWave ? ~0ull : (r <= 0 ? 0ull : (1ull << r) - 1ull); }
+
 DEV uint32_t lanes_below(uint64_t m, uint32_t acc) {
     return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, acc));
 }
@@ -267,6 +271,11 @@ struct Smem {
     int scal[8];
     int guess_ready;                    // set by wave 0 once T_spec is in scal[4..7]
 };
+// Passes over the lists read four 64-entry chunks at a time, up to 255
+// entries past a segment's count (masked afterwards): the list must be
+// followed by that much LDS.
+static_assert(offsetof(Smem, u) == sizeof(uint2) * kCap && sizeof(Smem::u) >= 4 * kWave * sizeof(uint2),
+              "LDS slack after the candidate list");
 
 // Block-wide exclusive scan of one int (all kBlock threads). Returns the total.
 DEV int block_excl_scan(int& a, Smem& sm, int tid) {
@@ -413,10 +422,10 @@ DEV void emit_segment(const Smem& sm, uint32_t T, int K, int take, int gb, int e
         const int rem = cnt - i0;
         uint2 en[4];   // four entries per lane read before any is written out
 #pragma unroll
-        for (int j = 0; j < 4; ++j) en[j] = j * kWave + lane < rem ? seg[i0 + j * kWave + lane] : make_uint2(0u, 0u);
+        for (int j = 0; j < 4; ++j) en[j] = seg[i0 + j * kWave + lane];   // past the count: masked below
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const uint64_t vm = __ballot(j * kWave + lane < rem);   // valid lanes
+            const uint64_t vm = first_lanes(rem - j * kWave);   // valid lanes
             const uint32_t kk = en[j].x;
             const uint64_t mg = __ballot(kk > T) & vm, me = __ballot(kk == T) & vm;
             const bool fg = (mg >> lane) & 1, fe = (me >> lane) & 1;
@@ -487,7 +496,7 @@ DEV void keys_in_place(Smem& sm, uint2* seg, int cnt, bool hist, uint32_t rlo, u
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int i = i0 + j * kWave + lane;
-            b[j] = i < cnt ? seg[i].x : 0u;
+            b[j] = seg[i].x;   // past the count: not written back
         }
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -585,10 +594,10 @@ DEV uint32_t refine_emit(Smem& sm, uint32_t rlo, uint32_t rhi, uint32_t bin_hi, 
         const int rem = cnt - i0;
         uint2 en[4];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) en[j] = j * kWave + lane < rem ? seg[i0 + j * kWave + lane] : make_uint2(0u, 0u);
+        for (int j = 0; j < 4; ++j) en[j] = seg[i0 + j * kWave + lane];   // past the count: masked below
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const uint64_t vm = __ballot(j * kWave + lane < rem);   // valid lanes
+            const uint64_t vm = first_lanes(rem - j * kWave);   // valid lanes
             gtl = add_lane_bit(gtl, __ballot(en[j].x > hi_b) & vm);
             const uint64_t m = __ballot(en[j].x - lo_b <= wid) & vm;
             if (m) {   // rare (wave-uniform)
@@ -1033,7 +1042,7 @@ DEV void topk_body(const Params& p) {
 #pragma unroll
                     for (int j = 0; j < 4; ++j) {
                         const int i = i0 + j * kWave + lane;
-                        e[j] = i < cnt ? seg[i] : make_uint2(0u, 0u);
+                        e[j] = seg[i];   // past the count: not published
                     }
 #pragma unroll
                     for (int j = 0; j < 4; ++j) {
