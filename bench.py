@@ -11,7 +11,10 @@ are not cache-resident (the 256 MB Infinity Cache holds < 5 steps).
 Prints one JSON line (see the fields below). `--gpus N` with N > 1 exits:
 this path runs on one GPU (rows would shard across GPUs with no exchange).
 Extra modes: `--mode copy` runs a plain device copy of known size (used to
-scale rocprofv3 FETCH_SIZE / WRITE_SIZE counters to bytes).
+scale rocprofv3 FETCH_SIZE / WRITE_SIZE counters to bytes); `--mode configs`
+prints one line per decode workload; `--mode rope` runs the paper's synthetic
+single-operator benchmark (one row of YaRN-RoPE scores per length N, guess =
+the static prior P_static), one line per N.
 """
 from __future__ import annotations
 
@@ -212,6 +215,96 @@ def run_configs(args, dev):
         torch.cuda.empty_cache()
 
 
+# Single-operator latencies on B200 with synthetic input (Sec. 6.3.1, Table 3):
+# N -> (GVR ns, production radix baseline ns). Another machine: context only.
+PAPER_TABLE3_NS = {8192: (16512, 11200), 16384: (21856, 21984), 32768: (26112, 32928),
+                   65536: (31904, 47936), 70690: (36864, 51200), 131072: (43392, 76128)}
+
+
+def run_rope(args, dev):
+    """The paper's synthetic benchmark (Sec. 6.3.1): for each N one row of
+    synthetic YaRN-RoPE scores (workloads/rope.py), guess = P_static from
+    gvr_rope_prior. Each timed call reads its own copy of the row (copies
+    span >= 512 MB where that fits 2048 copies, more than the Infinity Cache),
+    so rows come from HBM as in the paper's cache-flushed timing; the calls
+    are replayed from a HIP graph, so the per-call time includes the
+    graph's inter-kernel gap. Kernel durations come from rocprofv3."""
+    import numpy as np
+    import torch
+    import oracle
+    import paper_2604_22312_amd as g
+    from workloads import rope as WR
+
+    opts = {"flags": 4}
+
+    def secant(scores, row_len, prev, K, out_idx=None, stream=None):
+        return g.gvr_topk_ex(scores, row_len, prev, K, out_idx=out_idx, stream=stream, options=opts)
+
+    def radix(scores, row_len, prev, K, out_idx=None, stream=None):
+        return g.radix_topk(scores, row_len, None, K, out_idx=out_idx, stream=stream)
+
+    for n in WR.N_LIST:
+        host = WR.row_scores(n)
+        exp, _, _ = oracle.topk(host[None, :], K_TOPK)
+        copies = int(min(2048, max(64, -(-(512 << 20) // (4 * n)))))
+        row = torch.from_numpy(host).to(dev)
+        scores = row.view(1, n).repeat(copies, 1)                       # [copies][n]
+        row_len = torch.full((1,), n, dtype=torch.int32, device=dev)
+        outs = torch.empty((copies, K_TOPK), dtype=torch.int32, device=dev)
+        # the static prior (timed on its own: a one-off per model and length)
+        gbuf = torch.empty(n, dtype=torch.float64, device=dev)
+        prior = torch.empty(K_TOPK, dtype=torch.int32, device=dev)
+        ptimes = []
+        for _ in range(5):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            g.gvr_rope_prior(n, K_TOPK, device=dev, out=prior, g=gbuf)
+            e1.record()
+            torch.cuda.synchronize()
+            ptimes.append(e0.elapsed_time(e1) * 1e3)
+        prev = prior.view(1, K_TOPK)
+        line = {"mode": "rope", "workload": "rope_synthetic_n%d_b1" % n, "n": n, "rows_per_call": 1,
+                "K": K_TOPK, "copies": copies, "prior_us": round(float(np.median(ptimes)), 2)}
+        for name, fn in (("gvr_topk", g.gvr_topk), ("radix_topk", radix), ("paper_schedule", secant)):
+            stream = torch.cuda.Stream()
+            with torch.cuda.stream(stream):
+                for c in range(copies):
+                    fn(scores[c:c + 1], row_len, prev, K_TOPK, out_idx=outs[c:c + 1], stream=stream)
+            torch.cuda.synchronize()
+            if not np.array_equal(outs.cpu().numpy(), np.repeat(exp, copies, axis=0)):
+                raise SystemExit("bench: %s differs from the oracle on the synthetic row n=%d" % (name, n))
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(graph, stream=stream):
+                for c in range(copies):
+                    fn(scores[c:c + 1], row_len, prev, K_TOPK, out_idx=outs[c:c + 1], stream=stream)
+            graph.replay()
+            torch.cuda.synchronize()
+            reps = max(1, args.steps * 8 // copies)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(reps):
+                graph.replay()
+            e1.record()
+            torch.cuda.synchronize()
+            line[name + "_us"] = round(e0.elapsed_time(e1) * 1e3 / (reps * copies), 3)
+            del graph
+        for name, o in (("gvr", None), ("paper_schedule", opts)):
+            st = g.new_stats(1, dev)
+            g.gvr_topk_ex(scores[:1], row_len, prev, K_TOPK, stats=st, options=o)
+            d = g.decode_stats(st)
+            line[name + "_path"] = g.PATH_NAMES.get(int(d["path"][0]), "?")
+            line[name + "_passes"] = int(d["passes"][0])
+            line[name + "_candidates"] = int(d["candidates"][0])
+        line["prior_overlap"] = round(len(np.intersect1d(prior.cpu().numpy(), exp[0])) / K_TOPK, 4)
+        line["speedup_vs_radix"] = round(line["radix_topk_us"] / line["gvr_topk_us"], 3)
+        hns, bns = PAPER_TABLE3_NS[n]
+        line["paper_b200"] = {"gvr_us": hns / 1e3, "baseline_us": bns / 1e3, "speedup": round(bns / hns, 2)}
+        print(json.dumps(line))
+        sys.stdout.flush()
+        del scores, outs
+        torch.cuda.empty_cache()
+
+
 def read_traffic(n_launch_bytes):
     if not os.path.exists(TRAFFIC_FILE):
         return None
@@ -229,7 +322,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--mode", choices=["bench", "copy", "configs"], default="bench")
+    ap.add_argument("--mode", choices=["bench", "copy", "configs", "rope"], default="bench")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--no-radix", action="store_true", help="skip timing radix_topk")
     ap.add_argument("--no-secant", action="store_true",
@@ -258,6 +351,9 @@ def main():
 
     if args.mode == "configs":
         run_configs(args, dev)
+        return
+    if args.mode == "rope":
+        run_rope(args, dev)
         return
 
     w, outs, prevs = build_inputs(dev)

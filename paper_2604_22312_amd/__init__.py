@@ -3,7 +3,7 @@
 Thin Python binding over the C ABI of ``include/gvr_topk.h`` (library
 ``libgvr_topk.so`` built in-tree by ``paper_2604_22312_amd.build``). This module
 only validates tensors and marshals pointers; every step of the Top-K runs in
-the HIP kernels of ``csrc/gvr_topk.hip``. There is no CPU fallback: if the
+the HIP kernels of ``csrc/gvr_topk.hip`` and ``csrc/rope_prior.hip``. There is no CPU fallback: if the
 library is missing, importing the functions raises.
 
 Functions mirror the C entry points:
@@ -11,6 +11,9 @@ Functions mirror the C entry points:
 * ``gvr_topk(scores, row_len, prev_topk, K, out_idx=None, stream=None)``
 * ``radix_topk(scores, row_len, prev_topk, K, out_idx=None, stream=None)``
 * ``gvr_topk_ex`` / ``radix_topk_ex`` (options, per-row stats)
+* ``gvr_rope_g(n, params=None, device=...)`` -- g(Delta) of the RoPE/YaRN prior
+* ``gvr_rope_prior(n, K, params=None, device=...)`` -- its static index set
+  (``include/gvr_rope_prior.h``)
 """
 from .binding import (  # noqa: F401
     GVR_MAX_CANDIDATES,
@@ -18,7 +21,11 @@ from .binding import (  # noqa: F401
     PATH_NAMES,
     GvrError,
     Options,
+    RopeParams,
     decode_stats,
+    gvr_rope_g,
+    gvr_rope_params,
+    gvr_rope_prior,
     gvr_topk,
     gvr_topk_ex,
     lib,

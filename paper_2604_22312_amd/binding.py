@@ -31,6 +31,12 @@ class Options(ctypes.Structure):
                 ("parts", ctypes.c_int32), ("reserved1", ctypes.c_int32)]
 
 
+class RopeParams(ctypes.Structure):
+    """Mirror of ``gvr_rope_params`` (RoPE/YaRN angles of the static prior)."""
+    _fields_ = [("d_rope", ctypes.c_int32), ("orig_ctx", ctypes.c_int32), ("base", ctypes.c_double),
+                ("scale", ctypes.c_double), ("beta_fast", ctypes.c_double), ("beta_slow", ctypes.c_double)]
+
+
 def library_path() -> str:
     return _LIB_PATH
 
@@ -52,6 +58,12 @@ def lib():
         L.gvr_topk_ex.argtypes = [vp, i64, i64, vp, vp, i32, vp, vp, ctypes.POINTER(Options), vp]
         L.radix_topk_ex.restype = ctypes.c_int
         L.radix_topk_ex.argtypes = [vp, i64, i64, vp, i32, vp, vp, ctypes.POINTER(Options), vp]
+        L.gvr_rope_params_default.restype = None
+        L.gvr_rope_params_default.argtypes = [ctypes.POINTER(RopeParams)]
+        L.gvr_rope_g.restype = ctypes.c_int
+        L.gvr_rope_g.argtypes = [i64, ctypes.POINTER(RopeParams), vp, vp, vp]
+        L.gvr_rope_prior.restype = ctypes.c_int
+        L.gvr_rope_prior.argtypes = [i64, i32, ctypes.POINTER(RopeParams), vp, vp, vp]
         L.gvr_status_string.restype = ctypes.c_char_p
         L.gvr_status_string.argtypes = [ctypes.c_int]
         L.gvr_version.restype = ctypes.c_char_p
@@ -175,3 +187,67 @@ def decode_stats(stats: torch.Tensor) -> dict:
         "t_start": i64[:, 0].clone(), "t_guess": i64[:, 1].clone(), "t_search": i64[:, 2].clone(),
         "t_collect": i64[:, 3].clone(), "t_refine": i64[:, 4].clone(),
     }
+
+
+def gvr_rope_params(**kw) -> RopeParams:
+    """``gvr_rope_params`` holding the library defaults, with ``kw`` overrides."""
+    p = RopeParams()
+    lib().gvr_rope_params_default(ctypes.byref(p))
+    for k, v in kw.items():
+        if not hasattr(p, k):
+            raise ValueError("unknown RoPE parameter %r" % k)
+        setattr(p, k, v)
+    return p
+
+
+def _rope_args(params, device):
+    if params is None:
+        params = gvr_rope_params()
+    elif isinstance(params, dict):
+        params = gvr_rope_params(**params)
+    if device is None:
+        raise ValueError("device must be given")
+    dev = torch.device(device)
+    if dev.type != "cuda":
+        raise ValueError("the RoPE prior runs on a GPU (there is no CPU path)")
+    if dev.index is None:
+        dev = torch.device("cuda", torch.cuda.current_device())
+    return params, dev
+
+
+def gvr_rope_g(n, params=None, device="cuda", g=None, theta=None, stream=None):
+    """g(Delta), Delta = 0..n-1, as a float64 tensor on ``device``; ``theta``
+    (float64 [d/2], optional) receives the YaRN angles."""
+    params, dev = _rope_args(params, device)
+    n = int(n)
+    if g is None:
+        g = torch.empty(max(n, 0), dtype=torch.float64, device=dev)
+    for t, size in ((g, n), (theta, params.d_rope // 2)):
+        if t is not None and (t.dtype != torch.float64 or t.numel() != size or t.device != dev
+                              or not t.is_contiguous()):
+            raise ValueError("g / theta must be contiguous float64 tensors of n / d/2 elements on the device")
+    with torch.cuda.device(dev):
+        st = lib().gvr_rope_g(n, ctypes.byref(params), _ptr(g), _ptr(theta), _stream(stream, dev))
+    if st != 0:
+        raise GvrError("gvr_rope_g", st)
+    return g
+
+
+def gvr_rope_prior(n, K, params=None, device="cuda", out=None, g=None, stream=None):
+    """P_static (int32 [K], ascending) of the RoPE/YaRN prior over Delta = 0..n-1;
+    ``g`` (float64 [n], optional) receives g(Delta)."""
+    params, dev = _rope_args(params, device)
+    n, K = int(n), int(K)
+    if g is None:
+        g = torch.empty(max(n, 0), dtype=torch.float64, device=dev)
+    elif g.dtype != torch.float64 or g.numel() != n or g.device != dev or not g.is_contiguous():
+        raise ValueError("g must be a contiguous float64 tensor of n elements on the device")
+    if out is None:
+        out = torch.empty(max(K, 0), dtype=torch.int32, device=dev)
+    elif out.dtype != torch.int32 or out.numel() != K or out.device != dev or not out.is_contiguous():
+        raise ValueError("out must be a contiguous int32 tensor of K elements on the device")
+    with torch.cuda.device(dev):
+        st = lib().gvr_rope_prior(n, K, ctypes.byref(params), _ptr(g), _ptr(out), _stream(stream, dev))
+    if st != 0:
+        raise GvrError("gvr_rope_prior", st)
+    return out

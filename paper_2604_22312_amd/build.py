@@ -7,7 +7,7 @@ import sys
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
-SRC = os.path.join(PKG, "csrc", "gvr_topk.hip")
+SOURCES = [os.path.join(PKG, "csrc", f) for f in ("gvr_topk.hip", "rope_prior.hip")]
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libgvr_topk.so")
 ARCH = "gfx950"
@@ -28,15 +28,15 @@ def hipcc() -> str:
 
 
 def build(verbose: bool = False) -> str:
-    """Compile ``csrc/gvr_topk.hip`` into ``libgvr_topk.so`` (always rebuilds)."""
+    """Compile the ``csrc/*.hip`` sources into ``libgvr_topk.so`` (always rebuilds)."""
     tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = [hipcc()] + HIPCC_FLAGS + ["-I" + INCLUDE, "-o", tmp, SRC]
+    cmd = [hipcc()] + HIPCC_FLAGS + ["-I" + INCLUDE, "-o", tmp] + SOURCES
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         sys.stderr.write(r.stdout + r.stderr)
-        raise RuntimeError("hipcc failed building %s" % SRC)
+        raise RuntimeError("hipcc failed building %s" % LIB)
     os.replace(tmp, LIB)
     return LIB
 

@@ -1,22 +1,25 @@
-"""The C-ABI library loads and exports what include/gvr_topk.h declares (no GPU).
+"""The C-ABI library loads and exports what include/*.h declare (no GPU).
 
 Only host-side argument validation is exercised here: every call below
 returns before any HIP runtime call is made.
 """
 import ctypes
+import glob
+import math
 import os
 import re
 
 import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "gvr_topk.h")
+HEADERS = sorted(glob.glob(os.path.join(ROOT, "include", "*.h")))
 
 
 def declared_functions():
-    text = open(HEADER).read()
-    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    names = re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(\w+)\s*\(", text, flags=re.M)
+    names = []
+    for h in HEADERS:
+        text = re.sub(r"/\*.*?\*/", "", open(h).read(), flags=re.S)
+        names += re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(\w+)\s*\(", text, flags=re.M)
     return sorted(set(n for n in names if n not in ("if", "while")))
 
 
@@ -32,7 +35,8 @@ def L():
 def test_header_declares_the_boundary():
     names = declared_functions()
     for n in ("gvr_topk", "radix_topk", "gvr_topk_ex", "radix_topk_ex",
-              "gvr_status_string", "gvr_version"):
+              "gvr_status_string", "gvr_version", "gvr_rope_params_default", "gvr_rope_g",
+              "gvr_rope_prior"):
         assert n in names, n
 
 
@@ -92,3 +96,31 @@ def test_python_binding_refuses_cpu_tensors():
     import paper_2604_22312_amd as g
     with pytest.raises(ValueError):
         g.gvr_topk(torch.zeros(2, 10), None, None, 4)
+
+
+def test_rope_defaults_and_validation(L):
+    import paper_2604_22312_amd as g
+    vp = ctypes.c_void_p
+    p = g.gvr_rope_params()
+    assert (p.d_rope, p.orig_ctx, p.base, p.scale, p.beta_fast, p.beta_slow) == (64, 4096, 1e4, 40.0, 32.0, 1.0)
+    bad = [dict(d_rope=63), dict(d_rope=0), dict(d_rope=514), dict(orig_ctx=0), dict(base=1.0),
+           dict(base=math.inf), dict(scale=0.0), dict(scale=math.nan), dict(beta_fast=-1.0),
+           dict(beta_slow=0.0)]
+    for kw in bad:
+        q = g.gvr_rope_params(**kw)
+        assert L.gvr_rope_g(10, ctypes.byref(q), vp(1), None, None) == -1, kw
+        assert L.gvr_rope_prior(10, 16, ctypes.byref(q), vp(1), vp(1), None) == -1, kw
+    assert L.gvr_rope_g(-1, None, vp(1), None, None) == -1
+    assert L.gvr_rope_g(10, None, None, None, None) == -1          # g NULL with n > 0
+    assert L.gvr_rope_g(0, None, None, None, None) == 0            # nothing to do
+    assert L.gvr_rope_g(1 << 31, None, vp(1), None, None) == -5
+    assert L.gvr_rope_prior(10, 0, None, vp(1), vp(1), None) == -2
+    assert L.gvr_rope_prior(10, 2049, None, vp(1), vp(1), None) == -2
+    assert L.gvr_rope_prior(10, 16, None, vp(1), None, None) == -1  # out NULL
+    assert L.gvr_rope_prior(1 << 31, 16, None, vp(1), vp(1), None) == -5
+
+
+def test_rope_binding_refuses_cpu_device():
+    import paper_2604_22312_amd as g
+    with pytest.raises(ValueError):
+        g.gvr_rope_prior(100, 16, device="cpu")
