@@ -1019,6 +1019,85 @@ DEV void topk_body(const Params& p) {
         hist_ready = own_hist && !overflow;
         tthr = tspec;
 
+        if (overflow && S == 1) {
+            // A wave's list overflowed, but every wave counted past its
+            // capacity, so f(T_spec) is still exact. Candidates bunched in a
+            // few waves' ranges (positional structure: recent tokens, RoPE
+            // peaks) do this. If K <= f(T_spec) <= C a second pass over the
+            // part's slabs (just read, so L2-resident) collects them again at
+            // exact per-wave offsets instead of narrowing from scratch.
+            const int f_all = sum_over_waves(sm.wa, lane);
+            if (f_all >= K && f_all <= cap) {
+                const int off = sum_over_waves_below(sm.wa, lane, wave);
+                const int mine = sm.wa[wave];
+                lds_barrier();   // every count is read; the old lists are dead
+                if (nsl > 0) {
+#pragma unroll
+                    for (int u = 0; u < kSU; ++u) buf[u] = slab_load(u);
+                    const uint32_t base = lds_addr(sm.list + off);
+                    auto repack = [&](auto flip_tag) {
+                        constexpr uint32_t kFlip = decltype(flip_tag)::value ? 0x7FFFFFFFu : 0u;
+                        int run = 0;
+                        auto slab = [&](const float4& v, int s) {
+                            const int sg = (sqb >> 6) + s;
+                            const int e0 = 4 * lane - aoff + 256 * sg;
+                            uint32_t k[4] = {__float_as_uint(v.x), __float_as_uint(v.y), __float_as_uint(v.z),
+                                             __float_as_uint(v.w)};
+                            if ((unsigned)(sg - in_lo) >= (unsigned)(in_hi - in_lo)) {
+#pragma unroll
+                                for (int c = 0; c < 4; ++c)
+                                    if ((uint32_t)(e0 + c) >= (uint32_t)n) k[c] = kKeyZeroBits;
+                            }
+                            bool f[4];
+#pragma unroll
+                            for (int c = 0; c < 4; ++c) f[c] = (int32_t)(k[c] ^ kFlip) >= test.bound;
+                            const uint64_t m[4] = {__ballot(f[0]), __ballot(f[1]), __ballot(f[2]), __ballot(f[3])};
+                            int q = (int)lanes_below(m[3], lanes_below(m[2], lanes_below(m[1], lanes_below(m[0], (uint32_t)run))));
+#pragma unroll
+                            for (int c = 0; c < 4; ++c) {
+                                if (f[c] && q < mine) lds_store_pair(base + 8 * q, k[c], (uint32_t)(e0 + c));
+                                q = add_lane_bit(q, m[c]);
+                            }
+                            run += __popcll(m[0]) + __popcll(m[1]) + __popcll(m[2]) + __popcll(m[3]);
+                        };
+                        int s0 = 0;
+                        for (; s0 + 2 * kSU <= nsl; s0 += kSU) {
+#pragma unroll
+                            for (int u = 0; u < kSU; ++u) {
+                                slab(buf[u], s0 + u);
+                                buf[u] = slab_load(s0 + u + kSU);
+                            }
+                        }
+                        if (s0 + kSU <= nsl) {
+#pragma unroll
+                            for (int u = 0; u < kSU; ++u) {
+                                slab(buf[u], s0 + u);
+                                if (s0 + u + kSU < nsl) buf[u] = slab_load(s0 + u + kSU);
+                            }
+                            s0 += kSU;
+                        }
+#pragma unroll
+                        for (int u = 0; u < kSU; ++u)
+                            if (s0 + u < nsl) slab(buf[u], s0 + u);
+                    };
+                    if (test.flip)
+                        repack(std::true_type{});
+                    else
+                        repack(std::false_type{});
+                }
+                keys_in_place(sm, sm.list + off, mine, false, 0u, 0u, lane);
+                if (lane == 0) {
+                    sm.seg_off[wave] = off;
+                    sm.seg_cnt[wave] = mine;
+                }
+                ++passes;
+                lds_barrier();
+                overflow = false;
+                f_spec = f_all;
+                hist_ready = false;
+            }
+        }
+
         if (S > 1) {
             // ---------------- publish this part; the last part of the row goes on.
             // The parts of a row are launched on one XCD (the grid mapping),

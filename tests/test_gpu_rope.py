@@ -147,3 +147,36 @@ def test_gvr_with_static_prior_ragged_rows():
                      K_TOPK)
     torch.cuda.synchronize()
     assert_rows_equal(got.cpu().numpy(), exp, "gvr_topk ragged rows with the static prior")
+
+
+def test_gvr_repacks_bunched_candidates():
+    """Candidates bunched in a few waves' ranges overflow a wave's list when a
+    row runs in one workgroup: the synthetic RoPE row 0 at N = 131072 keeps
+    most of its Top-K in the first tenth of the row, and a decode row with a
+    recency bump keeps it in the last few thousand keys. f(T_spec) is still
+    exact, so when it lies in [K, C] the kernel collects the lists again at
+    packed offsets (two passes in all) instead of narrowing. (The recency rows
+    take the narrowing path: their guess puts f(T_spec) just below K.) Every
+    answer stays exact."""
+    import paper_2604_22312_amd as g
+    n = 131072
+    rows_rope = WR.batch_scores(n, 2)
+    rng = np.random.default_rng(77)
+    base = rng.standard_normal((2, n)).astype(np.float32)
+    base[:, -3500:] += 3.0                       # recent keys score higher
+    prev_rows = base + 0.05 * rng.standard_normal((2, n)).astype(np.float32)
+    s = np.concatenate([rows_rope, base]).astype(np.float32)
+    exp, _, _ = oracle.topk(s, K_TOPK)
+    prev_exp, _, _ = oracle.topk(prev_rows, K_TOPK)
+    note("gvr_topk bunched candidates, one workgroup per row")
+    prior = g.gvr_rope_prior(n, K_TOPK, device=DEV).cpu().numpy()
+    prev = torch.from_numpy(np.concatenate([np.stack([prior, prior]), prev_exp]).astype(np.int32)).to(DEV)
+    stats = g.new_stats(4, DEV)
+    got = g.gvr_topk_ex(torch.from_numpy(s).to(DEV), torch.full((4,), n, dtype=torch.int32, device=DEV), prev,
+                        K_TOPK, options={"parts": 1}, stats=stats)
+    torch.cuda.synchronize()
+    assert_rows_equal(got.cpu().numpy(), exp, "gvr_topk bunched candidates")
+    st = g.decode_stats(stats)
+    note("  paths %s passes %s" % (st["path"].tolist(), st["passes"].tolist()))
+    assert int(st["path"][0]) == 2 and int(st["passes"][0]) == 2, "the RoPE row was not repacked"
+    assert int(st["passes"].max()) <= 3
