@@ -1854,11 +1854,19 @@ gvr_status get_workspace(int device, void* stream, int rows, int parts, Workspac
 
 // Parts per row. Splitting a row over S workgroups divides its streaming
 // time (one workgroup reads about 33 GB/s on MI355X) but costs the merge of
-// the parts' candidate lists, about 8 us of memory round trips; split only
-// when the time saved is larger, keep parts >= kMinPartElems long and stay
-// within the compute units.
+// the parts' candidate lists, about 8 us of memory round trips when many
+// rows merge at once; split only when the time saved is larger, keep parts
+// >= kMinPartElems long and stay within the compute units. A call of one or
+// two rows leaves the chip nearly idle and its merges cost a few us: there
+// parts of 8K-16K elements pay from 32K elements on (8 parts below 192K,
+// then 16).
 int choose_parts(int64_t rows, int64_t ld, int cus) {
     if (rows <= 0 || rows >= cus) return 1;
+    if (rows <= 2 && ld >= 32768 && cus >= 32 * rows) {
+        int s = 1;
+        while (2 * s <= ld / 8192 && 2 * s <= kMaxParts) s *= 2;
+        return ld < 196608 ? std::min(s, 8) : s;
+    }
     int64_t s = cus / rows;
     s = std::min<int64_t>(s, std::max<int64_t>(1, ld / kMinPartElems));
     s = std::min<int64_t>(s, kMaxParts);

@@ -180,3 +180,20 @@ def test_gvr_repacks_bunched_candidates():
     note("  paths %s passes %s" % (st["path"].tolist(), st["passes"].tolist()))
     assert int(st["path"][0]) == 2 and int(st["passes"][0]) == 2, "the RoPE row was not repacked"
     assert int(st["passes"].max()) <= 3
+
+
+@pytest.mark.parametrize("rows", [1, 2])
+@pytest.mark.parametrize("n", [32768, 65537, 131072, 262144])
+def test_gvr_small_batch_split_rows(rows, n):
+    """Calls of one or two long rows split each row over several workgroups
+    (the chip is otherwise idle); the answer is exact whatever the split."""
+    import paper_2604_22312_amd as g
+    s = WR.batch_scores(n, rows)
+    exp, _, _ = oracle.topk(s, K_TOPK)
+    note("gvr_topk small batch rows=%d n=%d" % (rows, n))
+    prior = g.gvr_rope_prior(n, K_TOPK, device=DEV)
+    prev = prior.view(1, K_TOPK).expand(rows, K_TOPK).contiguous()
+    got = g.gvr_topk(torch.from_numpy(s).to(DEV), torch.full((rows,), n, dtype=torch.int32, device=DEV), prev,
+                     K_TOPK)
+    torch.cuda.synchronize()
+    assert_rows_equal(got.cpu().numpy(), exp, "gvr_topk small batch rows=%d n=%d" % (rows, n))
