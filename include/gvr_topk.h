@@ -107,7 +107,11 @@ typedef struct gvr_options {
                               bit 2: the paper's own threshold search -- every
                               guessed score, T0 = pmean, secant counting passes,
                               a collect pass (one workgroup per row) -- instead
-                              of the speculative first pass */
+                              of the speculative first pass;
+                              bit 3: the paper's own exact selection (Sec. 4.2.4:
+                              min / max, 2048-bin histogram with a wave-parallel
+                              bin search, snap iterations, partition) instead of
+                              the histogram + rank-count refine */
     int32_t parts;         /* workgroups per row, 1..16 (0 = chosen from B, ld
                               and the device's compute units; a forced value is
                               lowered so that B * parts <= 2048); never changes
@@ -129,7 +133,8 @@ typedef struct gvr_row_stats {
     int32_t spec_count;    /* f(T_spec) counted in the first pass (-1 if a
                               candidate list overflowed) */
     float pmean;           /* mean of the guessed scores (T0 of Sec. 4.2.1) */
-    int32_t reserved;
+    int32_t refine_iters;  /* snap iterations of the paper's selection (flag
+                              bit 3), else 0 */
     int64_t t_start;       /* s_memtime stamps of the row's workgroup (shader */
     int64_t t_guess;       /*   clock): start; guess ready;                    */
     int64_t t_search;      /*   threshold accepted (last pass done);           */

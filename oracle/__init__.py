@@ -15,6 +15,9 @@ module only builds/loads it and marshals numpy arrays. What it computes:
 * ``key``      -- the sortable 32-bit key of each fp32 value (the "sortable
                   FP32 score key" the radix baseline ranks, Sec. 2.2).
 
+The oracle of the static RoPE/YaRN prior (g(Delta), P_static; Sec. 3.2,
+3.3) is the numpy module ``oracle/rope_prior.py``.
+
 Parity status: ``topk``, ``count_ge`` and ``key`` are pinned by
 ``tests/test_oracle_pins.py`` (brute force, closed forms, invariants, numpy
 cross-checks and planted mistakes).

@@ -26,7 +26,8 @@ class GvrError(RuntimeError):
 class Options(ctypes.Structure):
     """Mirror of ``gvr_options``: capacity C, flags (bit 0: ignore the guess;
     bit 1: scatter a row's parts over XCDs; bit 2: the paper's secant
-    threshold search), parts (workgroups per row, 0 = automatic)."""
+    threshold search; bit 3: the paper's snap-iteration selection), parts
+    (workgroups per row, 0 = automatic)."""
     _fields_ = [("capacity", ctypes.c_int32), ("flags", ctypes.c_int32),
                 ("parts", ctypes.c_int32), ("reserved1", ctypes.c_int32)]
 
@@ -183,7 +184,7 @@ def decode_stats(stats: torch.Tensor) -> dict:
         "candidates": i32[:, 3].clone(), "threshold": u32(4), "kth_key": u32(5),
         "n_gt": i32[:, 6].clone(), "guess_valid": i32[:, 7].clone(),
         "spec_threshold": u32(8), "spec_count": i32[:, 9].clone(),
-        "pmean": i32[:, 10].clone().view(torch.float32),
+        "pmean": i32[:, 10].clone().view(torch.float32), "refine_iters": i32[:, 11].clone(),
         "t_start": i64[:, 0].clone(), "t_guess": i64[:, 1].clone(), "t_search": i64[:, 2].clone(),
         "t_collect": i64[:, 3].clone(), "t_refine": i64[:, 4].clone(),
     }

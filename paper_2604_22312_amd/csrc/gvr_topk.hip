@@ -107,6 +107,7 @@ struct Params {
     int32_t chunk;       // gridDim.x / 8: consecutive (row, part) slots per XCD
     int32_t scatter;     // 1: slot = blockIdx.x (parts of a row on different XCDs)
     int32_t secant;      // 1: the paper's Phase 2 (secant counting passes) instead of the speculative pass
+    int32_t paper_refine; // 1: the paper's Phase 4 (min/max, histogram, snap iterations) instead of refine_emit
     uint64_t* arrivals;  // [rows] parts that finished the speculative pass (S > 1), per XCD above
                          // bit 16; 0 between calls
     int32_t* part_count; // [rows][S] f(threshold) of each part, bit 31 = a wave list overflowed
@@ -473,6 +474,126 @@ DEV void emit_from_lists(Smem& sm, uint32_t T, int K, int32_t* out, int tid, int
     const int gtot = sum_over_waves(sm.wa, lane);
     emit_segment(sm, T, K, K - gtot, gb, eb, out, lane, wave);
     *n_gt_out = gtot;
+}
+
+// The paper's Phase 4 (Sec. 4.2.4), kept as an option for comparison with
+// refine_emit. (4a) min / max of the listed keys; (4b) a histogram of
+// kPaperBins bins over [min, max] and the wave-parallel K-th bin search: every
+// wave sums its kPaperBins / 16 bins (wave 0 holds the top ones), one thread
+// scans the 16 wave totals from the top, and one lane of the wave found scans
+// that wave's bins, 160 serial steps in all; (4d) snap iterations: T starts
+// inside the K-th bin where the bin's count places the K-th key (linear
+// interpolation over the bin's key range) and each iteration counts
+// #{key >= T} and #{key > T} and finds the nearest listed keys above and
+// below T in one pass over the lists, moving T to one of them until
+// #{key > T} < K <= #{key >= T}; (4e) every key > T and the first K - #{key > T}
+// keys == T (lower index first) are written out. T only visits listed keys
+// between its start and the K-th key, all inside one bin, so the iterations
+// end; after kMaxSnap of them the K-th key is isolated by refine_kth inside
+// the bin instead (not reached on the workloads measured).
+constexpr int kPaperBins = 2048;
+constexpr int kMaxSnap = 64;
+DEV uint32_t paper_refine_emit(Smem& sm, int K, int32_t* out, int tid, int* n_gt_out, int* snaps_out) {
+    const int lane = tid & 63, wave = tid >> 6;
+    const uint2* seg = sm.list + sm.seg_off[wave];
+    const int cnt = sm.seg_cnt[wave];
+    // (4a) min / max
+    uint32_t mn = 0xFFFFFFFFu, mx = 0u;
+    for (int i = lane; i < cnt; i += kWave) {
+        mn = min(mn, seg[i].x);
+        mx = max(mx, seg[i].x);
+    }
+    mn = wave_min_u(mn);
+    mx = wave_max_u(mx);
+    if (lane == 0) {
+        sm.red[2][wave] = (int)mn;
+        sm.red[3][wave] = (int)mx;
+    }
+    for (int i = tid; i < kPaperBins; i += kBlock) sm.u.rhist[i] = 0;
+    lds_barrier();
+    const uint32_t kmin = wave_min_u(lane < kNW ? (uint32_t)sm.red[2][lane] : 0xFFFFFFFFu);
+    const uint32_t kmax = wave_max_u(lane < kNW ? (uint32_t)sm.red[3][lane] : 0u);
+    // (4b) histogram over [kmin, kmax]
+    const uint32_t sh = bin_shift((uint64_t)kmax - kmin + 1, log2i(kPaperBins));
+    for (int i = lane; i < cnt; i += kWave)
+        __hip_atomic_fetch_add(&sm.u.rhist[(seg[i].x - kmin) >> sh], 1, __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_WORKGROUP);
+    lds_barrier();
+    constexpr int kPerWave = kPaperBins / kNW;   // 128: wave w holds bins [top - 128 (w + 1), top - 128 w)
+    {
+        const int b0 = kPaperBins - kPerWave * (wave + 1);
+        const int t = wave_sum(sm.u.rhist[b0 + lane] + sm.u.rhist[b0 + kWave + lane]);
+        if (lane == 0) sm.wa[wave] = t;
+    }
+    lds_barrier();
+    if (tid == 0) {   // target wave: 16 serial steps from the top
+        int run = 0, w = 0;
+        for (; w < kNW - 1 && run + sm.wa[w] < K; ++w) run += sm.wa[w];
+        sm.scal[0] = w;
+        sm.scal[1] = run;
+    }
+    lds_barrier();
+    if (wave == sm.scal[0] && lane == 0) {   // exact bin: up to 128 serial steps from the top of the wave's bins
+        int run = sm.scal[1];
+        int b = kPaperBins - kPerWave * wave - 1;
+        const int bend = kPaperBins - kPerWave * (wave + 1);
+        for (; b > bend && run + sm.u.rhist[b] < K; --b) run += sm.u.rhist[b];
+        sm.scal[2] = b;
+        sm.scal[3] = run;
+    }
+    lds_barrier();
+    const int kb = sm.scal[2];
+    const int above = sm.scal[3];
+    const int h = max(sm.u.rhist[kb], 1);
+    const uint64_t blo = (uint64_t)kmin + ((uint64_t)kb << sh);
+    const uint64_t bhi = std::min<uint64_t>(blo + ((uint64_t)1 << sh) - 1, kmax);
+    // (4d) snap iterations from the interpolated start
+    const int r = max(K - above, 1);   // rank of the K-th key inside the bin, from the top
+    uint32_t T = (uint32_t)(bhi - ((uint64_t)(2 * r - 1) * (bhi - blo + 1)) / (uint64_t)(2 * h));
+    T = (uint32_t)std::max<uint64_t>(T, blo);
+    int snaps = 0, ngt = 0;
+    bool found = false;
+    while (snaps < kMaxSnap) {
+        ++snaps;
+        int ge = 0, gt = 0;
+        uint32_t up = 0xFFFFFFFFu, down = 0u;
+        for (int i = lane; i < cnt; i += kWave) {
+            const uint32_t kk = seg[i].x;
+            ge += kk >= T;
+            gt += kk > T;
+            if (kk > T) up = min(up, kk);
+            if (kk < T) down = max(down, kk);
+        }
+        ge = wave_sum(ge);
+        gt = wave_sum(gt);
+        up = wave_min_u(up);
+        down = wave_max_u(down);
+        lds_barrier();   // the previous iteration's totals are read
+        if (lane == 0) {
+            sm.wa[wave] = ge;
+            sm.wb[wave] = gt;
+            sm.red[2][wave] = (int)up;
+            sm.red[3][wave] = (int)down;
+        }
+        lds_barrier();
+        const int GE = sum_over_waves(sm.wa, lane);
+        const int GT = sum_over_waves(sm.wb, lane);
+        if (GT < K && K <= GE) {
+            found = true;
+            ngt = GT;
+            break;
+        }
+        // fewer than K at or above T: step down; K or more above T: step up
+        T = (GE < K) ? wave_max_u(lane < kNW ? (uint32_t)sm.red[3][lane] : 0u)
+                     : wave_min_u(lane < kNW ? (uint32_t)sm.red[2][lane] : 0xFFFFFFFFu);
+    }
+    lds_barrier();
+    if (!found) T = refine_kth(sm, (uint32_t)blo, (uint32_t)bhi, above, K, tid);
+    (void)ngt;
+    // (4e) partition
+    emit_from_lists(sm, T, K, out, tid, n_gt_out);
+    *snaps_out = snaps;
+    return T;
 }
 
 // First refine level: kRefBins1 bins of 2^sh keys from rlo; keys at or above
@@ -1253,7 +1374,10 @@ DEV void topk_body(const Params& p) {
         lds_barrier();
         const int64_t t3f = stamp();
         int ngt = 0;
-        const uint32_t kth = refine_emit(sm, tthr, 0xFFFFFFFFu, max(gmax, tthr), 0, K, out, tid, &ngt, hist_ready);
+        int snaps = 0;
+        const uint32_t kth = p.paper_refine
+                                 ? paper_refine_emit(sm, K, out, tid, &ngt, &snaps)
+                                 : refine_emit(sm, tthr, 0xFFFFFFFFu, max(gmax, tthr), 0, K, out, tid, &ngt, hist_ready);
         if (st && tid == 0) {
             gvr_row_stats s = {};
             s.n = n;
@@ -1267,6 +1391,7 @@ DEV void topk_body(const Params& p) {
             s.spec_threshold = tspec;
             s.spec_count = f_spec;
             s.pmean = gvalid ? gsum / (float)gvalid : 0.f;
+            s.refine_iters = snaps;
             s.t_start = t0;
             s.t_guess = t1;
             s.t_search = t2;
@@ -1470,6 +1595,7 @@ DEV void topk_body(const Params& p) {
         }
         (void)fl;
         (void)fh;
+        t2 = stamp();   // Phase 2 done (threshold accepted, or the search gave up)
         if (sec_ok) {
             // Phase 3: collect every key >= T at per-wave offsets from the
             // last pass's per-wave counts (sm.wa), in index order.
@@ -1728,7 +1854,9 @@ DEV void topk_body(const Params& p) {
     t3 = stamp();
     // ---------------- (a5) refine the listed candidates and emit
     int ngt = 0;
-    const uint32_t kth = refine_emit(sm, rlo, rhi, bin_hi, above, K, out, tid, &ngt, use_hist);
+    int snaps = 0;
+    const uint32_t kth = p.paper_refine ? paper_refine_emit(sm, K, out, tid, &ngt, &snaps)
+                                        : refine_emit(sm, rlo, rhi, bin_hi, above, K, out, tid, &ngt, use_hist);
     if (st && tid == 0) {
         gvr_row_stats s = {};
         s.n = n;
@@ -1742,6 +1870,7 @@ DEV void topk_body(const Params& p) {
         s.spec_threshold = tspec;
         s.spec_count = f_spec;
         s.pmean = gvalid ? gsum / (float)gvalid : 0.f;
+        s.refine_iters = snaps;
         s.t_start = t0;
         s.t_guess = t1;
         s.t_search = t2;
@@ -1757,7 +1886,8 @@ __global__ __launch_bounds__(kBlock) void radix_topk_kernel(Params p) { topk_bod
 // ------------------------------------------------------------------ host side
 
 gvr_status validate(const float* scores, int64_t B, int64_t ld, int32_t K, const int32_t* out,
-                    const gvr_options* opt, int* capacity, int* use_guess, int* parts, int* scatter, int* secant) {
+                    const gvr_options* opt, int* capacity, int* use_guess, int* parts, int* scatter, int* secant,
+                    int* paper_refine) {
     if (K < 1 || K > GVR_MAX_K) return GVR_ERR_UNSUPPORTED_K;
     if (B < 0 || ld < 0) return GVR_ERR_INVALID_ARG;
     if (B > 0 && (!scores || !out)) return GVR_ERR_INVALID_ARG;
@@ -1768,11 +1898,12 @@ gvr_status validate(const float* scores, int64_t B, int64_t ld, int32_t K, const
             if (opt->capacity < K || opt->capacity > GVR_MAX_CANDIDATES) return GVR_ERR_INVALID_ARG;
             cap = opt->capacity;
         }
-        if ((opt->flags & ~7) || opt->reserved1) return GVR_ERR_INVALID_ARG;
+        if ((opt->flags & ~15) || opt->reserved1) return GVR_ERR_INVALID_ARG;
         if (opt->parts < 0 || opt->parts > kMaxParts) return GVR_ERR_INVALID_ARG;
         if (opt->flags & 1) *use_guess = 0;
         *scatter = (opt->flags >> 1) & 1;
         *secant = (opt->flags >> 2) & 1;
+        *paper_refine = (opt->flags >> 3) & 1;
         *parts = opt->parts;
     }
     *capacity = cap;
@@ -1879,8 +2010,9 @@ int choose_parts(int64_t rows, int64_t ld, int cus) {
 gvr_status run(const float* scores, int64_t B, int64_t ld, const int32_t* row_len, const int32_t* prev,
                int32_t K, int32_t* out, void* stream, const gvr_options* opt, gvr_row_stats* stats,
                int use_guess) {
-    int cap = 0, parts_opt = 0, scatter = 0, secant = 0;
-    gvr_status st = validate(scores, B, ld, K, out, opt, &cap, &use_guess, &parts_opt, &scatter, &secant);
+    int cap = 0, parts_opt = 0, scatter = 0, secant = 0, paper_refine = 0;
+    gvr_status st = validate(scores, B, ld, K, out, opt, &cap, &use_guess, &parts_opt, &scatter, &secant,
+                             &paper_refine);
     if (st != GVR_OK) return st;
     if (B == 0) return GVR_OK;
     const bool guess = use_guess && prev;
@@ -1915,6 +2047,7 @@ gvr_status run(const float* scores, int64_t B, int64_t ld, const int32_t* row_le
         q.chunk = (int32_t)(rows_pad / kXcds * parts);
         q.scatter = scatter;
         q.secant = secant;
+        q.paper_refine = paper_refine;
         q.arrivals = ws.arrivals;
         q.part_count = ws.part_count;
         q.part_thresh = ws.part_thresh;

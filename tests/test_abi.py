@@ -80,7 +80,7 @@ def test_options_validation(L):
     import paper_2604_22312_amd as g
     vp = ctypes.c_void_p
     bad = [g.Options(capacity=100, flags=0, parts=0, reserved1=0),      # capacity < K
-           g.Options(capacity=0, flags=8, parts=0, reserved1=0),        # unknown flag bit
+           g.Options(capacity=0, flags=32, parts=0, reserved1=0),       # unknown flag bit
            g.Options(capacity=0, flags=16, parts=0, reserved1=0),       # unknown flag bit
            g.Options(capacity=0, flags=0, parts=0, reserved1=1),        # reserved field set
            g.Options(capacity=0, flags=0, parts=17, reserved1=0),       # too many parts

@@ -440,3 +440,48 @@ def test_secant_schedule_parity(case):
                 assert K_TOPK <= f <= 16384
             if int(rl[r]) > K_TOPK:
                 assert int(st["kth_key"][r]) == int(kth[r])
+
+
+@pytest.mark.parametrize("flags", [8, 12], ids=["paper_refine", "paper_schedule_and_refine"])
+@pytest.mark.parametrize("case", [(0, 4, 1, None), (1, 3, 4, None), (2, 3, 4, None), (3, 2, 8, "a"),
+                                  (3, 2, 8, "b"), (3, 2, 8, "c"), (3, 2, 8, "d"), (4, 2, 2, None)],
+                         ids=lambda c: "c%d%s" % (c[0], c[3] or ""))
+def test_paper_refine_parity(case, flags):
+    """The paper's own exact selection (flag bit 3: min / max, 2048-bin
+    histogram with the wave-parallel bin search, snap iterations, partition),
+    alone and after the paper's threshold search, gives the oracle's answer;
+    the K-th key it reports is the oracle's."""
+    import paper_2604_22312_amd as g
+
+    def paper(scores, row_len, prev, K, stats=None):
+        return g.gvr_topk_ex(scores, row_len, prev, K, options={"flags": flags}, stats=stats)
+    paper.__name__ = "gvr_flags%d" % flags
+    cfg, steps, queries, sub = case
+    w, res = run_decode(paper, cfg, steps, queries, sub, dev=DEV, stats_check=True)
+    for i, st, kth, ngt in res:
+        rl = w.row_len[i].numpy()
+        for r in range(w.rows):
+            assert int(st["path"][r]) != -1
+            if int(rl[r]) > K_TOPK and int(st["path"][r]) != 4:   # the ties path emits without a refine
+                assert int(st["kth_key"][r]) == int(kth[r])
+                assert int(st["n_gt"][r]) == int(ngt[r])
+                assert 1 <= int(st["refine_iters"][r]) <= 64
+
+
+@pytest.mark.parametrize("ld,K", [(20001, 2048), (9999, 7), (70003, 1), (131071, 2000)])
+def test_paper_refine_special_rows(ld, K):
+    import paper_2604_22312_amd as g
+    rng = np.random.default_rng(ld + 3 * K)
+    rows, lens = _special_rows(ld, K, rng)
+    exp, _, _ = oracle.topk(rows, K, row_len=lens)
+    S = torch.from_numpy(rows).to(DEV)
+    RL = torch.from_numpy(lens).to(DEV)
+    prev = torch.from_numpy(np.ascontiguousarray(exp)).to(DEV)
+    for flags in (8, 12):
+        note("paper refine special rows ld=%d K=%d flags=%d" % (ld, K, flags))
+        out = g.gvr_topk_ex(S, RL, None, K, options={"flags": flags})
+        assert_rows_equal(out.cpu().numpy(), exp, "paper refine, no guess, ld=%d K=%d" % (ld, K))
+        out = g.gvr_topk_ex(S, RL, prev, K, options={"flags": flags})
+        assert_rows_equal(out.cpu().numpy(), exp, "paper refine with guess ld=%d K=%d" % (ld, K))
+        out = g.radix_topk_ex(S, RL, K, options={"flags": flags})
+        assert_rows_equal(out.cpu().numpy(), exp, "radix with the paper refine ld=%d K=%d" % (ld, K))
