@@ -14,7 +14,8 @@ Extra modes: `--mode copy` runs a plain device copy of known size (used to
 scale rocprofv3 FETCH_SIZE / WRITE_SIZE counters to bytes); `--mode configs`
 prints one line per decode workload; `--mode rope` runs the paper's synthetic
 single-operator benchmark (one row of YaRN-RoPE scores per length N, guess =
-the static prior P_static), one line per N.
+the static prior P_static), one line per N; `--mode phases` prints the
+per-phase time breakdown of gvr_topk and of the paper's own phases.
 """
 from __future__ import annotations
 
@@ -305,6 +306,133 @@ def run_rope(args, dev):
         torch.cuda.empty_cache()
 
 
+PHASE_VARIANTS = (("gvr", 0), ("gvr_paper_refine", 8), ("paper_schedule", 4), ("paper_schedule_paper_refine", 12))
+
+
+def _phase_table(st_list, rate_per_us):
+    """Median per-row phase times (us) from row stats: P1 guess statistics,
+    P2 threshold search, P3 collect, P4 exact selection. On the default path
+    P2 and P3 are one speculative pass (reported as P2) and P3 holds what
+    follows it before the refine: the merge of a split row's parts, or a
+    second collect after a list overflow."""
+    import numpy as np
+    d = {k: np.concatenate([s[k].numpy() for s in st_list]).astype(np.int64)
+         for k in ("t_start", "t_guess", "t_search", "t_collect", "t_refine", "path", "passes", "refine_iters")}
+    ok = d["path"] >= 0
+    us = lambda a, b: np.median((d[b][ok] - d[a][ok]) / rate_per_us)  # noqa: E731
+    p = {"p1_guess_us": us("t_start", "t_guess"), "p2_search_us": us("t_guess", "t_search"),
+         "p3_collect_us": us("t_search", "t_collect"), "p4_refine_us": us("t_collect", "t_refine"),
+         "stamped_total_us": us("t_start", "t_refine")}
+    p = {k: round(float(v), 3) for k, v in p.items()}
+    p["passes_mean"] = round(float(d["passes"][ok].mean()), 3)
+    p["snap_iters_mean"] = round(float(d["refine_iters"][ok].mean()), 3)
+    p["snap_iters_max"] = int(d["refine_iters"][ok].max())
+    return p
+
+
+def run_phases(args, dev):
+    """Per-phase time breakdown (the paper's Table 7 layout: P1 guess
+    statistics, P2 threshold search, P3 collect, P4 exact selection) of
+    gvr_topk and of the paper's own phases, from the row stats' clock stamps:
+    on the synthetic single row at N = 70690 (the paper's length) and on the
+    100K decode workload. Variants: the default path, the paper's Phase 4
+    (flag 8), the paper's Phase 2/3 (flag 4) and both (flag 12). The stamp
+    clock's rate is calibrated against HIP events over a graph of calls."""
+    import numpy as np
+    import torch
+    import oracle
+    import paper_2604_22312_amd as g
+    from workloads import rope as WR
+
+    def replay_us(calls, reps):
+        stream = torch.cuda.Stream()
+        with torch.cuda.stream(stream):
+            for c in calls:
+                c(stream)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=stream):
+            for c in calls:
+                c(stream)
+        graph.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            graph.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / (reps * len(calls))
+
+    # clock calibration: ticks vs events over a long eager sequence with stats
+    n = 70690
+    host = WR.row_scores(n)
+    exp, _, _ = oracle.topk(host[None, :], K_TOPK)
+    row = torch.from_numpy(host).to(dev).view(1, n)
+    rl = torch.full((1,), n, dtype=torch.int32, device=dev)
+    prior = g.gvr_rope_prior(n, K_TOPK, device=dev).view(1, K_TOPK)
+    st0, st1 = g.new_stats(1, dev), g.new_stats(1, dev)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    g.gvr_topk_ex(row, rl, prior, K_TOPK, stats=st0)
+    for _ in range(2000):
+        g.gvr_topk_ex(row, rl, prior, K_TOPK)
+    g.gvr_topk_ex(row, rl, prior, K_TOPK, stats=st1)
+    e1.record()
+    torch.cuda.synchronize()
+    ticks = int(g.decode_stats(st1)["t_refine"][0]) - int(g.decode_stats(st0)["t_start"][0])
+    rate = ticks / (e0.elapsed_time(e1) * 1e3)   # ticks per us (the span misses only launch edges)
+    print(json.dumps({"mode": "phases", "clock_ticks_per_us": round(rate, 2)}))
+
+    # synthetic single row, N = 70690, cache-cold copies
+    copies = 1899
+    scores = row.repeat(copies, 1)
+    outs = torch.empty((copies, K_TOPK), dtype=torch.int32, device=dev)
+    for name, flags in PHASE_VARIANTS:
+        opts = {"flags": flags}
+        calls = [lambda s, c=c: g.gvr_topk_ex(scores[c:c + 1], rl, prior, K_TOPK, out_idx=outs[c:c + 1],
+                                                 stream=s, options=opts) for c in range(copies)]
+        us = replay_us(calls, max(1, args.steps * 8 // copies))
+        if not np.array_equal(outs.cpu().numpy(), np.repeat(exp, copies, axis=0)):
+            raise SystemExit("bench: %s differs from the oracle (phases, synthetic row)" % name)
+        sts = []
+        for c in range(0, copies, 19):
+            st = g.new_stats(1, dev)
+            g.gvr_topk_ex(scores[c:c + 1], rl, prior, K_TOPK, stats=st, options=opts)
+            sts.append(st)
+        torch.cuda.synchronize()
+        line = {"mode": "phases", "workload": "rope_synthetic_n70690_b1", "variant": name, "flags": flags,
+                "kernel_us": round(us, 3)}
+        line.update(_phase_table([g.decode_stats(s) for s in sts], rate))
+        print(json.dumps(line))
+        sys.stdout.flush()
+    del scores, outs
+    torch.cuda.empty_cache()
+
+    # the 100K decode workload (128 rows per call)
+    w, outs_c, prevs = build_inputs(dev, CONFIG, None, list(range(16)))
+    out = torch.empty((w.rows, K_TOPK), dtype=torch.int32, device=dev)
+    T = w.scores.shape[0]
+    for name, flags in PHASE_VARIANTS:
+        opts = {"flags": flags}
+        calls = [lambda s, t=t: g.gvr_topk_ex(w.scores[t], w.row_len[t], prevs[t], K_TOPK, out_idx=out,
+                                                 stream=s, options=opts) for t in range(1, T)]
+        us = replay_us(calls, max(1, args.steps // (T - 1)))
+        sts = []
+        for t in range(1, T):
+            st = g.new_stats(w.rows, dev)
+            o = g.gvr_topk_ex(w.scores[t], w.row_len[t], prevs[t], K_TOPK, stats=st, options=opts)
+            if not torch.equal(o, outs_c[t]):
+                raise SystemExit("bench: %s differs from the reference chain (phases, decode step %d)" % (name, t))
+            sts.append(st)
+        torch.cuda.synchronize()
+        line = {"mode": "phases", "workload": w.name, "variant": name, "flags": flags, "kernel_us": round(us, 3)}
+        line.update(_phase_table([g.decode_stats(s) for s in sts], rate))
+        print(json.dumps(line))
+        sys.stdout.flush()
+
+
 def read_traffic(n_launch_bytes):
     if not os.path.exists(TRAFFIC_FILE):
         return None
@@ -322,7 +450,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--mode", choices=["bench", "copy", "configs", "rope"], default="bench")
+    ap.add_argument("--mode", choices=["bench", "copy", "configs", "rope", "phases"], default="bench")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--no-radix", action="store_true", help="skip timing radix_topk")
     ap.add_argument("--no-secant", action="store_true",
@@ -354,6 +482,9 @@ def main():
         return
     if args.mode == "rope":
         run_rope(args, dev)
+        return
+    if args.mode == "phases":
+        run_phases(args, dev)
         return
 
     w, outs, prevs = build_inputs(dev)

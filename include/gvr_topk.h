@@ -135,8 +135,9 @@ typedef struct gvr_row_stats {
     float pmean;           /* mean of the guessed scores (T0 of Sec. 4.2.1) */
     int32_t refine_iters;  /* snap iterations of the paper's selection (flag
                               bit 3), else 0 */
-    int64_t t_start;       /* s_memtime stamps of the row's workgroup (shader */
-    int64_t t_guess;       /*   clock): start; guess ready;                    */
+    int64_t t_start;       /* stamps of the row's workgroup on the GPU's     */
+    int64_t t_guess;       /*   constant-rate clock (s_memrealtime, 100 MHz  */
+                           /*   on MI355X): start; guess ready;              */
     int64_t t_search;      /*   threshold accepted (last pass done);           */
     int64_t t_collect;     /*   refine starts;                                 */
     int64_t t_refine;      /*   output written.                                */

@@ -196,7 +196,9 @@ DEV int wave_incl_scan(int v, int /*lane*/) {
 DEV int sum_over_waves(const int* vals, int lane) { return wave_sum(lane < kNW ? vals[lane] : 0); }
 DEV int sum_over_waves_below(const int* vals, int lane, int wave) { return wave_sum(lane < wave ? vals[lane] : 0); }
 
-DEV int64_t stamp() { return (int64_t)__builtin_amdgcn_s_memtime(); }
+// Time stamps of the row stats: the GPU's constant-rate clock (100 MHz on
+// MI355X), so phase times do not depend on the shader clock.
+DEV int64_t stamp() { return (int64_t)__builtin_amdgcn_s_memrealtime(); }
 
 // Workgroup barrier that orders LDS accesses only: unlike __syncthreads()
 // it does not wait for the wave's outstanding global loads, so prefetched
@@ -1133,8 +1135,8 @@ DEV void topk_body(const Params& p) {
             sm.seg_cnt[wave] = min(cnt_w, kCapW);
         }
         passes = 1;
-        t2 = stamp();
         lds_barrier();
+        t2 = stamp();   // every wave of the part has streamed its slabs
         overflow = wave_max_u(lane < kNW ? (uint32_t)sm.wa[lane] : 0u) > (uint32_t)kCapW;
         f_spec = overflow ? -1 : sum_over_waves(sm.wa, lane);
         hist_ready = own_hist && !overflow;

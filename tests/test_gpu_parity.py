@@ -99,6 +99,8 @@ def test_stats_invariants_config2():
             assert int(st["kth_key"][r]) == int(kth[r])
             assert int(st["n_gt"][r]) == int(ngt[r])
             assert int(st["n"][r]) == int(rl[r])
+            stamps = [int(st[k][r]) for k in ("t_start", "t_guess", "t_search", "t_collect", "t_refine")]
+            assert stamps == sorted(stamps) and stamps[0] > 0, stamps
 
 
 def test_guess_does_not_change_the_answer():
