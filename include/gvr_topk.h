@@ -85,7 +85,8 @@ typedef enum {
 /* Per-row outcome codes reported in gvr_row_stats.path. */
 enum {
     GVR_PATH_TRIVIAL = 0,      /* n <= K: iota / -1 padding */
-    GVR_PATH_ALL = 1,          /* K < n <= C: every element is a candidate */
+    GVR_PATH_ALL = 1,          /* K < n <= C and no guess, or K < n <= 2K:
+                                  every element is a candidate */
     GVR_PATH_GUESS = 2,        /* the guessed threshold held the answer: one pass */
     GVR_PATH_NARROWED = 3,     /* guess fell short; count passes narrowed the threshold */
     GVR_PATH_TIES = 4,         /* the K-th key isolated exactly (ties straddle
@@ -98,8 +99,9 @@ enum {
 /* Optional knobs (NULL = defaults). Zero fields mean "default". */
 typedef struct gvr_options {
     int32_t capacity;      /* refine capacity C, K <= C <= GVR_MAX_CANDIDATES
-                              (default GVR_MAX_CANDIDATES); a smaller C forces
-                              more narrowing passes, never another result */
+                              (default GVR_MAX_CANDIDATES, at most 4096 in the
+                              short-row shape); a smaller C forces more
+                              narrowing passes, never another result */
     int32_t flags;         /* bit 0: ignore prev_topk (run the radix schedule);
                               bit 1: place the parts of a row on different XCDs
                               (a test of the path that does not rely on their
@@ -111,7 +113,14 @@ typedef struct gvr_options {
                               bit 3: the paper's own exact selection (Sec. 4.2.4:
                               min / max, 2048-bin histogram with a wave-parallel
                               bin search, snap iterations, partition) instead of
-                              the histogram + rank-count refine */
+                              the histogram + rank-count refine;
+                              bit 4: force the short-row workgroup shape (4
+                              waves, C <= 4096, three workgroups per compute
+                              unit, no row splitting); bit 5: force the
+                              16-wave shape; neither: 4 waves when there are
+                              more than three rows per compute unit and
+                              ld <= 12288, else 16. Bits 4 and 5 together are
+                              an error. No bit changes the result. */
     int32_t parts;         /* workgroups per row, 1..16 (0 = chosen from B, ld
                               and the device's compute units; a forced value is
                               lowered so that B * parts <= 2048); never changes

@@ -64,16 +64,30 @@
 
 namespace {
 
-constexpr int kBlock = 1024;
 constexpr int kWave = 64;
-constexpr int kNW = kBlock / kWave;            // 16 waves
 constexpr int kU = 8;                          // slabs in flight per wave (count / collect passes)
 constexpr int kSU = 8;                         // slabs in flight per wave (speculative pass)
-constexpr int kSW = kNW - 1;                   // streaming waves of the speculative pass (wave 0: guess)
 constexpr int kBins = 256;                     // bins of a counting window
 constexpr int kBinsX = kBins + 1;              // + "at or above the window"
-constexpr int kCap = GVR_MAX_CANDIDATES;       // list capacity (LDS)
-constexpr int kCapW = kCap / kNW;              // per-wave list capacity, speculative pass
+constexpr int kCapW = 1024;                    // per-wave list capacity, speculative pass
+constexpr int kPartCap = GVR_MAX_CANDIDATES;   // entries per (row, part) list in the split-row workspace
+
+// Workgroup shape: NW wave64s, 1024 list entries per wave. The 16-wave shape
+// (128 KB of lists, one workgroup per compute unit) streams a long row as
+// fast as one compute unit can and is the only one that splits rows; the
+// 4-wave shape (32 KB of lists, three workgroups per compute unit) serves
+// large batches of short rows, whose time goes into per-row latency.
+template <int NW>
+struct Shape {
+    static constexpr int kNW = NW;
+    static constexpr int kBlock = NW * kWave;
+    static constexpr int kSW = NW - 1;          // streaming waves of the speculative pass (wave 0: guess)
+    static constexpr int kCap = NW * kCapW;     // list capacity C (LDS)
+};
+constexpr int kNWLong = 16;
+constexpr int kNWShort = 4;
+constexpr int64_t kShortMaxLd = 12288;        // longest row stride the 4-wave shape is chosen for
+static_assert(Shape<kNWLong>::kCap == GVR_MAX_CANDIDATES, "the long-row shape holds the largest capacity");
 constexpr int kRefBins = 4096;                 // bins of a narrowing refine level (12 bits of key)
 constexpr int kRefBins1 = 2048;                // bins of the first refine level (32 per lane of one wave)
 constexpr int kGuessSamples = 256;             // guessed indices gathered: a strided sample of prev_topk
@@ -88,7 +102,6 @@ constexpr int kMinPartElems = 16384;           // a row is split only into parts
 constexpr int kMaxSlots = 2048;                // (row, part) pairs of one split call: 256 MB of workspace
 constexpr int kXcds = 8;                       // gfx950 XCDs; workgroup i runs on XCD i % 8
 
-static_assert(GVR_MAX_CANDIDATES % kNW == 0, "per-wave capacity");
 static_assert((kBins & (kBins - 1)) == 0 && (kRefBins & (kRefBins - 1)) == 0 && (kRefBins1 & (kRefBins1 - 1)) == 0 &&
                   (kGuessBins & (kGuessBins - 1)) == 0, "bin counts are powers of two");
 static_assert(kSmall * 4 <= kRefBins, "refine candidates over the histogram");
@@ -112,7 +125,7 @@ struct Params {
                          // bit 16; 0 between calls
     int32_t* part_count; // [rows][S] f(threshold) of each part, bit 31 = a wave list overflowed
     uint32_t* part_thresh; // [rows][S] threshold of each part's list (T_spec, the same in every part)
-    uint64_t* part_list; // [rows][S][kCap] (fp32 bits | index << 32) of each part
+    uint64_t* part_list; // [rows][S][kPartCap] (fp32 bits | index << 32) of each part
 };
 
 // ------------------------------------------------------------------ helpers
@@ -193,7 +206,8 @@ DEV int wave_incl_scan(int v, int /*lane*/) {
 }
 // Lane v of every wave reads wave v's value: one LDS read + one wave
 // reduction per cross-wave sum.
-DEV int sum_over_waves(const int* vals, int lane) { return wave_sum(lane < kNW ? vals[lane] : 0); }
+template <int NW>
+DEV int sum_over_waves(const int* vals, int lane) { return wave_sum(lane < NW ? vals[lane] : 0); }
 DEV int sum_over_waves_below(const int* vals, int lane, int wave) { return wave_sum(lane < wave ? vals[lane] : 0); }
 
 // Time stamps of the row stats: the GPU's constant-rate clock (100 MHz on
@@ -258,36 +272,42 @@ DEV int add_lane_bit(int q, uint64_t m) {
 }
 
 // ------------------------------------------------------------------ LDS
+template <int NW>
 struct Smem {
-    uint2 list[kCap];                   // candidates (key, index), per-wave segments
+    uint2 list[Shape<NW>::kCap];                   // candidates (key, index), per-wave segments
     union alignas(16) {
-        int hist[kNW][kBinsX];          // wave-private counting histograms
+        int hist[NW][kBinsX];          // wave-private counting histograms
         int rhist[kRefBins];            // refine / guess histogram
     } u;
     int F[kBinsX + 1];                  // F[j] = f(edge j) over the row
-    int seg_off[kNW];                   // list segment of each wave
-    int seg_cnt[kNW];
-    int wa[kNW];
-    int wb[kNW];
-    int red[4][kNW];
-    float redf[kNW];
+    int seg_off[NW];                   // list segment of each wave
+    int seg_cnt[NW];
+    int wa[NW];
+    int wb[NW];
+    int red[4][NW];
+    float redf[NW];
     int scal[8];
     int guess_ready;                    // set by wave 0 once T_spec is in scal[4..7]
 };
 // Passes over the lists read four 64-entry chunks at a time, up to 255
 // entries past a segment's count (masked afterwards): the list must be
 // followed by that much LDS.
-static_assert(offsetof(Smem, u) == sizeof(uint2) * kCap && sizeof(Smem::u) >= 4 * kWave * sizeof(uint2),
-              "LDS slack after the candidate list");
+template <int NW>
+constexpr bool lds_slack_ok() {
+    return offsetof(Smem<NW>, u) == sizeof(uint2) * Shape<NW>::kCap && sizeof(Smem<NW>::u) >= 4 * kWave * sizeof(uint2);
+}
+static_assert(lds_slack_ok<kNWLong>() && lds_slack_ok<kNWShort>(), "LDS slack after the candidate list");
 
-// Block-wide exclusive scan of one int (all kBlock threads). Returns the total.
-DEV int block_excl_scan(int& a, Smem& sm, int tid) {
+// Block-wide exclusive scan of one int (all threads of the workgroup). Returns the total.
+template <int NW>
+DEV int block_excl_scan(int& a, Smem<NW>& sm, int tid) {
+    using W = Shape<NW>;
     const int lane = tid & 63, wave = tid >> 6;
     const int ia = wave_incl_scan(a, lane);
     if (lane == kWave - 1) sm.wa[wave] = ia;
     __syncthreads();
     const int before = sum_over_waves_below(sm.wa, lane, wave);
-    const int tot = sum_over_waves(sm.wa, lane);
+    const int tot = sum_over_waves<NW>(sm.wa, lane);
     __syncthreads();
     a = before + ia - a;
     return tot;
@@ -359,13 +379,15 @@ DEV void block_keys(const float4& v, uint32_t (&k)[4]) {
 // Exact K-th key among the listed candidates. The K-th key lies in
 // [wlo, whi]; `above` listed candidates lie above whi. Wave w's list segment
 // is list[seg_off[w] .. + seg_cnt[w]).
-DEV uint32_t refine_kth(Smem& sm, uint32_t wlo, uint32_t whi, int above, int K, int tid) {
+template <int NW>
+DEV uint32_t refine_kth(Smem<NW>& sm, uint32_t wlo, uint32_t whi, int above, int K, int tid) {
+    using W = Shape<NW>;
     const int lane = tid & 63, wave = tid >> 6;
     int need = K - above;   // >= 1
     for (int level = 0; level < 4 && wlo != whi; ++level) {
         const uint64_t width = (uint64_t)whi - wlo + 1;
         const uint32_t s = bin_shift(width, log2i(kRefBins));
-        for (int i = tid; i < kRefBins; i += kBlock) sm.u.rhist[i] = 0;
+        for (int i = tid; i < kRefBins; i += W::kBlock) sm.u.rhist[i] = 0;
         lds_barrier();
         {
             const uint2* seg = sm.list + sm.seg_off[wave];
@@ -378,7 +400,7 @@ DEV uint32_t refine_kth(Smem& sm, uint32_t wlo, uint32_t whi, int above, int K, 
             }
         }
         lds_barrier();
-        constexpr int PER = kRefBins / kBlock;   // 4 bins per thread
+        constexpr int PER = kRefBins / W::kBlock;   // 4 bins per thread
         int loc[PER];
         int mine = 0;
 #pragma unroll
@@ -418,7 +440,9 @@ DEV uint32_t refine_kth(Smem& sm, uint32_t wlo, uint32_t whi, int above, int K, 
 // Emission: this wave's list segment holds `gb` keys > T and `eb` keys == T
 // in the segments before it; write every key > T and the first `take` keys
 // == T (list order = index order) at their ranks: ascending index output.
-DEV void emit_segment(const Smem& sm, uint32_t T, int K, int take, int gb, int eb, int32_t* out, int lane, int wave) {
+template <int NW>
+DEV void emit_segment(const Smem<NW>& sm, uint32_t T, int K, int take, int gb, int eb, int32_t* out, int lane, int wave) {
+    using W = Shape<NW>;
     const uint2* seg = sm.list + sm.seg_off[wave];
     const int cnt = sm.seg_cnt[wave];
     for (int i0 = 0; i0 < cnt; i0 += 4 * kWave) {
@@ -454,7 +478,9 @@ DEV void emit_segment(const Smem& sm, uint32_t T, int K, int take, int gb, int e
 
 // Write the selection from the lists: every key > T, then the first `take`
 // keys == T in list (= index) order; output in ascending index order.
-DEV void emit_from_lists(Smem& sm, uint32_t T, int K, int32_t* out, int tid, int* n_gt_out) {
+template <int NW>
+DEV void emit_from_lists(Smem<NW>& sm, uint32_t T, int K, int32_t* out, int tid, int* n_gt_out) {
+    using W = Shape<NW>;
     const int lane = tid & 63, wave = tid >> 6;
     const uint2* seg = sm.list + sm.seg_off[wave];
     const int cnt = sm.seg_cnt[wave];
@@ -473,7 +499,7 @@ DEV void emit_from_lists(Smem& sm, uint32_t T, int K, int32_t* out, int tid, int
     lds_barrier();
     const int gb = sum_over_waves_below(sm.wa, lane, wave);
     const int eb = sum_over_waves_below(sm.wb, lane, wave);
-    const int gtot = sum_over_waves(sm.wa, lane);
+    const int gtot = sum_over_waves<NW>(sm.wa, lane);
     emit_segment(sm, T, K, K - gtot, gb, eb, out, lane, wave);
     *n_gt_out = gtot;
 }
@@ -495,7 +521,9 @@ DEV void emit_from_lists(Smem& sm, uint32_t T, int K, int32_t* out, int tid, int
 // the bin instead (not reached on the workloads measured).
 constexpr int kPaperBins = 2048;
 constexpr int kMaxSnap = 64;
-DEV uint32_t paper_refine_emit(Smem& sm, int K, int32_t* out, int tid, int* n_gt_out, int* snaps_out) {
+template <int NW>
+DEV uint32_t paper_refine_emit(Smem<NW>& sm, int K, int32_t* out, int tid, int* n_gt_out, int* snaps_out) {
+    using W = Shape<NW>;
     const int lane = tid & 63, wave = tid >> 6;
     const uint2* seg = sm.list + sm.seg_off[wave];
     const int cnt = sm.seg_cnt[wave];
@@ -511,31 +539,34 @@ DEV uint32_t paper_refine_emit(Smem& sm, int K, int32_t* out, int tid, int* n_gt
         sm.red[2][wave] = (int)mn;
         sm.red[3][wave] = (int)mx;
     }
-    for (int i = tid; i < kPaperBins; i += kBlock) sm.u.rhist[i] = 0;
+    for (int i = tid; i < kPaperBins; i += W::kBlock) sm.u.rhist[i] = 0;
     lds_barrier();
-    const uint32_t kmin = wave_min_u(lane < kNW ? (uint32_t)sm.red[2][lane] : 0xFFFFFFFFu);
-    const uint32_t kmax = wave_max_u(lane < kNW ? (uint32_t)sm.red[3][lane] : 0u);
+    const uint32_t kmin = wave_min_u(lane < NW ? (uint32_t)sm.red[2][lane] : 0xFFFFFFFFu);
+    const uint32_t kmax = wave_max_u(lane < NW ? (uint32_t)sm.red[3][lane] : 0u);
     // (4b) histogram over [kmin, kmax]
     const uint32_t sh = bin_shift((uint64_t)kmax - kmin + 1, log2i(kPaperBins));
     for (int i = lane; i < cnt; i += kWave)
         __hip_atomic_fetch_add(&sm.u.rhist[(seg[i].x - kmin) >> sh], 1, __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_WORKGROUP);
     lds_barrier();
-    constexpr int kPerWave = kPaperBins / kNW;   // 128: wave w holds bins [top - 128 (w + 1), top - 128 w)
+    constexpr int kPerWave = kPaperBins / NW;   // wave w holds bins [top - kPerWave (w + 1), top - kPerWave w)
     {
         const int b0 = kPaperBins - kPerWave * (wave + 1);
-        const int t = wave_sum(sm.u.rhist[b0 + lane] + sm.u.rhist[b0 + kWave + lane]);
+        int t = 0;
+#pragma unroll
+        for (int j = 0; j < kPerWave / kWave; ++j) t += sm.u.rhist[b0 + j * kWave + lane];
+        t = wave_sum(t);
         if (lane == 0) sm.wa[wave] = t;
     }
     lds_barrier();
-    if (tid == 0) {   // target wave: 16 serial steps from the top
+    if (tid == 0) {   // target wave: one serial step per wave from the top
         int run = 0, w = 0;
-        for (; w < kNW - 1 && run + sm.wa[w] < K; ++w) run += sm.wa[w];
+        for (; w < NW - 1 && run + sm.wa[w] < K; ++w) run += sm.wa[w];
         sm.scal[0] = w;
         sm.scal[1] = run;
     }
     lds_barrier();
-    if (wave == sm.scal[0] && lane == 0) {   // exact bin: up to 128 serial steps from the top of the wave's bins
+    if (wave == sm.scal[0] && lane == 0) {   // exact bin: up to kPerWave serial steps from the top of the wave's bins
         int run = sm.scal[1];
         int b = kPaperBins - kPerWave * wave - 1;
         const int bend = kPaperBins - kPerWave * (wave + 1);
@@ -578,16 +609,16 @@ DEV uint32_t paper_refine_emit(Smem& sm, int K, int32_t* out, int tid, int* n_gt
             sm.red[3][wave] = (int)down;
         }
         lds_barrier();
-        const int GE = sum_over_waves(sm.wa, lane);
-        const int GT = sum_over_waves(sm.wb, lane);
+        const int GE = sum_over_waves<NW>(sm.wa, lane);
+        const int GT = sum_over_waves<NW>(sm.wb, lane);
         if (GT < K && K <= GE) {
             found = true;
             ngt = GT;
             break;
         }
         // fewer than K at or above T: step down; K or more above T: step up
-        T = (GE < K) ? wave_max_u(lane < kNW ? (uint32_t)sm.red[3][lane] : 0u)
-                     : wave_min_u(lane < kNW ? (uint32_t)sm.red[2][lane] : 0xFFFFFFFFu);
+        T = (GE < K) ? wave_max_u(lane < NW ? (uint32_t)sm.red[3][lane] : 0u)
+                     : wave_min_u(lane < NW ? (uint32_t)sm.red[2][lane] : 0xFFFFFFFFu);
     }
     lds_barrier();
     if (!found) T = refine_kth(sm, (uint32_t)blo, (uint32_t)bhi, above, K, tid);
@@ -606,14 +637,18 @@ DEV uint32_t ref_shift(uint32_t rlo, uint32_t bin_hi) {
     return sh;
 }
 DEV int ref_bin(uint32_t kk, uint32_t rlo, uint32_t sh) { return (int)min((kk - rlo) >> sh, (uint32_t)kRefBins1 - 1); }
-DEV void ref_hist_add(Smem& sm, uint32_t kk, uint32_t rlo, uint32_t sh) {
+template <int NW>
+DEV void ref_hist_add(Smem<NW>& sm, uint32_t kk, uint32_t rlo, uint32_t sh) {
+    using W = Shape<NW>;
     __hip_atomic_fetch_add(&sm.u.rhist[ref_bin(kk, rlo, sh)], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 
 // One wave: turn the fp32 bit patterns of its list segment seg[0, cnt) into
 // keys in place and, if `hist`, add them to the first refine level from rlo.
 // Four entries per lane are read before any is written back.
-DEV void keys_in_place(Smem& sm, uint2* seg, int cnt, bool hist, uint32_t rlo, uint32_t sh, int lane) {
+template <int NW>
+DEV void keys_in_place(Smem<NW>& sm, uint2* seg, int cnt, bool hist, uint32_t rlo, uint32_t sh, int lane) {
+    using W = Shape<NW>;
     for (int i0 = 0; i0 < cnt; i0 += 4 * kWave) {
         uint32_t b[4];
 #pragma unroll
@@ -643,8 +678,10 @@ DEV void keys_in_place(Smem& sm, uint2* seg, int cnt, bool hist, uint32_t rlo, u
 // among them and the per-wave emission offsets, and every wave emits its
 // segment.
 // Otherwise histogram narrowing (refine_kth) continues inside b.
-DEV uint32_t refine_emit(Smem& sm, uint32_t rlo, uint32_t rhi, uint32_t bin_hi, int above, int K, int32_t* out,
+template <int NW>
+DEV uint32_t refine_emit(Smem<NW>& sm, uint32_t rlo, uint32_t rhi, uint32_t bin_hi, int above, int K, int32_t* out,
                          int tid, int* n_gt_out, bool hist_ready) {
+    using W = Shape<NW>;
     const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const uint2* seg = sm.list + sm.seg_off[wave];
     const int cnt = sm.seg_cnt[wave];
@@ -652,7 +689,7 @@ DEV uint32_t refine_emit(Smem& sm, uint32_t rlo, uint32_t rhi, uint32_t bin_hi, 
     int* hb = sm.u.rhist;
     if (tid == 0) sm.scal[1] = 0;
     if (!hist_ready) {
-        for (int i = tid; i < kRefBins1; i += kBlock) hb[i] = 0;
+        for (int i = tid; i < kRefBins1; i += W::kBlock) hb[i] = 0;
         lds_barrier();
         for (int i = lane; i < cnt; i += kWave) {
             const uint32_t kk = seg[i].x;
@@ -765,11 +802,11 @@ DEV uint32_t refine_emit(Smem& sm, uint32_t rlo, uint32_t rhi, uint32_t bin_hi, 
         // each candidate adds itself to its wave's counts.
         if (v && mine.x > kth) __hip_atomic_fetch_add(&sm.wa[mine.z], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
         if (v && mine.x == kth) __hip_atomic_fetch_add(&sm.wb[mine.z], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-        const int gw = lane < kNW ? sm.wa[lane] : 0;
-        const int ew = lane < kNW ? sm.wb[lane] : 0;
+        const int gw = lane < NW ? sm.wa[lane] : 0;
+        const int ew = lane < NW ? sm.wb[lane] : 0;
         const int gi = wave_incl_scan(gw, lane), ei = wave_incl_scan(ew, lane);
         const int gtot = __builtin_amdgcn_readlane(gi, 63);
-        if (lane < kNW) {
+        if (lane < NW) {
             sm.red[0][lane] = gi - gw;
             sm.red[1][lane] = ei - ew;
         }
@@ -809,9 +846,10 @@ constexpr uint32_t kKeyZeroBits = 0xFFFFFFFFu;
 
 DEV uint64_t pack_entry(uint32_t bits, uint32_t idx) { return (uint64_t)bits | ((uint64_t)idx << 32); }
 
-template <bool GUESS>
+template <bool GUESS, int NW>
 DEV void topk_body(const Params& p) {
-    __shared__ Smem sm;
+    __shared__ Smem<NW> sm;
+    using W = Shape<NW>;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int S = p.parts;
@@ -856,7 +894,7 @@ DEV void topk_body(const Params& p) {
     // (a1) row classify: n <= K -> 0..n-1 then -1 padding (part 0 writes).
     if (n <= K) {
         if (part != 0) return;
-        for (int i = tid; i < K; i += kBlock) out[i] = (i < n) ? i : -1;
+        for (int i = tid; i < K; i += W::kBlock) out[i] = (i < n) ? i : -1;
         if (st && tid == 0) {
             gvr_row_stats s = {};
             s.n = n;
@@ -876,22 +914,24 @@ DEV void topk_body(const Params& p) {
     const int nq = (n + aoff + 3) >> 2;
     const int qlast = nq - 1;
     const int nslab_row = (nq + 63) >> 6;
-    const int per = ((nslab_row + kNW - 1) / kNW) * 64;   // whole slabs per wave
+    const int per = ((nslab_row + NW - 1) / NW) * 64;   // whole slabs per wave
     const int qb = min(wave * per, nq), qe = min(qb + per, nq);
     // This part's slabs [ps0, ps1); waves 1..15 stream them in the
     // speculative pass, wave 0 computes the guess meanwhile and streams
     // nothing: this wave's float4 blocks [sqb, sqe).
     const int ps = (nslab_row + S - 1) / S;
     const int ps0 = min(part * ps, nslab_row), ps1 = min(ps0 + ps, nslab_row);
-    const int ws = (ps1 - ps0 + kSW - 1) / kSW;
+    const int ws = (ps1 - ps0 + W::kSW - 1) / W::kSW;
     const int sw = wave - 1;
     const int sqb = wave == 0 ? 0 : min((ps0 + sw * ws) * 64, min(ps1 * 64, nq));
     const int sqe = wave == 0 ? 0 : min((ps0 + min((sw + 1) * ws, ps1 - ps0)) * 64, nq);
     const int nsl = sqe > sqb ? (sqe - sqb + 63) >> 6 : 0;
 
-    // Without a guess, every element is a candidate when the row fits the
-    // lists (a guess, when given, also cuts a short row's candidates).
-    const bool all_mode = !(GUESS && p.prev) && (n <= cap) && (ws * 256 <= kCapW);
+    // Every element is a candidate when the row fits the lists and there is
+    // no guess, or the row is at most 2K long: there a guess cuts few
+    // candidates and often leaves f(T_spec) < K (a guess also cuts the
+    // candidates of longer short rows).
+    const bool all_mode = (!(GUESS && p.prev) || n <= 2 * K) && (n <= cap) && (ws * 256 <= kCapW);
     bool have_prev = GUESS && p.prev && !all_mode;
     // The paper's Phase 2 schedule (secant counting passes), when asked for.
     const bool secant = GUESS && p.secant && have_prev;
@@ -905,7 +945,7 @@ DEV void topk_body(const Params& p) {
     bool hist_ready = false; // the refine's first histogram level is built (lists at tthr)
     uint32_t tthr = 0u;      // threshold of the speculative lists
     bool overflow = false;
-    if (tid < kNW) sm.seg_off[tid] = tid * kCapW;
+    if (tid < NW) sm.seg_off[tid] = tid * kCapW;
 
     if (spec) {
         if (!all_mode) {
@@ -1137,8 +1177,8 @@ DEV void topk_body(const Params& p) {
         passes = 1;
         lds_barrier();
         t2 = stamp();   // every wave of the part has streamed its slabs
-        overflow = wave_max_u(lane < kNW ? (uint32_t)sm.wa[lane] : 0u) > (uint32_t)kCapW;
-        f_spec = overflow ? -1 : sum_over_waves(sm.wa, lane);
+        overflow = wave_max_u(lane < NW ? (uint32_t)sm.wa[lane] : 0u) > (uint32_t)kCapW;
+        f_spec = overflow ? -1 : sum_over_waves<NW>(sm.wa, lane);
         hist_ready = own_hist && !overflow;
         tthr = tspec;
 
@@ -1149,7 +1189,7 @@ DEV void topk_body(const Params& p) {
             // peaks) do this. If K <= f(T_spec) <= C a second pass over the
             // part's slabs (just read, so L2-resident) collects them again at
             // exact per-wave offsets instead of narrowing from scratch.
-            const int f_all = sum_over_waves(sm.wa, lane);
+            const int f_all = sum_over_waves<NW>(sm.wa, lane);
             if (f_all >= K && f_all <= cap) {
                 const int off = sum_over_waves_below(sm.wa, lane, wave);
                 const int mine = sm.wa[wave];
@@ -1233,7 +1273,7 @@ DEV void topk_body(const Params& p) {
             // whole row itself. A plain load by the last part cannot hit a
             // stale vector-L1 line: this workgroup never read those lines
             // before, and each launch starts with invalidated L1s.
-            uint64_t* plist = p.part_list + (row * S + part) * (int64_t)kCap;
+            uint64_t* plist = p.part_list + (row * S + part) * (int64_t)kPartCap;
             const bool publish = !overflow && f_spec <= cap;
             if (publish) {   // this part's entries, in index order
                 const int off = sum_over_waves_below(sm.wa, lane, wave);
@@ -1276,7 +1316,7 @@ DEV void topk_body(const Params& p) {
                 f_spec = -1;
             } else {
                 // Up to four parts: each thread loads the first entries of
-                // every part's list (positions tid + j * kBlock, j < kSpecJ)
+                // every part's list (positions tid + j * W::kBlock, j < kSpecJ)
                 // together with the counts, before it knows which of them
                 // exist: one round trip for the usual lists.
                 const int kSpecJ = S <= 2 ? 2 : 1;
@@ -1286,7 +1326,7 @@ DEV void topk_body(const Params& p) {
 #pragma unroll
                     for (int k = 0; k < 4; ++k) {
                         const int q = kSpecJ == 2 ? k >> 1 : k, j = kSpecJ == 2 ? k & 1 : 0;
-                        if (q < S) ev[k] = p.part_list[(row * S + q) * (int64_t)kCap + tid + j * kBlock];
+                        if (q < S) ev[k] = p.part_list[(row * S + q) * (int64_t)kPartCap + tid + j * W::kBlock];
                     }
                 }
                 // Totals and part offsets of the merged list (parts in index
@@ -1307,7 +1347,7 @@ DEV void topk_body(const Params& p) {
                     // Merged list in LDS, split evenly over the waves; the
                     // refine's first histogram level is built on the way.
                     const uint32_t msh = ref_shift(trow, max(gmax, trow));
-                    for (int i = tid; i < kRefBins1; i += kBlock) sm.u.rhist[i] = 0;
+                    for (int i = tid; i < kRefBins1; i += W::kBlock) sm.u.rhist[i] = 0;
                     lds_barrier();   // the histogram is cleared; the loads stay in flight
                     auto put = [&](int P, uint64_t e) {
                         sm.list[P] = make_uint2((uint32_t)e, (uint32_t)(e >> 32));
@@ -1318,27 +1358,27 @@ DEV void topk_body(const Params& p) {
                         for (int k = 0; k < 4; ++k) {
                             const int q = kSpecJ == 2 ? k >> 1 : k, j = kSpecJ == 2 ? k & 1 : 0;
                             const int cq = __builtin_amdgcn_readlane(cc, min(q, S - 1)), oq = __builtin_amdgcn_readlane(coff, min(q, S - 1));
-                            const int i = tid + j * kBlock;
+                            const int i = tid + j * W::kBlock;
                             if (q < S && i < cq) put(oq + i, ev[k]);
                         }
-                        // entries past the first kSpecJ * kBlock of a part (rare)
+                        // entries past the first kSpecJ * W::kBlock of a part (rare)
                         for (int q = 0; q < S; ++q) {
                             const int cq = __builtin_amdgcn_readlane(cc, q), oq = __builtin_amdgcn_readlane(coff, q);
-                            const uint64_t* src = p.part_list + (row * S + q) * (int64_t)kCap;
-                            for (int i = kSpecJ * kBlock + tid; i < cq; i += kBlock) put(oq + i, src[i]);
+                            const uint64_t* src = p.part_list + (row * S + q) * (int64_t)kPartCap;
+                            for (int i = kSpecJ * W::kBlock + tid; i < cq; i += W::kBlock) put(oq + i, src[i]);
                         }
                     } else {
-                        // Each thread owns merged positions tid + j * kBlock
+                        // Each thread owns merged positions tid + j * W::kBlock
                         // and loads four of them (from their parts' lists)
                         // before it stores any.
-                        const int jn = (f_spec + kBlock - 1) / kBlock;
+                        const int jn = (f_spec + W::kBlock - 1) / W::kBlock;
                         for (int j0 = 0; j0 < jn; j0 += 4) {
                             int qj[4] = {0, 0, 0, 0}, oj[4] = {0, 0, 0, 0};
                             for (int q = 1; q < S; ++q) {
                                 const int bq = __builtin_amdgcn_readlane(coff, q);
 #pragma unroll
                                 for (int jj = 0; jj < 4; ++jj) {
-                                    const bool past = tid + (j0 + jj) * kBlock >= bq;
+                                    const bool past = tid + (j0 + jj) * W::kBlock >= bq;
                                     qj[jj] += past;
                                     oj[jj] = past ? bq : oj[jj];
                                 }
@@ -1346,19 +1386,19 @@ DEV void topk_body(const Params& p) {
                             uint64_t e[4];
 #pragma unroll
                             for (int jj = 0; jj < 4; ++jj) {
-                                const int P = tid + (j0 + jj) * kBlock;
-                                e[jj] = P < f_spec ? p.part_list[(row * S + qj[jj]) * (int64_t)kCap + (P - oj[jj])] : 0ull;
+                                const int P = tid + (j0 + jj) * W::kBlock;
+                                e[jj] = P < f_spec ? p.part_list[(row * S + qj[jj]) * (int64_t)kPartCap + (P - oj[jj])] : 0ull;
                             }
 #pragma unroll
                             for (int jj = 0; jj < 4; ++jj) {
-                                const int P = tid + (j0 + jj) * kBlock;
+                                const int P = tid + (j0 + jj) * W::kBlock;
                                 if (P < f_spec) put(P, e[jj]);
                             }
                         }
                     }
                     hist_ready = true;
-                    const int chunk = (f_spec + kNW - 1) / kNW;
-                    if (tid < kNW) {
+                    const int chunk = (f_spec + NW - 1) / NW;
+                    if (tid < NW) {
                         const int o = min(tid * chunk, f_spec);
                         sm.seg_off[tid] = o;
                         sm.seg_cnt[tid] = min(chunk, f_spec - o);
@@ -1405,15 +1445,29 @@ DEV void topk_body(const Params& p) {
     }
 
     // Row-level decision (the single part, or the last part of the row).
+    // Thread t owns the kBinsX bins from the top in groups of kFper:
+    // bins kBins - kFper t - r, r < kFper (one bin each with 16 waves).
+    constexpr int kFper = (kBinsX + W::kBlock - 1) / W::kBlock;
     auto compute_F = [&]() {
         __syncthreads();   // every wave's histogram updates are done
-        int g = 0;
-        const int b = kBins - tid;   // thread t owns bin kBins - t (t < kBinsX)
-        if (b >= 0)
-            for (int v = 0; v < kNW; ++v) g += sm.u.hist[v][b];
-        int a = g;
-        block_excl_scan(a, sm, tid);
-        if (b >= 0) sm.F[b] = a + g;
+        int g[kFper];
+        int mine = 0;
+#pragma unroll
+        for (int r = 0; r < kFper; ++r) {
+            const int b = kBins - (kFper * tid + r);
+            g[r] = 0;
+            if (b >= 0)
+                for (int v = 0; v < NW; ++v) g[r] += sm.u.hist[v][b];
+            mine += g[r];
+        }
+        int a = mine;
+        block_excl_scan(a, sm, tid);   // keys in the bins above this thread's
+#pragma unroll
+        for (int r = 0; r < kFper; ++r) {
+            const int b = kBins - (kFper * tid + r);
+            a += g[r];
+            if (b >= 0) sm.F[b] = a;
+        }
         if (tid == 0) sm.F[kBinsX] = 0;
         __syncthreads();
     };
@@ -1421,7 +1475,8 @@ DEV void topk_body(const Params& p) {
     auto crossing = [&]() {
         if (tid == 0) sm.scal[2] = -1;
         __syncthreads();
-        if (tid < kBinsX && sm.F[tid] >= K && sm.F[tid + 1] < K) sm.scal[2] = tid;
+        for (int j = tid; j < kBinsX; j += W::kBlock)
+            if (sm.F[j] >= K && sm.F[j + 1] < K) sm.scal[2] = j;
         __syncthreads();
         const int j = sm.scal[2];
         __syncthreads();
@@ -1432,7 +1487,7 @@ DEV void topk_body(const Params& p) {
     // Count pass over window `win` (wave-private histograms, then F).
     auto count_pass = [&]() {
         __syncthreads();
-        for (int i = tid; i < kNW * kBinsX; i += kBlock) (&sm.u.hist[0][0])[i] = 0;
+        for (int i = tid; i < NW * kBinsX; i += W::kBlock) (&sm.u.hist[0][0])[i] = 0;
         __syncthreads();
         const uint32_t lo = win.lo, sh = win.shift;
         stream_wave(xa, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
@@ -1471,15 +1526,15 @@ DEV void topk_body(const Params& p) {
     uint32_t sec_lo = 0u, sec_hi = 0xFFFFFFFFu;   // f(sec_lo) > C, f(sec_hi) < K (bracket, keys)
     uint32_t row_max = 0xFFFFFFFFu;
     if (secant) {
-        if (tid < kNW) sm.seg_off[tid] = 0;
+        if (tid < NW) sm.seg_off[tid] = 0;
         // Phase 1: all K guessed scores, 2 per thread.
         const int32_t* pv = p.prev + row * (int64_t)K;
         uint32_t mn = 0xFFFFFFFFu, mx = 0u;
         float sum = 0.f;
         int cnt = 0;
 #pragma unroll
-        for (int m = 0; m < (GVR_MAX_K + kBlock - 1) / kBlock; ++m) {
-            const int j = tid + m * kBlock;
+        for (int m = 0; m < (GVR_MAX_K + W::kBlock - 1) / W::kBlock; ++m) {
+            const int j = tid + m * W::kBlock;
             const int idx = j < K ? pv[j] : -1;
             if (idx >= 0 && idx < n) {
                 const float v = x[idx];
@@ -1501,11 +1556,11 @@ DEV void topk_body(const Params& p) {
             sm.redf[wave] = sum;
         }
         __syncthreads();
-        gvalid = sum_over_waves(sm.red[0], lane);
-        gmin = wave_min_u(lane < kNW ? (uint32_t)sm.red[1][lane] : 0xFFFFFFFFu);
-        gmax = wave_max_u(lane < kNW ? (uint32_t)sm.red[2][lane] : 0u);
+        gvalid = sum_over_waves<NW>(sm.red[0], lane);
+        gmin = wave_min_u(lane < NW ? (uint32_t)sm.red[1][lane] : 0xFFFFFFFFu);
+        gmax = wave_max_u(lane < NW ? (uint32_t)sm.red[2][lane] : 0u);
         gsum = 0.f;
-        for (int v = 0; v < kNW; ++v) gsum += sm.redf[v];   // fixed order
+        for (int v = 0; v < NW; ++v) gsum += sm.redf[v];   // fixed order
         __syncthreads();
         t1 = stamp();
         // f(T) over the row (per-wave counts kept in sm.wa for the collect);
@@ -1539,10 +1594,10 @@ DEV void topk_body(const Params& p) {
                 sm.red[2][wave] = (int)hi;
             }
             __syncthreads();
-            const int f = sum_over_waves(sm.wa, lane);
+            const int f = sum_over_waves<NW>(sm.wa, lane);
             if (minmax) {
-                sec_lo = wave_min_u(lane < kNW ? (uint32_t)sm.red[1][lane] : 0xFFFFFFFFu);
-                row_max = wave_max_u(lane < kNW ? (uint32_t)sm.red[2][lane] : 0u);
+                sec_lo = wave_min_u(lane < NW ? (uint32_t)sm.red[1][lane] : 0xFFFFFFFFu);
+                row_max = wave_max_u(lane < NW ? (uint32_t)sm.red[2][lane] : 0u);
             }
             __syncthreads();
             return f;
@@ -1674,8 +1729,8 @@ DEV void topk_body(const Params& p) {
                 sm.red[3][wave] = (int)mx;
             }
             __syncthreads();
-            rlo = wave_min_u(lane < kNW ? (uint32_t)sm.red[2][lane] : 0xFFFFFFFFu);
-            rhi = bin_hi = wave_max_u(lane < kNW ? (uint32_t)sm.red[3][lane] : 0u);
+            rlo = wave_min_u(lane < NW ? (uint32_t)sm.red[2][lane] : 0xFFFFFFFFu);
+            rhi = bin_hi = wave_max_u(lane < NW ? (uint32_t)sm.red[3][lane] : 0u);
         }
     } else {
         if (secant) {
@@ -1842,7 +1897,7 @@ DEV void topk_body(const Params& p) {
         return;
     }
     if (!done_lists) {
-        for (int i = tid; i < K; i += kBlock) out[i] = -1;
+        for (int i = tid; i < K; i += W::kBlock) out[i] = -1;
         if (st && tid == 0) {
             gvr_row_stats s = {};
             s.n = n;
@@ -1882,14 +1937,16 @@ DEV void topk_body(const Params& p) {
     }
 }
 
-__global__ __launch_bounds__(kBlock) void gvr_topk_kernel(Params p) { topk_body<true>(p); }
-__global__ __launch_bounds__(kBlock) void radix_topk_kernel(Params p) { topk_body<false>(p); }
+template <int NW>
+__global__ __launch_bounds__(Shape<NW>::kBlock) void gvr_topk_kernel(Params p) { topk_body<true, NW>(p); }
+template <int NW>
+__global__ __launch_bounds__(Shape<NW>::kBlock) void radix_topk_kernel(Params p) { topk_body<false, NW>(p); }
 
 // ------------------------------------------------------------------ host side
 
 gvr_status validate(const float* scores, int64_t B, int64_t ld, int32_t K, const int32_t* out,
                     const gvr_options* opt, int* capacity, int* use_guess, int* parts, int* scatter, int* secant,
-                    int* paper_refine) {
+                    int* paper_refine, int* shape) {
     if (K < 1 || K > GVR_MAX_K) return GVR_ERR_UNSUPPORTED_K;
     if (B < 0 || ld < 0) return GVR_ERR_INVALID_ARG;
     if (B > 0 && (!scores || !out)) return GVR_ERR_INVALID_ARG;
@@ -1900,12 +1957,14 @@ gvr_status validate(const float* scores, int64_t B, int64_t ld, int32_t K, const
             if (opt->capacity < K || opt->capacity > GVR_MAX_CANDIDATES) return GVR_ERR_INVALID_ARG;
             cap = opt->capacity;
         }
-        if ((opt->flags & ~15) || opt->reserved1) return GVR_ERR_INVALID_ARG;
+        if ((opt->flags & ~63) || opt->reserved1) return GVR_ERR_INVALID_ARG;
+        if (((opt->flags >> 4) & 3) == 3) return GVR_ERR_INVALID_ARG;   // both shapes forced
         if (opt->parts < 0 || opt->parts > kMaxParts) return GVR_ERR_INVALID_ARG;
         if (opt->flags & 1) *use_guess = 0;
         *scatter = (opt->flags >> 1) & 1;
         *secant = (opt->flags >> 2) & 1;
         *paper_refine = (opt->flags >> 3) & 1;
+        *shape = (opt->flags >> 4) & 3;
         *parts = opt->parts;
     }
     *capacity = cap;
@@ -1964,7 +2023,7 @@ gvr_status get_workspace(int device, void* stream, int rows, int parts, Workspac
     const size_t a_bytes = align_up((size_t)slots * sizeof(uint64_t), 256);
     const size_t c_bytes = align_up((size_t)slots * sizeof(int32_t), 256);
     const size_t t_bytes = align_up((size_t)slots * sizeof(uint32_t), 256);
-    const size_t l_bytes = (size_t)slots * kCap * sizeof(uint64_t);
+    const size_t l_bytes = (size_t)slots * kPartCap * sizeof(uint64_t);
     void* base = nullptr;
     if (hipMalloc(&base, a_bytes + c_bytes + t_bytes + l_bytes) != hipSuccess) return GVR_ERR_HIP;
     if (hipMemset(base, 0, a_bytes) != hipSuccess) {
@@ -2009,18 +2068,29 @@ int choose_parts(int64_t rows, int64_t ld, int cus) {
     return saved_us > 8.0 ? (int)s : 1;
 }
 
+// Workgroup shape of a call. The 16-wave shape takes one compute unit per
+// row and has the shortest per-row latency (about 12 us for 8K elements, 20
+// with 4 waves, whose refine runs on a quarter of the waves); with many more
+// rows than compute units and short rows, three 4-wave workgroups per compute
+// unit overlap three rows' latencies and win (2048 rows of 8K: 65 us against
+// 82; at 512 rows the two are even).
+bool use_short_shape(int64_t rows, int64_t ld, int cus) { return rows > 3 * (int64_t)cus && ld <= kShortMaxLd; }
+
 gvr_status run(const float* scores, int64_t B, int64_t ld, const int32_t* row_len, const int32_t* prev,
                int32_t K, int32_t* out, void* stream, const gvr_options* opt, gvr_row_stats* stats,
                int use_guess) {
-    int cap = 0, parts_opt = 0, scatter = 0, secant = 0, paper_refine = 0;
+    int cap = 0, parts_opt = 0, scatter = 0, secant = 0, paper_refine = 0, shape = 0;
     gvr_status st = validate(scores, B, ld, K, out, opt, &cap, &use_guess, &parts_opt, &scatter, &secant,
-                             &paper_refine);
+                             &paper_refine, &shape);
     if (st != GVR_OK) return st;
     if (B == 0) return GVR_OK;
     const bool guess = use_guess && prev;
     int device = 0;
     if (hipGetDevice(&device) != hipSuccess) return GVR_ERR_HIP;
-    int parts = !guess ? 1 : (parts_opt > 0 ? parts_opt : choose_parts(B, ld, cu_count(device)));
+    const int cus = cu_count(device);
+    const bool short_shape = shape == 1 || (shape == 0 && use_short_shape(B, ld, cus));
+    if (short_shape) cap = std::min(cap, Shape<kNWShort>::kCap);   // a smaller C never changes the result
+    int parts = (!guess || short_shape) ? 1 : (parts_opt > 0 ? parts_opt : choose_parts(B, ld, cus));
     // A forced split is capped at kMaxSlots (row, part) pairs per call, which
     // bounds the workspace (128 KB of list per pair).
     if (parts > 1 && (int64_t)parts * B > kMaxSlots) parts = (int)std::max<int64_t>(1, kMaxSlots / B);
@@ -2055,10 +2125,20 @@ gvr_status run(const float* scores, int64_t B, int64_t ld, const int32_t* row_le
         q.part_thresh = ws.part_thresh;
         q.part_list = ws.part_list;
         const dim3 grid((unsigned)(rows_pad * parts));
-        if (guess)
-            hipLaunchKernelGGL(gvr_topk_kernel, grid, dim3(kBlock), 0, (hipStream_t)stream, q);
-        else
-            hipLaunchKernelGGL(radix_topk_kernel, grid, dim3(kBlock), 0, (hipStream_t)stream, q);
+        const hipStream_t hs = (hipStream_t)stream;
+        if (short_shape) {
+            const dim3 block(Shape<kNWShort>::kBlock);
+            if (guess)
+                hipLaunchKernelGGL(gvr_topk_kernel<kNWShort>, grid, block, 0, hs, q);
+            else
+                hipLaunchKernelGGL(radix_topk_kernel<kNWShort>, grid, block, 0, hs, q);
+        } else {
+            const dim3 block(Shape<kNWLong>::kBlock);
+            if (guess)
+                hipLaunchKernelGGL(gvr_topk_kernel<kNWLong>, grid, block, 0, hs, q);
+            else
+                hipLaunchKernelGGL(radix_topk_kernel<kNWLong>, grid, block, 0, hs, q);
+        }
         if (hipGetLastError() != hipSuccess) return GVR_ERR_HIP;
     }
     return GVR_OK;

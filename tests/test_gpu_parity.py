@@ -487,3 +487,73 @@ def test_paper_refine_special_rows(ld, K):
         assert_rows_equal(out.cpu().numpy(), exp, "paper refine with guess ld=%d K=%d" % (ld, K))
         out = g.radix_topk_ex(S, RL, K, options={"flags": flags})
         assert_rows_equal(out.cpu().numpy(), exp, "radix with the paper refine ld=%d K=%d" % (ld, K))
+
+
+SHAPES = [("short", 16), ("long", 32)]
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=[x[0] for x in SHAPES])
+@pytest.mark.parametrize("case", [(0, 4, 1, None), (1, 3, 8, None), (2, 2, 4, None), (3, 2, 8, "a"),
+                                  (3, 2, 8, "b"), (3, 2, 8, "c"), (3, 2, 8, "d")],
+                         ids=lambda c: "c%d%s" % (c[0], c[3] or ""))
+def test_forced_workgroup_shape_parity(case, shape):
+    """Either workgroup shape (flag bit 4: 4 waves, 4096-entry lists; bit 5:
+    16 waves) gives the oracle's answer on every decode workload, whatever
+    the automatic choice would be."""
+    import paper_2604_22312_amd as g
+    flags = shape[1]
+
+    def shaped(scores, row_len, prev, K, stats=None):
+        return g.gvr_topk_ex(scores, row_len, prev, K, options={"flags": flags}, stats=stats)
+    shaped.__name__ = "gvr_%s_shape" % shape[0]
+    cfg, steps, queries, sub = case
+    w, res = run_decode(shaped, cfg, steps, queries, sub, dev=DEV, stats_check=True)
+    for i, st, kth, ngt in res:
+        rl = w.row_len[i].numpy()
+        for r in range(w.rows):
+            assert int(st["path"][r]) != -1
+            if int(rl[r]) > K_TOPK and int(st["path"][r]) != 4:
+                assert int(st["kth_key"][r]) == int(kth[r])
+
+
+@pytest.mark.parametrize("ld,K", [(20001, 2048), (9999, 7), (4097, 2048), (70003, 1)])
+def test_short_shape_special_rows(ld, K):
+    import paper_2604_22312_amd as g
+    rng = np.random.default_rng(ld + 5 * K)
+    rows, lens = _special_rows(ld, K, rng)
+    exp, _, _ = oracle.topk(rows, K, row_len=lens)
+    S = torch.from_numpy(rows).to(DEV)
+    RL = torch.from_numpy(lens).to(DEV)
+    prev = torch.from_numpy(np.ascontiguousarray(exp)).to(DEV)
+    for flags in (16, 16 | 8, 16 | 4):
+        note("short shape special rows ld=%d K=%d flags=%d" % (ld, K, flags))
+        out = g.gvr_topk_ex(S, RL, None, K, options={"flags": flags})
+        assert_rows_equal(out.cpu().numpy(), exp, "short shape, no guess, ld=%d K=%d flags=%d" % (ld, K, flags))
+        out = g.gvr_topk_ex(S, RL, prev, K, options={"flags": flags})
+        assert_rows_equal(out.cpu().numpy(), exp, "short shape with guess ld=%d K=%d flags=%d" % (ld, K, flags))
+        out = g.radix_topk_ex(S, RL, K, options={"flags": flags})
+        assert_rows_equal(out.cpu().numpy(), exp, "radix, short shape ld=%d K=%d flags=%d" % (ld, K, flags))
+
+
+def test_many_short_rows_take_the_short_shape():
+    """More rows than compute units, rows <= 16K: the automatic choice runs
+    4-wave workgroups; ragged lengths, with and without a guess."""
+    import paper_2604_22312_amd as g
+    rng = np.random.default_rng(123)
+    B, ld, K = 600, 12000, 2048
+    x = rng.standard_normal((B, ld)).astype(np.float32)
+    lens = rng.integers(0, ld + 1, B).astype(np.int32)
+    lens[:4] = [ld, K, K + 1, 2 * K + 1]
+    exp, _, _ = oracle.topk(x, K, row_len=lens)
+    prev_rows = x + 0.1 * rng.standard_normal((B, ld)).astype(np.float32)
+    pexp, _, _ = oracle.topk(prev_rows, K, row_len=lens)
+    S = torch.from_numpy(x).to(DEV)
+    RL = torch.from_numpy(lens).to(DEV)
+    note("many short rows B=%d ld=%d" % (B, ld))
+    for prev in (None, torch.from_numpy(pexp).to(DEV)):
+        st = g.new_stats(B, DEV)
+        out = g.gvr_topk_ex(S, RL, prev, K, stats=st)
+        assert_rows_equal(out.cpu().numpy(), exp, "many short rows, guess=%s" % (prev is not None))
+        assert -1 not in set(g.decode_stats(st)["path"].tolist())
+    out = g.radix_topk(S, RL, None, K)
+    assert_rows_equal(out.cpu().numpy(), exp, "many short rows, radix")
