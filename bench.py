@@ -15,7 +15,8 @@ scale rocprofv3 FETCH_SIZE / WRITE_SIZE counters to bytes); `--mode configs`
 prints one line per decode workload; `--mode rope` runs the paper's synthetic
 single-operator benchmark (one row of YaRN-RoPE scores per length N, guess =
 the static prior P_static), one line per N; `--mode phases` prints the
-per-phase time breakdown of gvr_topk and of the paper's own phases.
+per-phase time breakdown of gvr_topk and of the paper's own phases;
+`--mode short` sweeps short rows over batch sizes (workgroup shapes).
 """
 from __future__ import annotations
 
@@ -433,6 +434,70 @@ def run_phases(args, dev):
         sys.stdout.flush()
 
 
+def run_short(args, dev):
+    """Short rows and small or large batches: per (N, B) the GPU time per call
+    of gvr_topk (guess = P_static) and radix_topk on synthetic YaRN-RoPE rows,
+    with the automatic workgroup shape, and, for B >= 512, with each shape
+    forced (flag 16: 4 waves, flag 32: 16 waves). Per-call time from a
+    replayed HIP graph of 4 calls."""
+    import numpy as np
+    import torch
+    import oracle
+    import paper_2604_22312_amd as g
+    from workloads import rope as WR
+
+    def graph_us(fn, reps):
+        stream = torch.cuda.Stream()
+        with torch.cuda.stream(stream):
+            fn(stream)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=stream):
+            for _ in range(4):
+                fn(stream)
+        graph.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            graph.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / (reps * 4)
+
+    for n in (2560, 4096, 8192, 16384, 32768):
+        host = WR.batch_scores(n, 16)
+        exp, _, _ = oracle.topk(host, K_TOPK)
+        base = torch.from_numpy(host).to(dev)
+        prior = g.gvr_rope_prior(n, K_TOPK, device=dev)
+        for B in (1, 64, 512, 2048):
+            reps = (B + 15) // 16
+            scores = base.repeat(reps, 1)[:B].contiguous()
+            rl = torch.full((B,), n, dtype=torch.int32, device=dev)
+            prev = prior.view(1, K_TOPK).expand(B, K_TOPK).contiguous()
+            out = torch.empty((B, K_TOPK), dtype=torch.int32, device=dev)
+            line = {"mode": "short", "workload": "rope_synthetic_n%d_b%d" % (n, B), "n": n, "rows": B}
+            g.gvr_topk(scores, rl, prev, K_TOPK, out_idx=out)
+            if not np.array_equal(out.cpu().numpy(), np.tile(exp, (reps, 1))[:B]):
+                raise SystemExit("bench: gvr_topk differs from the oracle (short rows n=%d B=%d)" % (n, B))
+            variants = [("gvr_topk", lambda s, o=None: g.gvr_topk_ex(scores, rl, prev, K_TOPK, out_idx=out, stream=s,
+                                                                     options=o)),
+                        ("radix_topk", lambda s, o=None: g.radix_topk_ex(scores, rl, K_TOPK, out_idx=out, stream=s,
+                                                                         options=o))]
+            for name, fn in variants:
+                line[name + "_us"] = round(graph_us(fn, max(2, args.steps // 20)), 3)
+                if B >= 512:
+                    for tag, fl in (("4w", 16), ("16w", 32)):
+                        line["%s_%s_us" % (name, tag)] = round(
+                            graph_us(lambda s, f=fn, o={"flags": fl}: f(s, o), max(2, args.steps // 20)), 3)
+            line["gvr_rows_per_s"] = round(B / (line["gvr_topk_us"] * 1e-6), 1)
+            line["speedup_vs_radix"] = round(line["radix_topk_us"] / line["gvr_topk_us"], 3)
+            print(json.dumps(line))
+            sys.stdout.flush()
+            del scores, prev, out
+        torch.cuda.empty_cache()
+
+
 def read_traffic(n_launch_bytes):
     if not os.path.exists(TRAFFIC_FILE):
         return None
@@ -450,7 +515,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--mode", choices=["bench", "copy", "configs", "rope", "phases"], default="bench")
+    ap.add_argument("--mode", choices=["bench", "copy", "configs", "rope", "phases", "short"], default="bench")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--no-radix", action="store_true", help="skip timing radix_topk")
     ap.add_argument("--no-secant", action="store_true",
@@ -485,6 +550,9 @@ def main():
         return
     if args.mode == "phases":
         run_phases(args, dev)
+        return
+    if args.mode == "short":
+        run_short(args, dev)
         return
 
     w, outs, prevs = build_inputs(dev)

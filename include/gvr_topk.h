@@ -119,8 +119,9 @@ typedef struct gvr_options {
                               unit, no row splitting); bit 5: force the
                               16-wave shape; neither: 4 waves when there are
                               more than three rows per compute unit and
-                              ld <= 12288, else 16. Bits 4 and 5 together are
-                              an error. No bit changes the result. */
+                              ld <= 12288, or more than one and ld <= 4096,
+                              else 16. Bits 4 and 5 together are an error.
+                              No bit changes the result. */
     int32_t parts;         /* workgroups per row, 1..16 (0 = chosen from B, ld
                               and the device's compute units; a forced value is
                               lowered so that B * parts <= 2048); never changes

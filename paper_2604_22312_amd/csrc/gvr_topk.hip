@@ -2073,8 +2073,11 @@ int choose_parts(int64_t rows, int64_t ld, int cus) {
 // with 4 waves, whose refine runs on a quarter of the waves); with many more
 // rows than compute units and short rows, three 4-wave workgroups per compute
 // unit overlap three rows' latencies and win (2048 rows of 8K: 65 us against
-// 82; at 512 rows the two are even).
-bool use_short_shape(int64_t rows, int64_t ld, int cus) { return rows > 3 * (int64_t)cus && ld <= kShortMaxLd; }
+// 82; at 512 rows of 8K the two are even, at 512 rows of 4K the 4-wave shape
+// wins by 15 %).
+bool use_short_shape(int64_t rows, int64_t ld, int cus) {
+    return (rows > 3 * (int64_t)cus && ld <= kShortMaxLd) || (rows > cus && ld <= 4096);
+}
 
 gvr_status run(const float* scores, int64_t B, int64_t ld, const int32_t* row_len, const int32_t* prev,
                int32_t K, int32_t* out, void* stream, const gvr_options* opt, gvr_row_stats* stats,
@@ -2084,7 +2087,9 @@ gvr_status run(const float* scores, int64_t B, int64_t ld, const int32_t* row_le
                              &paper_refine, &shape);
     if (st != GVR_OK) return st;
     if (B == 0) return GVR_OK;
-    const bool guess = use_guess && prev;
+    // Rows of at most 2K elements list every element (the guess would cut
+    // few candidates): when no row is longer, the guess-free kernel runs.
+    const bool guess = use_guess && prev && ld > 2 * (int64_t)K;
     int device = 0;
     if (hipGetDevice(&device) != hipSuccess) return GVR_ERR_HIP;
     const int cus = cu_count(device);
