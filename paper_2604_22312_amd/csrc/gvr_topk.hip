@@ -5,6 +5,8 @@
 // workgroup, or split over S of them ("parts", up to 16) when few long rows
 // would leave compute units idle and the streaming time saved outweighs the
 // merge; the parts of one row are placed on one XCD so they share its L2.
+// The same code, instantiated for 4 waves (4096-entry lists, three
+// workgroups per compute unit), serves calls with many short rows.
 //
 //   Guess (Sec. 4.2.1, Phase 1). Wave 0 of every part gathers the scores at a
 //   strided sample of prev_topk (every 8th entry for K = 2048, 256 in all)
@@ -47,7 +49,9 @@
 //   On request (option flag 4) the paper's own Phase 2 schedule runs instead
 //   of the speculative pass: T0 = pmean of all guessed scores, one threshold
 //   counted per full-row pass, damped secant steps with a bisection fallback,
-//   then one collect pass at the accepted threshold.
+//   then one collect pass at the accepted threshold. Option flag 8 runs the
+//   paper's own Phase 4 (min / max, histogram, snap iterations) instead of
+//   the refine above.
 
 #include <hip/hip_runtime.h>
 
