@@ -3,7 +3,8 @@
 Thin Python binding over the C ABI of ``include/gvr_topk.h`` (library
 ``libgvr_topk.so`` built in-tree by ``paper_2604_22312_amd.build``). This module
 only validates tensors and marshals pointers; every step of the Top-K runs in
-the HIP kernels of ``csrc/gvr_topk.hip`` and ``csrc/rope_prior.hip``. There is no CPU fallback: if the
+the HIP kernels of ``csrc/gvr_topk.hip``, ``csrc/rope_prior.hip`` and
+``csrc/indexer.hip``. There is no CPU fallback: if the
 library is missing, importing the functions raises.
 
 Functions mirror the C entry points:
@@ -14,6 +15,9 @@ Functions mirror the C entry points:
 * ``gvr_rope_g(n, params=None, device=...)`` -- g(Delta) of the RoPE/YaRN prior
 * ``gvr_rope_prior(n, K, params=None, device=...)`` -- its static index set
   (``include/gvr_rope_prior.h``)
+* ``gvr_indexer_scores(q, w, k, k_scale, ...)`` / ``gvr_indexer_topk(...)`` --
+  the FP8 indexer scores, and the indexer followed by gvr_topk
+  (``include/gvr_indexer.h``)
 """
 from .binding import (  # noqa: F401
     GVR_MAX_CANDIDATES,
@@ -23,6 +27,8 @@ from .binding import (  # noqa: F401
     Options,
     RopeParams,
     decode_stats,
+    gvr_indexer_scores,
+    gvr_indexer_topk,
     gvr_rope_g,
     gvr_rope_params,
     gvr_rope_prior,

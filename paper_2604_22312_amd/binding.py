@@ -66,6 +66,11 @@ def lib():
         L.gvr_rope_g.argtypes = [i64, ctypes.POINTER(RopeParams), vp, vp, vp]
         L.gvr_rope_prior.restype = ctypes.c_int
         L.gvr_rope_prior.argtypes = [i64, i32, ctypes.POINTER(RopeParams), vp, vp, vp]
+        L.gvr_indexer_scores.restype = ctypes.c_int
+        L.gvr_indexer_scores.argtypes = [vp, vp, vp, vp, i64, i32, i32, i32, i64, vp, vp, vp]
+        L.gvr_indexer_topk.restype = ctypes.c_int
+        L.gvr_indexer_topk.argtypes = [vp, vp, vp, vp, i64, i32, i32, i32, i64, vp, vp, vp, i32, vp, vp,
+                                       ctypes.POINTER(Options), vp]
         L.gvr_status_string.restype = ctypes.c_char_p
         L.gvr_status_string.argtypes = [ctypes.c_int]
         L.gvr_version.restype = ctypes.c_char_p
@@ -253,3 +258,61 @@ def gvr_rope_prior(n, K, params=None, device="cuda", out=None, g=None, stream=No
     if st != 0:
         raise GvrError("gvr_rope_prior", st)
     return out
+
+
+def _check_indexer(q, w, k, k_scale, row_len, scores):
+    for name, t, dt in (("q", q, torch.uint8), ("w", w, torch.float32), ("k", k, torch.uint8),
+                        ("k_scale", k_scale, torch.float32)):
+        if not isinstance(t, torch.Tensor) or t.dtype != dt or not t.is_cuda or not t.is_contiguous():
+            raise ValueError("%s must be a contiguous %s tensor on a GPU (there is no CPU path)" % (name, dt))
+    if q.dim() != 3 or w.dim() != 2 or k.dim() != 3 or k_scale.dim() != 2:
+        raise ValueError("shapes: q [B][H][D], w [B][H], k [C][ld][D], k_scale [C][ld]")
+    B, H, D = q.shape
+    C, ld, Dk = k.shape
+    dev = q.device
+    if w.shape != (B, H) or Dk != D or k_scale.shape != (C, ld) or C == 0 or B % C != 0:
+        raise ValueError("inconsistent indexer shapes: q %s w %s k %s k_scale %s"
+                         % (tuple(q.shape), tuple(w.shape), tuple(k.shape), tuple(k_scale.shape)))
+    for t in (w, k, k_scale):
+        if t.device != dev:
+            raise ValueError("indexer tensors must be on one device")
+    if row_len is not None and (row_len.dtype != torch.int32 or row_len.shape != (B,) or row_len.device != dev
+                                or not row_len.is_contiguous()):
+        raise ValueError("row_len must be a contiguous int32 tensor [B] on the device")
+    if scores is None:
+        scores = torch.empty((B, ld), dtype=torch.float32, device=dev)
+    elif (scores.dtype != torch.float32 or scores.shape != (B, ld) or scores.device != dev
+          or not scores.is_contiguous()):
+        raise ValueError("scores must be a contiguous float32 tensor [B][ld] on the device")
+    return B, H, D, B // C, ld, scores
+
+
+def gvr_indexer_scores(q, w, k, k_scale, row_len=None, scores=None, stream=None):
+    """Indexer scores I [B][ld] (float32; entries s >= n_b are not written)
+    from FP8 E4M3 bytes q [B][H][D], key cache k [C][ld][D] shared by B / C
+    consecutive rows, k_scale [C][ld] and head weights w [B][H]."""
+    B, H, D, group, ld, scores = _check_indexer(q, w, k, k_scale, row_len, scores)
+    with torch.cuda.device(q.device):
+        st = lib().gvr_indexer_scores(_ptr(q), _ptr(w), _ptr(k), _ptr(k_scale), B, H, D, group, ld,
+                                      _ptr(row_len), _ptr(scores), _stream(stream, q.device))
+    if st != 0:
+        raise GvrError("gvr_indexer_scores", st)
+    return scores
+
+
+def gvr_indexer_topk(q, w, k, k_scale, row_len, prev_topk, K, scores=None, out_idx=None, stream=None,
+                     options=None, stats=None):
+    """The indexer, then gvr_topk_ex on its scores; returns (out_idx [B][K], scores [B][ld])."""
+    B, H, D, group, ld, scores = _check_indexer(q, w, k, k_scale, row_len, scores)
+    _, _, K, out_idx = _check(scores, row_len, prev_topk, K, out_idx)
+    opt = None
+    if options is not None:
+        opt = Options(**options) if isinstance(options, dict) else options
+    with torch.cuda.device(q.device):
+        st = lib().gvr_indexer_topk(_ptr(q), _ptr(w), _ptr(k), _ptr(k_scale), B, H, D, group, ld,
+                                    _ptr(row_len), _ptr(scores), _ptr(prev_topk), K, _ptr(out_idx),
+                                    _stream(stream, q.device), ctypes.byref(opt) if opt is not None else None,
+                                    _ptr(stats))
+    if st != 0:
+        raise GvrError("gvr_indexer_topk", st)
+    return out_idx, scores

@@ -36,7 +36,7 @@ def test_header_declares_the_boundary():
     names = declared_functions()
     for n in ("gvr_topk", "radix_topk", "gvr_topk_ex", "radix_topk_ex",
               "gvr_status_string", "gvr_version", "gvr_rope_params_default", "gvr_rope_g",
-              "gvr_rope_prior"):
+              "gvr_rope_prior", "gvr_indexer_scores", "gvr_indexer_topk"):
         assert n in names, n
 
 
@@ -125,3 +125,25 @@ def test_rope_binding_refuses_cpu_device():
     import paper_2604_22312_amd as g
     with pytest.raises(ValueError):
         g.gvr_rope_prior(100, 16, device="cpu")
+
+
+def test_indexer_validation(L):
+    vp = ctypes.c_void_p
+    a = vp(256)   # 16-byte aligned stand-in; no call below reaches the GPU
+    def call(B=4, H=64, D=128, group=2, ld=100, q=a, k=a, out=a):
+        return L.gvr_indexer_scores(q, a, k, a, B, H, D, group, ld, None, out, None)
+    assert call(B=-1) == -1 and call(ld=-1) == -1
+    assert call(H=48) == -1 and call(H=256) == -1 and call(D=96) == -1
+    assert call(group=0) == -1 and call(group=5) == -1 and call(B=5, group=2) == -1
+    assert call(q=None) == -1 and call(out=None) == -1
+    assert call(q=vp(257)) == -1 and call(k=vp(264)) == -1      # not 16-byte aligned
+    assert call(ld=1 << 31) == -5
+    assert call(B=0) == 0 and call(ld=0) == 0
+    # the combined call checks K and the Top-K options first
+    assert L.gvr_indexer_topk(a, a, a, a, 4, 64, 128, 2, 100, None, a, None, 0, a, None, None, None) == -2
+    assert L.gvr_indexer_topk(a, a, a, a, 4, 64, 128, 2, 100, None, a, None, 2049, a, None, None, None) == -2
+    import paper_2604_22312_amd as g
+    bad = g.Options(capacity=0, flags=128, parts=0, reserved1=0)
+    assert L.gvr_indexer_topk(a, a, a, a, 4, 64, 128, 2, 100, None, a, None, 16, a, None, ctypes.byref(bad),
+                              None) == -1
+    assert L.gvr_indexer_topk(a, a, a, a, 4, 64, 128, 2, 100, None, a, None, 16, None, None, None, None) == -1

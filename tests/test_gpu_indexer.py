@@ -1,0 +1,154 @@
+"""GPU parity of the FP8 indexer (Sec. 2.1, Eq. indexer) and of the indexer
+followed by gvr_topk, against the float64 oracle on the same FP8 bytes.
+
+Scores: the GPU accumulates each dot product of D FP8 products (exact in
+float32) in float32 on the matrix cores, scales, applies ReLU and sums the H
+weighted heads in float32. Recursive summation bounds the error of a sum of
+m terms by (m - 1) u times the sum of their magnitudes (u = 2^-24), so
+|I_gpu - I| <= (D + H + 4) u * mag, mag = sum_j |w_j| sum_d |q_jd k'_d|
+(the oracle's ``magnitude``), whatever order the hardware adds in.
+
+Top-K: the answer on the GPU's float32 scores and the oracle's on its exact
+scores may differ only among keys within that tolerance of the K-th score:
+every key clearly above it is selected, none clearly below it is, and the
+output is K distinct indices in ascending order.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import indexer as IX
+from tests.gpu_cases import K_TOPK, note
+from workloads import indexer as WI
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2604_22312_amd as g
+    g.lib()
+
+
+def tol_of(mag, H, D):
+    return (D + H + 4) * 2.0 ** -24 * mag
+
+
+def inputs(requests, group, ld, lengths, H, D, seed, steps=1):
+    x = WI.generate(requests, group, ld, lengths, steps=steps, H=H, D=D, seed=seed, device="cpu")
+    return x
+
+
+def gpu_scores(x, t=0, sentinel=-7.0):
+    import paper_2604_22312_amd as g
+    B, ld = x.rows, x.ld
+    sc = torch.full((B, ld), sentinel, dtype=torch.float32, device=DEV)
+    g.gvr_indexer_scores(x.q[t].to(DEV), x.w.to(DEV), x.k.to(DEV), x.k_scale.to(DEV), x.row_len[t].to(DEV),
+                         scores=sc)
+    torch.cuda.synchronize()
+    return sc.cpu().numpy().astype(np.float64)
+
+
+def oracle_scores(x, t=0):
+    args = (x.q[t].numpy(), x.w.numpy(), x.k.numpy(), x.k_scale.numpy())
+    rl = x.row_len[t].numpy()
+    return (IX.indexer_scores(*args, group=x.group, row_len=rl),
+            IX.magnitude(*args, group=x.group, row_len=rl))
+
+
+SHAPES = [(64, 128, 2), (64, 128, 1), (32, 64, 3), (128, 128, 4), (64, 64, 1), (32, 128, 2)]
+
+
+@pytest.mark.parametrize("H,D,group", SHAPES, ids=["h%d_d%d_g%d" % s for s in SHAPES])
+def test_indexer_scores_parity(H, D, group):
+    ld = 5000
+    lengths = [ld, 1, 0, 31, 33, 1024, 1025, 2047][:3]
+    x = inputs(3, group, ld, lengths[:3], H, D, seed=H + D + group)
+    # ragged lengths inside each request's group too
+    x.row_len[0, :] = torch.tensor(([ld, 4999, 1, 0, 33, 1025, 32, 2049, 1024, 4097, 3, 64] * 2)[:x.rows],
+                                   dtype=torch.int32)
+    note("indexer scores H=%d D=%d group=%d" % (H, D, group))
+    got = gpu_scores(x)
+    exp, mag = oracle_scores(x)
+    rl = x.row_len[0].numpy()
+    for b in range(x.rows):
+        n = int(rl[b])
+        err = np.abs(got[b, :n] - exp[b, :n])
+        assert np.all(err <= tol_of(mag[b, :n], H, D)), (b, float(err.max()))
+        assert np.all(got[b, n:] == -7.0), "row %d: scores past its length were written" % b
+
+
+def check_topk(got, exp_scores, mag, rl, K, H, D):
+    for b in range(got.shape[0]):
+        n = int(rl[b])
+        sel = got[b]
+        if n <= K:
+            assert sel.tolist() == list(range(n)) + [-1] * (K - n)
+            continue
+        assert np.all(np.diff(sel) > 0) and sel[0] >= 0 and sel[-1] < n
+        s = exp_scores[b, :n]
+        tol = tol_of(mag[b, :n], H, D)
+        kth = np.sort(s)[-K]
+        mask = np.zeros(n, bool)
+        mask[sel] = True
+        assert np.all(mask[s - tol > kth + tol.max()]), "row %d: a clearly larger score was left out" % b
+        assert not np.any(mask[s + tol < kth - tol.max()]), "row %d: a clearly smaller score was taken" % b
+
+
+@pytest.mark.parametrize("group", [1, 2])
+def test_indexer_topk_parity(group):
+    """Two decode steps: the second is guided by the first step's Top-K."""
+    import paper_2604_22312_amd as g
+    H, D, ld = 64, 128, 40000
+    x = inputs(4, group, ld, [39000, 2100, 20000, 2048], H, D, seed=17 + group, steps=2)
+    ex0, _ = oracle_scores(x, 0)
+    prev = np.full((x.rows, K_TOPK), -1, np.int32)
+    for b in range(x.rows):
+        n = int(x.row_len[0, b])
+        prev[b, :min(n, K_TOPK)] = IX_argtopk(ex0[b, :n], K_TOPK)
+    ex1, mag1 = oracle_scores(x, 1)
+    note("indexer + topk group=%d" % group)
+    st = g.new_stats(x.rows, DEV)
+    out, sc = g.gvr_indexer_topk(x.q[1].to(DEV), x.w.to(DEV), x.k.to(DEV), x.k_scale.to(DEV), x.row_len[1].to(DEV),
+                                 torch.from_numpy(prev).to(DEV), K_TOPK, stats=st)
+    torch.cuda.synchronize()
+    check_topk(out.cpu().numpy(), ex1, mag1, x.row_len[1].numpy(), K_TOPK, H, D)
+    # and without a guess (radix schedule inside gvr_topk)
+    out2, _ = g.gvr_indexer_topk(x.q[1].to(DEV), x.w.to(DEV), x.k.to(DEV), x.k_scale.to(DEV), x.row_len[1].to(DEV),
+                                 None, K_TOPK)
+    torch.cuda.synchronize()
+    assert np.array_equal(out2.cpu().numpy(), out.cpu().numpy())
+    d = g.decode_stats(st)
+    note("  paths %s passes %s" % (d["path"].tolist(), d["passes"].tolist()))
+
+
+def IX_argtopk(s, K):
+    """K largest (lower index first among equals), ascending: from the oracle's scores."""
+    order = np.argsort(-s, kind="stable")[:K]
+    return np.sort(order).astype(np.int32)
+
+
+def test_indexer_full_size_sampled_rows():
+    """The benchmark's shape (64 requests x 2 draft rows, ~100K keys, H = 64,
+    D = 128) on the GPU, checked on four sampled rows."""
+    import paper_2604_22312_amd as g
+    H, D, ld = 64, 128, 102463
+    x = WI.generate(64, 2, ld, [102400] * 64, steps=1, H=H, D=D, seed=3, device=DEV)
+    note("indexer full size B=%d ld=%d" % (x.rows, ld))
+    sc = g.gvr_indexer_scores(x.q[0], x.w, x.k, x.k_scale, x.row_len[0])
+    torch.cuda.synchronize()
+    for b in (0, 1, 77, 127):
+        g_idx = b // 2
+        args = (x.q[0][b:b + 1].cpu().numpy(), x.w[b:b + 1].cpu().numpy(), x.k[g_idx:g_idx + 1].cpu().numpy(),
+                x.k_scale[g_idx:g_idx + 1].cpu().numpy())
+        rl = x.row_len[0][b:b + 1].cpu().numpy()
+        exp = IX.indexer_scores(*args, group=1, row_len=rl)[0]
+        mag = IX.magnitude(*args, group=1, row_len=rl)[0]
+        n = int(rl[0])
+        got = sc[b, :n].cpu().numpy().astype(np.float64)
+        assert np.all(np.abs(got - exp[:n]) <= tol_of(mag[:n], H, D)), b
