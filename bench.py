@@ -16,7 +16,8 @@ prints one line per decode workload; `--mode rope` runs the paper's synthetic
 single-operator benchmark (one row of YaRN-RoPE scores per length N, guess =
 the static prior P_static), one line per N; `--mode phases` prints the
 per-phase time breakdown of gvr_topk and of the paper's own phases;
-`--mode short` sweeps short rows over batch sizes (workgroup shapes).
+`--mode short` sweeps short rows over batch sizes (workgroup shapes);
+`--mode indexer` times the FP8 indexer before the Top-K.
 """
 from __future__ import annotations
 
@@ -498,6 +499,87 @@ def run_short(args, dev):
         torch.cuda.empty_cache()
 
 
+def run_indexer(args, dev):
+    """The step before the Top-K (Sec. 2.1, Eq. indexer): FP8 indexer scores
+    for 64 requests x 2 draft rows over ~100K keys (H = 64 heads, D = 128,
+    synthetic FP8 inputs, workloads/indexer.py), then the Top-K. Lines: the
+    indexer alone (HBM roofline: key cache + scales read once per request,
+    scores written), the indexer followed by gvr_topk guided by the previous
+    step, and gvr_topk alone on the same scores. GPU time per call from a
+    replayed HIP graph; the 0.87 GB key cache exceeds the Infinity Cache."""
+    import numpy as np
+    import torch
+    import oracle
+    from oracle import indexer as IX
+    import paper_2604_22312_amd as g
+    from workloads import indexer as WI
+
+    H, D, group, requests, ld = 64, 128, 2, 64, 102463
+    x = WI.generate(requests, group, ld, [102400] * requests, steps=2, H=H, D=D, seed=11, device=dev)
+    rows = x.rows
+    rl0, rl1 = x.row_len[0], x.row_len[1]
+    scores = torch.empty((rows, ld), dtype=torch.float32, device=dev)
+    out = torch.empty((rows, K_TOPK), dtype=torch.int32, device=dev)
+    # step 0 gives the guess of step 1
+    prev, _ = g.gvr_indexer_topk(x.q[0], x.w, x.k, x.k_scale, rl0, None, K_TOPK, scores=scores)
+    prev = prev.clone()
+    g.gvr_indexer_topk(x.q[1], x.w, x.k, x.k_scale, rl1, prev, K_TOPK, scores=scores, out_idx=out)
+    torch.cuda.synchronize()
+    # spot check of one row's scores against the oracle
+    b = 77
+    c = b // group
+    args1 = (x.q[1][b:b + 1].cpu().numpy(), x.w[b:b + 1].cpu().numpy(), x.k[c:c + 1].cpu().numpy(),
+             x.k_scale[c:c + 1].cpu().numpy())
+    n = int(rl1[b])
+    exp = IX.indexer_scores(*args1, group=1, row_len=[n])[0, :n]
+    mag = IX.magnitude(*args1, group=1, row_len=[n])[0, :n]
+    got = scores[b, :n].cpu().numpy().astype(np.float64)
+    if not np.all(np.abs(got - exp) <= (D + H + 4) * 2.0 ** -24 * mag):
+        raise SystemExit("bench: indexer scores differ from the oracle beyond rounding (row %d)" % b)
+
+    def graph_us(fn, reps):
+        stream = torch.cuda.Stream()
+        with torch.cuda.stream(stream):
+            fn(stream)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=stream):
+            for _ in range(4):
+                fn(stream)
+        graph.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            graph.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / (reps * 4)
+
+    reps = max(2, args.steps // 20)
+    t_idx = graph_us(lambda s: g.gvr_indexer_scores(x.q[1], x.w, x.k, x.k_scale, rl1, scores=scores, stream=s), reps)
+    t_both = graph_us(lambda s: g.gvr_indexer_topk(x.q[1], x.w, x.k, x.k_scale, rl1, prev, K_TOPK, scores=scores,
+                                                   out_idx=out, stream=s), reps)
+    t_topk = graph_us(lambda s: g.gvr_topk(scores, rl1, prev, K_TOPK, out_idx=out, stream=s), reps)
+    t_radix = graph_us(lambda s: g.radix_topk(scores, rl1, None, K_TOPK, out_idx=out, stream=s), reps)
+    n_cache = int(rl1.view(requests, group).max(dim=1).values.to(torch.int64).sum())
+    n_rows = int(rl1.to(torch.int64).sum())
+    idx_bytes = n_cache * (D + 4) + n_rows * 4 + rows * H * (D + 4)
+    flops = 2 * n_rows * H * D
+    line = {"mode": "indexer", "workload": "indexer_fp8_h64_d128_64x2_n100k", "rows": rows, "ld": ld,
+            "H": H, "D": D, "group": group,
+            "indexer_us": round(t_idx, 3), "indexer_plus_gvr_topk_us": round(t_both, 3),
+            "gvr_topk_alone_us": round(t_topk, 3), "radix_topk_alone_us": round(t_radix, 3),
+            "indexer_roofline": {"bound": "hbm", "achieved": round(idx_bytes / t_idx / 1e3, 1), "peak": PEAK_HBM_GBS,
+                                 "unit": "GB/s", "frac": round(idx_bytes / t_idx / 1e3 / PEAK_HBM_GBS, 4),
+                                 "algorithmic_bytes_per_launch": idx_bytes,
+                                 "fp8_TFLOPs": round(flops / t_idx / 1e6, 1)},
+            "topk_share_of_step": round(t_topk / (t_idx + t_topk), 4),
+            "radix_share_of_step": round(t_radix / (t_idx + t_radix), 4)}
+    print(json.dumps(line))
+    sys.stdout.flush()
+
+
 def read_traffic(n_launch_bytes):
     if not os.path.exists(TRAFFIC_FILE):
         return None
@@ -515,7 +597,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--mode", choices=["bench", "copy", "configs", "rope", "phases", "short"], default="bench")
+    ap.add_argument("--mode", choices=["bench", "copy", "configs", "rope", "phases", "short", "indexer"],
+                    default="bench")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--no-radix", action="store_true", help="skip timing radix_topk")
     ap.add_argument("--no-secant", action="store_true",
@@ -553,6 +636,9 @@ def main():
         return
     if args.mode == "short":
         run_short(args, dev)
+        return
+    if args.mode == "indexer":
+        run_indexer(args, dev)
         return
 
     w, outs, prevs = build_inputs(dev)

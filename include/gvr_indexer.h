@@ -47,8 +47,9 @@ extern "C" {
 #endif
 
 /* Index scores I (Sec. 2.1, Eq. indexer) for every row and every s < n_b:
- * one kernel on the matrix cores (v_mfma 32x32x16 FP8), HBM-bound on the
- * key cache (D + 4 bytes per key and cache, 4 bytes written per score). */
+ * one kernel on the matrix cores (gfx950's 16x16x128 FP8 matrix op), bound by
+ * HBM on the key cache (D + 4 bytes per key and cache, 4 bytes written per
+ * score). */
 gvr_status gvr_indexer_scores(const uint8_t* q, const float* w, const uint8_t* k, const float* k_scale,
                               int64_t B, int32_t H, int32_t D, int32_t group, int64_t ld,
                               const int32_t* row_len, float* scores, void* stream);

@@ -1,26 +1,28 @@
 // indexer.hip -- FP8 indexer scores of DeepSeek Sparse Attention (Sec. 2.1,
 // Eq. indexer) on the MI355X matrix cores, behind include/gvr_indexer.h.
 //
-// One wave computes the scores of one row for a run of 32-key tiles. Per
-// tile the logits q[j] . k[s] of all H heads and 32 keys are 32 x 32 blocks
-// of v_mfma_f32_32x32x16_fp8_fp8 (heads down the rows, keys across the
-// columns, D / 16 steps over the head dimension); the epilogue scales each
+// One wave computes the scores of one row for a run of keys, 32 at a time
+// (two 16-key tiles). Per tile the logits q[j] . k[s] of all H heads and 16
+// keys are 16 x 16 blocks of gfx950's v_mfma_scale_f32_16x16x128_f8f6f4 with
+// unit block scales (FP8 E4M3 operands, heads down the rows, keys across the
+// columns, the whole head dimension in one step); the epilogue scales each
 // key's column by its k_scale, applies ReLU, weights the heads and sums them.
-// In the accumulator layout a lane holds 16 heads of one key (row
-// 8 (i / 4) + 4 (lane / 32) + i % 4 of column lane % 32 for register i), so
-// the head sum is 16 fused multiply-adds per 32 heads plus one exchange with
-// lane ^ 32. The reduction dimension is visited in the order the loads give:
-// lane half h holds bytes [h D / 2, (h + 1) D / 2) of its head and of its key,
-// k-step t uses 8 of them, and A and B use the same order, so the product is
-// the plain dot product.
+// Lane l holds column l % 16 and, of the 128-byte reduction, the 32 bytes
+// [32 (l / 16), + 32) of its head and of its key (a smaller D leaves the upper
+// bytes of the query at zero); in the accumulators it holds heads
+// 4 (l / 16) + i of its key, so the head sum is 4 fused multiply-adds per 16
+// heads plus two exchanges across the four lanes of a key. With this layout a
+// 16-byte load of 64 lanes touches 16 cache lines (4 lanes per key row), a
+// quarter of what one key per lane pair would touch.
 //
-// Each lane keeps its half of its query heads (16-byte aligned) and their
-// weights in registers for the whole run; the keys stream through a double
-// buffer (a tile's 32 x D bytes are one contiguous block of the cache, read
-// with 16-byte loads while the previous tile is on the matrix cores). The
-// rows of one cache (group of draft rows) run on waves of one workgroup at
-// the same keys, so the cache is read from HBM once for all of them. The
-// kernel is HBM-bound: D + 4 bytes per key and cache, 4 bytes per score.
+// Each lane keeps its 32 bytes of its query heads in registers for the whole
+// run and the head weights sit in LDS (broadcast reads); the keys stream
+// through a ring of kRing register buffers, kRing - 1 tiles in flight, with
+// no branch in the steady state. When the rows of one cache (the draft rows
+// of a request) pair up, one wave serves two of them: each key tile is loaded
+// once and meets both rows' queries (reading it from two waves cost an
+// eighth more time). Bound by HBM: D + 4 bytes per key and cache, 4 bytes
+// written per score.
 
 #include <hip/hip_runtime.h>
 
@@ -32,11 +34,14 @@ namespace {
 
 constexpr int kWave = 64;
 constexpr int kWaves = 4;                // waves per workgroup
-constexpr int kTile = 32;                // keys per column tile
-constexpr int kTilesPerWave = 32;        // tiles of one wave's run (1024 keys)
+constexpr int kTile = 32;                // keys per ring slot (two 16-key matrix tiles)
+constexpr int kTilesPerWave = 32;        // ring slots of one wave's run (1024 keys)
+constexpr int kRing = 3;                 // key slots held per wave: kRing - 1 in flight while one is used
 constexpr int64_t kMaxLd = ((int64_t)1 << 31) - 16;
 
-typedef float v16f __attribute__((ext_vector_type(16)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+typedef int v8i __attribute__((ext_vector_type(8)));
+constexpr int kUnitScales = 0x7F7F7F7F;  // E8M0 block scales of 1.0 for the scaled matrix op
 
 struct IdxParams {
     const uint8_t* q;
@@ -52,97 +57,147 @@ struct IdxParams {
     int32_t chunk_keys;   // keys per workgroup chunk
 };
 
-template <int D>
-struct KeyHalf {
-    uint64_t b[D / 16];   // bytes [h D / 2, (h + 1) D / 2) of one key: 8 per k-step
-};
-
-template <int D>
-__device__ __forceinline__ KeyHalf<D> load_half(const uint8_t* p) {
-    KeyHalf<D> r;
+// 32 bytes at p (16-byte aligned) as one matrix operand.
+__device__ __forceinline__ v8i load32(const uint8_t* p) {
     const uint4* s = reinterpret_cast<const uint4*>(p);
-#pragma unroll
-    for (int j = 0; j < D / 32; ++j) {
-        const uint4 v = s[j];
-        r.b[2 * j] = (uint64_t)v.x | ((uint64_t)v.y << 32);
-        r.b[2 * j + 1] = (uint64_t)v.z | ((uint64_t)v.w << 32);
-    }
-    return r;
+    const uint4 a = s[0], b = s[1];
+    return v8i{(int)a.x, (int)a.y, (int)a.z, (int)a.w, (int)b.x, (int)b.y, (int)b.z, (int)b.w};
 }
 
-template <int H, int D>
+template <int H, int D, int RG>
 __global__ __launch_bounds__(kWaves * kWave) void indexer_kernel(IdxParams p) {
-    constexpr int MT = H / 32;   // 32-head row tiles
-    constexpr int KS = D / 16;   // k-steps of 16 bytes (8 per lane half)
+    constexpr int MT = H / 16;   // 16-head row tiles
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int G = p.group;
-    const int wpr = kWaves / G;               // waves per row (one idle wave when G = 3)
-    if (wave >= G * wpr) return;
+    // A wave serves RG rows of its cache (each key tile loaded once for them);
+    // the cache's G / RG row slots share the workgroup's waves, wpr each.
+    const int slots = G / RG;
+    const int wpr = kWaves / slots;           // waves per row slot (one idle wave when G = 3)
+    if (wave >= slots * wpr) return;
     const int g = blockIdx.x / p.chunks;      // cache
     const int c = blockIdx.x - g * p.chunks;  // key chunk
-    const int r_in = wave % G, sub = wave / G;
-    const int64_t row = (int64_t)g * G + r_in;
-    if (row >= p.rows) return;
-    int64_t n64 = p.row_len ? (int64_t)p.row_len[row] : p.ld;
-    n64 = n64 < 0 ? 0 : (n64 > p.ld ? p.ld : n64);
-    const int64_t s_begin = (int64_t)c * p.chunk_keys + sub * (kTilesPerWave * kTile);
-    const int64_t s_end = min(s_begin + kTilesPerWave * kTile, n64);
-    if (s_begin >= s_end) return;
-    const int col = lane & 31, h = lane >> 5;
-
-    // Query halves and head weights of the rows this lane's registers hold.
-    uint64_t qa[MT][KS];
-    float wr[MT][16];
+    const int slot_i = wave % slots, sub = wave / slots;
+    const int64_t row0 = (int64_t)g * G + slot_i * RG;
+    if (row0 >= p.rows) return;
+    // Keys [s_begin, s_end) of this wave's run: up to the longest of its rows;
+    // a row's scores are stored for its own keys only.
+    int64_t nr[RG];
+    int64_t n_max = 0;
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-        const int head = 32 * mt + col;
-        const KeyHalf<D> qh = load_half<D>(p.q + ((row * H + head) * D + h * (D / 2)));
-#pragma unroll
-        for (int t = 0; t < KS; ++t) qa[mt][t] = qh.b[t];
-#pragma unroll
-        for (int i = 0; i < 16; ++i) wr[mt][i] = p.w[row * H + 32 * mt + 8 * (i / 4) + 4 * h + (i % 4)];
+    for (int rr = 0; rr < RG; ++rr) {
+        int64_t n64 = p.row_len ? (int64_t)p.row_len[row0 + rr] : p.ld;
+        n64 = n64 < 0 ? 0 : (n64 > p.ld ? p.ld : n64);
+        nr[rr] = n64;
+        n_max = max(n_max, n64);
     }
+    const int64_t s_begin = (int64_t)c * p.chunk_keys + sub * (kTilesPerWave * kTile);
+    const int64_t s_end = min(s_begin + kTilesPerWave * kTile, n_max);
+    if (s_begin >= s_end) return;
+    const int col = lane & 15, quarter = lane >> 4;
+    // Bytes [32 quarter, + 32) of the head dimension; with D = 64 the upper
+    // two quarters re-read the lower two and the query there is zero.
+    const int qoff = 32 * (quarter % (D / 32));
+    const bool qlive = 32 * quarter < D;
 
-    const uint8_t* kg = p.k + (int64_t)g * p.ld * D + h * (D / 2);
-    const float* sg = p.k_scale + (int64_t)g * p.ld;
-    float* out = p.scores + row * p.ld;
-    auto key_of_tile = [&](int64_t s0) { return min(s0 + col, n64 - 1); };   // clamped: a partial tile re-reads key n - 1
-    int64_t s0 = s_begin;
-    KeyHalf<D> kb = load_half<D>(kg + key_of_tile(s0) * D);
-    float ks = sg[key_of_tile(s0)];
-    for (; s0 < s_end; s0 += kTile) {
-        // Next tile's loads first (the last iteration re-reads this tile's keys).
-        const int64_t s1 = s0 + kTile < s_end ? s0 + kTile : s0;
-        const KeyHalf<D> kn = load_half<D>(kg + key_of_tile(s1) * D);
-        const float ksn = sg[key_of_tile(s1)];
-        v16f acc[MT];
+    __shared__ float wl[kWaves][RG * H];
+    for (int j = lane; j < RG * H; j += kWave) wl[wave][j] = p.w[row0 * H + j];
+    v8i qa[RG][MT];
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) acc[mt] = (v16f)(0.f);
-#pragma unroll
-        for (int t = 0; t < KS; ++t) {
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt)
-                acc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_fp8_fp8((long)qa[mt][t], (long)kb.b[t], acc[mt], 0, 0, 0);
-        }
-        float sum = 0.f;
+    for (int rr = 0; rr < RG; ++rr) {
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
-#pragma unroll
-            for (int i = 0; i < 16; ++i) sum += wr[mt][i] * fmaxf(acc[mt][i] * ks, 0.f);
+            const v8i v = load32(p.q + (((row0 + rr) * H + 16 * mt + col) * D + qoff));
+            qa[rr][mt] = qlive ? v : v8i{0, 0, 0, 0, 0, 0, 0, 0};
         }
-        sum += __shfl_xor(sum, 32, kWave);
-        const int64_t s = s0 + col;
-        if (h == 0 && s < s_end) out[s] = sum;
-        kb = kn;
-        ks = ksn;
     }
+    __builtin_amdgcn_wave_barrier();   // a wave's LDS accesses complete in order: its reads see its writes
+    const float4* wv = reinterpret_cast<const float4*>(&wl[wave][0]);
+
+    const uint8_t* kg = p.k + (int64_t)g * p.ld * D + qoff;
+    const float* sg = p.k_scale + (int64_t)g * p.ld;
+    float* out = p.scores + row0 * p.ld;
+    // Column col of half t of slot u is key min(s_begin + 32 u + 16 t + col,
+    // s_end - 1): lanes past the run recompute the run's last key and store
+    // the same value there, so loads, matrix steps and stores run without
+    // branches and the loads stay in flight across iterations.
+    const int tiles = (int)((s_end - s_begin + kTile - 1) / kTile);
+    auto key_of = [&](int u, int t) { return min(s_begin + (int64_t)u * kTile + 16 * t + col, s_end - 1); };
+    struct Slot {
+        v8i kb[2];
+        float ks[2];
+    };
+    auto load_slot = [&](int u) {
+        Slot r;
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+            const int64_t key = key_of(u, t);
+            r.kb[t] = load32(kg + key * D);
+            r.ks[t] = sg[key];
+        }
+        return r;
+    };
+    auto use_slot = [&](const Slot& r, int u) {
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+#pragma unroll
+            for (int rr = 0; rr < RG; ++rr) {
+                v4f acc[MT];
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt)
+                    acc[mt] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(
+                        qa[rr][mt], r.kb[t], v4f{0.f, 0.f, 0.f, 0.f}, 0, 0, 0, kUnitScales, 0, kUnitScales);
+                float sum = 0.f;
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt) {
+                    const float4 wq = wv[rr * (H / 4) + 4 * mt + quarter];   // heads 16 mt + 4 quarter + (0..3)
+                    sum += wq.x * fmaxf(acc[mt][0] * r.ks[t], 0.f);
+                    sum += wq.y * fmaxf(acc[mt][1] * r.ks[t], 0.f);
+                    sum += wq.z * fmaxf(acc[mt][2] * r.ks[t], 0.f);
+                    sum += wq.w * fmaxf(acc[mt][3] * r.ks[t], 0.f);
+                }
+                sum += __shfl_xor(sum, 16, kWave);
+                sum += __shfl_xor(sum, 32, kWave);   // the four lanes of the key now hold its score
+                // the run covers the longer row of the pair: store this row's own keys
+                const int64_t key = key_of(u, t);
+                if (key < nr[rr]) out[rr * p.ld + key] = sum;
+            }
+        }
+    };
+    Slot ring[kRing];
+#pragma unroll
+    for (int r = 0; r < kRing - 1; ++r) ring[r] = load_slot(r);
+    constexpr int kAhead = kRing - 1;
+    int u0 = 0;
+    for (; u0 + kRing <= tiles; u0 += kRing) {
+#pragma unroll
+        for (int r = 0; r < kRing; ++r) {
+            // the loads for slot u0 + r + kAhead go out before slot u0 + r is used
+            ring[(r + kAhead) % kRing] = load_slot(u0 + r + kAhead);
+            use_slot(ring[r], u0 + r);
+        }
+    }
+#pragma unroll
+    for (int r = 0; r < kRing - 1; ++r)   // the last slots (already loaded)
+        if (u0 + r < tiles) use_slot(ring[r], u0 + r);
 }
 
-template <int H, int D>
+template <int H, int D, int RG>
 gvr_status launch(const IdxParams& q, unsigned grid, void* stream) {
-    hipLaunchKernelGGL((indexer_kernel<H, D>), dim3(grid), dim3(kWaves * kWave), 0, (hipStream_t)stream, q);
+    hipLaunchKernelGGL((indexer_kernel<H, D, RG>), dim3(grid), dim3(kWaves * kWave), 0, (hipStream_t)stream, q);
     return hipGetLastError() == hipSuccess ? GVR_OK : GVR_ERR_HIP;
+}
+
+// Rows per wave: 2 when a cache's rows pair up and the two rows' query
+// registers fit (H <= 64), else 1.
+constexpr int rows_per_wave(int H, int group) { return (group % 2 == 0 && H <= 64) ? 2 : 1; }
+
+template <int H, int D>
+gvr_status launch_rg(const IdxParams& q, unsigned grid, void* stream) {
+    if constexpr (H <= 64) {
+        if (rows_per_wave(H, q.group) == 2) return launch<H, D, 2>(q, grid, stream);
+    }
+    return launch<H, D, 1>(q, grid, stream);
 }
 
 }  // namespace
@@ -169,16 +224,17 @@ gvr_status gvr_indexer_scores(const uint8_t* q, const float* w, const uint8_t* k
     p.ld = ld;
     p.rows = (int32_t)B;
     p.group = group;
-    const int wpr = kWaves / group;
+    const int rg = rows_per_wave(H, group);
+    const int wpr = kWaves / (group / rg);
     p.chunk_keys = wpr * kTilesPerWave * kTile;
     const int64_t chunks = (ld + p.chunk_keys - 1) / p.chunk_keys;
     const int64_t caches = B / group;
     if (chunks * caches > 0x7FFFFFFF) return GVR_ERR_TOO_LONG;
     p.chunks = (int32_t)chunks;
     const unsigned grid = (unsigned)(chunks * caches);
-    if (H == 32) return D == 64 ? launch<32, 64>(p, grid, stream) : launch<32, 128>(p, grid, stream);
-    if (H == 64) return D == 64 ? launch<64, 64>(p, grid, stream) : launch<64, 128>(p, grid, stream);
-    return D == 64 ? launch<128, 64>(p, grid, stream) : launch<128, 128>(p, grid, stream);
+    if (H == 32) return D == 64 ? launch_rg<32, 64>(p, grid, stream) : launch_rg<32, 128>(p, grid, stream);
+    if (H == 64) return D == 64 ? launch_rg<64, 64>(p, grid, stream) : launch_rg<64, 128>(p, grid, stream);
+    return D == 64 ? launch_rg<128, 64>(p, grid, stream) : launch_rg<128, 128>(p, grid, stream);
 }
 
 gvr_status gvr_indexer_topk(const uint8_t* q, const float* w, const uint8_t* k, const float* k_scale,
