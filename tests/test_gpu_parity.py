@@ -557,3 +557,44 @@ def test_many_short_rows_take_the_short_shape():
         assert -1 not in set(g.decode_stats(st)["path"].tolist())
     out = g.radix_topk(S, RL, None, K)
     assert_rows_equal(out.cpu().numpy(), exp, "many short rows, radix")
+
+
+def test_graph_replays_match_the_oracle():
+    """Calls captured into a HIP graph (split rows through the workspace, the
+    4-wave shape, the guess-free kernel) give the oracle's answer on every
+    replay, with eager calls and synchronisations between replays."""
+    import paper_2604_22312_amd as g
+    rng = np.random.default_rng(31)
+    K = 2048
+    cases = []
+    # two long rows: split into parts (workspace); 800 short rows: 4-wave shape; 3 rows <= 2K
+    for B, ld in ((2, 131072), (800, 9000), (3, 4000)):
+        x = rng.standard_normal((B, ld)).astype(np.float32)
+        prevx = x + 0.05 * rng.standard_normal((B, ld)).astype(np.float32)
+        exp, _, _ = oracle.topk(x, K)
+        pexp, _, _ = oracle.topk(prevx, K)
+        cases.append((torch.from_numpy(x).to(DEV), torch.from_numpy(pexp).to(DEV), exp))
+    outs = [torch.empty((c[0].shape[0], K), dtype=torch.int32, device=DEV) for c in cases]
+    stream = torch.cuda.Stream()
+    with torch.cuda.stream(stream):   # eager calls first: the workspace exists before capture
+        for (S, P, _), o in zip(cases, outs):
+            g.gvr_topk(S, None, P, K, out_idx=o, stream=stream)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    note("graph capture of gvr_topk calls")
+    with torch.cuda.graph(graph, stream=stream):
+        for (S, P, _), o in zip(cases, outs):
+            g.gvr_topk(S, None, P, K, out_idx=o, stream=stream)
+    for rep in range(4):
+        for o in outs:
+            o.fill_(-7)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for (_, _, exp), o in zip(cases, outs):
+            assert_rows_equal(o.cpu().numpy(), exp, "graph replay %d" % rep)
+        # eager work between replays on the same buffers
+        S, P, exp = cases[0]
+        o = g.gvr_topk(S, None, P, K)
+        torch.cuda.synchronize()
+        assert_rows_equal(o.cpu().numpy(), exp, "eager call between replays")
