@@ -61,7 +61,8 @@ def oracle_scores(x, t=0):
             IX.magnitude(*args, group=x.group, row_len=rl))
 
 
-SHAPES = [(64, 128, 2), (64, 128, 1), (32, 64, 3), (128, 128, 4), (64, 64, 1), (32, 128, 2)]
+SHAPES = [(64, 128, 2), (64, 128, 1), (32, 64, 3), (128, 128, 4), (64, 64, 1), (32, 128, 2), (64, 128, 4),
+          (32, 64, 4), (128, 64, 2)]
 
 
 @pytest.mark.parametrize("H,D,group", SHAPES, ids=["h%d_d%d_g%d" % s for s in SHAPES])
