@@ -598,3 +598,25 @@ def test_graph_replays_match_the_oracle():
         o = g.gvr_topk(S, None, P, K)
         torch.cuda.synchronize()
         assert_rows_equal(o.cpu().numpy(), exp, "eager call between replays")
+
+
+@pytest.mark.parametrize("opts", [{"flags": 16, "capacity": 2048}, {"flags": 16, "capacity": 2500},
+                                  {"flags": 16 | 1}, {"flags": 16 | 8, "capacity": 3000}],
+                         ids=["short_cap_K", "short_cap_2500", "short_no_guess", "short_paper_refine_cap"])
+def test_short_shape_forced_paths(opts):
+    """The 4-wave shape through its narrowing, ties and guess-free paths
+    (small capacities force them); same answer as the oracle."""
+    import paper_2604_22312_amd as g
+    w = workload(1, 3, 8, None)
+    K = w.K
+    S = w.scores[2].to(DEV)
+    RL = w.row_len[2].to(DEV)
+    exp, _, _ = oracle.topk(w.scores[2].numpy(), K, row_len=w.row_len[2].numpy())
+    prev, _, _ = oracle.topk(w.scores[1].numpy(), K, row_len=w.row_len[1].numpy())
+    note("short shape forced paths %s" % opts)
+    st = g.new_stats(w.rows, DEV)
+    out = g.gvr_topk_ex(S, RL, torch.from_numpy(prev).to(DEV), K, options=opts, stats=st)
+    assert_rows_equal(out.cpu().numpy(), exp, "short shape %s" % opts)
+    assert -1 not in set(g.decode_stats(st)["path"].tolist())
+    out = g.radix_topk_ex(S, RL, K, options=opts)
+    assert_rows_equal(out.cpu().numpy(), exp, "radix short shape %s" % opts)
