@@ -99,9 +99,10 @@ enum {
 /* Optional knobs (NULL = defaults). Zero fields mean "default". */
 typedef struct gvr_options {
     int32_t capacity;      /* refine capacity C, K <= C <= GVR_MAX_CANDIDATES
-                              (default GVR_MAX_CANDIDATES, at most 4096 in the
-                              short-row shape); a smaller C forces more
-                              narrowing passes, never another result */
+                              (default GVR_MAX_CANDIDATES; at most 4096 in
+                              the 4-wave and 6144 in the 8-wave shape); a
+                              smaller C forces more narrowing passes, never
+                              another result */
     int32_t flags;         /* bit 0: ignore prev_topk (run the radix schedule);
                               bit 1: place the parts of a row on different XCDs
                               (a test of the path that does not rely on their
@@ -114,13 +115,17 @@ typedef struct gvr_options {
                               min / max, 2048-bin histogram with a wave-parallel
                               bin search, snap iterations, partition) instead of
                               the histogram + rank-count refine;
-                              bit 4: force the short-row workgroup shape (4
-                              waves, C <= 4096, three workgroups per compute
-                              unit, no row splitting); bit 5: force the
-                              16-wave shape; neither: 4 waves when there are
-                              more than three rows per compute unit and
-                              ld <= 12288, or more than one and ld <= 4096,
-                              else 16. Bits 4 and 5 together are an error.
+                              bits 4-6 force a workgroup shape (no row
+                              splitting except with 16 waves): bit 4: 4 waves,
+                              C <= 4096, three workgroups per compute unit;
+                              bit 5: 16 waves, one per compute unit; bit 6: 8
+                              waves, C <= 6144, two per compute unit. None
+                              set: 16 waves when B <= the compute units;
+                              above that, with a usable guess (prev_topk and
+                              ld > 2K), 8 waves unless ld > 40960 and
+                              B <= 2 x the compute units (then 16); without
+                              one, 4 waves for ld <= 4096, else 8. Two of
+                              bits 4-6 together are an error.
                               No bit changes the result. */
     int32_t parts;         /* workgroups per row, 1..16 (0 = chosen from B, ld
                               and the device's compute units; a forced value is

@@ -27,8 +27,8 @@ class Options(ctypes.Structure):
     """Mirror of ``gvr_options``: capacity C, flags (bit 0: ignore the guess;
     bit 1: scatter a row's parts over XCDs; bit 2: the paper's secant
     threshold search; bit 3: the paper's snap-iteration selection; bit 4 /
-    bit 5: force the 4-wave / 16-wave workgroup shape), parts (workgroups per
-    row, 0 = automatic)."""
+    5 / 6: force the 4-wave / 16-wave / 8-wave workgroup shape), parts
+    (workgroups per row, 0 = automatic)."""
     _fields_ = [("capacity", ctypes.c_int32), ("flags", ctypes.c_int32),
                 ("parts", ctypes.c_int32), ("reserved1", ctypes.c_int32)]
 

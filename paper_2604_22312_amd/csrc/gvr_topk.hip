@@ -73,24 +73,28 @@ constexpr int kU = 8;                          // slabs in flight per wave (coun
 constexpr int kSU = 8;                         // slabs in flight per wave (speculative pass)
 constexpr int kBins = 256;                     // bins of a counting window
 constexpr int kBinsX = kBins + 1;              // + "at or above the window"
-constexpr int kCapW = 1024;                    // per-wave list capacity, speculative pass
+constexpr int kCapWLong = 1024;                // per-wave list capacity of the 16- and 4-wave shapes
+constexpr int kCapWMid = 768;                  // per-wave list capacity of the 8-wave shape
 constexpr int kPartCap = GVR_MAX_CANDIDATES;   // entries per (row, part) list in the split-row workspace
 
-// Workgroup shape: NW wave64s, 1024 list entries per wave. The 16-wave shape
-// (128 KB of lists, one workgroup per compute unit) streams a long row as
-// fast as one compute unit can and is the only one that splits rows; the
-// 4-wave shape (32 KB of lists, three workgroups per compute unit) serves
-// large batches of short rows, whose time goes into per-row latency.
+// Workgroup shape: NW wave64s. The 16-wave shape (1024 list entries per wave,
+// 128 KB of lists, one workgroup per compute unit) streams a long row as fast
+// as one compute unit can and is the only one that splits rows. The 8-wave
+// shape (768 entries per wave, 48 KB, two workgroups per compute unit) and
+// the 4-wave shape (1024 per wave, 32 KB, three per compute unit) serve
+// batches with more rows than compute units, whose time goes into per-row
+// latency that several resident rows overlap.
 template <int NW>
 struct Shape {
     static constexpr int kNW = NW;
     static constexpr int kBlock = NW * kWave;
     static constexpr int kSW = NW - 1;          // streaming waves of the speculative pass (wave 0: guess)
+    static constexpr int kCapW = NW == 8 ? kCapWMid : kCapWLong;   // per-wave list capacity, speculative pass
     static constexpr int kCap = NW * kCapW;     // list capacity C (LDS)
 };
 constexpr int kNWLong = 16;
 constexpr int kNWShort = 4;
-constexpr int64_t kShortMaxLd = 12288;        // longest row stride the 4-wave shape is chosen for
+constexpr int kNWMid = 8;
 static_assert(Shape<kNWLong>::kCap == GVR_MAX_CANDIDATES, "the long-row shape holds the largest capacity");
 constexpr int kRefBins = 4096;                 // bins of a narrowing refine level (12 bits of key)
 constexpr int kRefBins1 = 2048;                // bins of the first refine level (32 per lane of one wave)
@@ -300,7 +304,8 @@ template <int NW>
 constexpr bool lds_slack_ok() {
     return offsetof(Smem<NW>, u) == sizeof(uint2) * Shape<NW>::kCap && sizeof(Smem<NW>::u) >= 4 * kWave * sizeof(uint2);
 }
-static_assert(lds_slack_ok<kNWLong>() && lds_slack_ok<kNWShort>(), "LDS slack after the candidate list");
+static_assert(lds_slack_ok<kNWLong>() && lds_slack_ok<kNWShort>() && lds_slack_ok<kNWMid>(),
+              "LDS slack after the candidate list");
 
 // Block-wide exclusive scan of one int (all threads of the workgroup). Returns the total.
 template <int NW>
@@ -935,7 +940,7 @@ DEV void topk_body(const Params& p) {
     // no guess, or the row is at most 2K long: there a guess cuts few
     // candidates and often leaves f(T_spec) < K (a guess also cuts the
     // candidates of longer short rows).
-    const bool all_mode = (!(GUESS && p.prev) || n <= 2 * K) && (n <= cap) && (ws * 256 <= kCapW);
+    const bool all_mode = (!(GUESS && p.prev) || n <= 2 * K) && (n <= cap) && (ws * 256 <= W::kCapW);
     bool have_prev = GUESS && p.prev && !all_mode;
     // The paper's Phase 2 schedule (secant counting passes), when asked for.
     const bool secant = GUESS && p.secant && have_prev;
@@ -949,7 +954,7 @@ DEV void topk_body(const Params& p) {
     bool hist_ready = false; // the refine's first histogram level is built (lists at tthr)
     uint32_t tthr = 0u;      // threshold of the speculative lists
     bool overflow = false;
-    if (tid < NW) sm.seg_off[tid] = tid * kCapW;
+    if (tid < NW) sm.seg_off[tid] = tid * W::kCapW;
 
     if (spec) {
         if (!all_mode) {
@@ -1075,7 +1080,7 @@ DEV void topk_body(const Params& p) {
         // every list stays in index order; one capacity check per slab
         // (wave-uniform), and a wave whose list would overflow keeps counting.
         int cnt_w = 0;
-        uint2* lw = sm.list + wave * kCapW;
+        uint2* lw = sm.list + wave * W::kCapW;
         // The streaming waves wait for T_spec here, with their first slabs in
         // flight (polling an LDS flag, not a barrier: issuing those loads may
         // stall a wave, which must not hold up wave 0).
@@ -1129,7 +1134,7 @@ DEV void topk_body(const Params& p) {
                     cnt_w = __builtin_amdgcn_readlane(q, kWave - 1);
                 } else {
                     const int total = __popcll(m[0]) + __popcll(m[1]) + __popcll(m[2]) + __popcll(m[3]);
-                    if (cnt_w + total <= kCapW) {
+                    if (cnt_w + total <= W::kCapW) {
                         int q = below;
 #pragma unroll
                         for (int c = 0; c < 4; ++c) {
@@ -1147,14 +1152,14 @@ DEV void topk_body(const Params& p) {
             for (; s0 + 2 * kSU <= nsl; s0 += kSU) {
 #pragma unroll
                 for (int u = 0; u < kSU; ++u) {
-                    slab(buf[u], s0 + u, cnt_w <= kCapW - 256);
+                    slab(buf[u], s0 + u, cnt_w <= W::kCapW - 256);
                     buf[u] = slab_load(s0 + u + kSU);
                 }
             }
             if (s0 + kSU <= nsl) {
 #pragma unroll
                 for (int u = 0; u < kSU; ++u) {
-                    slab(buf[u], s0 + u, cnt_w <= kCapW - 256);
+                    slab(buf[u], s0 + u, cnt_w <= W::kCapW - 256);
                     if (s0 + u + kSU < nsl) buf[u] = slab_load(s0 + u + kSU);
                 }
                 s0 += kSU;
@@ -1173,15 +1178,15 @@ DEV void topk_body(const Params& p) {
         // [T_spec, max(pmax, T_spec)] (cleared by wave 0 before its flag):
         // waves done with their slabs do this while the others still stream.
         const bool own_hist = S == 1 && !all_mode;
-        if (cnt_w <= kCapW) keys_in_place(sm, lw, cnt_w, own_hist, tspec, ref_shift(tspec, max(gmax, tspec)), lane);
+        if (cnt_w <= W::kCapW) keys_in_place(sm, lw, cnt_w, own_hist, tspec, ref_shift(tspec, max(gmax, tspec)), lane);
         if (lane == 0) {
             sm.wa[wave] = cnt_w;
-            sm.seg_cnt[wave] = min(cnt_w, kCapW);
+            sm.seg_cnt[wave] = min(cnt_w, W::kCapW);
         }
         passes = 1;
         lds_barrier();
         t2 = stamp();   // every wave of the part has streamed its slabs
-        overflow = wave_max_u(lane < NW ? (uint32_t)sm.wa[lane] : 0u) > (uint32_t)kCapW;
+        overflow = wave_max_u(lane < NW ? (uint32_t)sm.wa[lane] : 0u) > (uint32_t)W::kCapW;
         f_spec = overflow ? -1 : sum_over_waves<NW>(sm.wa, lane);
         hist_ready = own_hist && !overflow;
         tthr = tspec;
@@ -1281,7 +1286,7 @@ DEV void topk_body(const Params& p) {
             const bool publish = !overflow && f_spec <= cap;
             if (publish) {   // this part's entries, in index order
                 const int off = sum_over_waves_below(sm.wa, lane, wave);
-                const uint2* seg = sm.list + wave * kCapW;
+                const uint2* seg = sm.list + wave * W::kCapW;
                 const int cnt = sm.seg_cnt[wave];
                 for (int i0 = 0; i0 < cnt; i0 += 4 * kWave) {
                     uint2 e[4];
@@ -1961,14 +1966,15 @@ gvr_status validate(const float* scores, int64_t B, int64_t ld, int32_t K, const
             if (opt->capacity < K || opt->capacity > GVR_MAX_CANDIDATES) return GVR_ERR_INVALID_ARG;
             cap = opt->capacity;
         }
-        if ((opt->flags & ~63) || opt->reserved1) return GVR_ERR_INVALID_ARG;
-        if (((opt->flags >> 4) & 3) == 3) return GVR_ERR_INVALID_ARG;   // both shapes forced
+        if ((opt->flags & ~127) || opt->reserved1) return GVR_ERR_INVALID_ARG;
+        const int forced = (opt->flags >> 4) & 7;
+        if (forced & (forced - 1)) return GVR_ERR_INVALID_ARG;   // two shapes forced
         if (opt->parts < 0 || opt->parts > kMaxParts) return GVR_ERR_INVALID_ARG;
         if (opt->flags & 1) *use_guess = 0;
         *scatter = (opt->flags >> 1) & 1;
         *secant = (opt->flags >> 2) & 1;
         *paper_refine = (opt->flags >> 3) & 1;
-        *shape = (opt->flags >> 4) & 3;
+        *shape = forced == 1 ? kNWShort : forced == 2 ? kNWLong : forced == 4 ? kNWMid : 0;
         *parts = opt->parts;
     }
     *capacity = cap;
@@ -2072,15 +2078,23 @@ int choose_parts(int64_t rows, int64_t ld, int cus) {
     return saved_us > 8.0 ? (int)s : 1;
 }
 
-// Workgroup shape of a call. The 16-wave shape takes one compute unit per
-// row and has the shortest per-row latency (about 12 us for 8K elements, 20
-// with 4 waves, whose refine runs on a quarter of the waves); with many more
-// rows than compute units and short rows, three 4-wave workgroups per compute
-// unit overlap three rows' latencies and win (2048 rows of 8K: 65 us against
-// 82; at 512 rows of 8K the two are even, at 512 rows of 4K the 4-wave shape
-// wins by 15 %).
-bool use_short_shape(int64_t rows, int64_t ld, int cus) {
-    return (rows > 3 * (int64_t)cus && ld <= kShortMaxLd) || (rows > cus && ld <= 4096);
+// Workgroup shape of a call: waves per workgroup (16, 8 or 4). Up to one row
+// per compute unit, 16 waves: one round of rows at the shortest per-row
+// latency, and row splitting. With more rows, the rows run in rounds of one
+// (16 waves), two (8) or three (4) workgroups per compute unit; the 8-wave
+// shape has the best rate of rows per compute unit when the previous Top-K
+// guides the rows (decode rows of 8K-64K elements: 1024 rows of 32K take
+// 42 us against 55 with 16 waves and 73 with 4), except for rows longer
+// than 40K in at most two rows per compute unit, where the 16-wave shape's
+// shorter latency wins (512 rows of 64K: 40 us against 47); from 48K on
+// the two are even at four rows per compute unit. Without a usable guess
+// the radix schedule runs, where rows of at most 4K go to 4 waves (2048
+// rows of 4K: 47 us against 73 with 8 waves) and longer ones to 8.
+int choose_shape(int64_t rows, int64_t ld, int cus, bool guess) {
+    if (rows <= cus) return kNWLong;
+    if (!guess) return ld <= 4096 ? kNWShort : kNWMid;
+    if (ld <= 40960 || rows > 2 * (int64_t)cus) return kNWMid;
+    return kNWLong;
 }
 
 gvr_status run(const float* scores, int64_t B, int64_t ld, const int32_t* row_len, const int32_t* prev,
@@ -2097,9 +2111,11 @@ gvr_status run(const float* scores, int64_t B, int64_t ld, const int32_t* row_le
     int device = 0;
     if (hipGetDevice(&device) != hipSuccess) return GVR_ERR_HIP;
     const int cus = cu_count(device);
-    const bool short_shape = shape == 1 || (shape == 0 && use_short_shape(B, ld, cus));
-    if (short_shape) cap = std::min(cap, Shape<kNWShort>::kCap);   // a smaller C never changes the result
-    int parts = (!guess || short_shape) ? 1 : (parts_opt > 0 ? parts_opt : choose_parts(B, ld, cus));
+    if (shape == 0) shape = choose_shape(B, ld, cus, guess);
+    // A smaller C never changes the result.
+    if (shape == kNWShort) cap = std::min(cap, Shape<kNWShort>::kCap);
+    if (shape == kNWMid) cap = std::min(cap, Shape<kNWMid>::kCap);
+    int parts = (!guess || shape != kNWLong) ? 1 : (parts_opt > 0 ? parts_opt : choose_parts(B, ld, cus));
     // A forced split is capped at kMaxSlots (row, part) pairs per call, which
     // bounds the workspace (128 KB of list per pair).
     if (parts > 1 && (int64_t)parts * B > kMaxSlots) parts = (int)std::max<int64_t>(1, kMaxSlots / B);
@@ -2135,7 +2151,13 @@ gvr_status run(const float* scores, int64_t B, int64_t ld, const int32_t* row_le
         q.part_list = ws.part_list;
         const dim3 grid((unsigned)(rows_pad * parts));
         const hipStream_t hs = (hipStream_t)stream;
-        if (short_shape) {
+        if (shape == kNWMid) {
+            const dim3 block(Shape<kNWMid>::kBlock);
+            if (guess)
+                hipLaunchKernelGGL(gvr_topk_kernel<kNWMid>, grid, block, 0, hs, q);
+            else
+                hipLaunchKernelGGL(radix_topk_kernel<kNWMid>, grid, block, 0, hs, q);
+        } else if (shape == kNWShort) {
             const dim3 block(Shape<kNWShort>::kBlock);
             if (guess)
                 hipLaunchKernelGGL(gvr_topk_kernel<kNWShort>, grid, block, 0, hs, q);

@@ -80,8 +80,10 @@ def test_options_validation(L):
     import paper_2604_22312_amd as g
     vp = ctypes.c_void_p
     bad = [g.Options(capacity=100, flags=0, parts=0, reserved1=0),      # capacity < K
-           g.Options(capacity=0, flags=64, parts=0, reserved1=0),       # unknown flag bit
-           g.Options(capacity=0, flags=48, parts=0, reserved1=0),       # both workgroup shapes forced
+           g.Options(capacity=0, flags=48, parts=0, reserved1=0),       # two workgroup shapes forced
+           g.Options(capacity=0, flags=80, parts=0, reserved1=0),       # two workgroup shapes forced
+           g.Options(capacity=0, flags=96, parts=0, reserved1=0),       # two workgroup shapes forced
+           g.Options(capacity=0, flags=112, parts=0, reserved1=0),      # three workgroup shapes forced
            g.Options(capacity=0, flags=128, parts=0, reserved1=0),      # unknown flag bit
            g.Options(capacity=0, flags=0, parts=0, reserved1=1),        # reserved field set
            g.Options(capacity=0, flags=0, parts=17, reserved1=0),       # too many parts

@@ -489,7 +489,7 @@ def test_paper_refine_special_rows(ld, K):
         assert_rows_equal(out.cpu().numpy(), exp, "radix with the paper refine ld=%d K=%d" % (ld, K))
 
 
-SHAPES = [("short", 16), ("long", 32)]
+SHAPES = [("short", 16), ("long", 32), ("mid", 64)]
 
 
 @pytest.mark.parametrize("shape", SHAPES, ids=[x[0] for x in SHAPES])
@@ -497,9 +497,9 @@ SHAPES = [("short", 16), ("long", 32)]
                                   (3, 2, 8, "b"), (3, 2, 8, "c"), (3, 2, 8, "d")],
                          ids=lambda c: "c%d%s" % (c[0], c[3] or ""))
 def test_forced_workgroup_shape_parity(case, shape):
-    """Either workgroup shape (flag bit 4: 4 waves, 4096-entry lists; bit 5:
-    16 waves) gives the oracle's answer on every decode workload, whatever
-    the automatic choice would be."""
+    """Every workgroup shape (flag bit 4: 4 waves, 4096-entry lists; bit 5:
+    16 waves; bit 6: 8 waves, 6144-entry lists) gives the oracle's answer on
+    every decode workload, whatever the automatic choice would be."""
     import paper_2604_22312_amd as g
     flags = shape[1]
 
@@ -516,8 +516,9 @@ def test_forced_workgroup_shape_parity(case, shape):
                 assert int(st["kth_key"][r]) == int(kth[r])
 
 
+@pytest.mark.parametrize("shape", [16, 64], ids=["short", "mid"])
 @pytest.mark.parametrize("ld,K", [(20001, 2048), (9999, 7), (4097, 2048), (70003, 1)])
-def test_short_shape_special_rows(ld, K):
+def test_short_shape_special_rows(ld, K, shape):
     import paper_2604_22312_amd as g
     rng = np.random.default_rng(ld + 5 * K)
     rows, lens = _special_rows(ld, K, rng)
@@ -525,7 +526,7 @@ def test_short_shape_special_rows(ld, K):
     S = torch.from_numpy(rows).to(DEV)
     RL = torch.from_numpy(lens).to(DEV)
     prev = torch.from_numpy(np.ascontiguousarray(exp)).to(DEV)
-    for flags in (16, 16 | 8, 16 | 4):
+    for flags in (shape, shape | 8, shape | 4):
         note("short shape special rows ld=%d K=%d flags=%d" % (ld, K, flags))
         out = g.gvr_topk_ex(S, RL, None, K, options={"flags": flags})
         assert_rows_equal(out.cpu().numpy(), exp, "short shape, no guess, ld=%d K=%d flags=%d" % (ld, K, flags))
@@ -535,40 +536,49 @@ def test_short_shape_special_rows(ld, K):
         assert_rows_equal(out.cpu().numpy(), exp, "radix, short shape ld=%d K=%d flags=%d" % (ld, K, flags))
 
 
-def test_many_short_rows_take_the_short_shape():
-    """More rows than compute units, rows <= 16K: the automatic choice runs
-    4-wave workgroups; ragged lengths, with and without a guess."""
+@pytest.mark.parametrize("B,ld,guess", [(600, 12000, True), (600, 12000, False), (700, 3000, False),
+                                         (500, 45000, True), (600, 45000, True)],
+                         ids=["8w_guess", "8w_radix", "4w_radix", "16w_long", "8w_long_many"])
+def test_many_rows_automatic_shape(B, ld, guess):
+    """More rows than compute units: the automatic choice runs 8-wave
+    workgroups (rows <= 40K with a guess, rows > 4K without), 4-wave ones
+    (rows <= 4K without a guess) or 16-wave ones (rows > 40K, at most two
+    per compute unit); ragged lengths; the answer is the oracle's."""
     import paper_2604_22312_amd as g
-    rng = np.random.default_rng(123)
-    B, ld, K = 600, 12000, 2048
+    rng = np.random.default_rng(123 + ld)
+    K = 2048
     x = rng.standard_normal((B, ld)).astype(np.float32)
     lens = rng.integers(0, ld + 1, B).astype(np.int32)
     lens[:4] = [ld, K, K + 1, 2 * K + 1]
     exp, _, _ = oracle.topk(x, K, row_len=lens)
-    prev_rows = x + 0.1 * rng.standard_normal((B, ld)).astype(np.float32)
-    pexp, _, _ = oracle.topk(prev_rows, K, row_len=lens)
+    prev = None
+    if guess:
+        prev_rows = x + 0.1 * rng.standard_normal((B, ld)).astype(np.float32)
+        pexp, _, _ = oracle.topk(prev_rows, K, row_len=lens)
+        prev = torch.from_numpy(pexp).to(DEV)
     S = torch.from_numpy(x).to(DEV)
     RL = torch.from_numpy(lens).to(DEV)
-    note("many short rows B=%d ld=%d" % (B, ld))
-    for prev in (None, torch.from_numpy(pexp).to(DEV)):
-        st = g.new_stats(B, DEV)
-        out = g.gvr_topk_ex(S, RL, prev, K, stats=st)
-        assert_rows_equal(out.cpu().numpy(), exp, "many short rows, guess=%s" % (prev is not None))
-        assert -1 not in set(g.decode_stats(st)["path"].tolist())
+    note("many rows B=%d ld=%d guess=%s" % (B, ld, guess))
+    st = g.new_stats(B, DEV)
+    out = g.gvr_topk_ex(S, RL, prev, K, stats=st)
+    assert_rows_equal(out.cpu().numpy(), exp, "many rows B=%d ld=%d guess=%s" % (B, ld, guess))
+    assert -1 not in set(g.decode_stats(st)["path"].tolist())
     out = g.radix_topk(S, RL, None, K)
-    assert_rows_equal(out.cpu().numpy(), exp, "many short rows, radix")
+    assert_rows_equal(out.cpu().numpy(), exp, "many rows, radix B=%d ld=%d" % (B, ld))
 
 
 def test_graph_replays_match_the_oracle():
     """Calls captured into a HIP graph (split rows through the workspace, the
-    4-wave shape, the guess-free kernel) give the oracle's answer on every
-    replay, with eager calls and synchronisations between replays."""
+    8-wave shape, the guess-free kernel in the 4-wave shape) give the
+    oracle's answer on every replay, with eager calls and synchronisations
+    between replays."""
     import paper_2604_22312_amd as g
     rng = np.random.default_rng(31)
     K = 2048
     cases = []
-    # two long rows: split into parts (workspace); 800 short rows: 4-wave shape; 3 rows <= 2K
-    for B, ld in ((2, 131072), (800, 9000), (3, 4000)):
+    # two long rows: split into parts (workspace); 800 short rows: 8-wave
+    # shape; 3 rows <= 2K; 600 rows <= 2K: guess-free, 4-wave shape
+    for B, ld in ((2, 131072), (800, 9000), (3, 4000), (600, 4000)):
         x = rng.standard_normal((B, ld)).astype(np.float32)
         prevx = x + 0.05 * rng.standard_normal((B, ld)).astype(np.float32)
         exp, _, _ = oracle.topk(x, K)
@@ -601,11 +611,17 @@ def test_graph_replays_match_the_oracle():
 
 
 @pytest.mark.parametrize("opts", [{"flags": 16, "capacity": 2048}, {"flags": 16, "capacity": 2500},
-                                  {"flags": 16 | 1}, {"flags": 16 | 8, "capacity": 3000}],
-                         ids=["short_cap_K", "short_cap_2500", "short_no_guess", "short_paper_refine_cap"])
+                                  {"flags": 16 | 1}, {"flags": 16 | 8, "capacity": 3000},
+                                  {"flags": 64, "capacity": 2048}, {"flags": 64, "capacity": 2500},
+                                  {"flags": 64, "capacity": 6144}, {"flags": 64 | 1},
+                                  {"flags": 64 | 8, "capacity": 3000}, {"flags": 64 | 4}],
+                         ids=["short_cap_K", "short_cap_2500", "short_no_guess", "short_paper_refine_cap",
+                              "mid_cap_K", "mid_cap_2500", "mid_cap_max", "mid_no_guess", "mid_paper_refine_cap",
+                              "mid_secant"])
 def test_short_shape_forced_paths(opts):
-    """The 4-wave shape through its narrowing, ties and guess-free paths
-    (small capacities force them); same answer as the oracle."""
+    """The 4-wave and 8-wave shapes through their narrowing, ties and
+    guess-free paths (small capacities force them); same answer as the
+    oracle."""
     import paper_2604_22312_amd as g
     w = workload(1, 3, 8, None)
     K = w.K

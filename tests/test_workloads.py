@@ -1,5 +1,6 @@
 """Shape and determinism checks of the seeded decode workloads (no GPU)."""
 import numpy as np
+import pytest
 import torch
 
 import workloads
@@ -50,3 +51,15 @@ def test_config4_lengths_fit_stride():
     assert spec["ld"] == 262144
     lo, hi = spec["L0"]
     assert hi + (spec["steps"] - 1) * spec["next_n"] + spec["next_n"] - 1 < spec["ld"]
+
+
+def test_l0_override():
+    w = workloads.generate(1, steps=[0, 1], queries=3, L0=5000)
+    assert w.ld == 5000 + 63 and w.name == "c1_L5000"
+    assert w.row_len.tolist() == [[5000] * 3, [5001] * 3]
+    assert w.scores.shape == (2, 3, 5063)
+    assert torch.isfinite(w.scores).all() and (w.scores >= 0).all()
+    with pytest.raises(ValueError):
+        workloads.generate(4, steps=[0], queries=1, L0=5000)
+    with pytest.raises(ValueError):
+        workloads.generate(3, steps=[0], queries=1, sub="a", L0=5000)

@@ -84,7 +84,7 @@ def _rng(config: int, sub: str | None, b: int) -> np.random.Generator:
 
 
 def generate(config: int, steps=None, queries=None, sub: str | None = None,
-             device="cpu", K: int = K_TOPK) -> Workload:
+             device="cpu", K: int = K_TOPK, L0: int | None = None) -> Workload:
     """Build the score rows of ``config`` for the decode ``steps`` requested.
 
     ``steps``   -- iterable of step numbers (default: all of the config's steps);
@@ -93,8 +93,16 @@ def generate(config: int, steps=None, queries=None, sub: str | None = None,
     ``queries`` -- number of queries B to build (default: the config's B).
     ``sub``     -- config 3 sub-case: 'a' random guess, 'b' bf16-quantised,
                    'c' ragged lengths with -inf padding, 'd' lengths <= K.
+    ``L0``      -- another first-step length for the config's rows (configs
+                   with one L0 only; the stride follows as in ``spec``).
     """
     c = spec(config)
+    if L0 is not None:
+        if isinstance(c["L0"], tuple) or sub is not None:
+            raise ValueError("L0 override needs a config with one L0 and no sub-case")
+        c["L0"] = int(L0)
+        c["ld"] = c["L0"] + (c["steps"] - 1) * c["next_n"] + c["next_n"] - 1
+        c["name"] = "%s_L%d" % (c["name"].split("_")[0], c["L0"])
     if config == 3 and sub not in SUBCASES_3:
         raise ValueError("config 3 needs sub in %s" % (SUBCASES_3,))
     if config != 3 and sub is not None:
