@@ -17,7 +17,9 @@ single-operator benchmark (one row of YaRN-RoPE scores per length N, guess =
 the static prior P_static), one line per N; `--mode phases` prints the
 per-phase time breakdown of gvr_topk and of the paper's own phases;
 `--mode short` sweeps short rows over batch sizes (workgroup shapes);
-`--mode indexer` times the FP8 indexer before the Top-K.
+`--mode indexer` times the FP8 indexer before the Top-K; `--mode floor`
+times torch's own row-sum and copy kernels over the headline workload's
+score buffers (the practical HBM rate at that size).
 """
 from __future__ import annotations
 
@@ -590,6 +592,39 @@ def run_indexer(args, dev):
     sys.stdout.flush()
 
 
+def run_floor(args, dev):
+    """The practical HBM ceiling at the headline workload's size: torch's own
+    kernels over the same 128 rows x ~102.4K fp32 score buffers (52 MB per
+    step, 31 steps cycled, 1.6 GB in all, more than the last-level cache):
+    a row-sum reduction (reads each step once) and a device copy (reads and
+    writes it). Per-launch time from HIP events over the timed launches; the
+    rate counts the bytes each kernel must move."""
+    import torch
+
+    w, _, _ = build_inputs(dev)
+    T = w.scores.shape[0]
+    nbytes = w.scores[0].numel() * 4
+    dst = torch.empty_like(w.scores[0])
+    sums = torch.empty(w.rows, dtype=torch.float32, device=dev)
+    steps = max(args.steps, 100)
+    for name, fn, moved in (("torch_sum_rows", lambda t: torch.sum(w.scores[t], dim=1, out=sums), nbytes),
+                            ("torch_copy", lambda t: dst.copy_(w.scores[t]), 2 * nbytes)):
+        for i in range(args.warmup):
+            fn(1 + i % (T - 1))
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for i in range(steps):
+            fn(1 + i % (T - 1))
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / steps
+        print(json.dumps({"mode": "floor", "workload": w.name, "kernel": name, "bytes_per_launch": moved,
+                          "us_per_launch": round(us, 3), "achieved_GBs": round(moved / us / 1e3, 1),
+                          "frac_of_peak": round(moved / us / 1e3 / PEAK_HBM_GBS, 4)}))
+        sys.stdout.flush()
+
+
 def read_traffic(n_launch_bytes):
     if not os.path.exists(TRAFFIC_FILE):
         return None
@@ -607,7 +642,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--mode", choices=["bench", "copy", "configs", "rope", "phases", "short", "indexer"],
+    ap.add_argument("--mode", choices=["bench", "copy", "configs", "rope", "phases", "short", "indexer", "floor"],
                     default="bench")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--no-radix", action="store_true", help="skip timing radix_topk")
@@ -649,6 +684,9 @@ def main():
         return
     if args.mode == "indexer":
         run_indexer(args, dev)
+        return
+    if args.mode == "floor":
+        run_floor(args, dev)
         return
 
     w, outs, prevs = build_inputs(dev)
