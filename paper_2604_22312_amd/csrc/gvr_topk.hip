@@ -22,7 +22,7 @@
 //   part's slabs counts f(T_spec) and appends every element at or above it
 //   to per-wave LDS lists (ballot + mbcnt ranks, no atomics; each wave
 //   streams a contiguous range, so its list is in index order). The test
-//   runs on raw fp32 bits (one compare, see spec_keep), and every lane stores
+//   runs on raw fp32 bits (one compare, see SpecTest), and every lane stores
 //   each element, kept ones at their rank and the others to a dummy slot, so
 //   a slab costs a few scalar instructions. With S > 1 each part
 //   publishes its list and count to a workspace and the last part of the row
@@ -310,7 +310,6 @@ static_assert(lds_slack_ok<kNWLong>() && lds_slack_ok<kNWShort>() && lds_slack_o
 // Block-wide exclusive scan of one int (all threads of the workgroup). Returns the total.
 template <int NW>
 DEV int block_excl_scan(int& a, Smem<NW>& sm, int tid) {
-    using W = Shape<NW>;
     const int lane = tid & 63, wave = tid >> 6;
     const int ia = wave_incl_scan(a, lane);
     if (lane == kWave - 1) sm.wa[wave] = ia;
@@ -451,7 +450,6 @@ DEV uint32_t refine_kth(Smem<NW>& sm, uint32_t wlo, uint32_t whi, int above, int
 // == T (list order = index order) at their ranks: ascending index output.
 template <int NW>
 DEV void emit_segment(const Smem<NW>& sm, uint32_t T, int K, int take, int gb, int eb, int32_t* out, int lane, int wave) {
-    using W = Shape<NW>;
     const uint2* seg = sm.list + sm.seg_off[wave];
     const int cnt = sm.seg_cnt[wave];
     for (int i0 = 0; i0 < cnt; i0 += 4 * kWave) {
@@ -489,7 +487,6 @@ DEV void emit_segment(const Smem<NW>& sm, uint32_t T, int K, int take, int gb, i
 // keys == T in list (= index) order; output in ascending index order.
 template <int NW>
 DEV void emit_from_lists(Smem<NW>& sm, uint32_t T, int K, int32_t* out, int tid, int* n_gt_out) {
-    using W = Shape<NW>;
     const int lane = tid & 63, wave = tid >> 6;
     const uint2* seg = sm.list + sm.seg_off[wave];
     const int cnt = sm.seg_cnt[wave];
@@ -648,7 +645,6 @@ DEV uint32_t ref_shift(uint32_t rlo, uint32_t bin_hi) {
 DEV int ref_bin(uint32_t kk, uint32_t rlo, uint32_t sh) { return (int)min((kk - rlo) >> sh, (uint32_t)kRefBins1 - 1); }
 template <int NW>
 DEV void ref_hist_add(Smem<NW>& sm, uint32_t kk, uint32_t rlo, uint32_t sh) {
-    using W = Shape<NW>;
     __hip_atomic_fetch_add(&sm.u.rhist[ref_bin(kk, rlo, sh)], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 
@@ -657,7 +653,6 @@ DEV void ref_hist_add(Smem<NW>& sm, uint32_t kk, uint32_t rlo, uint32_t sh) {
 // Four entries per lane are read before any is written back.
 template <int NW>
 DEV void keys_in_place(Smem<NW>& sm, uint2* seg, int cnt, bool hist, uint32_t rlo, uint32_t sh, int lane) {
-    using W = Shape<NW>;
     for (int i0 = 0; i0 < cnt; i0 += 4 * kWave) {
         uint32_t b[4];
 #pragma unroll
@@ -848,7 +843,6 @@ struct SpecTest {
 DEV SpecTest make_spec_test(uint32_t tkey) {
     return SpecTest{tkey >= 0x80000000u ? 0u : 0x7FFFFFFFu, (int32_t)(tkey ^ 0x80000000u)};
 }
-DEV bool spec_keep(uint32_t u, const SpecTest& t) { return (int32_t)(u ^ t.flip) >= t.bound; }
 // The fp32 pattern whose key is 0 (a NaN): it never passes a test with
 // tkey >= 1, so it stands in for elements outside the row.
 constexpr uint32_t kKeyZeroBits = 0xFFFFFFFFu;
@@ -946,7 +940,7 @@ DEV void topk_body(const Params& p) {
     const bool secant = GUESS && p.secant && have_prev;
     const bool spec = (all_mode || have_prev) && !secant;
     int gvalid = 0;
-    uint32_t gmin = 0xFFFFFFFFu, gmax = 0u, tspec = 0xFFFFFFFFu;
+    uint32_t gmax = 0u, tspec = 0xFFFFFFFFu;
     float gsum = 0.f;
     int64_t t1 = t0, t2 = t0;
     int passes = 0;
@@ -1069,7 +1063,7 @@ DEV void topk_body(const Params& p) {
         // ---------------- (a3)+(a4) speculative pass over the part's slabs:
         // count and append every (fp32 bits, index) at or above T_spec.
         //
-        // The test runs on the raw bits (spec_keep): one signed compare, plus
+        // The test runs on the raw bits (SpecTest): one signed compare, plus
         // one xor for thresholds <= -0; the two forms are two copies of the
         // loop, chosen once. Thresholds are >= key 1, so the key-0 pattern
         // never passes: elements outside [0, n) in the row's two edge slabs
@@ -1090,7 +1084,6 @@ DEV void topk_body(const Params& p) {
             __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
             tspec = (uint32_t)sm.scal[4];
             gvalid = sm.scal[5];
-            gmin = (uint32_t)sm.scal[6];
             gmax = (uint32_t)sm.scal[7];
             gsum = sm.redf[0];
             if (gvalid == 0) have_prev = false;   // no usable guess: the pass keeps (almost) nothing
@@ -1566,7 +1559,6 @@ DEV void topk_body(const Params& p) {
         }
         __syncthreads();
         gvalid = sum_over_waves<NW>(sm.red[0], lane);
-        gmin = wave_min_u(lane < NW ? (uint32_t)sm.red[1][lane] : 0xFFFFFFFFu);
         gmax = wave_max_u(lane < NW ? (uint32_t)sm.red[2][lane] : 0u);
         gsum = 0.f;
         for (int v = 0; v < NW; ++v) gsum += sm.redf[v];   // fixed order

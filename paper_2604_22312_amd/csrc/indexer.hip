@@ -28,6 +28,8 @@
 
 #include <stdint.h>
 
+#include <algorithm>
+
 #include "gvr_indexer.h"
 
 namespace {
@@ -37,6 +39,7 @@ constexpr int kWaves = 4;                // waves per workgroup
 constexpr int kTile = 32;                // keys per ring slot (two 16-key matrix tiles)
 constexpr int kTilesPerWave = 32;        // ring slots of one wave's run (1024 keys)
 constexpr int kRing = 3;                 // key slots held per wave: kRing - 1 in flight while one is used
+constexpr int kMinRun = 8 * kTile;       // shortest wave run the grid sizing picks (256 keys)
 constexpr int64_t kMaxLd = ((int64_t)1 << 31) - 16;
 
 typedef float v4f __attribute__((ext_vector_type(4)));
@@ -55,6 +58,7 @@ struct IdxParams {
     int32_t group;
     int32_t chunks;       // workgroups per cache (key chunks)
     int32_t chunk_keys;   // keys per workgroup chunk
+    int32_t run_keys;     // keys per wave run (a multiple of kTile)
 };
 
 // 32 bytes at p (16-byte aligned) as one matrix operand.
@@ -91,8 +95,8 @@ __global__ __launch_bounds__(kWaves * kWave) void indexer_kernel(IdxParams p) {
         nr[rr] = n64;
         n_max = max(n_max, n64);
     }
-    const int64_t s_begin = (int64_t)c * p.chunk_keys + sub * (kTilesPerWave * kTile);
-    const int64_t s_end = min(s_begin + kTilesPerWave * kTile, n_max);
+    const int64_t s_begin = (int64_t)c * p.chunk_keys + (int64_t)sub * p.run_keys;
+    const int64_t s_end = min(s_begin + p.run_keys, n_max);
     if (s_begin >= s_end) return;
     const int col = lane & 15, quarter = lane >> 4;
     // Bytes [32 quarter, + 32) of the head dimension; with D = 64 the upper
@@ -182,8 +186,47 @@ __global__ __launch_bounds__(kWaves * kWave) void indexer_kernel(IdxParams p) {
         if (u0 + r < tiles) use_slot(ring[r], u0 + r);
 }
 
+// Workgroups of one instance resident on the device at once.
 template <int H, int D, int RG>
-gvr_status launch(const IdxParams& q, unsigned grid, void* stream) {
+int resident_workgroups() {
+    static int cached[64] = {};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+    if (cached[dev] == 0) {
+        int per_cu = 0, cus = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, indexer_kernel<H, D, RG>, kWaves * kWave, 0) != hipSuccess)
+            return 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+        cached[dev] = std::max(1, per_cu * cus);
+    }
+    return cached[dev];
+}
+
+template <int H, int D, int RG>
+gvr_status launch(IdxParams q, int64_t caches, void* stream) {
+    // Key chunks per cache. The natural size gives every wave a run of
+    // kTilesPerWave tiles; the grid is then resized to whole rounds of the
+    // workgroups the device holds at once: one round when the natural grid
+    // fits (small batches get finer chunks that reach more compute units, runs
+    // of at least kMinRun keys), else as many full rounds as it fills (no
+    // partly filled last round).
+    const int wpr = q.chunk_keys / (kTilesPerWave * kTile);
+    int run = kTilesPerWave * kTile;
+    const int slots = resident_workgroups<H, D, RG>();
+    if (slots > 0) {
+        const int64_t nat = (q.ld + (int64_t)wpr * run - 1) / ((int64_t)wpr * run);
+        const int64_t rounds = std::max<int64_t>(1, nat * caches / slots);
+        const int64_t chunks = std::max<int64_t>(1, rounds * slots / caches);
+        const int64_t per = (q.ld + chunks - 1) / chunks;                        // keys per chunk
+        const int64_t r = ((per + wpr - 1) / wpr + kTile - 1) / kTile * kTile;   // per wave, whole tiles
+        run = (int)std::max<int64_t>(std::min<int64_t>(r, 1 << 24), kMinRun);
+    }
+    q.run_keys = run;
+    q.chunk_keys = wpr * run;
+    const int64_t chunks = (q.ld + q.chunk_keys - 1) / q.chunk_keys;
+    if (chunks * caches > 0x7FFFFFFF) return GVR_ERR_TOO_LONG;
+    q.chunks = (int32_t)chunks;
+    const unsigned grid = (unsigned)(chunks * caches);
     hipLaunchKernelGGL((indexer_kernel<H, D, RG>), dim3(grid), dim3(kWaves * kWave), 0, (hipStream_t)stream, q);
     return hipGetLastError() == hipSuccess ? GVR_OK : GVR_ERR_HIP;
 }
@@ -193,11 +236,11 @@ gvr_status launch(const IdxParams& q, unsigned grid, void* stream) {
 constexpr int rows_per_wave(int H, int group) { return (group % 2 == 0 && H <= 64) ? 2 : 1; }
 
 template <int H, int D>
-gvr_status launch_rg(const IdxParams& q, unsigned grid, void* stream) {
+gvr_status launch_rg(const IdxParams& q, int64_t caches, void* stream) {
     if constexpr (H <= 64) {
-        if (rows_per_wave(H, q.group) == 2) return launch<H, D, 2>(q, grid, stream);
+        if (rows_per_wave(H, q.group) == 2) return launch<H, D, 2>(q, caches, stream);
     }
-    return launch<H, D, 1>(q, grid, stream);
+    return launch<H, D, 1>(q, caches, stream);
 }
 
 }  // namespace
@@ -227,14 +270,12 @@ gvr_status gvr_indexer_scores(const uint8_t* q, const float* w, const uint8_t* k
     const int rg = rows_per_wave(H, group);
     const int wpr = kWaves / (group / rg);
     p.chunk_keys = wpr * kTilesPerWave * kTile;
-    const int64_t chunks = (ld + p.chunk_keys - 1) / p.chunk_keys;
+    p.run_keys = kTilesPerWave * kTile;
+    p.chunks = 0;
     const int64_t caches = B / group;
-    if (chunks * caches > 0x7FFFFFFF) return GVR_ERR_TOO_LONG;
-    p.chunks = (int32_t)chunks;
-    const unsigned grid = (unsigned)(chunks * caches);
-    if (H == 32) return D == 64 ? launch_rg<32, 64>(p, grid, stream) : launch_rg<32, 128>(p, grid, stream);
-    if (H == 64) return D == 64 ? launch_rg<64, 64>(p, grid, stream) : launch_rg<64, 128>(p, grid, stream);
-    return D == 64 ? launch_rg<128, 64>(p, grid, stream) : launch_rg<128, 128>(p, grid, stream);
+    if (H == 32) return D == 64 ? launch_rg<32, 64>(p, caches, stream) : launch_rg<32, 128>(p, caches, stream);
+    if (H == 64) return D == 64 ? launch_rg<64, 64>(p, caches, stream) : launch_rg<64, 128>(p, caches, stream);
+    return D == 64 ? launch_rg<128, 64>(p, caches, stream) : launch_rg<128, 128>(p, caches, stream);
 }
 
 gvr_status gvr_indexer_topk(const uint8_t* q, const float* w, const uint8_t* k, const float* k_scale,

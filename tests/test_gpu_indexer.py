@@ -84,6 +84,29 @@ def test_indexer_scores_parity(H, D, group):
         assert np.all(got[b, n:] == -7.0), "row %d: scores past its length were written" % b
 
 
+@pytest.mark.parametrize("requests,group,ld,H,D", [(1, 2, 40000, 64, 128), (3, 1, 70001, 32, 64),
+                                                    (500, 1, 4200, 32, 64), (200, 3, 4500, 64, 64)],
+                         ids=["one_request_long", "three_rows_long", "many_caches", "many_caches_g3"])
+def test_indexer_grid_sizing(requests, group, ld, H, D):
+    """The launch resizes the key chunks to the device (a few caches: fine
+    chunks over many compute units; many caches: whole rounds of resident
+    workgroups, the last chunk of a cache partial); every score matches the
+    oracle and nothing past a row's length is written."""
+    rng = np.random.default_rng(ld + requests)
+    lengths = [int(v) for v in rng.integers(1, ld + 1, requests)]
+    lengths[0] = ld - group + 1
+    x = inputs(requests, group, ld, lengths, H, D, seed=requests + ld)
+    note("indexer grid sizing requests=%d group=%d ld=%d H=%d D=%d" % (requests, group, ld, H, D))
+    got = gpu_scores(x)
+    exp, mag = oracle_scores(x)
+    rl = x.row_len[0].numpy()
+    for b in range(x.rows):
+        n = int(rl[b])
+        err = np.abs(got[b, :n] - exp[b, :n])
+        assert np.all(err <= tol_of(mag[b, :n], H, D)), (b, float(err.max()))
+        assert np.all(got[b, n:] == -7.0), "row %d: scores past its length were written" % b
+
+
 def check_topk(got, exp_scores, mag, rl, K, H, D):
     for b in range(got.shape[0]):
         n = int(rl[b])
