@@ -33,7 +33,9 @@
  *   - scores: [B][ld] fp32, row stride ld elements, 4-byte aligned.
  *   - row_len: [B] int32 (device-resident, so values are clamped, not checked).
  *   - prev_topk: [B][K] int32 or NULL. Entries outside [0, n) (e.g. -1
- *     padding) are ignored; duplicates are tolerated.
+ *     padding) are ignored; duplicates are tolerated. It guides calls with
+ *     2K < ld <= 2^29 - 4096; for a longer stride the guess-free schedule
+ *     runs (same result).
  *   - out_idx: [B][K] int32, written in full; must not overlap the inputs.
  *   - stream: a hipStream_t passed as void* (NULL = the null stream).
  *

@@ -109,6 +109,11 @@ constexpr int kMaxParts = 16;                  // workgroups per row
 constexpr int kMinPartElems = 16384;           // a row is split only into parts at least this long
 constexpr int kMaxSlots = 2048;                // (row, part) pairs of one split call: 256 MB of workspace
 constexpr int kXcds = 8;                       // gfx950 XCDs; workgroup i runs on XCD i % 8
+// Longest row stride of the guess path: its speculative pass addresses a row
+// through one buffer resource with 32-bit byte offsets (lane offset included),
+// so 4 (ld + 3) + 1024 must stay below 2^31. Longer rows take the guess-free
+// schedule, whose passes index the row with 64-bit addresses.
+constexpr int64_t kMaxSpecLd = ((int64_t)1 << 29) - 4096;
 
 static_assert((kBins & (kBins - 1)) == 0 && (kRefBins & (kRefBins - 1)) == 0 && (kRefBins1 & (kRefBins1 - 1)) == 0 &&
                   (kGuessBins & (kGuessBins - 1)) == 0, "bin counts are powers of two");
@@ -2099,7 +2104,7 @@ gvr_status run(const float* scores, int64_t B, int64_t ld, const int32_t* row_le
     if (B == 0) return GVR_OK;
     // Rows of at most 2K elements list every element (the guess would cut
     // few candidates): when no row is longer, the guess-free kernel runs.
-    const bool guess = use_guess && prev && ld > 2 * (int64_t)K;
+    const bool guess = use_guess && prev && ld > 2 * (int64_t)K && ld <= kMaxSpecLd;
     int device = 0;
     if (hipGetDevice(&device) != hipSuccess) return GVR_ERR_HIP;
     const int cus = cu_count(device);

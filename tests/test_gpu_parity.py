@@ -636,3 +636,35 @@ def test_short_shape_forced_paths(opts):
     assert -1 not in set(g.decode_stats(st)["path"].tolist())
     out = g.radix_topk_ex(S, RL, K, options=opts)
     assert_rows_equal(out.cpu().numpy(), exp, "radix short shape %s" % opts)
+
+
+@pytest.mark.parametrize("ld", [(1 << 29) - 4096, (1 << 29) - 4095], ids=["guess_path_limit", "past_the_limit"])
+def test_rows_at_the_offset_limit(ld):
+    """The longest stride the guess path takes (its byte offsets are 32-bit)
+    and one past it, which runs the guess-free schedule: 4096 planted values
+    (1, 2, ..., 4096 at random indices, the rest 0) in a 2 GB row, the guess
+    the planted values of ranks 1025..3072. The answer is known by
+    construction: the indices of the 2048 largest planted values."""
+    import paper_2604_22312_amd as g
+    rng = np.random.default_rng(ld & 0xFFFF)
+    K = 2048
+    idx = rng.choice(ld, size=4096, replace=False)
+    idx[-1] = ld - 1   # the largest value in the row's last element
+    vals = np.arange(1, 4097, dtype=np.float32)
+    exp = np.sort(idx[2048:]).astype(np.int32)[None, :]
+    guess = np.sort(idx[1024:3072]).astype(np.int32)[None, :]
+    note("row at the offset limit ld=%d" % ld)
+    S = torch.zeros((1, ld), dtype=torch.float32, device=DEV)
+    S[0, torch.from_numpy(idx).to(DEV)] = torch.from_numpy(vals).to(DEV)
+    prev = torch.from_numpy(guess).to(DEV)
+    st = g.new_stats(1, DEV)
+    out = g.gvr_topk_ex(S, None, prev, K, stats=st)
+    torch.cuda.synchronize()
+    assert_rows_equal(out.cpu().numpy(), exp, "gvr_topk ld=%d" % ld)
+    path = g.PATH_NAMES[int(g.decode_stats(st)["path"][0])]
+    if ld <= (1 << 29) - 4096:
+        assert path not in ("error", "no_guess"), path
+    else:
+        assert path == "no_guess", path
+    del S
+    torch.cuda.empty_cache()
