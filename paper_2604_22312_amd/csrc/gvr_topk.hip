@@ -5,8 +5,9 @@
 // workgroup, or split over S of them ("parts", up to 16) when few long rows
 // would leave compute units idle and the streaming time saved outweighs the
 // merge; the parts of one row are placed on one XCD so they share its L2.
-// The same code, instantiated for 4 waves (4096-entry lists, three
-// workgroups per compute unit), serves calls with many short rows.
+// The same code, instantiated for 8 waves (6144-entry lists, two workgroups
+// per compute unit) and 4 waves (4096-entry lists, three per compute unit),
+// serves calls with more rows than compute units.
 //
 //   Guess (Sec. 4.2.1, Phase 1). Wave 0 of every part gathers the scores at a
 //   strided sample of prev_topk (every 8th entry for K = 2048, 256 in all)
