@@ -511,14 +511,21 @@ def run_short(args, dev):
             del scores, prev, out, rl
         torch.cuda.empty_cache()
 
+    keep = lambda n, B: (args.short_n in (None, n)) and (args.short_rows in (None, B))   # noqa: E731
     for n in (2560, 4096, 8192, 16384, 32768):
+        batches = tuple(B for B in (1, 64, 512, 2048) if keep(n, B))
+        if not batches:
+            continue
         host = WR.batch_scores(n, 16)
         prior = g.gvr_rope_prior(n, K_TOPK, device=dev)
-        measure("rope_synthetic", n, host, np.full(16, n), prior.view(1, K_TOPK).repeat(16, 1), (1, 64, 512, 2048))
+        measure("rope_synthetic", n, host, np.full(16, n), prior.view(1, K_TOPK).repeat(16, 1), batches)
     for L0 in (8192, 16384, 32768, 65536):
+        batches = tuple(B for B in (64, 512, 1024, 2048) if keep(L0 + 1, B))
+        if not batches:
+            continue
         w = WD.generate(1, steps=[0, 1], queries=64, L0=L0)
         prev = g.radix_topk(w.scores[0].to(dev), w.row_len[0].to(dev), None, K_TOPK)   # step 0's Top-K
-        measure("decode", L0 + 1, w.scores[1].numpy(), w.row_len[1].numpy(), prev, (64, 512, 1024, 2048))
+        measure("decode", L0 + 1, w.scores[1].numpy(), w.row_len[1].numpy(), prev, batches)
 
 
 def run_indexer(args, dev):
@@ -645,6 +652,8 @@ def main():
     ap.add_argument("--mode", choices=["bench", "copy", "configs", "rope", "phases", "short", "indexer", "floor"],
                     default="bench")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
+    ap.add_argument("--short-n", type=int, default=None, help="--mode short: only rows of this length")
+    ap.add_argument("--short-rows", type=int, default=None, help="--mode short: only this batch size")
     ap.add_argument("--no-radix", action="store_true", help="skip timing radix_topk")
     ap.add_argument("--no-secant", action="store_true",
                     help="skip timing the paper's own threshold schedule (gvr_topk_ex flag bit 2)")
