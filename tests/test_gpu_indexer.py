@@ -151,6 +151,35 @@ def test_indexer_topk_parity(group):
     note("  paths %s passes %s" % (d["path"].tolist(), d["passes"].tolist()))
 
 
+def test_indexer_topk_many_rows():
+    """More rows than compute units (160 requests x 2 draft rows): the
+    Top-K inside gvr_indexer_topk runs the 8-wave workgroup shape, guided by
+    the first step's Top-K; same checks, and the same answer without the
+    guess."""
+    import paper_2604_22312_amd as g
+    H, D, ld, requests = 32, 64, 6000, 160
+    rng = np.random.default_rng(29)
+    lengths = [int(v) for v in rng.integers(2100, ld - 1, requests)]
+    x = inputs(requests, 2, ld, lengths, H, D, seed=29, steps=2)
+    ex0, _ = oracle_scores(x, 0)
+    prev = np.full((x.rows, K_TOPK), -1, np.int32)
+    for b in range(x.rows):
+        n = int(x.row_len[0, b])
+        prev[b, :min(n, K_TOPK)] = IX_argtopk(ex0[b, :n], K_TOPK)
+    ex1, mag1 = oracle_scores(x, 1)
+    note("indexer + topk, %d rows" % x.rows)
+    st = g.new_stats(x.rows, DEV)
+    out, _ = g.gvr_indexer_topk(x.q[1].to(DEV), x.w.to(DEV), x.k.to(DEV), x.k_scale.to(DEV), x.row_len[1].to(DEV),
+                                torch.from_numpy(prev).to(DEV), K_TOPK, stats=st)
+    torch.cuda.synchronize()
+    check_topk(out.cpu().numpy(), ex1, mag1, x.row_len[1].numpy(), K_TOPK, H, D)
+    assert "error" not in {g.PATH_NAMES[int(v)] for v in g.decode_stats(st)["path"].tolist()}
+    out2, _ = g.gvr_indexer_topk(x.q[1].to(DEV), x.w.to(DEV), x.k.to(DEV), x.k_scale.to(DEV), x.row_len[1].to(DEV),
+                                 None, K_TOPK)
+    torch.cuda.synchronize()
+    assert np.array_equal(out2.cpu().numpy(), out.cpu().numpy())
+
+
 def IX_argtopk(s, K):
     """K largest (lower index first among equals), ascending: from the oracle's scores."""
     order = np.argsort(-s, kind="stable")[:K]
