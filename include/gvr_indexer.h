@@ -33,7 +33,10 @@
  * NULL pointer, a negative size or an unsupported H, D or group;
  * GVR_ERR_TOO_LONG for ld > 2^31 - 16; GVR_ERR_HIP if a launch fails.
  * B == 0 is a no-op. Work is enqueued on `stream` (hipStream_t as void*);
- * the calls do not synchronise.
+ * the calls do not synchronise. gvr_indexer_scores allocates nothing and may
+ * be captured into a HIP graph: the first call on a device sizes its grid
+ * from the device's resident workgroup count (queried once, not during a
+ * capture; a captured first call uses a fixed chunk size, same result).
  */
 #ifndef GVR_INDEXER_H
 #define GVR_INDEXER_H

@@ -186,13 +186,18 @@ __global__ __launch_bounds__(kWaves * kWave) void indexer_kernel(IdxParams p) {
         if (u0 + r < tiles) use_slot(ring[r], u0 + r);
 }
 
-// Workgroups of one instance resident on the device at once.
+// Workgroups of one instance resident on the device at once (0 = unknown:
+// the natural chunk size is used). Queried once per device, never while the
+// stream is being captured into a graph.
 template <int H, int D, int RG>
-int resident_workgroups() {
+int resident_workgroups(void* stream) {
     static int cached[64] = {};
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
     if (cached[dev] == 0) {
+        hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+        if (hipStreamIsCapturing((hipStream_t)stream, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone)
+            return 0;
         int per_cu = 0, cus = 0;
         if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, indexer_kernel<H, D, RG>, kWaves * kWave, 0) != hipSuccess)
             return 0;
@@ -212,7 +217,7 @@ gvr_status launch(IdxParams q, int64_t caches, void* stream) {
     // partly filled last round).
     const int wpr = q.chunk_keys / (kTilesPerWave * kTile);
     int run = kTilesPerWave * kTile;
-    const int slots = resident_workgroups<H, D, RG>();
+    const int slots = resident_workgroups<H, D, RG>(stream);
     if (slots > 0) {
         const int64_t nat = (q.ld + (int64_t)wpr * run - 1) / ((int64_t)wpr * run);
         const int64_t rounds = std::max<int64_t>(1, nat * caches / slots);

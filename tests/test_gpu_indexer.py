@@ -13,6 +13,8 @@ scores may differ only among keys within that tolerance of the K-th score:
 every key clearly above it is selected, none clearly below it is, and the
 output is K distinct indices in ascending order.
 """
+import os
+
 import numpy as np
 import pytest
 import torch
@@ -205,3 +207,50 @@ def test_indexer_full_size_sampled_rows():
         n = int(rl[0])
         got = sc[b, :n].cpu().numpy().astype(np.float64)
         assert np.all(np.abs(got - exp[:n]) <= tol_of(mag[:n], H, D)), b
+
+
+CAPTURE_FIRST = r"""
+import sys, numpy as np, torch
+sys.path.insert(0, sys.argv[1])
+import paper_2604_22312_amd as g
+from oracle import indexer as IX
+from workloads import indexer as WI
+x = WI.generate(2, 2, 7000, [6900, 5000], steps=1, H=64, D=128, seed=41, device="cpu")
+dev = torch.device("cuda:0")
+q, w, k, ks, rl = (t.to(dev) for t in (x.q[0], x.w, x.k, x.k_scale, x.row_len[0]))
+sc = torch.full((x.rows, x.ld), -7.0, dtype=torch.float32, device=dev)
+stream = torch.cuda.Stream()
+graph = torch.cuda.CUDAGraph()
+with torch.cuda.graph(graph, stream=stream):   # the process's first indexer call
+    g.gvr_indexer_scores(q, w, k, ks, rl, scores=sc, stream=stream)
+args = (x.q[0].numpy(), x.w.numpy(), x.k.numpy(), x.k_scale.numpy())
+exp = IX.indexer_scores(*args, group=2, row_len=x.row_len[0].numpy())
+mag = IX.magnitude(*args, group=2, row_len=x.row_len[0].numpy())
+for rep in range(3):
+    sc.fill_(-7.0)
+    torch.cuda.synchronize()
+    graph.replay()
+    torch.cuda.synchronize()
+    got = sc.cpu().numpy().astype(np.float64)
+    for b in range(x.rows):
+        n = int(x.row_len[0, b])
+        assert np.all(np.abs(got[b, :n] - exp[b, :n]) <= (128 + 64 + 4) * 2.0 ** -24 * mag[b, :n]), (rep, b)
+        assert np.all(got[b, n:] == -7.0)
+    g.gvr_indexer_scores(q, w, k, ks, rl, scores=sc)   # eager work between replays
+    torch.cuda.synchronize()
+print("ok")
+"""
+
+
+def test_indexer_captured_as_first_call(tmp_path):
+    """A fresh process whose first indexer call is captured into a HIP graph
+    (the launch then sizes its grid without querying the device): every
+    replay matches the oracle, with eager calls between replays."""
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    script = tmp_path / "capture_first.py"
+    script.write_text(CAPTURE_FIRST)
+    note("indexer captured as the first call (subprocess)")
+    r = subprocess.run([sys.executable, str(script), root], capture_output=True, text=True, timeout=240)
+    assert r.returncode == 0 and r.stdout.strip().endswith("ok"), r.stdout + r.stderr
