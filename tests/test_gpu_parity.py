@@ -668,3 +668,48 @@ def test_rows_at_the_offset_limit(ld):
         assert path == "no_guess", path
     del S
     torch.cuda.empty_cache()
+
+
+CAPTURE_FIRST_TOPK = r"""
+import sys, numpy as np, torch
+sys.path.insert(0, sys.argv[1])
+import oracle
+import paper_2604_22312_amd as g
+rng = np.random.default_rng(43)
+B, ld, K = 600, 9000, 2048
+x = rng.standard_normal((B, ld)).astype(np.float32)
+exp, _, _ = oracle.topk(x, K)
+pexp, _, _ = oracle.topk(x + 0.05 * rng.standard_normal((B, ld)).astype(np.float32), K)
+dev = torch.device("cuda:0")
+S, P = torch.from_numpy(x).to(dev), torch.from_numpy(pexp).to(dev)
+out = torch.full((B, K), -7, dtype=torch.int32, device=dev)
+stream = torch.cuda.Stream()
+graph = torch.cuda.CUDAGraph()
+with torch.cuda.graph(graph, stream=stream):   # the process's first Top-K call (no split: no workspace)
+    g.gvr_topk(S, None, P, K, out_idx=out, stream=stream)
+for rep in range(3):
+    out.fill_(-7)
+    torch.cuda.synchronize()
+    graph.replay()
+    torch.cuda.synchronize()
+    assert np.array_equal(out.cpu().numpy(), exp), rep
+    o2 = g.gvr_topk(S, None, P, K)   # eager work between replays
+    torch.cuda.synchronize()
+    assert np.array_equal(o2.cpu().numpy(), exp)
+print("ok")
+"""
+
+
+def test_topk_captured_as_first_call(tmp_path):
+    """A fresh process whose first gvr_topk call (600 rows of 9000: the
+    8-wave shape, no row split, so no workspace) is captured into a HIP
+    graph: every replay and the eager calls between them equal the oracle."""
+    import os
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    script = tmp_path / "capture_first_topk.py"
+    script.write_text(CAPTURE_FIRST_TOPK)
+    note("gvr_topk captured as the first call (subprocess)")
+    r = subprocess.run([sys.executable, str(script), root], capture_output=True, text=True, timeout=240)
+    assert r.returncode == 0 and r.stdout.strip().endswith("ok"), r.stdout + r.stderr
