@@ -19,7 +19,10 @@
  *   - w, k_scale, I: float32. Products of two FP8 values are exact in
  *     float32; the dot products accumulate in float32 on the matrix cores,
  *     the head sum in float32, so I differs from the exact value by rounding
- *     only (a relative 2^-20 of sum_j |w_j| sum_d |q_jd k'_d| bounds it).
+ *     only: |I - I_exact| <= (D + H + 4) 2^-24 sum_j |w_j| sum_d |q_jd k'_d|
+ *     (D - 1 additions per dot product in any order, one rounding each for
+ *     the key scale and the head weight, H - 1 head additions, and slack
+ *     for second-order terms).
  *
  * Layouts (all DEVICE pointers, owned by the caller; row stride ld):
  *   q       [B][H][D] bytes        w       [B][H] f32

@@ -50,14 +50,22 @@
  *   - gvr_topk may split a long row over several workgroups (few rows, long
  *     rows: see gvr_options.parts). The parts exchange their candidate lists
  *     through a device workspace that the library allocates on the first
- *     such call for each (device, stream) pair (hipMalloc, kept until the
- *     process ends; arrival counters + 128 KB per row part) and reuses for
- *     every later call on that stream. Calls on one stream run in order and
- *     share it; calls on different streams use different workspaces and may
- *     overlap. A call that has to allocate or grow the workspace synchronises
- *     the stream and must not be captured into a HIP graph: issue one call of
- *     the same shape before capturing. radix_topk and unsplit gvr_topk calls
- *     use no workspace.
+ *     such call for each (device, stream) pair (hipMalloc; arrival counters
+ *     + 128 KB per row part) and reuses for every later call on that stream.
+ *     A call that needs more room allocates a larger one; the outgrown one is
+ *     never freed. Every workspace stays allocated until the process ends,
+ *     so a graph captured earlier can still be replayed after a later call
+ *     has grown the stream's workspace.
+ *   - Calls on one stream run in order and share its workspace; calls on
+ *     different streams use different workspaces and may overlap.
+ *   - A call that has to allocate returns GVR_ERR_HIP while its stream is
+ *     being captured into a HIP graph: issue one eager call of the same (or
+ *     a larger) shape on that stream before capturing.
+ *   - A captured graph keeps the capture stream's workspace. Replayed on
+ *     another stream, it must not overlap split calls on the capture stream
+ *     (eager calls or replays of other graphs captured there): overlapping
+ *     calls that share a workspace corrupt each other's merge.
+ *   - radix_topk and unsplit gvr_topk calls use no workspace.
  */
 #ifndef GVR_TOPK_H
 #define GVR_TOPK_H

@@ -19,7 +19,8 @@ exact float64 operations up to the final rounding of each dot product.
 Parity status: pinned by ``tests/test_indexer_pins.py`` (every byte decoded
 against torch's float8_e4m3fn, hand-decoded values, a pure-Python loop
 version on small shapes, ReLU and scale-sign cases, linearity in w, cache
-sharing by group, planted mistakes).
+sharing by group; ``magnitude`` against a pure-Python loop, equal to the
+score when no term can cancel and never below |score|; planted mistakes).
 """
 from __future__ import annotations
 

@@ -1996,6 +1996,10 @@ struct Workspace {
 
 std::mutex g_ws_mutex;
 std::vector<Workspace> g_ws;
+// Buffers a stream has outgrown. A HIP graph captured earlier may still hold
+// their addresses in its kernel arguments, so they are never freed: they stay
+// allocated until the process ends, like the current ones.
+std::vector<void*> g_ws_retired;
 
 int cu_count(int device) {
     static std::mutex m;
@@ -2021,9 +2025,11 @@ gvr_status get_workspace(int device, void* stream, int rows, int parts, Workspac
                 *out = w;
                 return GVR_OK;
             }
-            // Grow: the old buffer may still be read by queued launches.
-            if (hipStreamSynchronize((hipStream_t)stream) != hipSuccess) return GVR_ERR_HIP;
-            (void)hipFree(w.base);
+            // Grow: the old buffer is retired, not freed (queued launches and
+            // graphs captured on this stream may still use it). Its arrival
+            // words are zero again once those launches end, so a graph that
+            // holds it keeps working.
+            g_ws_retired.push_back(w.base);
             w = g_ws.back();
             g_ws.pop_back();
             break;
@@ -2032,9 +2038,14 @@ gvr_status get_workspace(int device, void* stream, int rows, int parts, Workspac
     const size_t c_bytes = align_up((size_t)slots * sizeof(int32_t), 256);
     const size_t t_bytes = align_up((size_t)slots * sizeof(uint32_t), 256);
     const size_t l_bytes = (size_t)slots * kPartCap * sizeof(uint64_t);
+    // Allocating is not possible while the stream is being captured.
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing((hipStream_t)stream, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone)
+        return GVR_ERR_HIP;
     void* base = nullptr;
     if (hipMalloc(&base, a_bytes + c_bytes + t_bytes + l_bytes) != hipSuccess) return GVR_ERR_HIP;
-    if (hipMemset(base, 0, a_bytes) != hipSuccess) {
+    // Arrival words start at zero; cleared on the call's own stream, ahead of its launch.
+    if (hipMemsetAsync(base, 0, a_bytes, (hipStream_t)stream) != hipSuccess) {
         (void)hipFree(base);
         return GVR_ERR_HIP;
     }

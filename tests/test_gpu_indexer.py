@@ -8,10 +8,13 @@ m terms by (m - 1) u times the sum of their magnitudes (u = 2^-24), so
 |I_gpu - I| <= (D + H + 4) u * mag, mag = sum_j |w_j| sum_d |q_jd k'_d|
 (the oracle's ``magnitude``), whatever order the hardware adds in.
 
-Top-K: the answer on the GPU's float32 scores and the oracle's on its exact
-scores may differ only among keys within that tolerance of the K-th score:
-every key clearly above it is selected, none clearly below it is, and the
-output is K distinct indices in ascending order.
+Top-K, two checks. (1) Bit-exact: gvr_indexer_topk returns the float32
+scores it selected from, and its out_idx must equal the oracle's Top-K over
+exactly those scores (the Top-K parity bar). (2) Against the float64 scores:
+the answer on the GPU's float32 scores and the oracle's on its exact scores
+may differ only among keys within that tolerance of the K-th score: every
+key clearly above it is selected, none clearly below it is, and the output
+is K distinct indices in ascending order.
 """
 import os
 
@@ -21,7 +24,7 @@ import torch
 
 import oracle
 from oracle import indexer as IX
-from tests.gpu_cases import K_TOPK, note
+from tests.gpu_cases import K_TOPK, assert_rows_equal, note
 from workloads import indexer as WI
 
 pytestmark = pytest.mark.gpu
@@ -109,6 +112,13 @@ def test_indexer_grid_sizing(requests, group, ld, H, D):
         assert np.all(got[b, n:] == -7.0), "row %d: scores past its length were written" % b
 
 
+def check_topk_exact(got, gpu_scores, rl, K, what):
+    """The Top-K the call returned equals the oracle's Top-K over the very
+    float32 scores the call wrote, on every row (bit-exact)."""
+    exp, _, _ = oracle.topk(np.ascontiguousarray(gpu_scores, dtype=np.float32), K, row_len=np.asarray(rl))
+    assert_rows_equal(got, exp, what)
+
+
 def check_topk(got, exp_scores, mag, rl, K, H, D):
     for b in range(got.shape[0]):
         n = int(rl[b])
@@ -143,6 +153,8 @@ def test_indexer_topk_parity(group):
     out, sc = g.gvr_indexer_topk(x.q[1].to(DEV), x.w.to(DEV), x.k.to(DEV), x.k_scale.to(DEV), x.row_len[1].to(DEV),
                                  torch.from_numpy(prev).to(DEV), K_TOPK, stats=st)
     torch.cuda.synchronize()
+    check_topk_exact(out.cpu().numpy(), sc.cpu().numpy(), x.row_len[1].numpy(), K_TOPK,
+                     "indexer + topk group=%d" % group)
     check_topk(out.cpu().numpy(), ex1, mag1, x.row_len[1].numpy(), K_TOPK, H, D)
     # and without a guess (radix schedule inside gvr_topk)
     out2, _ = g.gvr_indexer_topk(x.q[1].to(DEV), x.w.to(DEV), x.k.to(DEV), x.k_scale.to(DEV), x.row_len[1].to(DEV),
@@ -171,9 +183,11 @@ def test_indexer_topk_many_rows():
     ex1, mag1 = oracle_scores(x, 1)
     note("indexer + topk, %d rows" % x.rows)
     st = g.new_stats(x.rows, DEV)
-    out, _ = g.gvr_indexer_topk(x.q[1].to(DEV), x.w.to(DEV), x.k.to(DEV), x.k_scale.to(DEV), x.row_len[1].to(DEV),
-                                torch.from_numpy(prev).to(DEV), K_TOPK, stats=st)
+    out, sc = g.gvr_indexer_topk(x.q[1].to(DEV), x.w.to(DEV), x.k.to(DEV), x.k_scale.to(DEV), x.row_len[1].to(DEV),
+                                 torch.from_numpy(prev).to(DEV), K_TOPK, stats=st)
     torch.cuda.synchronize()
+    check_topk_exact(out.cpu().numpy(), sc.cpu().numpy(), x.row_len[1].numpy(), K_TOPK,
+                     "indexer + topk, %d rows" % x.rows)
     check_topk(out.cpu().numpy(), ex1, mag1, x.row_len[1].numpy(), K_TOPK, H, D)
     assert "error" not in {g.PATH_NAMES[int(v)] for v in g.decode_stats(st)["path"].tolist()}
     out2, _ = g.gvr_indexer_topk(x.q[1].to(DEV), x.w.to(DEV), x.k.to(DEV), x.k_scale.to(DEV), x.row_len[1].to(DEV),

@@ -69,6 +69,12 @@ def test_full_size_config2(fn):
 
 
 @pytest.mark.parametrize("fn", FNS, ids=lambda f: f.__name__)
+def test_full_size_config1(fn):
+    """32 queries at ~32.8K (the whole 32-row launch), four decode steps."""
+    run_decode(fn, 1, 4, 32, dev=DEV)
+
+
+@pytest.mark.parametrize("fn", FNS, ids=lambda f: f.__name__)
 def test_full_size_config4(fn):
     """16 queries x 3 draft rows, rows of 65K..262K keys (48 rows)."""
     run_decode(fn, 4, 2, 16, dev=DEV)
@@ -608,6 +614,42 @@ def test_graph_replays_match_the_oracle():
         o = g.gvr_topk(S, None, P, K)
         torch.cuda.synchronize()
         assert_rows_equal(o.cpu().numpy(), exp, "eager call between replays")
+
+
+def test_graph_survives_workspace_growth():
+    """A graph captured with a split call keeps its workspace after a later,
+    larger eager call on the same stream has made the stream's workspace
+    grow: every replay still equals the oracle (the outgrown workspace is
+    kept, not freed)."""
+    import paper_2604_22312_amd as g
+    rng = np.random.default_rng(37)
+    K, ld = 2048, 70000
+    x = rng.standard_normal((8, ld)).astype(np.float32)
+    prevx = x + 0.05 * rng.standard_normal((8, ld)).astype(np.float32)
+    exp, _, _ = oracle.topk(x, K)
+    pexp, _, _ = oracle.topk(prevx, K)
+    S, P = torch.from_numpy(x).to(DEV), torch.from_numpy(pexp).to(DEV)
+    small = {"parts": 4}
+    out2 = torch.empty((2, K), dtype=torch.int32, device=DEV)
+    stream = torch.cuda.Stream()
+    note("workspace growth after capture: eager 2 x 4 parts, capture, eager 8 x 4 parts, replays")
+    with torch.cuda.stream(stream):   # 8 (row, part) slots: the stream's first workspace
+        g.gvr_topk_ex(S[:2], None, P[:2], K, out_idx=out2, stream=stream, options=small)
+    torch.cuda.synchronize()
+    assert_rows_equal(out2.cpu().numpy(), exp[:2], "eager 2-row split call")
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=stream):
+        g.gvr_topk_ex(S[:2], None, P[:2], K, out_idx=out2, stream=stream, options=small)
+    for rep in range(3):
+        with torch.cuda.stream(stream):   # 32 slots: the workspace grows (new buffer)
+            o8 = g.gvr_topk_ex(S, None, P, K, stream=stream, options=small)
+        torch.cuda.synchronize()
+        assert_rows_equal(o8.cpu().numpy(), exp, "eager 8-row split call %d" % rep)
+        out2.fill_(-7)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert_rows_equal(out2.cpu().numpy(), exp[:2], "replay %d after the workspace grew" % rep)
 
 
 @pytest.mark.parametrize("opts", [{"flags": 16, "capacity": 2048}, {"flags": 16, "capacity": 2500},

@@ -14,7 +14,10 @@ other than its own formulas:
   positive logits gives k_scale * numpy.dot;
 * linearity in the head weights and invariance under a permutation of the
   heads; a row reads its own request's cache;
-* planted mistakes in copies of the oracle.
+* the magnitude (the scale of the GPU tolerances) from both sides: a
+  pure-Python loop on mixed signs, equality with the score when nothing can
+  cancel, and |I| <= magnitude;
+* planted mistakes in copies of the oracle (also in the magnitude).
 """
 import importlib.util
 import math
@@ -117,8 +120,57 @@ def check_weights_and_heads(m):
     assert np.allclose(b[[2, 3, 0, 1]], a, rtol=1e-14)
 
 
+def _magnitude_by_hand(q, w, k, ks, group, row_len):
+    """Pure-Python sum_j |w_j| sum_d |q_jd| |k_scale k_d|, every term written out."""
+    def dec(byte):
+        s = -1.0 if byte & 0x80 else 1.0
+        e, mm = (byte >> 3) & 15, byte & 7
+        return s * (mm / 8.0 * 2.0 ** -6 if e == 0 else (1 + mm / 8.0) * 2.0 ** (e - 7))
+    B, H, D = q.shape
+    ld = k.shape[1]
+    out = np.full((B, ld), np.nan)
+    for b in range(B):
+        g = b // group
+        for s in range(min(int(row_len[b]), ld)):
+            out[b, s] = math.fsum(abs(float(w[b, j])) * math.fsum(abs(dec(int(q[b, j, d])))
+                                                                 * abs(float(ks[g, s]) * dec(int(k[g, s, d])))
+                                                                 for d in range(D))
+                                  for j in range(H))
+    return out
+
+
+def check_magnitude_by_hand(m):
+    """The error scale the GPU tolerances come from, against a pure-Python
+    loop on mixed-sign inputs: a factor too many or too few (a dropped key
+    scale, a missing absolute value) fails here."""
+    for seed in range(4):
+        q, w, k, ks, rl = _small(20 + seed, H=4, D=8)
+        got = m.magnitude(q, w, k, ks, group=2, row_len=rl)
+        ref = _magnitude_by_hand(q, w, k, ks, 2, rl)
+        assert np.array_equal(np.isnan(got), np.isnan(ref))
+        ok = ~np.isnan(ref)
+        assert np.allclose(got[ok], ref[ok], rtol=1e-12, atol=0.0), seed
+
+
+def check_magnitude_all_positive(m):
+    """With every weight, query byte, key byte and key scale non-negative no
+    term cancels and the ReLU passes everything: the magnitude equals the
+    score itself (the upper side of |I| <= magnitude is reached)."""
+    rng = np.random.default_rng(5)
+    B, H, D, ld = 2, 4, 16, 11
+    q = WI.to_e4m3_bytes(torch.from_numpy(np.abs(rng.standard_normal((B, H, D))))).numpy()
+    k = WI.to_e4m3_bytes(torch.from_numpy(np.abs(rng.standard_normal((1, ld, D))))).numpy()
+    assert not ((q & 0x80).any() or (k & 0x80).any())
+    ks = rng.uniform(0.2, 1.5, (1, ld))
+    w = rng.uniform(0.1, 2.0, (B, H))
+    s = m.indexer_scores(q, w, k, ks, group=2)
+    mag = m.magnitude(q, w, k, ks, group=2)
+    assert np.all(s > 0)
+    assert np.allclose(mag, s, rtol=1e-13, atol=0.0)
+
+
 ALL_CHECKS = [check_decoder_vs_torch, check_decoder_hand_values, check_loops, check_relu_and_scale_sign,
-              check_weights_and_heads]
+              check_weights_and_heads, check_magnitude_by_hand, check_magnitude_all_positive]
 
 
 @pytest.mark.parametrize("check", ALL_CHECKS, ids=[c.__name__ for c in ALL_CHECKS])
@@ -127,6 +179,8 @@ def test_oracle_pin(check):
 
 
 def test_magnitude_bounds_scores():
+    """Lower side of the two-sided pin: |I| <= magnitude on mixed signs
+    (the upper side, equality, is check_magnitude_all_positive)."""
     q, w, k, ks, rl = _small(3, requests=2, group=2, ld=9, H=4, D=16)
     s = IX.indexer_scores(q, w, k, ks, group=2, row_len=rl)
     mag = IX.magnitude(q, w, k, ks, group=2, row_len=rl)
@@ -152,6 +206,13 @@ MUTATIONS = [
     ("subnormal scale", r"\(m / 8\.0\) \* 2\.0 \*\* -6", "(m / 8.0) * 2.0 ** -7"),
     ("wrong cache", r"g = b // group", "g = b % max(k.shape[0], 1)"),
     ("sign ignored", r"sign = np\.where\(u >> 7, -1\.0, 1\.0\)", "sign = 1.0"),
+    ("magnitude: key scale dropped",
+     r"np\.abs\(decode_e4m3\(k\[g, :n\]\) \* np\.asarray\(k_scale, dtype=np\.float64\)\[g, :n, None\]\)",
+     "np.abs(decode_e4m3(k[g, :n]))"),
+    ("magnitude: |w| dropped", r"np\.abs\(np\.asarray\(w, dtype=np\.float64\)\[b\]\) @",
+     "np.asarray(w, dtype=np.float64)[b] @"),
+    ("magnitude: |q| dropped", r"Q = np\.abs\(decode_e4m3\(q\[b\]\)\)", "Q = decode_e4m3(q[b])"),
+    ("magnitude: extra factor", r"@ \(Q @ Kd\.T\)", "@ (Q @ Kd.T) * 2.0"),
 ]
 
 
