@@ -81,6 +81,8 @@ typedef enum {
     GVR_OK = 0,
     GVR_ERR_INVALID_ARG = -1,    /* B < 0, ld < 0, NULL required pointer, bad option */
     GVR_ERR_UNSUPPORTED_K = -2,  /* K < 1 or K > GVR_MAX_K */
+    GVR_ERR_WORKSPACE = -3,      /* gvr_topk_ex_noalloc: a forced split needs more
+                                    than GVR_NOALLOC_SLOTS (row, part) slots */
     GVR_ERR_HIP = -4,            /* the kernel launch failed */
     GVR_ERR_TOO_LONG = -5        /* ld > 2^31 - 16 */
 } gvr_status;
@@ -182,6 +184,29 @@ gvr_status radix_topk(const float* scores, int64_t B, int64_t ld, const int32_t*
 gvr_status gvr_topk_ex(const float* scores, int64_t B, int64_t ld, const int32_t* row_len,
                        const int32_t* prev_topk, int32_t K, int32_t* out_idx, void* stream,
                        const gvr_options* options, gvr_row_stats* stats);
+
+/* Largest number of (row, part) slots of one gvr_topk_ex_noalloc call. */
+#define GVR_NOALLOC_SLOTS 256
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * call and result as gvr_topk_ex, with the split-row workspace taken from a
+ * static device array of the library instead of a library allocation. It
+ * calls no hipMalloc, hipFree or other allocating routine, so it may be
+ * captured into a HIP graph as any call's first, on any stream.
+ *   - The array holds GVR_NOALLOC_SLOTS (row, part) slots: 32 MiB per device
+ *     the library runs on, held until the process ends. An automatic split
+ *     (options->parts == 0) is lowered to fit; a forced split with
+ *     B * parts > GVR_NOALLOC_SLOTS returns GVR_ERR_WORKSPACE before
+ *     anything is enqueued. Unsplit calls do not touch the array.
+ *   - Every call on one device shares that device's array: calls that
+ *     overlap on one device (other streams, graph replays, other threads)
+ *     race and corrupt each other's merge; serialise them. The array's
+ *     arrival words start at zero and every call leaves them at zero.
+ *   - All other arguments, errors and semantics as gvr_topk_ex. */
+gvr_status gvr_topk_ex_noalloc(const float* scores, int64_t B, int64_t ld, const int32_t* row_len,
+                               const int32_t* prev_topk, int32_t K, int32_t* out_idx, void* stream,
+                               const gvr_options* options, gvr_row_stats* stats);
 
 /* Radix-select counterpart of gvr_topk_ex. */
 gvr_status radix_topk_ex(const float* scores, int64_t B, int64_t ld, const int32_t* row_len,

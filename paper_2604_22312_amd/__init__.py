@@ -12,6 +12,8 @@ Functions mirror the C entry points:
 * ``gvr_topk(scores, row_len, prev_topk, K, out_idx=None, stream=None)``
 * ``radix_topk(scores, row_len, prev_topk, K, out_idx=None, stream=None)``
 * ``gvr_topk_ex`` / ``radix_topk_ex`` (options, per-row stats)
+* ``gvr_topk_ex_noalloc`` -- ``gvr_topk_ex`` with no allocation inside the
+  call (split-row workspace in a static device array)
 * ``gvr_rope_g(n, params=None, device=...)`` -- g(Delta) of the RoPE/YaRN prior
 * ``gvr_rope_prior(n, K, params=None, device=...)`` -- its static index set
   (``include/gvr_rope_prior.h``)
@@ -34,6 +36,7 @@ from .binding import (  # noqa: F401
     gvr_rope_prior,
     gvr_topk,
     gvr_topk_ex,
+    gvr_topk_ex_noalloc,
     lib,
     library_path,
     new_stats,

@@ -56,8 +56,10 @@ def lib():
             f = getattr(L, name)
             f.restype = ctypes.c_int
             f.argtypes = [vp, i64, i64, vp, vp, i32, vp, vp]
-        L.gvr_topk_ex.restype = ctypes.c_int
-        L.gvr_topk_ex.argtypes = [vp, i64, i64, vp, vp, i32, vp, vp, ctypes.POINTER(Options), vp]
+        for name in ("gvr_topk_ex", "gvr_topk_ex_noalloc"):
+            f = getattr(L, name)
+            f.restype = ctypes.c_int
+            f.argtypes = [vp, i64, i64, vp, vp, i32, vp, vp, ctypes.POINTER(Options), vp]
         L.radix_topk_ex.restype = ctypes.c_int
         L.radix_topk_ex.argtypes = [vp, i64, i64, vp, i32, vp, vp, ctypes.POINTER(Options), vp]
         L.gvr_rope_params_default.restype = None
@@ -142,7 +144,7 @@ def radix_topk(scores, row_len, prev_topk, K, out_idx=None, stream=None):
     return _call("radix_topk", scores, row_len, prev_topk, K, out_idx, stream)
 
 
-def _call_ex(radix, scores, row_len, prev_topk, K, out_idx, stream, options, stats):
+def _call_ex(radix, scores, row_len, prev_topk, K, out_idx, stream, options, stats, fn="gvr_topk_ex"):
     B, ld, K, out_idx = _check(scores, row_len, prev_topk, K, out_idx)
     if stats is not None and (stats.dtype != torch.int32 or stats.shape != (B, STATS_INTS)
                               or stats.device != scores.device or not stats.is_contiguous()):
@@ -157,10 +159,10 @@ def _call_ex(radix, scores, row_len, prev_topk, K, out_idx, stream, options, sta
             st = L.radix_topk_ex(_ptr(scores), B, ld, _ptr(row_len), K, _ptr(out_idx),
                                  _stream(stream, scores.device), optp, _ptr(stats))
         else:
-            st = L.gvr_topk_ex(_ptr(scores), B, ld, _ptr(row_len), _ptr(prev_topk), K, _ptr(out_idx),
-                               _stream(stream, scores.device), optp, _ptr(stats))
+            st = getattr(L, fn)(_ptr(scores), B, ld, _ptr(row_len), _ptr(prev_topk), K, _ptr(out_idx),
+                                _stream(stream, scores.device), optp, _ptr(stats))
     if st != 0:
-        raise GvrError("radix_topk_ex" if radix else "gvr_topk_ex", st)
+        raise GvrError("radix_topk_ex" if radix else fn, st)
     return out_idx
 
 
@@ -168,6 +170,13 @@ def gvr_topk_ex(scores, row_len, prev_topk, K, out_idx=None, stream=None, option
     """``gvr_topk`` with options (dict or ``Options``) and an optional stats
     tensor ([B][22] int32, see ``decode_stats``)."""
     return _call_ex(False, scores, row_len, prev_topk, K, out_idx, stream, options, stats)
+
+
+def gvr_topk_ex_noalloc(scores, row_len, prev_topk, K, out_idx=None, stream=None, options=None, stats=None):
+    """``gvr_topk_ex`` taking its split-row workspace from the library's static
+    device array (no allocation inside the call). ``out_idx`` is allocated
+    here when it is None, before the call."""
+    return _call_ex(False, scores, row_len, prev_topk, K, out_idx, stream, options, stats, fn="gvr_topk_ex_noalloc")
 
 
 def radix_topk_ex(scores, row_len, K, out_idx=None, stream=None, options=None, stats=None):

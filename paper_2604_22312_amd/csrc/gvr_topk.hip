@@ -64,10 +64,20 @@
 #include <vector>
 
 #include "gvr_topk.h"
+#include "host_plan.h"
 
 #define DEV __device__ __forceinline__
 
 namespace {
+
+using gvr_host::kMaxParts;
+using gvr_host::kMaxSpecLd;
+using gvr_host::kNWLong;
+using gvr_host::kNWMid;
+using gvr_host::kNWShort;
+using gvr_host::kPartCap;
+using gvr_host::kSlotWaves;
+using gvr_host::kXcds;
 
 constexpr int kWave = 64;
 constexpr int kU = 8;                          // slabs in flight per wave (count / collect passes)
@@ -76,7 +86,6 @@ constexpr int kBins = 256;                     // bins of a counting window
 constexpr int kBinsX = kBins + 1;              // + "at or above the window"
 constexpr int kCapWLong = 1024;                // per-wave list capacity of the 16- and 4-wave shapes
 constexpr int kCapWMid = 768;                  // per-wave list capacity of the 8-wave shape
-constexpr int kPartCap = GVR_MAX_CANDIDATES;   // entries per (row, part) list in the split-row workspace
 
 // Workgroup shape: NW wave64s. The 16-wave shape (1024 list entries per wave,
 // 128 KB of lists, one workgroup per compute unit) streams a long row as fast
@@ -93,10 +102,11 @@ struct Shape {
     static constexpr int kCapW = NW == 8 ? kCapWMid : kCapWLong;   // per-wave list capacity, speculative pass
     static constexpr int kCap = NW * kCapW;     // list capacity C (LDS)
 };
-constexpr int kNWLong = 16;
-constexpr int kNWShort = 4;
-constexpr int kNWMid = 8;
+static_assert(Shape<kNWLong>::kCap == gvr_host::kCapLong && Shape<kNWMid>::kCap == gvr_host::kCapMid &&
+                  Shape<kNWShort>::kCap == gvr_host::kCapShort,
+              "shape capacities as the host plans them");
 static_assert(Shape<kNWLong>::kCap == GVR_MAX_CANDIDATES, "the long-row shape holds the largest capacity");
+static_assert(kSlotWaves == kNWLong && kPartCap == Shape<kNWLong>::kCap, "a workspace slot holds one part's lists");
 constexpr int kRefBins = 4096;                 // bins of a narrowing refine level (12 bits of key)
 constexpr int kRefBins1 = 2048;                // bins of the first refine level (32 per lane of one wave)
 constexpr int kGuessSamples = 256;             // guessed indices gathered: a strided sample of prev_topk
@@ -106,15 +116,6 @@ constexpr int kSpecQuantile = 65;              // T_spec: gathered key of rank c
 constexpr int kSmall = 64;                     // refine: K-th key's bin resolved by one wave up to this size
 constexpr int kMaxPasses = 8;                  // 2 + at most 4 narrowing passes + 1 final pass suffice
 constexpr int kMaxSecant = 8;                  // probes of the secant search after T0 (I_max)
-constexpr int kMaxParts = 16;                  // workgroups per row
-constexpr int kMinPartElems = 16384;           // a row is split only into parts at least this long
-constexpr int kMaxSlots = 2048;                // (row, part) pairs of one split call: 256 MB of workspace
-constexpr int kXcds = 8;                       // gfx950 XCDs; workgroup i runs on XCD i % 8
-// Longest row stride of the guess path: its speculative pass addresses a row
-// through one buffer resource with 32-bit byte offsets (lane offset included),
-// so 4 (ld + 3) + 1024 must stay below 2^31. Longer rows take the guess-free
-// schedule, whose passes index the row with 64-bit addresses.
-constexpr int64_t kMaxSpecLd = ((int64_t)1 << 29) - 4096;
 
 static_assert((kBins & (kBins - 1)) == 0 && (kRefBins & (kRefBins - 1)) == 0 && (kRefBins1 & (kRefBins1 - 1)) == 0 &&
                   (kGuessBins & (kGuessBins - 1)) == 0, "bin counts are powers of two");
@@ -139,6 +140,7 @@ struct Params {
                          // bit 16; 0 between calls
     int32_t* part_count; // [rows][S] f(threshold) of each part, bit 31 = a wave list overflowed
     uint32_t* part_thresh; // [rows][S] threshold of each part's list (T_spec, the same in every part)
+    int32_t* part_wcnt;  // [rows][S][kSlotWaves] list length of each wave of each part
     uint64_t* part_list; // [rows][S][kPartCap] (fp32 bits | index << 32) of each part
 };
 
@@ -1951,56 +1953,6 @@ __global__ __launch_bounds__(Shape<NW>::kBlock) void radix_topk_kernel(Params p)
 
 // ------------------------------------------------------------------ host side
 
-gvr_status validate(const float* scores, int64_t B, int64_t ld, int32_t K, const int32_t* out,
-                    const gvr_options* opt, int* capacity, int* use_guess, int* parts, int* scatter, int* secant,
-                    int* paper_refine, int* shape) {
-    if (K < 1 || K > GVR_MAX_K) return GVR_ERR_UNSUPPORTED_K;
-    if (B < 0 || ld < 0) return GVR_ERR_INVALID_ARG;
-    if (B > 0 && (!scores || !out)) return GVR_ERR_INVALID_ARG;
-    if (ld > (int64_t)0x7FFFFFF0) return GVR_ERR_TOO_LONG;
-    int cap = GVR_MAX_CANDIDATES;
-    if (opt) {
-        if (opt->capacity != 0) {
-            if (opt->capacity < K || opt->capacity > GVR_MAX_CANDIDATES) return GVR_ERR_INVALID_ARG;
-            cap = opt->capacity;
-        }
-        if ((opt->flags & ~127) || opt->reserved1) return GVR_ERR_INVALID_ARG;
-        const int forced = (opt->flags >> 4) & 7;
-        if (forced & (forced - 1)) return GVR_ERR_INVALID_ARG;   // two shapes forced
-        if (opt->parts < 0 || opt->parts > kMaxParts) return GVR_ERR_INVALID_ARG;
-        if (opt->flags & 1) *use_guess = 0;
-        *scatter = (opt->flags >> 1) & 1;
-        *secant = (opt->flags >> 2) & 1;
-        *paper_refine = (opt->flags >> 3) & 1;
-        *shape = forced == 1 ? kNWShort : forced == 2 ? kNWLong : forced == 4 ? kNWMid : 0;
-        *parts = opt->parts;
-    }
-    *capacity = cap;
-    return GVR_OK;
-}
-
-// Split-row workspace of one (device, stream): arrival counters, part counts
-// and part lists for up to `slots` (row, part) pairs of one launch. Calls on
-// one stream run in order, so they can share it; the counters are zeroed
-// when the buffer is made and every launch leaves them at zero.
-struct Workspace {
-    int device;
-    void* stream;
-    int slots;
-    uint64_t* arrivals;
-    int32_t* part_count;
-    uint32_t* part_thresh;
-    uint64_t* part_list;
-    void* base;
-};
-
-std::mutex g_ws_mutex;
-std::vector<Workspace> g_ws;
-// Buffers a stream has outgrown. A HIP graph captured earlier may still hold
-// their addresses in its kernel arguments, so they are never freed: they stay
-// allocated until the process ends, like the current ones.
-std::vector<void*> g_ws_retired;
-
 int cu_count(int device) {
     static std::mutex m;
     static std::vector<int> cache;
@@ -2014,125 +1966,79 @@ int cu_count(int device) {
     return cache[device];
 }
 
-size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
-
-gvr_status get_workspace(int device, void* stream, int rows, int parts, Workspace* out) {
-    std::lock_guard<std::mutex> lk(g_ws_mutex);
-    const int slots = rows * parts;
-    for (auto& w : g_ws)
-        if (w.device == device && w.stream == stream) {
-            if (w.slots >= slots) {
-                *out = w;
-                return GVR_OK;
-            }
-            // Grow: the old buffer is retired, not freed (queued launches and
-            // graphs captured on this stream may still use it). Its arrival
-            // words are zero again once those launches end, so a graph that
-            // holds it keeps working.
-            g_ws_retired.push_back(w.base);
-            w = g_ws.back();
-            g_ws.pop_back();
-            break;
-        }
-    const size_t a_bytes = align_up((size_t)slots * sizeof(uint64_t), 256);
-    const size_t c_bytes = align_up((size_t)slots * sizeof(int32_t), 256);
-    const size_t t_bytes = align_up((size_t)slots * sizeof(uint32_t), 256);
-    const size_t l_bytes = (size_t)slots * kPartCap * sizeof(uint64_t);
-    // Allocating is not possible while the stream is being captured.
-    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
-    if (hipStreamIsCapturing((hipStream_t)stream, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone)
-        return GVR_ERR_HIP;
-    void* base = nullptr;
-    if (hipMalloc(&base, a_bytes + c_bytes + t_bytes + l_bytes) != hipSuccess) return GVR_ERR_HIP;
-    // Arrival words start at zero; cleared on the call's own stream, ahead of its launch.
-    if (hipMemsetAsync(base, 0, a_bytes, (hipStream_t)stream) != hipSuccess) {
-        (void)hipFree(base);
-        return GVR_ERR_HIP;
+// Device calls of the library-owned workspace cache.
+struct HipDev {
+    static int capturing(void* stream, bool* yes) {
+        hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+        if (hipStreamIsCapturing((hipStream_t)stream, &cs) != hipSuccess) return 1;
+        *yes = cs != hipStreamCaptureStatusNone;
+        return 0;
     }
-    Workspace w;
-    w.device = device;
-    w.stream = stream;
-    w.slots = slots;
-    w.base = base;
-    w.arrivals = static_cast<uint64_t*>(base);
-    w.part_count = reinterpret_cast<int32_t*>(static_cast<char*>(base) + a_bytes);
-    w.part_thresh = reinterpret_cast<uint32_t*>(static_cast<char*>(base) + a_bytes + c_bytes);
-    w.part_list = reinterpret_cast<uint64_t*>(static_cast<char*>(base) + a_bytes + c_bytes + t_bytes);
-    g_ws.push_back(w);
-    *out = w;
+    static int alloc(void** p, size_t bytes) { return hipMalloc(p, bytes) == hipSuccess ? 0 : 1; }
+    static int clear_async(void* p, size_t bytes, void* stream) {
+        return hipMemsetAsync(p, 0, bytes, (hipStream_t)stream) == hipSuccess ? 0 : 1;
+    }
+};
+
+gvr_host::WorkspaceCache<HipDev> g_workspaces;
+
+// Scratch of the allocation-free entry point: the split-row workspace of up
+// to kStaticSlots (row, part) slots (arrival words, counts, thresholds,
+// per-wave counts, 128 KB of lists per slot: 32 MiB) as one device array.
+// Each device that runs the library holds its own copy until the process
+// ends. Its arrival words are zero when the library is loaded, and every
+// launch leaves the words it used at zero again (the last part of a row
+// resets its word), so they start at zero on every call.
+constexpr size_t kScratchBytes = gvr_host::ws_layout(gvr_host::kStaticSlots).total;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+// The array's device address per device (hipGetSymbolAddress, once per
+// device with that device current): host code uses it, never the array's
+// name, which is a host-side stand-in.
+gvr_status static_scratch(int device, void** out) {
+    static std::mutex m;
+    static std::vector<void*> ptrs;
+    std::lock_guard<std::mutex> lk(m);
+    if ((int)ptrs.size() <= device) ptrs.resize(device + 1, nullptr);
+    if (!ptrs[device]) {
+        void* ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return GVR_ERR_HIP;
+        ptrs[device] = ptr;
+    }
+    *out = ptrs[device];
     return GVR_OK;
 }
 
-// Parts per row. Splitting a row over S workgroups divides its streaming
-// time (one workgroup reads about 33 GB/s on MI355X) but costs the merge of
-// the parts' candidate lists, about 8 us of memory round trips when many
-// rows merge at once; split only when the time saved is larger, keep parts
-// >= kMinPartElems long and stay within the compute units. A call of one or
-// two rows leaves the chip nearly idle and its merges cost a few us: there
-// parts of 8K-16K elements pay from 32K elements on (8 parts below 192K,
-// then 16).
-int choose_parts(int64_t rows, int64_t ld, int cus) {
-    if (rows <= 0 || rows >= cus) return 1;
-    if (rows <= 2 && ld >= 32768 && cus >= 32 * rows) {
-        int s = 1;
-        while (2 * s <= ld / 8192 && 2 * s <= kMaxParts) s *= 2;
-        return ld < 196608 ? std::min(s, 8) : s;
-    }
-    int64_t s = cus / rows;
-    s = std::min<int64_t>(s, std::max<int64_t>(1, ld / kMinPartElems));
-    s = std::min<int64_t>(s, kMaxParts);
-    if (s <= 1) return 1;
-    const double stream_us = (double)ld * 4.0 / 33.0e3;   // one workgroup, whole row
-    const double saved_us = stream_us * (1.0 - 1.0 / (double)s);
-    return saved_us > 8.0 ? (int)s : 1;
-}
-
-// Workgroup shape of a call: waves per workgroup (16, 8 or 4). Up to one row
-// per compute unit, 16 waves: one round of rows at the shortest per-row
-// latency, and row splitting. With more rows, the rows run in rounds of one
-// (16 waves), two (8) or three (4) workgroups per compute unit; the 8-wave
-// shape has the best rate of rows per compute unit when the previous Top-K
-// guides the rows (decode rows of 8K-64K elements: 1024 rows of 32K take
-// 42 us against 55 with 16 waves and 73 with 4), except for rows longer
-// than 40K in at most two rows per compute unit, where the 16-wave shape's
-// shorter latency wins (512 rows of 64K: 40 us against 47); from 48K on
-// the two are even at four rows per compute unit. Without a usable guess
-// the radix schedule runs, where rows of at most 4K go to 4 waves (2048
-// rows of 4K: 47 us against 73 with 8 waves) and longer ones to 8.
-int choose_shape(int64_t rows, int64_t ld, int cus, bool guess) {
-    if (rows <= cus) return kNWLong;
-    if (!guess) return ld <= 4096 ? kNWShort : kNWMid;
-    if (ld <= 40960 || rows > 2 * (int64_t)cus) return kNWMid;
-    return kNWLong;
-}
+enum WsSource { kWsLibrary = 0, kWsStatic = 1 };
 
 gvr_status run(const float* scores, int64_t B, int64_t ld, const int32_t* row_len, const int32_t* prev,
                int32_t K, int32_t* out, void* stream, const gvr_options* opt, gvr_row_stats* stats,
-               int use_guess) {
-    int cap = 0, parts_opt = 0, scatter = 0, secant = 0, paper_refine = 0, shape = 0;
-    gvr_status st = validate(scores, B, ld, K, out, opt, &cap, &use_guess, &parts_opt, &scatter, &secant,
-                             &paper_refine, &shape);
+               int use_guess, WsSource ws_source) {
+    gvr_host::CallOptions o;
+    gvr_status st = gvr_host::validate(scores, B, ld, K, out, opt, use_guess, &o);
     if (st != GVR_OK) return st;
     if (B == 0) return GVR_OK;
-    // Rows of at most 2K elements list every element (the guess would cut
-    // few candidates): when no row is longer, the guess-free kernel runs.
-    const bool guess = use_guess && prev && ld > 2 * (int64_t)K && ld <= kMaxSpecLd;
     int device = 0;
     if (hipGetDevice(&device) != hipSuccess) return GVR_ERR_HIP;
     const int cus = cu_count(device);
-    if (shape == 0) shape = choose_shape(B, ld, cus, guess);
-    // A smaller C never changes the result.
-    if (shape == kNWShort) cap = std::min(cap, Shape<kNWShort>::kCap);
-    if (shape == kNWMid) cap = std::min(cap, Shape<kNWMid>::kCap);
-    int parts = (!guess || shape != kNWLong) ? 1 : (parts_opt > 0 ? parts_opt : choose_parts(B, ld, cus));
-    // A forced split is capped at kMaxSlots (row, part) pairs per call, which
-    // bounds the workspace (128 KB of list per pair).
-    if (parts > 1 && (int64_t)parts * B > kMaxSlots) parts = (int)std::max<int64_t>(1, kMaxSlots / B);
-    if (secant) parts = 1;   // the secant search reads whole rows
-    Workspace ws = {};
+    gvr_host::Plan plan;
+    const bool is_static = ws_source == kWsStatic;
+    st = gvr_host::plan_call(B, ld, K, prev != nullptr, o, cus,
+                             is_static ? gvr_host::kStaticSlots : gvr_host::kMaxSlots, is_static, &plan);
+    if (st != GVR_OK) return st;
+    const bool guess = plan.guess;
+    const int parts = plan.parts;
+    gvr_host::WsPtrs ws;
     if (parts > 1) {
-        st = get_workspace(device, stream, (int)B, parts, &ws);
-        if (st != GVR_OK) return st;
+        if (is_static) {
+            void* base = nullptr;
+            st = static_scratch(device, &base);
+            if (st != GVR_OK) return st;
+            ws = gvr_host::ws_carve(base, gvr_host::kStaticSlots);
+        } else {
+            st = g_workspaces.get(device, stream, B * (int64_t)parts, &ws);
+            if (st != GVR_OK) return st;
+        }
     }
     // Rows in launches of at most 2^24 (the grid holds 8 * chunk slots).
     const int64_t kRowsPerLaunch = (int64_t)1 << 24;
@@ -2147,26 +2053,27 @@ gvr_status run(const float* scores, int64_t B, int64_t ld, const int32_t* row_le
         q.out = out + r0 * K;
         q.stats = stats ? stats + r0 : nullptr;
         q.K = K;
-        q.capacity = cap;
+        q.capacity = plan.capacity;
         q.rows = (int32_t)rows;
         q.parts = parts;
         q.chunk = (int32_t)(rows_pad / kXcds * parts);
-        q.scatter = scatter;
-        q.secant = secant;
-        q.paper_refine = paper_refine;
+        q.scatter = o.scatter;
+        q.secant = o.secant;
+        q.paper_refine = o.paper_refine;
         q.arrivals = ws.arrivals;
         q.part_count = ws.part_count;
         q.part_thresh = ws.part_thresh;
+        q.part_wcnt = ws.part_wcnt;
         q.part_list = ws.part_list;
         const dim3 grid((unsigned)(rows_pad * parts));
         const hipStream_t hs = (hipStream_t)stream;
-        if (shape == kNWMid) {
+        if (plan.shape == kNWMid) {
             const dim3 block(Shape<kNWMid>::kBlock);
             if (guess)
                 hipLaunchKernelGGL(gvr_topk_kernel<kNWMid>, grid, block, 0, hs, q);
             else
                 hipLaunchKernelGGL(radix_topk_kernel<kNWMid>, grid, block, 0, hs, q);
-        } else if (shape == kNWShort) {
+        } else if (plan.shape == kNWShort) {
             const dim3 block(Shape<kNWShort>::kBlock);
             if (guess)
                 hipLaunchKernelGGL(gvr_topk_kernel<kNWShort>, grid, block, 0, hs, q);
@@ -2190,24 +2097,30 @@ extern "C" {
 
 gvr_status gvr_topk(const float* scores, int64_t B, int64_t ld, const int32_t* row_len, const int32_t* prev_topk,
                     int32_t K, int32_t* out_idx, void* stream) {
-    return run(scores, B, ld, row_len, prev_topk, K, out_idx, stream, nullptr, nullptr, 1);
+    return run(scores, B, ld, row_len, prev_topk, K, out_idx, stream, nullptr, nullptr, 1, kWsLibrary);
 }
 
 gvr_status radix_topk(const float* scores, int64_t B, int64_t ld, const int32_t* row_len, const int32_t* prev_topk,
                       int32_t K, int32_t* out_idx, void* stream) {
     (void)prev_topk;
-    return run(scores, B, ld, row_len, nullptr, K, out_idx, stream, nullptr, nullptr, 0);
+    return run(scores, B, ld, row_len, nullptr, K, out_idx, stream, nullptr, nullptr, 0, kWsLibrary);
 }
 
 gvr_status gvr_topk_ex(const float* scores, int64_t B, int64_t ld, const int32_t* row_len, const int32_t* prev_topk,
                        int32_t K, int32_t* out_idx, void* stream, const gvr_options* options,
                        gvr_row_stats* stats) {
-    return run(scores, B, ld, row_len, prev_topk, K, out_idx, stream, options, stats, 1);
+    return run(scores, B, ld, row_len, prev_topk, K, out_idx, stream, options, stats, 1, kWsLibrary);
+}
+
+gvr_status gvr_topk_ex_noalloc(const float* scores, int64_t B, int64_t ld, const int32_t* row_len,
+                               const int32_t* prev_topk, int32_t K, int32_t* out_idx, void* stream,
+                               const gvr_options* options, gvr_row_stats* stats) {
+    return run(scores, B, ld, row_len, prev_topk, K, out_idx, stream, options, stats, 1, kWsStatic);
 }
 
 gvr_status radix_topk_ex(const float* scores, int64_t B, int64_t ld, const int32_t* row_len, int32_t K,
                          int32_t* out_idx, void* stream, const gvr_options* options, gvr_row_stats* stats) {
-    return run(scores, B, ld, row_len, nullptr, K, out_idx, stream, options, stats, 0);
+    return run(scores, B, ld, row_len, nullptr, K, out_idx, stream, options, stats, 0, kWsLibrary);
 }
 
 const char* gvr_status_string(gvr_status s) {
@@ -2215,6 +2128,7 @@ const char* gvr_status_string(gvr_status s) {
         case GVR_OK: return "ok";
         case GVR_ERR_INVALID_ARG: return "invalid argument";
         case GVR_ERR_UNSUPPORTED_K: return "unsupported K (1 <= K <= 2048)";
+        case GVR_ERR_WORKSPACE: return "the call needs more scratch than the allocation-free entry point holds";
         case GVR_ERR_HIP: return "HIP runtime error";
         case GVR_ERR_TOO_LONG: return "row stride too long";
     }

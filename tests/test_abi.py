@@ -34,7 +34,7 @@ def L():
 
 def test_header_declares_the_boundary():
     names = declared_functions()
-    for n in ("gvr_topk", "radix_topk", "gvr_topk_ex", "radix_topk_ex",
+    for n in ("gvr_topk", "radix_topk", "gvr_topk_ex", "radix_topk_ex", "gvr_topk_ex_noalloc",
               "gvr_status_string", "gvr_version", "gvr_rope_params_default", "gvr_rope_g",
               "gvr_rope_prior", "gvr_indexer_scores", "gvr_indexer_topk"):
         assert n in names, n
@@ -47,7 +47,7 @@ def test_every_declared_symbol_is_exported(L):
 
 def test_status_strings(L):
     import paper_2604_22312_amd as g
-    for code in (0, -1, -2, -4, -5):
+    for code in (0, -1, -2, -3, -4, -5):
         assert g.status_string(code) and "unknown" not in g.status_string(code)
     assert "unknown" in g.status_string(-99)
     assert "gfx950" in g.version()
@@ -92,6 +92,11 @@ def test_options_validation(L):
     for opt in bad:
         assert L.gvr_topk_ex(vp(1), 2, 100, None, None, 128, vp(1), None, ctypes.byref(opt), None) == -1
         assert L.radix_topk_ex(vp(1), 2, 100, None, 128, vp(1), None, ctypes.byref(opt), None) == -1
+        assert L.gvr_topk_ex_noalloc(vp(1), 2, 100, None, None, 128, vp(1), None, ctypes.byref(opt), None) == -1
+    # the allocation-free entry point checks its arguments like gvr_topk_ex
+    assert L.gvr_topk_ex_noalloc(vp(1), 2, 100, None, None, 0, vp(1), None, None, None) == -2
+    assert L.gvr_topk_ex_noalloc(None, 2, 100, None, None, 16, vp(1), None, None, None) == -1
+    assert L.gvr_topk_ex_noalloc(None, 0, 100, None, None, 16, None, None, None, None) == 0
 
 
 def test_python_binding_refuses_cpu_tensors():
