@@ -112,6 +112,7 @@ constexpr int kRefBins1 = 2048;                // bins of the first refine level
 constexpr int kGuessSamples = 256;             // guessed indices gathered: a strided sample of prev_topk
 constexpr int kGuessBins = 1024;               // bins of the gathered-key histogram (16 per lane of wave 0)
 static_assert(kRefBins1 + kGuessBins <= kRefBins, "guess histogram above the first refine level");
+static_assert(kRefBins1 == gvr_host::kSlotHistBins, "a workspace slot holds one part's first refine level");
 constexpr int kSpecQuantile = 65;              // T_spec: gathered key of rank ceil(65 / 2048 * sample size)
 constexpr int kSmall = 64;                     // refine: K-th key's bin resolved by one wave up to this size
 constexpr int kMaxPasses = 8;                  // 2 + at most 4 narrowing passes + 1 final pass suffice
@@ -141,6 +142,7 @@ struct Params {
     int32_t* part_count; // [rows][S] f(threshold) of each part, bit 31 = a wave list overflowed
     uint32_t* part_thresh; // [rows][S] threshold of each part's list (T_spec, the same in every part)
     int32_t* part_wcnt;  // [rows][S][kSlotWaves] list length of each wave of each part
+    int32_t* part_hist;  // [rows][S][kRefBins1] each part's first refine level over [T_spec, pmax]
     uint64_t* part_list; // [rows][S][kPartCap] (fp32 bits | index << 32) of each part
 };
 
@@ -266,10 +268,17 @@ constexpr int kBufWord3 = 0x00020000;   // 32-bit data format, no swizzle
 DEV __amdgpu_buffer_rsrc_t row_rsrc(const void* base, int bytes) {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, kBufWord3);
 }
-DEV float4 buf_load16(__amdgpu_buffer_rsrc_t r, int off) {
-    const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+// 16-byte buffer load with the non-temporal hint: a streamed row is read
+// once, and the hint keeps it from displacing reused lines.
+constexpr int kCpolNT = 2;
+DEV float4 buf_load16_nt(__amdgpu_buffer_rsrc_t r, int off) {
+    const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kCpolNT);
     return make_float4(__uint_as_float(v.x), __uint_as_float(v.y), __uint_as_float(v.z), __uint_as_float(v.w));
 }
+// Device-scope loads of what other workgroups published (they skip the
+// vector L1).
+DEV int ld_agent(const int32_t* p) { return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
+DEV uint64_t ld_agent(const uint64_t* p) { return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
 // Byte offset of an LDS object (its address in the LDS aperture).
 DEV uint32_t lds_addr(const void* p) {
     return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)p;
@@ -288,21 +297,33 @@ DEV int add_lane_bit(int q, uint64_t m) {
 }
 
 // ------------------------------------------------------------------ LDS
+// List segments: the candidate list is a sequence of segments in index order
+// (the waves of one part, then the next part's), segment j held at
+// list[seg_off[j] .. + seg_cnt[j]). Wave w handles segments w, w + NW, ...
+// (nq of them): one per wave for a row held by one workgroup, one per part
+// after a split row's merge.
+template <int NW>
+struct SegCount {
+    static constexpr int value = NW * (NW == kNWLong ? kMaxParts : 1);
+};
 template <int NW>
 struct Smem {
-    uint2 list[Shape<NW>::kCap];                   // candidates (key, index), per-wave segments
+    uint2 list[Shape<NW>::kCap];                   // candidates (key, index), in segments
     union alignas(16) {
         int hist[NW][kBinsX];          // wave-private counting histograms
         int rhist[kRefBins];            // refine / guess histogram
     } u;
     int F[kBinsX + 1];                  // F[j] = f(edge j) over the row
-    int seg_off[NW];                   // list segment of each wave
-    int seg_cnt[NW];
+    int seg_off[SegCount<NW>::value];
+    int seg_cnt[SegCount<NW>::value];
+    int sga[SegCount<NW>::value];       // per-segment counts (keys > T, keys == T), then exclusive offsets
+    int sgb[SegCount<NW>::value];
     int wa[NW];
     int wb[NW];
     int red[4][NW];
     float redf[NW];
     int scal[8];
+    int nq;                             // segments per wave
     int guess_ready;                    // set by wave 0 once T_spec is in scal[4..7]
 };
 // Passes over the lists read four 64-entry chunks at a time, up to 255
@@ -392,22 +413,56 @@ DEV void block_keys(const float4& v, uint32_t (&k)[4]) {
 }
 
 // ------------------------------------------------------------------ refine
+// Exclusive offsets of the per-segment counts sga[] and sgb[] over the nseg
+// segments (in place), by wave 0; the totals go to scal[5] and scal[6].
+template <int NW>
+DEV void seg_scan(Smem<NW>& sm, int nseg, int lane) {
+    constexpr int PER = (SegCount<NW>::value + kWave - 1) / kWave;
+    int a[PER], b[PER];
+    int sa = 0, sb = 0;
+#pragma unroll
+    for (int r = 0; r < PER; ++r) {
+        const int j = lane * PER + r;
+        a[r] = j < nseg ? sm.sga[j] : 0;
+        b[r] = j < nseg ? sm.sgb[j] : 0;
+        sa += a[r];
+        sb += b[r];
+    }
+    const int ia = wave_incl_scan(sa, lane), ib = wave_incl_scan(sb, lane);
+    int ra = ia - sa, rb = ib - sb;
+#pragma unroll
+    for (int r = 0; r < PER; ++r) {
+        const int j = lane * PER + r;
+        if (j < nseg) {
+            sm.sga[j] = ra;
+            sm.sgb[j] = rb;
+        }
+        ra += a[r];
+        rb += b[r];
+    }
+    if (lane == kWave - 1) {
+        sm.scal[5] = ia;
+        sm.scal[6] = ib;
+    }
+}
+
 // Exact K-th key among the listed candidates. The K-th key lies in
-// [wlo, whi]; `above` listed candidates lie above whi. Wave w's list segment
-// is list[seg_off[w] .. + seg_cnt[w]).
+// [wlo, whi]; `above` listed candidates lie above whi.
 template <int NW>
 DEV uint32_t refine_kth(Smem<NW>& sm, uint32_t wlo, uint32_t whi, int above, int K, int tid) {
     using W = Shape<NW>;
     const int lane = tid & 63, wave = tid >> 6;
+    const int nq = sm.nq;
     int need = K - above;   // >= 1
     for (int level = 0; level < 4 && wlo != whi; ++level) {
         const uint64_t width = (uint64_t)whi - wlo + 1;
         const uint32_t s = bin_shift(width, log2i(kRefBins));
         for (int i = tid; i < kRefBins; i += W::kBlock) sm.u.rhist[i] = 0;
         lds_barrier();
-        {
-            const uint2* seg = sm.list + sm.seg_off[wave];
-            const int cnt = sm.seg_cnt[wave];
+        for (int q = 0; q < nq; ++q) {
+            const int j = wave + NW * q;
+            const uint2* seg = sm.list + sm.seg_off[j];
+            const int cnt = sm.seg_cnt[j];
             for (int i = lane; i < cnt; i += kWave) {
                 const uint32_t kk = seg[i].x;
                 if (kk >= wlo && kk <= whi)
@@ -453,36 +508,37 @@ DEV uint32_t refine_kth(Smem<NW>& sm, uint32_t wlo, uint32_t whi, int above, int
     return wlo;
 }
 
-// Emission: this wave's list segment holds `gb` keys > T and `eb` keys == T
-// in the segments before it; write every key > T and the first `take` keys
-// == T (list order = index order) at their ranks: ascending index output.
+// Emission of segment j: the segments before it hold `gb` keys > T and `eb`
+// keys == T; write every key > T and the first `take` keys == T (list order =
+// index order) at their ranks: ascending index output.
 template <int NW>
-DEV void emit_segment(const Smem<NW>& sm, uint32_t T, int K, int take, int gb, int eb, int32_t* out, int lane, int wave) {
-    const uint2* seg = sm.list + sm.seg_off[wave];
-    const int cnt = sm.seg_cnt[wave];
+DEV void emit_segment(const Smem<NW>& sm, int j, uint32_t T, int K, int take, int gb, int eb, int32_t* out,
+                      int lane) {
+    const uint2* seg = sm.list + sm.seg_off[j];
+    const int cnt = sm.seg_cnt[j];
     for (int i0 = 0; i0 < cnt; i0 += 4 * kWave) {
         const int rem = cnt - i0;
         uint2 en[4];   // four entries per lane read before any is written out
 #pragma unroll
-        for (int j = 0; j < 4; ++j) en[j] = seg[i0 + j * kWave + lane];   // past the count: masked below
+        for (int c = 0; c < 4; ++c) en[c] = seg[i0 + c * kWave + lane];   // past the count: masked below
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const uint64_t vm = first_lanes(rem - j * kWave);   // valid lanes
-            const uint32_t kk = en[j].x;
+        for (int c = 0; c < 4; ++c) {
+            const uint64_t vm = first_lanes(rem - c * kWave);   // valid lanes
+            const uint32_t kk = en[c].x;
             const uint64_t mg = __ballot(kk > T) & vm, me = __ballot(kk == T) & vm;
             const bool fg = (mg >> lane) & 1, fe = (me >> lane) & 1;
             const int g = gb + (int)lanes_below(mg, 0);
             if (me == 0) {   // no key == T here (wave-uniform): keys > T go after min(eb, take) ties
                 const int o = g + min(eb, take);
-                if (fg && o < K) out[o] = (int)en[j].y;
+                if (fg && o < K) out[o] = (int)en[c].y;
             } else {
                 const int e = eb + (int)lanes_below(me, 0);
                 if (fg) {
                     const int o = g + min(e, take);
-                    if (o >= 0 && o < K) out[o] = (int)en[j].y;
+                    if (o >= 0 && o < K) out[o] = (int)en[c].y;
                 } else if (fe && e < take) {
                     const int o = g + e;
-                    if (o >= 0 && o < K) out[o] = (int)en[j].y;
+                    if (o >= 0 && o < K) out[o] = (int)en[c].y;
                 }
             }
             gb += __popcll(mg);
@@ -491,31 +547,55 @@ DEV void emit_segment(const Smem<NW>& sm, uint32_t T, int K, int take, int gb, i
     }
 }
 
+// Every wave emits its segments at the offsets in sga / sgb (after seg_scan).
+template <int NW>
+DEV void emit_segments(const Smem<NW>& sm, uint32_t T, int K, int take, int32_t* out, int lane, int wave) {
+    for (int q = 0; q < sm.nq; ++q) {
+        const int j = wave + NW * q;
+        emit_segment(sm, j, T, K, take, sm.sga[j], sm.sgb[j], out, lane);
+    }
+}
+
 // Write the selection from the lists: every key > T, then the first `take`
 // keys == T in list (= index) order; output in ascending index order.
 template <int NW>
 DEV void emit_from_lists(Smem<NW>& sm, uint32_t T, int K, int32_t* out, int tid, int* n_gt_out) {
     const int lane = tid & 63, wave = tid >> 6;
-    const uint2* seg = sm.list + sm.seg_off[wave];
-    const int cnt = sm.seg_cnt[wave];
-    int gt = 0, eq = 0;
-    for (int i = lane; i < cnt; i += kWave) {
-        const uint32_t kk = seg[i].x;
-        gt += kk > T;
-        eq += kk == T;
-    }
-    gt = wave_sum(gt);
-    eq = wave_sum(eq);
-    if (lane == 0) {
-        sm.wa[wave] = gt;
-        sm.wb[wave] = eq;
+    const int nq = sm.nq;
+    for (int q = 0; q < nq; ++q) {
+        const int j = wave + NW * q;
+        const uint2* seg = sm.list + sm.seg_off[j];
+        const int cnt = sm.seg_cnt[j];
+        int gt = 0, eq = 0;
+        for (int i = lane; i < cnt; i += kWave) {
+            const uint32_t kk = seg[i].x;
+            gt += kk > T;
+            eq += kk == T;
+        }
+        gt = wave_sum(gt);
+        eq = wave_sum(eq);
+        if (lane == 0) {
+            sm.sga[j] = gt;
+            sm.sgb[j] = eq;
+        }
     }
     lds_barrier();
-    const int gb = sum_over_waves_below(sm.wa, lane, wave);
-    const int eb = sum_over_waves_below(sm.wb, lane, wave);
-    const int gtot = sum_over_waves<NW>(sm.wa, lane);
-    emit_segment(sm, T, K, K - gtot, gb, eb, out, lane, wave);
+    if (wave == 0) seg_scan(sm, NW * nq, lane);
+    lds_barrier();
+    const int gtot = sm.scal[5];
+    emit_segments(sm, T, K, K - gtot, out, lane, wave);
     *n_gt_out = gtot;
+}
+
+// f(key) for every listed entry of this wave's segments (lane-strided).
+template <int NW, typename F>
+DEV void for_my_keys(const Smem<NW>& sm, int wave, int lane, F&& f) {
+    for (int q = 0; q < sm.nq; ++q) {
+        const int j = wave + NW * q;
+        const uint2* seg = sm.list + sm.seg_off[j];
+        const int cnt = sm.seg_cnt[j];
+        for (int i = lane; i < cnt; i += kWave) f(seg[i].x);
+    }
 }
 
 // The paper's Phase 4 (Sec. 4.2.4), kept as an option for comparison with
@@ -539,14 +619,12 @@ template <int NW>
 DEV uint32_t paper_refine_emit(Smem<NW>& sm, int K, int32_t* out, int tid, int* n_gt_out, int* snaps_out) {
     using W = Shape<NW>;
     const int lane = tid & 63, wave = tid >> 6;
-    const uint2* seg = sm.list + sm.seg_off[wave];
-    const int cnt = sm.seg_cnt[wave];
     // (4a) min / max
     uint32_t mn = 0xFFFFFFFFu, mx = 0u;
-    for (int i = lane; i < cnt; i += kWave) {
-        mn = min(mn, seg[i].x);
-        mx = max(mx, seg[i].x);
-    }
+    for_my_keys(sm, wave, lane, [&](uint32_t kk) {
+        mn = min(mn, kk);
+        mx = max(mx, kk);
+    });
     mn = wave_min_u(mn);
     mx = wave_max_u(mx);
     if (lane == 0) {
@@ -559,9 +637,9 @@ DEV uint32_t paper_refine_emit(Smem<NW>& sm, int K, int32_t* out, int tid, int* 
     const uint32_t kmax = wave_max_u(lane < NW ? (uint32_t)sm.red[3][lane] : 0u);
     // (4b) histogram over [kmin, kmax]
     const uint32_t sh = bin_shift((uint64_t)kmax - kmin + 1, log2i(kPaperBins));
-    for (int i = lane; i < cnt; i += kWave)
-        __hip_atomic_fetch_add(&sm.u.rhist[(seg[i].x - kmin) >> sh], 1, __ATOMIC_RELAXED,
-                               __HIP_MEMORY_SCOPE_WORKGROUP);
+    for_my_keys(sm, wave, lane, [&](uint32_t kk) {
+        __hip_atomic_fetch_add(&sm.u.rhist[(kk - kmin) >> sh], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    });
     lds_barrier();
     constexpr int kPerWave = kPaperBins / NW;   // wave w holds bins [top - kPerWave (w + 1), top - kPerWave w)
     {
@@ -604,13 +682,12 @@ DEV uint32_t paper_refine_emit(Smem<NW>& sm, int K, int32_t* out, int tid, int* 
         ++snaps;
         int ge = 0, gt = 0;
         uint32_t up = 0xFFFFFFFFu, down = 0u;
-        for (int i = lane; i < cnt; i += kWave) {
-            const uint32_t kk = seg[i].x;
+        for_my_keys(sm, wave, lane, [&](uint32_t kk) {
             ge += kk >= T;
             gt += kk > T;
             if (kk > T) up = min(up, kk);
             if (kk < T) down = max(down, kk);
-        }
+        });
         ge = wave_sum(ge);
         gt = wave_sum(gt);
         up = wave_min_u(up);
@@ -685,30 +762,29 @@ DEV void keys_in_place(Smem<NW>& sm, uint2* seg, int cnt, bool hist, uint32_t rl
 // level of kRefBins1 bins over [rlo, bin_hi] (keys in (bin_hi, rhi] count in
 // the top bin; built here unless `hist_ready`), then wave 0 finds the
 // bin b holding the K-th key with two wave scans. If b holds at most kSmall
-// candidates, the waves copy them (with their wave) to a small LDS array and
-// count their keys above b; wave 0 takes one candidate per lane, selects T*
-// among them and the per-wave emission offsets, and every wave emits its
-// segment.
+// candidates, the waves copy them (with their segment) to a small LDS array
+// and count their keys above b per segment; wave 0 takes one candidate per
+// lane, selects T* among them and the per-segment emission offsets, and every
+// wave emits its segments.
 // Otherwise histogram narrowing (refine_kth) continues inside b.
 template <int NW>
 DEV uint32_t refine_emit(Smem<NW>& sm, uint32_t rlo, uint32_t rhi, uint32_t bin_hi, int above, int K, int32_t* out,
                          int tid, int* n_gt_out, bool hist_ready) {
     using W = Shape<NW>;
     const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const uint2* seg = sm.list + sm.seg_off[wave];
-    const int cnt = sm.seg_cnt[wave];
+    const int nq = sm.nq;
     const uint32_t sh = ref_shift(rlo, bin_hi);
     int* hb = sm.u.rhist;
-    if (tid == 0) sm.scal[1] = 0;
+    if (tid == 0) sm.scal[1] = 0;   // ordered before its atomics by the barrier after the bin search
     if (!hist_ready) {
         for (int i = tid; i < kRefBins1; i += W::kBlock) hb[i] = 0;
         lds_barrier();
-        for (int i = lane; i < cnt; i += kWave) {
-            const uint32_t kk = seg[i].x;
+        for_my_keys(sm, wave, lane, [&](uint32_t kk) {
             if (kk >= rlo && kk <= rhi) ref_hist_add(sm, kk, rlo, sh);
-        }
+        });
+        lds_barrier();
     }
-    lds_barrier();
+    // (a ready histogram is complete behind the caller's last barrier)
     const int need0 = K - above;   // >= 1: rank of T* among the keys in [rlo, rhi], from the top
     if (wave == 0) {
         // lane l owns bins [32 l, 32 l + 32)
@@ -755,38 +831,43 @@ DEV uint32_t refine_emit(Smem<NW>& sm, uint32_t rlo, uint32_t rhi, uint32_t bin_
         emit_from_lists(sm, kth, K, out, tid, n_gt_out);
         return kth;
     }
-    // Copy bin b's candidates, with their wave, to one small LDS array over
+    // Copy bin b's candidates, with their segment, to one small LDS array over
     // the histogram (no longer needed; at most kSmall of them): a chunk that
     // holds some (rare) reserves room with one LDS atomic. Each wave counts
-    // its keys above the bin.
+    // its segments' keys above the bin.
     uint4* const small = reinterpret_cast<uint4*>(sm.u.rhist);
     const uint32_t wid = hi_b - lo_b;
-    int gtl = 0;
-    for (int i0 = 0; i0 < cnt; i0 += 4 * kWave) {
-        const int rem = cnt - i0;
-        uint2 en[4];
+    for (int q = 0; q < nq; ++q) {
+        const int j = wave + NW * q;
+        const uint2* seg = sm.list + sm.seg_off[j];
+        const int cnt = sm.seg_cnt[j];
+        int gtl = 0;
+        for (int i0 = 0; i0 < cnt; i0 += 4 * kWave) {
+            const int rem = cnt - i0;
+            uint2 en[4];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) en[j] = seg[i0 + j * kWave + lane];   // past the count: masked below
+            for (int c = 0; c < 4; ++c) en[c] = seg[i0 + c * kWave + lane];   // past the count: masked below
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const uint64_t vm = first_lanes(rem - j * kWave);   // valid lanes
-            gtl = add_lane_bit(gtl, __ballot(en[j].x > hi_b) & vm);
-            const uint64_t m = __ballot(en[j].x - lo_b <= wid) & vm;
-            if (m) {   // rare (wave-uniform)
-                int base = 0;
-                if (lane == 0)
-                    base = __hip_atomic_fetch_add(&sm.scal[1], (int)__popcll(m), __ATOMIC_RELAXED,
-                                                  __HIP_MEMORY_SCOPE_WORKGROUP);
-                base = __builtin_amdgcn_readfirstlane(base);
-                const int pos = base + (int)lanes_below(m, 0);
-                if (((m >> lane) & 1) && pos < kSmall) small[pos] = make_uint4(en[j].x, en[j].y, (uint32_t)wave, 0u);
+            for (int c = 0; c < 4; ++c) {
+                const uint64_t vm = first_lanes(rem - c * kWave);   // valid lanes
+                gtl = add_lane_bit(gtl, __ballot(en[c].x > hi_b) & vm);
+                const uint64_t m = __ballot(en[c].x - lo_b <= wid) & vm;
+                if (m) {   // rare (wave-uniform)
+                    int base = 0;
+                    if (lane == 0)
+                        base = __hip_atomic_fetch_add(&sm.scal[1], (int)__popcll(m), __ATOMIC_RELAXED,
+                                                      __HIP_MEMORY_SCOPE_WORKGROUP);
+                    base = __builtin_amdgcn_readfirstlane(base);
+                    const int pos = base + (int)lanes_below(m, 0);
+                    if (((m >> lane) & 1) && pos < kSmall) small[pos] = make_uint4(en[c].x, en[c].y, (uint32_t)j, 0u);
+                }
             }
         }
-    }
-    const int gt_hi = wave_sum(gtl);
-    if (lane == 0) {
-        sm.wa[wave] = gt_hi;
-        sm.wb[wave] = 0;
+        const int gt_hi = wave_sum(gtl);
+        if (lane == 0) {
+            sm.sga[j] = gt_hi;
+            sm.sgb[j] = 0;
+        }
     }
     lds_barrier();
     if (wave == 0) {
@@ -810,27 +891,17 @@ DEV uint32_t refine_emit(Smem<NW>& sm, uint32_t rlo, uint32_t rhi, uint32_t bin_
         }
         const uint64_t hitk = __ballot(v && gt < need && ge >= need);
         const uint32_t kth = __builtin_amdgcn_readlane(mine.x, hitk ? (int)__builtin_ctzll(hitk) : 0);
-        // Per wave: keys > T* (above the bin, plus the bin's) and == T*;
-        // each candidate adds itself to its wave's counts.
-        if (v && mine.x > kth) __hip_atomic_fetch_add(&sm.wa[mine.z], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-        if (v && mine.x == kth) __hip_atomic_fetch_add(&sm.wb[mine.z], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-        const int gw = lane < NW ? sm.wa[lane] : 0;
-        const int ew = lane < NW ? sm.wb[lane] : 0;
-        const int gi = wave_incl_scan(gw, lane), ei = wave_incl_scan(ew, lane);
-        const int gtot = __builtin_amdgcn_readlane(gi, 63);
-        if (lane < NW) {
-            sm.red[0][lane] = gi - gw;
-            sm.red[1][lane] = ei - ew;
-        }
-        if (lane == 0) {
-            sm.scal[0] = (int)kth;
-            sm.scal[2] = gtot;
-        }
+        // Per segment: keys > T* (above the bin, plus the bin's) and == T*;
+        // each candidate adds itself to its segment's counts.
+        if (v && mine.x > kth) __hip_atomic_fetch_add(&sm.sga[mine.z], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        if (v && mine.x == kth) __hip_atomic_fetch_add(&sm.sgb[mine.z], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        seg_scan(sm, NW * nq, lane);
+        if (lane == 0) sm.scal[0] = (int)kth;
     }
     lds_barrier();
     const uint32_t kth = (uint32_t)sm.scal[0];
-    const int gtot = sm.scal[2];
-    emit_segment(sm, kth, K, K - gtot, sm.red[0][wave], sm.red[1][wave], out, lane, wave);
+    const int gtot = sm.scal[5];
+    emit_segments(sm, kth, K, K - gtot, out, lane, wave);
     *n_gt_out = gtot;
     return kth;
 }
@@ -872,7 +943,11 @@ DEV void topk_body(const Params& p) {
     const int part = slot - row_i * S;
     if (row_i >= p.rows) return;   // padding slot of the XCD-aligned grid
     const int64_t row = row_i;
-    const int64_t t0 = stamp();
+    // Phase stamps are taken only when row stats are asked for: a clock read
+    // is a scalar memory operation, and the next LDS wait would wait for it.
+    const bool timed = p.stats != nullptr;
+    auto tstamp = [&]() -> int64_t { return timed ? stamp() : (int64_t)0; };
+    const int64_t t0 = tstamp();
 
     // Wave 0 samples the guess: every st_g-th entry of prev_topk (at most
     // kGuessSamples of them). The sample indices go out with the row length;
@@ -957,6 +1032,7 @@ DEV void topk_body(const Params& p) {
     uint32_t tthr = 0u;      // threshold of the speculative lists
     bool overflow = false;
     if (tid < NW) sm.seg_off[tid] = tid * W::kCapW;
+    if (tid == 0) sm.nq = 1;
 
     if (spec) {
         if (!all_mode) {
@@ -972,7 +1048,9 @@ DEV void topk_body(const Params& p) {
         const __amdgpu_buffer_rsrc_t rrow = row_rsrc(xa, nq * 16);
         const int lane16 = lane * 16, qlast16 = qlast * 16;
         const int off_last = (sqb + max(nsl - 1, 0) * 64) * 16;   // the wave's last slab
-        auto slab_load = [&](int s) { return buf_load16(rrow, min(lane16 + min((sqb + s * 64) * 16, off_last), qlast16)); };
+        auto slab_load = [&](int s) {
+            return buf_load16_nt(rrow, min(lane16 + min((sqb + s * 64) * 16, off_last), qlast16));
+        };
         float4 buf[kSU];
         if (nsl > 0) {
 #pragma unroll
@@ -1051,7 +1129,7 @@ DEV void topk_body(const Params& p) {
                     jsel = __builtin_amdgcn_readlane(jsel, L);
                     ts = mn + ((uint32_t)(L * 16 + jsel) << sh);
                 }
-                if (S == 1) {   // the refine's first level, filled after the pass
+                {   // the refine's first level, filled after the pass
                     int4* r4 = reinterpret_cast<int4*>(sm.u.rhist) + lane * (kRefBins1 / 4 / kWave);
 #pragma unroll
                     for (int j = 0; j < kRefBins1 / 4 / kWave; ++j) r4[j] = make_int4(0, 0, 0, 0);
@@ -1096,7 +1174,7 @@ DEV void topk_body(const Params& p) {
             gsum = sm.redf[0];
             if (gvalid == 0) have_prev = false;   // no usable guess: the pass keeps (almost) nothing
         }
-        t1 = stamp();
+        t1 = tstamp();
         tspec = max(tspec, 1u);
         const SpecTest test = make_spec_test(tspec);
         // Slab s of this wave is the row's slab sg = sqb / 64 + s; slabs
@@ -1174,19 +1252,29 @@ DEV void topk_body(const Params& p) {
         else
             spec_pass(std::false_type{});
 
-        // Every wave turns its list into keys in place and, for a whole row,
-        // adds them to the refine's first histogram level over
-        // [T_spec, max(pmax, T_spec)] (cleared by wave 0 before its flag):
-        // waves done with their slabs do this while the others still stream.
-        const bool own_hist = S == 1 && !all_mode;
+        // Every wave turns its list into keys in place and adds them to the
+        // refine's first histogram level over [T_spec, max(pmax, T_spec)]
+        // (cleared by wave 0 before its flag): waves done with their slabs
+        // do this while the others still stream. A part of a split row also
+        // publishes the wave's list and its length right away (no wait): the
+        // row's last part may merge it.
+        const bool own_hist = !all_mode;
         if (cnt_w <= W::kCapW) keys_in_place(sm, lw, cnt_w, own_hist, tspec, ref_shift(tspec, max(gmax, tspec)), lane);
+        if (S > 1) {
+            const int64_t slot = row * S + part;
+            if (cnt_w <= W::kCapW) {
+                uint64_t* pl = p.part_list + slot * kPartCap + wave * W::kCapW;
+                for (int i = lane; i < cnt_w; i += kWave) pl[i] = pack_entry(lw[i].x, lw[i].y);
+            }
+            if (lane == 0) p.part_wcnt[slot * kSlotWaves + wave] = cnt_w;
+        }
         if (lane == 0) {
             sm.wa[wave] = cnt_w;
             sm.seg_cnt[wave] = min(cnt_w, W::kCapW);
         }
         passes = 1;
         lds_barrier();
-        t2 = stamp();   // every wave of the part has streamed its slabs
+        t2 = tstamp();   // every wave of the part has streamed its slabs
         overflow = wave_max_u(lane < NW ? (uint32_t)sm.wa[lane] : 0u) > (uint32_t)W::kCapW;
         f_spec = overflow ? -1 : sum_over_waves<NW>(sm.wa, lane);
         hist_ready = own_hist && !overflow;
@@ -1272,40 +1360,25 @@ DEV void topk_body(const Params& p) {
         }
 
         if (S > 1) {
-            // ---------------- publish this part; the last part of the row goes on.
-            // The parts of a row are launched on one XCD (the grid mapping),
-            // so they share its L2: a part's plain stores have reached that
-            // L2 once they complete (the vector L1 writes through), and the
-            // last part reads them back from it. The arrival word, updated by
-            // a device-scope atomic, also counts the parts per XCD (5 bits per
-            // XCD above 16 bits of arrivals): the last part uses the lists
-            // only if every part ran on its XCD, and otherwise reads the
-            // whole row itself. A plain load by the last part cannot hit a
-            // stale vector-L1 line: this workgroup never read those lines
-            // before, and each launch starts with invalidated L1s.
-            uint64_t* plist = p.part_list + (row * S + part) * (int64_t)kPartCap;
-            const bool publish = !overflow && f_spec <= cap;
-            if (publish) {   // this part's entries, in index order
-                const int off = sum_over_waves_below(sm.wa, lane, wave);
-                const uint2* seg = sm.list + wave * W::kCapW;
-                const int cnt = sm.seg_cnt[wave];
-                for (int i0 = 0; i0 < cnt; i0 += 4 * kWave) {
-                    uint2 e[4];
-#pragma unroll
-                    for (int j = 0; j < 4; ++j) {
-                        const int i = i0 + j * kWave + lane;
-                        e[j] = seg[i];   // past the count: not published
-                    }
-#pragma unroll
-                    for (int j = 0; j < 4; ++j) {
-                        const int i = i0 + j * kWave + lane;
-                        if (i < cnt) plist[off + i] = pack_entry(e[j].x, e[j].y);
-                    }
-                }
-            }
+            // ---------------- the part's count; the last part of the row goes on.
+            // The waves published their lists and list lengths as they
+            // finished. The parts of a row are launched on one XCD (the grid
+            // mapping), so they share its L2: a part's plain stores have
+            // reached that L2 once they complete (the vector L1 writes
+            // through), and the last part reads them back from it with
+            // device-scope loads, which do not use its L1. The arrival word,
+            // updated by a device-scope atomic after the stores completed,
+            // also counts the parts per XCD (5 bits per XCD above 16 bits of
+            // arrivals): the last part uses the lists only if every part ran
+            // on its XCD, and otherwise reads the whole row itself.
+            const int64_t slot0 = row * S;
             if (tid == 0) {
-                p.part_count[row * S + part] = (int32_t)((uint32_t)max(f_spec, 0) | (overflow ? 0x80000000u : 0u));
-                p.part_thresh[row * S + part] = tthr;
+                p.part_count[slot0 + part] = (int32_t)((uint32_t)max(f_spec, 0) | (overflow ? 0x80000000u : 0u));
+                p.part_thresh[slot0 + part] = tthr;
+            }
+            if (own_hist) {   // this part's first refine level, as bin pairs
+                uint64_t* ph = reinterpret_cast<uint64_t*>(p.part_hist + (slot0 + part) * kRefBins1);
+                for (int i = tid; i < kRefBins1 / 2; i += W::kBlock) ph[i] = reinterpret_cast<const uint64_t*>(sm.u.rhist)[i];
             }
             __builtin_amdgcn_s_waitcnt(0);   // this wave's stores have completed (reached L2)
             __syncthreads();
@@ -1325,95 +1398,143 @@ DEV void topk_body(const Params& p) {
                 overflow = true;   // lists unusable: the fallback reads the whole row
                 f_spec = -1;
             } else {
-                // Up to four parts: each thread loads the first entries of
-                // every part's list (positions tid + j * W::kBlock, j < kSpecJ)
-                // together with the counts, before it knows which of them
-                // exist: one round trip for the usual lists.
-                const int kSpecJ = S <= 2 ? 2 : 1;
-                const bool spec_ld = S <= 4;
-                uint64_t ev[4] = {0ull, 0ull, 0ull, 0ull};
-                if (spec_ld) {
+                // One round trip: every part's count and threshold (lane q of
+                // every wave: part q), the length of list segment `wave` of
+                // every part, and the first entries of that segment of the
+                // other parts, loaded before it is known how many exist: d
+                // chunks of 64 entries per lane for each of the first
+                // `covered` other parts.
+                const int c_tot = lane < S ? ld_agent(p.part_count + slot0 + lane) : 0;
+                const uint32_t tp = lane < S ? (uint32_t)ld_agent((const int32_t*)p.part_thresh + slot0 + lane) : 0u;
+                const int c_w = lane < S ? ld_agent(p.part_wcnt + (slot0 + lane) * kSlotWaves + wave) : 0;
+                const int others = S - 1;
+                const int d = others == 1 ? 4 : (others <= 4 ? 2 : 1);
+                const int covered = min(others, 8 / d);
+                uint64_t ev[8];
 #pragma unroll
-                    for (int k = 0; k < 4; ++k) {
-                        const int q = kSpecJ == 2 ? k >> 1 : k, j = kSpecJ == 2 ? k & 1 : 0;
-                        if (q < S) ev[k] = p.part_list[(row * S + q) * (int64_t)kPartCap + tid + j * W::kBlock];
+                for (int k = 0; k < 8; ++k) {
+                    const int oq = k / d, e = k - oq * d;
+                    const int q = oq < part ? oq : oq + 1;
+                    ev[k] = oq < covered ? ld_agent(p.part_list + (slot0 + q) * kPartCap + wave * W::kCapW + e * kWave + lane)
+                                         : 0ull;
+                }
+                // The other parts' first refine levels: bin pair tid of each
+                // (one 8-byte load per part, all in this round trip).
+                constexpr int kHPairs = kRefBins1 / 2;
+                constexpr int kHPer = (kHPairs + W::kBlock - 1) / W::kBlock;   // bin pairs per thread
+                uint64_t hv[kMaxParts - 1][kHPer];
+                const bool sum_hist = !all_mode && kHPer == 1;
+#pragma unroll
+                for (int k = 0; k < kMaxParts - 1; ++k) {
+                    const int q = k < part ? k : k + 1;
+#pragma unroll
+                    for (int r = 0; r < kHPer; ++r) {
+                        const int i = tid + r * W::kBlock;
+                        hv[k][r] = (sum_hist && k < others && i < kHPairs)
+                                       ? ld_agent(reinterpret_cast<const uint64_t*>(p.part_hist + (slot0 + q) * kRefBins1) + i)
+                                       : 0ull;
                     }
                 }
-                // Totals and part offsets of the merged list (parts in index
-                // order). Every part computes the same T_spec from the same
-                // data; a part that kept another threshold (or overflowed)
-                // sends the row to the fallback.
-                const int c = lane < S ? p.part_count[row * S + lane] : 0;
-                const uint32_t tp = lane < S ? p.part_thresh[row * S + lane] : 0u;
-                const bool ovf = wave_max_u(lane < S && c < 0 ? 1u : 0u) != 0u;
+                // Totals of the row. Every part computes the same T_spec from
+                // the same data; a part that kept another threshold (or
+                // overflowed) sends the row to the fallback.
+                const bool ovf = wave_max_u(lane < S && c_tot < 0 ? 1u : 0u) != 0u;
                 const uint32_t trow = wave_max_u(tp);
                 const bool mixed = wave_min_u(lane < S ? tp : 0xFFFFFFFFu) != trow;
-                const int cc = c & 0x7FFFFFFF;
-                f_spec = wave_sum(cc);
+                f_spec = wave_sum(c_tot & 0x7FFFFFFF);
                 overflow = ovf || mixed;
                 tthr = trow;
-                const int coff = wave_incl_scan(cc, lane) - cc;
                 if (!overflow && f_spec >= K && f_spec <= cap) {
-                    // Merged list in LDS, split evenly over the waves; the
-                    // refine's first histogram level is built on the way.
+                    // Segment (q, w) of the merged list: part q's wave w. The
+                    // own part's segments stay where its waves wrote them;
+                    // each wave appends the other parts' segment `wave` after
+                    // its own, if its list slot holds them all (the usual
+                    // case), and adds their keys to the refine's first level.
+                    const int own_c = sm.seg_cnt[wave];
+                    const int cw_o = (lane < S && lane != part) ? c_w : 0;
+                    const int ex = wave_incl_scan(cw_o, lane) - cw_o;   // lane q: other parts' entries before part q
+                    const int tot_w = own_c + __builtin_amdgcn_readlane(ex + cw_o, kWave - 1);
+                    if (lane == 0) sm.wa[wave] = tot_w;
+                    lds_barrier();
+                    const bool fits = wave_max_u(lane < NW ? (uint32_t)sm.wa[lane] : 0u) <= (uint32_t)W::kCapW;
                     const uint32_t msh = ref_shift(trow, max(gmax, trow));
-                    for (int i = tid; i < kRefBins1; i += W::kBlock) sm.u.rhist[i] = 0;
-                    lds_barrier();   // the histogram is cleared; the loads stay in flight
+                    // The refine's first level over the merged list: the own
+                    // part's (built during the stream) plus the other parts'
+                    // published ones; with another workgroup shape, each
+                    // merged entry is added to it.
+                    const bool add_hist = !all_mode && !sum_hist;
                     auto put = [&](int P, uint64_t e) {
                         sm.list[P] = make_uint2((uint32_t)e, (uint32_t)(e >> 32));
-                        ref_hist_add(sm, (uint32_t)e, trow, msh);
+                        if (add_hist) ref_hist_add(sm, (uint32_t)e, trow, msh);
                     };
-                    if (spec_ld) {
+                    if (fits) {
+                        if (sum_hist && tid < kHPairs) {
+                            int sx = 0, sy = 0;
 #pragma unroll
-                        for (int k = 0; k < 4; ++k) {
-                            const int q = kSpecJ == 2 ? k >> 1 : k, j = kSpecJ == 2 ? k & 1 : 0;
-                            const int cq = __builtin_amdgcn_readlane(cc, min(q, S - 1)), oq = __builtin_amdgcn_readlane(coff, min(q, S - 1));
-                            const int i = tid + j * W::kBlock;
-                            if (q < S && i < cq) put(oq + i, ev[k]);
+                            for (int k = 0; k < kMaxParts - 1; ++k) {
+                                sx += (int)(uint32_t)hv[k][0];
+                                sy += (int)(uint32_t)(hv[k][0] >> 32);
+                            }
+                            int2* h2 = reinterpret_cast<int2*>(sm.u.rhist) + tid;
+                            const int2 o = *h2;
+                            *h2 = make_int2(o.x + sx, o.y + sy);
                         }
-                        // entries past the first kSpecJ * W::kBlock of a part (rare)
+                        if (lane < S) {
+                            const int j = lane * NW + wave;
+                            sm.seg_off[j] = wave * W::kCapW + (lane == part ? 0 : own_c + ex);
+                            sm.seg_cnt[j] = lane == part ? own_c : c_w;
+                        }
+#pragma unroll
+                        for (int k = 0; k < 8; ++k) {
+                            const int oq = k / d, e = k - oq * d;
+                            if (oq < covered) {
+                                const int q = oq < part ? oq : oq + 1;
+                                const int cq = __builtin_amdgcn_readlane(c_w, q);
+                                const int i = e * kWave + lane;
+                                if (i < cq) put(wave * W::kCapW + own_c + __builtin_amdgcn_readlane(ex, q) + i, ev[k]);
+                            }
+                        }
+                        // entries past the speculative chunks (rare)
                         for (int q = 0; q < S; ++q) {
-                            const int cq = __builtin_amdgcn_readlane(cc, q), oq = __builtin_amdgcn_readlane(coff, q);
-                            const uint64_t* src = p.part_list + (row * S + q) * (int64_t)kPartCap;
-                            for (int i = kSpecJ * W::kBlock + tid; i < cq; i += W::kBlock) put(oq + i, src[i]);
+                            if (q == part) continue;
+                            const int oq = q < part ? q : q - 1;
+                            const int cq = __builtin_amdgcn_readlane(c_w, q);
+                            const int base = wave * W::kCapW + own_c + __builtin_amdgcn_readlane(ex, q);
+                            const uint64_t* src = p.part_list + (slot0 + q) * kPartCap + wave * W::kCapW;
+                            for (int i = (oq < covered ? d * kWave : 0) + lane; i < cq; i += kWave)
+                                put(base + i, ld_agent(src + i));
                         }
+                        hist_ready = !all_mode;
                     } else {
-                        // Each thread owns merged positions tid + j * W::kBlock
-                        // and loads four of them (from their parts' lists)
-                        // before it stores any.
-                        const int jn = (f_spec + W::kBlock - 1) / W::kBlock;
-                        for (int j0 = 0; j0 < jn; j0 += 4) {
-                            int qj[4] = {0, 0, 0, 0}, oj[4] = {0, 0, 0, 0};
-                            for (int q = 1; q < S; ++q) {
-                                const int bq = __builtin_amdgcn_readlane(coff, q);
-#pragma unroll
-                                for (int jj = 0; jj < 4; ++jj) {
-                                    const bool past = tid + (j0 + jj) * W::kBlock >= bq;
-                                    qj[jj] += past;
-                                    oj[jj] = past ? bq : oj[jj];
-                                }
+                        // Packed: segment (q, w) at the sum of the segments
+                        // before it, every part's entries (the own part's
+                        // too) copied from the workspace; the refine builds
+                        // its histogram itself.
+                        if (lane < S) {
+                            sm.sga[lane * NW + wave] = c_w;
+                            sm.sgb[lane * NW + wave] = 0;
+                        }
+                        lds_barrier();
+                        if (wave == 0) seg_scan(sm, S * NW, lane);
+                        lds_barrier();
+                        for (int q = 0; q < S; ++q) {
+                            const int j = q * NW + wave;
+                            const int cq = __builtin_amdgcn_readlane(c_w, q);
+                            const int base = sm.sga[j];
+                            const uint64_t* src = p.part_list + (slot0 + q) * kPartCap + wave * W::kCapW;
+                            for (int i = lane; i < cq; i += kWave) {
+                                const uint64_t e = ld_agent(src + i);
+                                sm.list[base + i] = make_uint2((uint32_t)e, (uint32_t)(e >> 32));
                             }
-                            uint64_t e[4];
-#pragma unroll
-                            for (int jj = 0; jj < 4; ++jj) {
-                                const int P = tid + (j0 + jj) * W::kBlock;
-                                e[jj] = P < f_spec ? p.part_list[(row * S + qj[jj]) * (int64_t)kPartCap + (P - oj[jj])] : 0ull;
-                            }
-#pragma unroll
-                            for (int jj = 0; jj < 4; ++jj) {
-                                const int P = tid + (j0 + jj) * W::kBlock;
-                                if (P < f_spec) put(P, e[jj]);
+                            if (lane == 0) {
+                                sm.seg_off[j] = base;
+                                sm.seg_cnt[j] = cq;
                             }
                         }
+                        hist_ready = false;
                     }
-                    hist_ready = true;
-                    const int chunk = (f_spec + NW - 1) / NW;
-                    if (tid < NW) {
-                        const int o = min(tid * chunk, f_spec);
-                        sm.seg_off[tid] = o;
-                        sm.seg_cnt[tid] = min(chunk, f_spec - o);
-                    }
-                    lds_barrier();   // every wave reads its new segment bounds after this
+                    if (tid == 0) sm.nq = S;
+                    lds_barrier();   // every wave reads the merged segment table after this
                 }
             }
             // Ready for the next call (issued after the loads above).
@@ -1421,10 +1542,11 @@ DEV void topk_body(const Params& p) {
         }
     }
 
-    // The guess delivered (the usual case): refine the lists right away.
+    // The guess delivered (the usual case): refine the lists right away (the
+    // lists, their segment table and the histogram are complete behind the
+    // last barrier).
     if (spec && !all_mode && !overflow && f_spec >= K && f_spec <= cap) {
-        lds_barrier();
-        const int64_t t3f = stamp();
+        const int64_t t3f = tstamp();
         int ngt = 0;
         int snaps = 0;
         const uint32_t kth = p.paper_refine
@@ -1571,7 +1693,7 @@ DEV void topk_body(const Params& p) {
         gsum = 0.f;
         for (int v = 0; v < NW; ++v) gsum += sm.redf[v];   // fixed order
         __syncthreads();
-        t1 = stamp();
+        t1 = tstamp();
         // f(T) over the row (per-wave counts kept in sm.wa for the collect);
         // the first pass also finds the row's smallest and largest key.
         auto count_ge = [&](uint32_t tk, bool minmax) {
@@ -1661,7 +1783,7 @@ DEV void topk_body(const Params& p) {
         }
         (void)fl;
         (void)fh;
-        t2 = stamp();   // Phase 2 done (threshold accepted, or the search gave up)
+        t2 = tstamp();   // Phase 2 done (threshold accepted, or the search gave up)
         if (sec_ok) {
             // Phase 3: collect every key >= T at per-wave offsets from the
             // last pass's per-wave counts (sm.wa), in index order.
@@ -1725,12 +1847,10 @@ DEV void topk_body(const Params& p) {
         above = 0;
         if (all_mode) {   // no guess range: bin [min, max] of the (few) listed keys
             uint32_t mn = 0xFFFFFFFFu, mx = 0u;
-            uint2* seg = sm.list + sm.seg_off[wave];
-            const int cnt = sm.seg_cnt[wave];
-            for (int i = lane; i < cnt; i += kWave) {
-                mn = min(mn, seg[i].x);
-                mx = max(mx, seg[i].x);
-            }
+            for_my_keys(sm, wave, lane, [&](uint32_t kk) {
+                mn = min(mn, kk);
+                mx = max(mx, kk);
+            });
             mn = wave_min_u(mn);
             mx = wave_max_u(mx);
             if (lane == 0) {
@@ -1879,7 +1999,7 @@ DEV void topk_body(const Params& p) {
             win = nw;
             count_pass();
         }
-        t2 = stamp();
+        t2 = tstamp();
     }
 
     if (ties) {
@@ -1917,7 +2037,7 @@ DEV void topk_body(const Params& p) {
         return;
     }
     lds_barrier();
-    t3 = stamp();
+    t3 = tstamp();
     // ---------------- (a5) refine the listed candidates and emit
     int ngt = 0;
     int snaps = 0;
@@ -1984,7 +2104,7 @@ gvr_host::WorkspaceCache<HipDev> g_workspaces;
 
 // Scratch of the allocation-free entry point: the split-row workspace of up
 // to kStaticSlots (row, part) slots (arrival words, counts, thresholds,
-// per-wave counts, 128 KB of lists per slot: 32 MiB) as one device array.
+// per-wave counts, histograms, 128 KB of lists per slot: 34 MiB) as one device array.
 // Each device that runs the library holds its own copy until the process
 // ends. Its arrival words are zero when the library is loaded, and every
 // launch leaves the words it used at zero again (the last part of a row
@@ -2064,6 +2184,7 @@ gvr_status run(const float* scores, int64_t B, int64_t ld, const int32_t* row_le
         q.part_count = ws.part_count;
         q.part_thresh = ws.part_thresh;
         q.part_wcnt = ws.part_wcnt;
+        q.part_hist = ws.part_hist;
         q.part_list = ws.part_list;
         const dim3 grid((unsigned)(rows_pad * parts));
         const hipStream_t hs = (hipStream_t)stream;
