@@ -111,6 +111,57 @@ def time_calls(fn, w, prevs, steps, warmup, out):
     return e0.elapsed_time(e1) / 1e3   # seconds
 
 
+def per_call_times(fn, w, prevs, calls, out, warm):
+    """Per-call GPU times (us) from HIP events around each call on its stream.
+    Cold: the calls cycle through steps 1..T-1 (1.6 GB of scores, more than
+    the last-level cache), so each reads rows from HBM. Warm: each step is
+    called twice back to back and the second call is timed (its rows were
+    just read, as right after the indexer wrote them)."""
+    import torch
+
+    T = w.scores.shape[0]
+    stream = torch.cuda.current_stream()
+    times = []
+    order = [1 + (i % (T - 1)) for i in range(calls)]
+    for t in order[:4]:
+        fn(w.scores[t], w.row_len[t], prevs[t], K_TOPK, out_idx=out, stream=stream)
+    torch.cuda.synchronize()
+    for t in order:
+        if warm:
+            fn(w.scores[t], w.row_len[t], prevs[t], K_TOPK, out_idx=out, stream=stream)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        fn(w.scores[t], w.row_len[t], prevs[t], K_TOPK, out_idx=out, stream=stream)
+        e1.record(stream)
+        e1.synchronize()
+        times.append(e0.elapsed_time(e1) * 1e3)
+    return order, times
+
+
+def summary(times):
+    import numpy as np
+    a = np.asarray(times)
+    return {"p50_us": round(float(np.percentile(a, 50)), 3), "p90_us": round(float(np.percentile(a, 90)), 3),
+            "mean_us": round(float(a.mean()), 3)}
+
+
+def read_floor(w, reps, prevs=None, out=None):
+    """The plain read rate of the same rows (gvr_read_floor: every element
+    read once with the Top-K's loads, nothing else), and gvr_topk's own time
+    measured the same way: per-launch GPU time from a replayed HIP graph of
+    the launches for steps 1..T-1 (no host launch overhead in either)."""
+    import torch
+    import paper_2604_22312_amd as g
+
+    words = torch.empty((w.rows, 16), dtype=torch.int32, device=w.scores.device)
+
+    def floor(scores, row_len, prev, K, out_idx=None, stream=None):
+        return g.gvr_read_floor(scores, row_len, out_words=words, stream=stream)
+    fl = time_graph(floor, w, prevs if prevs is not None else [None] * w.scores.shape[0], reps, out) * 1e6
+    gv = time_graph(g.gvr_topk, w, prevs, reps, out) * 1e6 if prevs is not None else None
+    return fl, gv
+
+
 def pass_stats(fn_ex, w, prevs, radix, options=None):
     import numpy as np
     import paper_2604_22312_amd as g
@@ -132,35 +183,44 @@ def pass_stats(fn_ex, w, prevs, radix, options=None):
             "candidates_mean": round(float(c.mean()), 1)}
 
 
-def cpu_baseline(w, outs, min_seconds=15.0, max_steps=8):
-    """The oracle, as it is, on a bounded sample of the same rows: the rows
-    of the first `max_steps` timed decode steps, cycled until `min_seconds`
-    of CPU work have been done. Its answers for those steps are also compared
-    with the GPU's (`outs`), row by row."""
+def cpu_baseline(w, outs, repeats=5, steps_all=4, rows_one=32):
+    """The oracle, as it is, on a bounded sample of the same rows, timed on
+    the host: with one thread per host core (os.cpu_count()) over the rows of
+    `steps_all` decode steps, and with one thread over `rows_one` of those
+    rows; each the median of `repeats` runs (steady clock, generation and
+    copies outside the timing). The answers for the sampled steps are
+    compared with the GPU's (`outs`) row by row."""
     import numpy as np
     import oracle
 
-    threads = min(16, os.cpu_count() or 1)
+    cores = os.cpu_count() or 1
     T = w.scores.shape[0]
-    steps = list(range(1, min(T, 1 + max_steps)))
+    steps = list(range(1, min(T, 1 + steps_all)))
     host = [(w.scores[t].cpu().numpy(), w.row_len[t].cpu().numpy()) for t in steps]
-    rows_done = calls = 0
-    t0 = time.time()
-    while True:
-        s, rl = host[calls % len(host)]
-        exp, _, _ = oracle.topk(s, K_TOPK, row_len=rl, threads=threads)
-        if calls < len(host) and not np.array_equal(exp, outs[steps[calls]].cpu().numpy()):
-            raise SystemExit("bench: GPU Top-K differs from the oracle at step %d" % steps[calls])
-        rows_done += s.shape[0]
-        calls += 1
-        dt = time.time() - t0
-        if dt >= min_seconds:
-            break
-    return {"value": round(rows_done / dt, 1), "unit": "rows/s", "cores": threads, "kind": "oracle",
-            "sample": "%d calls cycling over %d decode steps x %d rows of the same workload (%d rows; "
-                      "qsort by key, ties by index; rows split over %d threads; the answers of the %d "
-                      "steps equal the GPU's); %.1f s"
-                      % (calls, len(host), w.rows, rows_done, threads, min(calls, len(host)), dt)}
+    for t, (s, rl) in zip(steps, host):
+        exp, _, _ = oracle.topk(s, K_TOPK, row_len=rl, threads=cores)
+        if not np.array_equal(exp, outs[t].cpu().numpy()):
+            raise SystemExit("bench: GPU Top-K differs from the oracle at step %d" % t)
+
+    def timed(threads, sample):
+        runs = []
+        for _ in range(repeats):
+            t0 = time.perf_counter()
+            rows = 0
+            for s, rl in sample:
+                oracle.topk(s, K_TOPK, row_len=rl, threads=threads)
+                rows += s.shape[0]
+            runs.append(rows / (time.perf_counter() - t0))
+        return float(np.median(runs)), rows
+
+    all_rate, all_rows = timed(cores, host)
+    one_rate, one_rows = timed(1, [(host[0][0][:rows_one], host[0][1][:rows_one])])
+    return {"value": round(all_rate, 1), "unit": "rows/s", "cores": cores, "kind": "oracle",
+            "one_thread": {"value": round(one_rate, 1), "unit": "rows/s", "cores": 1},
+            "sample": "median of %d runs each: %d rows (%d decode steps x %d rows of the same workload) on %d "
+                      "threads, and %d rows on 1 thread; qsort by (key desc, index asc) per row; the oracle's "
+                      "answers for the sampled steps equal the GPU's"
+                      % (repeats, all_rows, len(host), w.rows, cores, one_rows)}
 
 
 def time_graph(fn, w, prevs, reps, out):
@@ -730,14 +790,31 @@ def main():
                        "algorithmic_bytes_per_launch": alg_bytes,
                        "avg_launch_us": round(per * 1e6, 3)}
     res["passes_per_row"] = pass_stats(g.gvr_topk_ex, w, prevs, radix=False)
+    calls = max(args.steps, 30)
+    order, cold = per_call_times(g.gvr_topk, w, prevs, calls, out, warm=False)
+    _, warm = per_call_times(g.gvr_topk, w, prevs, calls, out, warm=True)
+    res["per_call"] = {"calls": calls, "cold": summary(cold), "warm": summary(warm)}
+    fl_us, gv_us = read_floor(w, 4, prevs, out)
+    res["read_floor"] = {"kernel": "gvr_read_floor (every element of the rows read once, nothing computed)",
+                         "timing": "per launch from a replayed HIP graph of the launches for every step",
+                         "us_per_launch": round(fl_us, 3), "GBs": round(4 * int(rl1.sum()) / fl_us / 1e3, 1),
+                         "frac_of_peak": round(4 * int(rl1.sum()) / fl_us / 1e3 / PEAK_HBM_GBS, 4),
+                         "gvr_topk_us_same_timing": round(gv_us, 3),
+                         "gvr_over_floor": round(gv_us / fl_us, 3)}
     if not args.no_radix:
         rsecs = time_calls(g.radix_topk, w, prevs, args.steps, args.warmup, out)
         rper = rsecs / args.steps
+        _, rcold = per_call_times(g.radix_topk, w, prevs, calls, out, warm=False)
         res["radix_topk"] = {"value": round(rows * args.steps / rsecs, 1), "unit": "rows/s",
                              "ms_per_step": round(rper * 1e3, 5),
                              "achieved_GBs": round(alg_bytes / rper / 1e9, 1),
+                             "per_call_cold": summary(rcold),
                              "passes_per_row": pass_stats(g.radix_topk_ex, w, prevs, radix=True)}
+        ratios = [r / c for r, c in zip(rcold, cold)]
         res["speedup_vs_radix"] = round(rper / per, 3)
+        res["speedup_vs_radix_forms"] = {"ratio_of_means": round(sum(rcold) / sum(cold), 3),
+                                         "mean_of_per_call_ratios": round(sum(ratios) / len(ratios), 3),
+                                         "calls": calls}
     if not args.no_secant:
         # The paper's schedule (T0 = pmean, secant counting passes, collect
         # pass) on the same rows: same answers, reported for comparison.

@@ -16,7 +16,8 @@
  *
  * Result definition, shared by both entry points:
  *   - n = clamp(row_len[b], 0, ld); only scores[b*ld + 0 .. b*ld + n) are used
- *     (loads never leave the 16-byte-aligned blocks holding those elements).
+ *     (loads never leave the 128-byte-aligned lines holding those elements,
+ *     so they never touch a page the row does not).
  *   - Order: each fp32 bit pattern u maps to the 32-bit key
  *       (u & 0x80000000) ? ~u : (u | 0x80000000)
  *     compared as unsigned, i.e. -NaN < -inf < ... < -0.0 < +0.0 < ... <
@@ -212,6 +213,19 @@ gvr_status gvr_topk_ex_noalloc(const float* scores, int64_t B, int64_t ld, const
 gvr_status radix_topk_ex(const float* scores, int64_t B, int64_t ld, const int32_t* row_len,
                          int32_t K, int32_t* out_idx, void* stream, const gvr_options* options,
                          gvr_row_stats* stats);
+
+/* Measurement helper, not a step of the Top-K: reads every element of
+ * scores[b][0, n_b) once (n_b = clamp(row_len[b], 0, ld), row_len NULL = ld)
+ * with the same 16-byte non-temporal loads the Top-K streams with, computing
+ * nothing but an xor of the bits: the plain read rate of the rows, the
+ * ceiling of the Top-K's streaming pass. out_words [B][16] uint32 (device):
+ * row b's part p writes word p and the unused words are zeroed, so the xor of
+ * a row's 16 words is the xor of its elements' bit patterns. One launch on
+ * `stream`; no allocation. Errors: GVR_ERR_INVALID_ARG (negative sizes, NULL
+ * pointers with B > 0), GVR_ERR_TOO_LONG (ld > 2^31 - 16 or B > 2^26),
+ * GVR_ERR_HIP. */
+gvr_status gvr_read_floor(const float* scores, int64_t B, int64_t ld, const int32_t* row_len,
+                          uint32_t* out_words, void* stream);
 
 /* Human-readable name of a status code (static string). */
 const char* gvr_status_string(gvr_status status);

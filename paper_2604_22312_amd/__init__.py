@@ -33,6 +33,7 @@ from .binding import (  # noqa: F401
     gvr_indexer_topk,
     gvr_rope_g,
     gvr_rope_params,
+    gvr_read_floor,
     gvr_rope_prior,
     gvr_topk,
     gvr_topk_ex,

@@ -73,6 +73,8 @@ def lib():
         L.gvr_indexer_topk.restype = ctypes.c_int
         L.gvr_indexer_topk.argtypes = [vp, vp, vp, vp, i64, i32, i32, i32, i64, vp, vp, vp, i32, vp, vp,
                                        ctypes.POINTER(Options), vp]
+        L.gvr_read_floor.restype = ctypes.c_int
+        L.gvr_read_floor.argtypes = [vp, i64, i64, vp, vp, vp]
         L.gvr_status_string.restype = ctypes.c_char_p
         L.gvr_status_string.argtypes = [ctypes.c_int]
         L.gvr_version.restype = ctypes.c_char_p
@@ -325,3 +327,27 @@ def gvr_indexer_topk(q, w, k, k_scale, row_len, prev_topk, K, scores=None, out_i
     if st != 0:
         raise GvrError("gvr_indexer_topk", st)
     return out_idx, scores
+
+
+def gvr_read_floor(scores, row_len=None, out_words=None, stream=None):
+    """Measurement helper: read every element of each row once (the plain
+    read rate of the rows). Returns ``out_words`` [B][16] uint32 as int32;
+    the xor of a row's 16 words is the xor of its elements' bits."""
+    if not isinstance(scores, torch.Tensor) or scores.dtype != torch.float32 or scores.dim() != 2:
+        raise ValueError("scores must be a float32 tensor [B][ld]")
+    if not scores.is_cuda or not scores.is_contiguous():
+        raise ValueError("scores must be a contiguous tensor on a GPU (there is no CPU path)")
+    B, ld = scores.shape
+    if row_len is not None and (row_len.dtype != torch.int32 or row_len.shape != (B,)
+                                or row_len.device != scores.device or not row_len.is_contiguous()):
+        raise ValueError("row_len must be a contiguous int32 tensor [B] on the scores' device")
+    if out_words is None:
+        out_words = torch.empty((B, 16), dtype=torch.int32, device=scores.device)
+    elif (out_words.dtype != torch.int32 or out_words.shape != (B, 16) or out_words.device != scores.device
+          or not out_words.is_contiguous()):
+        raise ValueError("out_words must be a contiguous int32 tensor [B][16] on the scores' device")
+    with torch.cuda.device(scores.device):
+        st = lib().gvr_read_floor(_ptr(scores), B, ld, _ptr(row_len), _ptr(out_words), _stream(stream, scores.device))
+    if st != 0:
+        raise GvrError("gvr_read_floor", st)
+    return out_words

@@ -7,7 +7,7 @@ import sys
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
-SOURCES = [os.path.join(PKG, "csrc", f) for f in ("gvr_topk.hip", "rope_prior.hip", "indexer.hip")]
+SOURCES = [os.path.join(PKG, "csrc", f) for f in ("gvr_topk.hip", "rope_prior.hip", "indexer.hip", "read_floor.hip")]
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libgvr_topk.so")
 ARCH = "gfx950"

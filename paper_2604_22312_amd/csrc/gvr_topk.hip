@@ -993,9 +993,11 @@ DEV void topk_body(const Params& p) {
     }
 
     // Float4 blocks of the row (virtual index = element index + aoff, so a
-    // block is one aligned 16-byte load); slabs of 64 blocks. Full-row share
-    // of each wave (count / collect passes): [qb, qe).
-    const int aoff = (int)(((uintptr_t)x >> 2) & 3);
+    // block is one aligned 16-byte load and a slab of 64 blocks is eight
+    // whole 128-byte lines: the first block starts the row's first line,
+    // which never leaves the page holding the row's first element). Full-row
+    // share of each wave (count / collect passes): [qb, qe).
+    const int aoff = (int)(((uintptr_t)x >> 2) & 31);   // slabs start on 128-byte lines
     const float4* xa = reinterpret_cast<const float4*>(x - aoff);
     const int nq = (n + aoff + 3) >> 2;
     const int qlast = nq - 1;
@@ -1372,8 +1374,11 @@ DEV void topk_body(const Params& p) {
             // arrivals): the last part uses the lists only if every part ran
             // on its XCD, and otherwise reads the whole row itself.
             const int64_t slot0 = row * S;
+            // The part's exact f(T_spec): every wave counted past its list's
+            // capacity, so the sum is exact even after an overflow (bit 31).
+            const int f_part = sum_over_waves<NW>(sm.wa, lane);
             if (tid == 0) {
-                p.part_count[slot0 + part] = (int32_t)((uint32_t)max(f_spec, 0) | (overflow ? 0x80000000u : 0u));
+                p.part_count[slot0 + part] = (int32_t)((uint32_t)f_part | (overflow ? 0x80000000u : 0u));
                 p.part_thresh[slot0 + part] = tthr;
             }
             if (own_hist) {   // this part's first refine level, as bin pairs

@@ -99,6 +99,16 @@ def test_options_validation(L):
     assert L.gvr_topk_ex_noalloc(None, 0, 100, None, None, 16, None, None, None, None) == 0
 
 
+def test_read_floor_validation(L):
+    vp = ctypes.c_void_p
+    assert L.gvr_read_floor(None, 0, 100, None, None, None) == 0
+    assert L.gvr_read_floor(vp(1), -1, 100, None, vp(1), None) == -1
+    assert L.gvr_read_floor(vp(1), 2, -1, None, vp(1), None) == -1
+    assert L.gvr_read_floor(None, 2, 100, None, vp(1), None) == -1
+    assert L.gvr_read_floor(vp(1), 2, 100, None, None, None) == -1
+    assert L.gvr_read_floor(vp(1), 2, 1 << 40, None, vp(1), None) == -5
+
+
 def test_python_binding_refuses_cpu_tensors():
     import torch
     import paper_2604_22312_amd as g

@@ -755,3 +755,26 @@ def test_topk_captured_as_first_call(tmp_path):
     note("gvr_topk captured as the first call (subprocess)")
     r = subprocess.run([sys.executable, str(script), root], capture_output=True, text=True, timeout=240)
     assert r.returncode == 0 and r.stdout.strip().endswith("ok"), r.stdout + r.stderr
+
+
+def test_read_floor_reads_every_element_once():
+    """gvr_read_floor (the plain read-rate helper the bench reports beside the
+    Top-K): the xor of a row's 16 words equals the xor of the bit patterns of
+    its elements [0, n_b), for misaligned row starts, ragged lengths, empty
+    rows and batches that give a row 1 to 16 parts."""
+    import paper_2604_22312_amd as g
+    rng = np.random.default_rng(43)
+    for B, ld in ((1, 131071), (3, 70003), (128, 102463), (600, 5001)):
+        x = rng.standard_normal((B, ld)).astype(np.float32)
+        lens = rng.integers(0, ld + 1, B).astype(np.int32)
+        lens[0] = ld
+        if B > 2:
+            lens[1] = 0
+            lens[2] = 1
+        note("read floor B=%d ld=%d" % (B, ld))
+        words = g.gvr_read_floor(torch.from_numpy(x).to(DEV), torch.from_numpy(lens).to(DEV)).cpu().numpy()
+        got = np.bitwise_xor.reduce(words.view(np.uint32), axis=1)
+        bits = x.view(np.uint32)
+        exp = np.array([np.bitwise_xor.reduce(bits[b, :lens[b]]) if lens[b] > 0 else 0 for b in range(B)],
+                       dtype=np.uint32)
+        assert np.array_equal(got, exp), (B, ld)
