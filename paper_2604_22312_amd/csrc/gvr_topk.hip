@@ -112,7 +112,6 @@ constexpr int kRefBins1 = 2048;                // bins of the first refine level
 constexpr int kGuessSamples = 256;             // guessed indices gathered: a strided sample of prev_topk
 constexpr int kGuessBins = 1024;               // bins of the gathered-key histogram (16 per lane of wave 0)
 static_assert(kRefBins1 + kGuessBins <= kRefBins, "guess histogram above the first refine level");
-static_assert(kRefBins1 == gvr_host::kSlotHistBins, "a workspace slot holds one part's first refine level");
 constexpr int kSpecQuantile = 65;              // T_spec: gathered key of rank ceil(65 / 2048 * sample size)
 constexpr int kSmall = 64;                     // refine: K-th key's bin resolved by one wave up to this size
 constexpr int kMaxPasses = 8;                  // 2 + at most 4 narrowing passes + 1 final pass suffice
@@ -142,7 +141,6 @@ struct Params {
     int32_t* part_count; // [rows][S] f(threshold) of each part, bit 31 = a wave list overflowed
     uint32_t* part_thresh; // [rows][S] threshold of each part's list (T_spec, the same in every part)
     int32_t* part_wcnt;  // [rows][S][kSlotWaves] list length of each wave of each part
-    int32_t* part_hist;  // [rows][S][kRefBins1] each part's first refine level over [T_spec, pmax]
     uint64_t* part_list; // [rows][S][kPartCap] (fp32 bits | index << 32) of each part
 };
 
@@ -403,6 +401,27 @@ DEV void hist_add(int* hw, uint32_t k, bool in, uint32_t lo, uint32_t sh) {
     } else if (in) {
         __hip_atomic_fetch_add(&hw[b], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
     }
+}
+
+// Count key k (if `in`) into bin min((k - lo) >> sh, kBins) of a wave-private
+// histogram, for counting passes: the lanes of the (at most) two most common
+// bins of this instruction add with one atomic per bin (a window the data
+// crowds into few bins, and ties, would otherwise serialise on one LDS
+// address); the remaining lanes, spread over other bins, add one each.
+DEV void hist_add_peel(int* hw, uint32_t k, bool in, uint32_t lo, uint32_t sh, int lane) {
+    const uint32_t b = min((k - lo) >> sh, (uint32_t)kBins);
+    uint64_t act = __ballot(in);
+#pragma unroll
+    for (int it = 0; it < 2; ++it) {
+        if (!act) return;
+        const int first = (int)__builtin_ctzll(act);
+        const uint32_t lead = __builtin_amdgcn_readlane(b, first);
+        const uint64_t same = __ballot(b == lead) & act;
+        if (lane == first)
+            __hip_atomic_fetch_add(&hw[lead], (int)__popcll(same), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        act &= ~same;
+    }
+    if ((act >> lane) & 1) __hip_atomic_fetch_add(&hw[b], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 
 DEV void block_keys(const float4& v, uint32_t (&k)[4]) {
@@ -1290,6 +1309,7 @@ DEV void topk_body(const Params& p) {
             // part's slabs (just read, so L2-resident) collects them again at
             // exact per-wave offsets instead of narrowing from scratch.
             const int f_all = sum_over_waves<NW>(sm.wa, lane);
+            if (f_all < K || f_all > cap) f_spec = f_all;   // exact: the narrowing starts on the right side of T_spec
             if (f_all >= K && f_all <= cap) {
                 const int off = sum_over_waves_below(sm.wa, lane, wave);
                 const int mine = sm.wa[wave];
@@ -1381,10 +1401,6 @@ DEV void topk_body(const Params& p) {
                 p.part_count[slot0 + part] = (int32_t)((uint32_t)f_part | (overflow ? 0x80000000u : 0u));
                 p.part_thresh[slot0 + part] = tthr;
             }
-            if (own_hist) {   // this part's first refine level, as bin pairs
-                uint64_t* ph = reinterpret_cast<uint64_t*>(p.part_hist + (slot0 + part) * kRefBins1);
-                for (int i = tid; i < kRefBins1 / 2; i += W::kBlock) ph[i] = reinterpret_cast<const uint64_t*>(sm.u.rhist)[i];
-            }
             __builtin_amdgcn_s_waitcnt(0);   // this wave's stores have completed (reached L2)
             __syncthreads();
             if (tid == 0) {
@@ -1403,43 +1419,12 @@ DEV void topk_body(const Params& p) {
                 overflow = true;   // lists unusable: the fallback reads the whole row
                 f_spec = -1;
             } else {
-                // One round trip: every part's count and threshold (lane q of
-                // every wave: part q), the length of list segment `wave` of
-                // every part, and the first entries of that segment of the
-                // other parts, loaded before it is known how many exist: d
-                // chunks of 64 entries per lane for each of the first
-                // `covered` other parts.
+                // Round trip 1: every part's count and threshold (lane q of
+                // every wave: part q) and the length of list segment `wave`
+                // of every part.
                 const int c_tot = lane < S ? ld_agent(p.part_count + slot0 + lane) : 0;
                 const uint32_t tp = lane < S ? (uint32_t)ld_agent((const int32_t*)p.part_thresh + slot0 + lane) : 0u;
                 const int c_w = lane < S ? ld_agent(p.part_wcnt + (slot0 + lane) * kSlotWaves + wave) : 0;
-                const int others = S - 1;
-                const int d = others == 1 ? 4 : (others <= 4 ? 2 : 1);
-                const int covered = min(others, 8 / d);
-                uint64_t ev[8];
-#pragma unroll
-                for (int k = 0; k < 8; ++k) {
-                    const int oq = k / d, e = k - oq * d;
-                    const int q = oq < part ? oq : oq + 1;
-                    ev[k] = oq < covered ? ld_agent(p.part_list + (slot0 + q) * kPartCap + wave * W::kCapW + e * kWave + lane)
-                                         : 0ull;
-                }
-                // The other parts' first refine levels: bin pair tid of each
-                // (one 8-byte load per part, all in this round trip).
-                constexpr int kHPairs = kRefBins1 / 2;
-                constexpr int kHPer = (kHPairs + W::kBlock - 1) / W::kBlock;   // bin pairs per thread
-                uint64_t hv[kMaxParts - 1][kHPer];
-                const bool sum_hist = !all_mode && kHPer == 1;
-#pragma unroll
-                for (int k = 0; k < kMaxParts - 1; ++k) {
-                    const int q = k < part ? k : k + 1;
-#pragma unroll
-                    for (int r = 0; r < kHPer; ++r) {
-                        const int i = tid + r * W::kBlock;
-                        hv[k][r] = (sum_hist && k < others && i < kHPairs)
-                                       ? ld_agent(reinterpret_cast<const uint64_t*>(p.part_hist + (slot0 + q) * kRefBins1) + i)
-                                       : 0ull;
-                    }
-                }
                 // Totals of the row. Every part computes the same T_spec from
                 // the same data; a part that kept another threshold (or
                 // overflowed) sends the row to the fallback.
@@ -1450,96 +1435,62 @@ DEV void topk_body(const Params& p) {
                 overflow = ovf || mixed;
                 tthr = trow;
                 if (!overflow && f_spec >= K && f_spec <= cap) {
-                    // Segment (q, w) of the merged list: part q's wave w. The
-                    // own part's segments stay where its waves wrote them;
-                    // each wave appends the other parts' segment `wave` after
-                    // its own, if its list slot holds them all (the usual
-                    // case), and adds their keys to the refine's first level.
-                    const int own_c = sm.seg_cnt[wave];
-                    const int cw_o = (lane < S && lane != part) ? c_w : 0;
-                    const int ex = wave_incl_scan(cw_o, lane) - cw_o;   // lane q: other parts' entries before part q
-                    const int tot_w = own_c + __builtin_amdgcn_readlane(ex + cw_o, kWave - 1);
-                    if (lane == 0) sm.wa[wave] = tot_w;
-                    lds_barrier();
-                    const bool fits = wave_max_u(lane < NW ? (uint32_t)sm.wa[lane] : 0u) <= (uint32_t)W::kCapW;
-                    const uint32_t msh = ref_shift(trow, max(gmax, trow));
-                    // The refine's first level over the merged list: the own
-                    // part's (built during the stream) plus the other parts'
-                    // published ones; with another workgroup shape, each
-                    // merged entry is added to it.
-                    const bool add_hist = !all_mode && !sum_hist;
-                    auto put = [&](int P, uint64_t e) {
-                        sm.list[P] = make_uint2((uint32_t)e, (uint32_t)(e >> 32));
-                        if (add_hist) ref_hist_add(sm, (uint32_t)e, trow, msh);
-                    };
-                    if (fits) {
-                        if (sum_hist && tid < kHPairs) {
-                            int sx = 0, sy = 0;
-#pragma unroll
-                            for (int k = 0; k < kMaxParts - 1; ++k) {
-                                sx += (int)(uint32_t)hv[k][0];
-                                sy += (int)(uint32_t)(hv[k][0] >> 32);
-                            }
-                            int2* h2 = reinterpret_cast<int2*>(sm.u.rhist) + tid;
-                            const int2 o = *h2;
-                            *h2 = make_int2(o.x + sx, o.y + sy);
-                        }
-                        if (lane < S) {
-                            const int j = lane * NW + wave;
-                            sm.seg_off[j] = wave * W::kCapW + (lane == part ? 0 : own_c + ex);
-                            sm.seg_cnt[j] = lane == part ? own_c : c_w;
-                        }
-#pragma unroll
-                        for (int k = 0; k < 8; ++k) {
-                            const int oq = k / d, e = k - oq * d;
-                            if (oq < covered) {
-                                const int q = oq < part ? oq : oq + 1;
-                                const int cq = __builtin_amdgcn_readlane(c_w, q);
-                                const int i = e * kWave + lane;
-                                if (i < cq) put(wave * W::kCapW + own_c + __builtin_amdgcn_readlane(ex, q) + i, ev[k]);
-                            }
-                        }
-                        // entries past the speculative chunks (rare)
-                        for (int q = 0; q < S; ++q) {
-                            if (q == part) continue;
-                            const int oq = q < part ? q : q - 1;
-                            const int cq = __builtin_amdgcn_readlane(c_w, q);
-                            const int base = wave * W::kCapW + own_c + __builtin_amdgcn_readlane(ex, q);
-                            const uint64_t* src = p.part_list + (slot0 + q) * kPartCap + wave * W::kCapW;
-                            for (int i = (oq < covered ? d * kWave : 0) + lane; i < cq; i += kWave)
-                                put(base + i, ld_agent(src + i));
-                        }
-                        hist_ready = !all_mode;
-                    } else {
-                        // Packed: segment (q, w) at the sum of the segments
-                        // before it, every part's entries (the own part's
-                        // too) copied from the workspace; the refine builds
-                        // its histogram itself.
-                        if (lane < S) {
-                            sm.sga[lane * NW + wave] = c_w;
-                            sm.sgb[lane * NW + wave] = 0;
-                        }
-                        lds_barrier();
-                        if (wave == 0) seg_scan(sm, S * NW, lane);
-                        lds_barrier();
-                        for (int q = 0; q < S; ++q) {
-                            const int j = q * NW + wave;
-                            const int cq = __builtin_amdgcn_readlane(c_w, q);
-                            const int base = sm.sga[j];
-                            const uint64_t* src = p.part_list + (slot0 + q) * kPartCap + wave * W::kCapW;
-                            for (int i = lane; i < cq; i += kWave) {
-                                const uint64_t e = ld_agent(src + i);
-                                sm.list[base + i] = make_uint2((uint32_t)e, (uint32_t)(e >> 32));
-                            }
-                            if (lane == 0) {
-                                sm.seg_off[j] = base;
-                                sm.seg_cnt[j] = cq;
-                            }
-                        }
-                        hist_ready = false;
+                    // The merged list: every part's segments (the own part's
+                    // too, from the workspace) packed in (part, wave) order,
+                    // which is index order, then cut into one even segment
+                    // per wave, so that the refine walks NW segments whatever
+                    // the number of parts. Segment (q, w) starts at the sum
+                    // of the segments before it.
+                    if (lane < S) {
+                        sm.sga[lane * NW + wave] = c_w;
+                        sm.sgb[lane * NW + wave] = 0;
                     }
-                    if (tid == 0) sm.nq = S;
-                    lds_barrier();   // every wave reads the merged segment table after this
+                    lds_barrier();
+                    if (wave == 0) seg_scan(sm, S * NW, lane);
+                    lds_barrier();
+                    const int base_q = lane < S ? sm.sga[lane * NW + wave] : 0;   // lane q: start of segment (q, wave)
+                    // Round trip 2: wave w copies segments (q, w) of every
+                    // part q, entry t of their concatenation per lane (part
+                    // q holds t in [excl_q, incl_q)), four loads per lane in
+                    // flight. The other parts' keys join the refine's first
+                    // level, which holds the own part's already.
+                    const int incl = wave_incl_scan(c_w, lane);
+                    const int excl = incl - c_w;
+                    const int tot_w = __builtin_amdgcn_readlane(incl, kWave - 1);
+                    const uint32_t msh = ref_shift(trow, max(gmax, trow));
+                    const uint64_t* src_w = p.part_list + slot0 * kPartCap + wave * W::kCapW;
+                    for (int t0 = 0; t0 < tot_w; t0 += 4 * kWave) {
+                        uint64_t e[4];
+                        int dst[4], qs[4];
+#pragma unroll
+                        for (int c = 0; c < 4; ++c) {
+                            const int t = t0 + c * kWave + lane;
+                            int q = 0;
+#pragma unroll
+                            for (int r = 0; r < kMaxParts; ++r) q += (r < S && __builtin_amdgcn_readlane(incl, r) <= t);
+                            q = min(q, S - 1);
+                            const int i = t - __shfl(excl, q);
+                            dst[c] = __shfl(base_q, q) + i;
+                            qs[c] = q;
+                            e[c] = t < tot_w ? ld_agent(src_w + (int64_t)q * kPartCap + i) : 0ull;
+                        }
+#pragma unroll
+                        for (int c = 0; c < 4; ++c) {
+                            if (t0 + c * kWave + lane < tot_w) {
+                                sm.list[dst[c]] = make_uint2((uint32_t)e[c], (uint32_t)(e[c] >> 32));
+                                if (!all_mode && qs[c] != part) ref_hist_add(sm, (uint32_t)e[c], trow, msh);
+                            }
+                        }
+                    }
+                    hist_ready = !all_mode;
+                    const int chunk = (f_spec + NW - 1) / NW;
+                    if (tid < NW) {
+                        const int o = min(tid * chunk, f_spec);
+                        sm.seg_off[tid] = o;
+                        sm.seg_cnt[tid] = min(chunk, f_spec - o);
+                    }
+                    if (tid == 0) sm.nq = 1;
+                    lds_barrier();   // every wave reads the merged list, its segment table and histogram after this
                 }
             }
             // Ready for the next call (issued after the loads above).
@@ -1635,12 +1586,43 @@ DEV void topk_body(const Params& p) {
 #pragma unroll
             for (int c = 0; c < 4; ++c) {
                 const bool okc = !edge || (e0 + c >= 0 && e0 + c < n);
-                hist_add<true>(hw, k[c], okc && k[c] >= lo, lo, sh);
+                hist_add<false>(hw, k[c], okc && k[c] >= lo, lo, sh);
             }
         });
         ++passes;
         __syncthreads();
         compute_F();
+    };
+    // The smallest and largest key of the row, in one pass: a count window
+    // over the whole key range would crowd typical rows (values of a few
+    // binades) into two or three of its bins and need an extra pass; the
+    // first window spans [min, max] instead.
+    auto minmax_pass = [&]() {
+        uint32_t mn = 0xFFFFFFFFu, mx = 0u;
+        stream_wave(xa, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
+            uint32_t k[4];
+            block_keys(v, k);
+            const int e0 = 4 * q - aoff;
+            const bool edge = (4 * qs - aoff < 0 || 4 * qs + 255 - aoff >= n);
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const bool okc = !edge || (e0 + c >= 0 && e0 + c < n);
+                mn = okc ? min(mn, k[c]) : mn;
+                mx = okc ? max(mx, k[c]) : mx;
+            }
+        });
+        ++passes;
+        mn = wave_min_u(mn);
+        mx = wave_max_u(mx);
+        __syncthreads();
+        if (lane == 0) {
+            sm.red[2][wave] = (int)mn;
+            sm.red[3][wave] = (int)mx;
+        }
+        __syncthreads();
+        const uint32_t kmin = wave_min_u(lane < NW ? (uint32_t)sm.red[2][lane] : 0xFFFFFFFFu);
+        const uint32_t kmax = wave_max_u(lane < NW ? (uint32_t)sm.red[3][lane] : 0u);
+        win = make_window(kmin, max(kmin, kmax));
     };
 
     int path = all_mode ? GVR_PATH_ALL : (have_prev ? GVR_PATH_GUESS : GVR_PATH_NO_GUESS);
@@ -1867,18 +1849,23 @@ DEV void topk_body(const Params& p) {
             rhi = bin_hi = wave_max_u(lane < NW ? (uint32_t)sm.red[3][lane] : 0u);
         }
     } else {
+        bool whole_range = true;   // nothing bounds the K-th key yet
         if (secant) {
             // The secant search gave up: narrow inside its counted bracket.
             path = GVR_PATH_NARROWED;
             win = make_window(sec_lo, sec_hi - 1u);
+            whole_range = false;
         }
         if (spec) {
             // The guess fell short (or a wave's list overflowed): count passes
             // over the whole row around T_spec, whose f is known.
             if (path == GVR_PATH_GUESS) path = GVR_PATH_NARROWED;
-            if (f_spec >= 0)   // else: unknown (lists unusable or overflowed), count the whole key range
+            if (f_spec >= 0) {   // else: unknown (lists unusable or overflowed), count the whole key range
                 win = (f_spec < K) ? make_window(0u, tthr - 1u) : make_window(tthr, 0xFFFFFFFFu);
+                whole_range = false;
+            }
         }
+        if (whole_range) minmax_pass();   // the first window spans the row's [min, max]
         count_pass();
         for (;;) {
             const int j = crossing();
@@ -2109,7 +2096,7 @@ gvr_host::WorkspaceCache<HipDev> g_workspaces;
 
 // Scratch of the allocation-free entry point: the split-row workspace of up
 // to kStaticSlots (row, part) slots (arrival words, counts, thresholds,
-// per-wave counts, histograms, 128 KB of lists per slot: 34 MiB) as one device array.
+// per-wave counts, 128 KB of lists per slot: 32 MiB) as one device array.
 // Each device that runs the library holds its own copy until the process
 // ends. Its arrival words are zero when the library is loaded, and every
 // launch leaves the words it used at zero again (the last part of a row
@@ -2189,7 +2176,6 @@ gvr_status run(const float* scores, int64_t B, int64_t ld, const int32_t* row_le
         q.part_count = ws.part_count;
         q.part_thresh = ws.part_thresh;
         q.part_wcnt = ws.part_wcnt;
-        q.part_hist = ws.part_hist;
         q.part_list = ws.part_list;
         const dim3 grid((unsigned)(rows_pad * parts));
         const hipStream_t hs = (hipStream_t)stream;

@@ -109,11 +109,16 @@ def count_ge(xk: np.ndarray, t: int) -> int:
 
 
 def narrow(xk: np.ndarray, K: int, cap: int, lo: int, hi: int, passes: int):
-    """Count passes over 256-bin windows starting from [lo, hi]; returns
-    (outcome, passes, threshold, candidates)."""
+    """Count passes over 256-bin windows starting from [lo, hi] (from the
+    row's [min, max] after one min/max pass when nothing bounds the K-th key,
+    [lo, hi] = the whole key range); returns (outcome, passes, threshold,
+    candidates)."""
     def window(a, b):
         return a, bin_shift(b - a + 1, WINDOW_BINS_LG)
 
+    if lo == 0 and hi == 0xFFFFFFFF:
+        passes += 1
+        lo, hi = int(xk.min()), int(xk.max())
     wlo, ws = window(lo, hi)
     while True:
         passes += 1                                   # one count pass
@@ -170,9 +175,8 @@ def replay_row(x: np.ndarray, n: int, prev: np.ndarray | None, K: int, parts: in
             c = count_ge(xk[lo:hi], t) if hi > lo else 0
             overflow |= c > WAVE_CAP
             f += c
-    # a one-workgroup row reports -1 after a list overflow unless it collects
-    # again at packed offsets (K <= f <= C); split rows report the exact sum
-    res["spec_count"] = -1 if (overflow and parts == 1 and not K <= f <= cap) else f
+    # every wave counts past its list's capacity: f(T_spec) is exact on every path
+    res["spec_count"] = f
     path = "guess" if have_prev else "no_guess"
     if not overflow and K <= f <= cap:
         res.update(path=PATH[path], passes=1, threshold=t, candidates=f)
@@ -180,9 +184,7 @@ def replay_row(x: np.ndarray, n: int, prev: np.ndarray | None, K: int, parts: in
     if overflow and parts == 1 and K <= f <= cap:      # collected again at packed offsets
         res.update(path=PATH[path], passes=2, threshold=t, candidates=f)
         return res
-    if overflow and parts == 1:
-        lo, hi = 0, 0xFFFFFFFF                          # f unknown to the kernel
-    elif f < K:
+    if f < K:
         lo, hi = 0, t - 1
     else:
         lo, hi = t, 0xFFFFFFFF
