@@ -277,6 +277,13 @@ DEV float4 buf_load16_nt(__amdgpu_buffer_rsrc_t r, int off) {
 // vector L1).
 DEV int ld_agent(const int32_t* p) { return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
 DEV uint64_t ld_agent(const uint64_t* p) { return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
+// 16 bytes with the cache policy of those loads (device scope: sc1), from a
+// buffer resource: lanes past its end read zeros.
+constexpr int kCpolSC1 = 16;
+DEV int4 ld_agent16(__amdgpu_buffer_rsrc_t r, int off) {
+    const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kCpolSC1);
+    return make_int4((int)v.x, (int)v.y, (int)v.z, (int)v.w);
+}
 // Byte offset of an LDS object (its address in the LDS aperture).
 DEV uint32_t lds_addr(const void* p) {
     return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)p;
@@ -436,6 +443,19 @@ DEV void block_keys(const float4& v, uint32_t (&k)[4]) {
 // segments (in place), by wave 0; the totals go to scal[5] and scal[6].
 template <int NW>
 DEV void seg_scan(Smem<NW>& sm, int nseg, int lane) {
+    if (nseg <= kWave) {   // one segment per lane
+        const int a = lane < nseg ? sm.sga[lane] : 0, b = lane < nseg ? sm.sgb[lane] : 0;
+        const int ia = wave_incl_scan(a, lane), ib = wave_incl_scan(b, lane);
+        if (lane < nseg) {
+            sm.sga[lane] = ia - a;
+            sm.sgb[lane] = ib - b;
+        }
+        if (lane == kWave - 1) {
+            sm.scal[5] = ia;
+            sm.scal[6] = ib;
+        }
+        return;
+    }
     constexpr int PER = (SegCount<NW>::value + kWave - 1) / kWave;
     int a[PER], b[PER];
     int sa = 0, sb = 0;
@@ -780,12 +800,14 @@ DEV void keys_in_place(Smem<NW>& sm, uint2* seg, int cnt, bool hist, uint32_t rl
 // key lies in [rlo, rhi]; `above` listed keys lie above rhi. One histogram
 // level of kRefBins1 bins over [rlo, bin_hi] (keys in (bin_hi, rhi] count in
 // the top bin; built here unless `hist_ready`), then wave 0 finds the
-// bin b holding the K-th key with two wave scans. If b holds at most kSmall
-// candidates, the waves copy them (with their segment) to a small LDS array
-// and count their keys above b per segment; wave 0 takes one candidate per
-// lane, selects T* among them and the per-segment emission offsets, and every
-// wave emits its segments.
-// Otherwise histogram narrowing (refine_kth) continues inside b.
+// bin b holding the K-th key with two wave scans. One pass over the lists
+// counts each segment's keys above b. If b holds at most kSmall candidates,
+// the pass also copies them (with their segment) to a small LDS array; wave 0
+// takes one candidate per lane, selects T* among them and the per-segment
+// emission offsets, and every wave emits its segments. Otherwise the pass
+// finds b's smallest and largest candidate keys and its count per segment:
+// if they are one key, that key is T*; else histogram narrowing (refine_kth)
+// continues between them.
 template <int NW>
 DEV uint32_t refine_emit(Smem<NW>& sm, uint32_t rlo, uint32_t rhi, uint32_t bin_hi, int above, int K, int32_t* out,
                          int tid, int* n_gt_out, bool hist_ready) {
@@ -844,23 +866,23 @@ DEV uint32_t refine_emit(Smem<NW>& sm, uint32_t rlo, uint32_t rhi, uint32_t bin_
         emit_from_lists(sm, lo_b, K, out, tid, n_gt_out);
         return lo_b;
     }
-    if (cnt_b > kSmall) {
-        lds_barrier();
-        const uint32_t kth = refine_kth(sm, lo_b, hi_b, above_b, K, tid);
-        emit_from_lists(sm, kth, K, out, tid, n_gt_out);
-        return kth;
-    }
     // Copy bin b's candidates, with their segment, to one small LDS array over
-    // the histogram (no longer needed; at most kSmall of them): a chunk that
+    // the histogram (no longer needed; up to kSmall of them): a chunk that
     // holds some (rare) reserves room with one LDS atomic. Each wave counts
-    // its segments' keys above the bin.
+    // its segments' keys above the bin. A bin of more than kSmall candidates
+    // also gets its smallest and largest key and its count per segment: a bin
+    // whose candidates are all one key (ties, as in rounded scores) is
+    // resolved by this pass alone.
     uint4* const small = reinterpret_cast<uint4*>(sm.u.rhist);
+    uint32_t* const skey = reinterpret_cast<uint32_t*>(small + kSmall);   // their keys alone, for the rank
     const uint32_t wid = hi_b - lo_b;
+    const bool big = cnt_b > kSmall;
+    uint32_t bmin = 0xFFFFFFFFu, bmax = 0u;
     for (int q = 0; q < nq; ++q) {
         const int j = wave + NW * q;
         const uint2* seg = sm.list + sm.seg_off[j];
         const int cnt = sm.seg_cnt[j];
-        int gtl = 0;
+        int gtl = 0, inl = 0;
         for (int i0 = 0; i0 < cnt; i0 += 4 * kWave) {
             const int rem = cnt - i0;
             uint2 en[4];
@@ -872,40 +894,82 @@ DEV uint32_t refine_emit(Smem<NW>& sm, uint32_t rlo, uint32_t rhi, uint32_t bin_
                 gtl = add_lane_bit(gtl, __ballot(en[c].x > hi_b) & vm);
                 const uint64_t m = __ballot(en[c].x - lo_b <= wid) & vm;
                 if (m) {   // rare (wave-uniform)
-                    int base = 0;
-                    if (lane == 0)
-                        base = __hip_atomic_fetch_add(&sm.scal[1], (int)__popcll(m), __ATOMIC_RELAXED,
-                                                      __HIP_MEMORY_SCOPE_WORKGROUP);
-                    base = __builtin_amdgcn_readfirstlane(base);
-                    const int pos = base + (int)lanes_below(m, 0);
-                    if (((m >> lane) & 1) && pos < kSmall) small[pos] = make_uint4(en[c].x, en[c].y, (uint32_t)j, 0u);
+                    const bool in = (m >> lane) & 1;
+                    if (big) {
+                        inl += in;
+                        bmin = in ? min(bmin, en[c].x) : bmin;
+                        bmax = in ? max(bmax, en[c].x) : bmax;
+                    } else {
+                        int base = 0;
+                        if (lane == 0)
+                            base = __hip_atomic_fetch_add(&sm.scal[1], (int)__popcll(m), __ATOMIC_RELAXED,
+                                                          __HIP_MEMORY_SCOPE_WORKGROUP);
+                        base = __builtin_amdgcn_readfirstlane(base);
+                        const int pos = base + (int)lanes_below(m, 0);
+                        if (in && pos < kSmall) {
+                            small[pos] = make_uint4(en[c].x, en[c].y, (uint32_t)j, 0u);
+                            skey[pos] = en[c].x;
+                        }
+                    }
                 }
             }
         }
         const int gt_hi = wave_sum(gtl);
+        const int in_b = big ? wave_sum(inl) : 0;
         if (lane == 0) {
             sm.sga[j] = gt_hi;
-            sm.sgb[j] = 0;
+            sm.sgb[j] = in_b;
+        }
+    }
+    if (big) {
+        bmin = wave_min_u(bmin);
+        bmax = wave_max_u(bmax);
+        if (lane == 0) {
+            sm.wa[wave] = (int)bmin;
+            sm.wb[wave] = (int)bmax;
         }
     }
     lds_barrier();
+    if (big) {
+        uint32_t mn = 0xFFFFFFFFu, mx = 0u;
+#pragma unroll
+        for (int w = 0; w < NW; ++w) {
+            mn = min(mn, (uint32_t)sm.wa[w]);
+            mx = max(mx, (uint32_t)sm.wb[w]);
+        }
+        if (mn == mx) {   // every candidate of bin b is T* = mn: sga / sgb hold keys > T* / == T*
+            if (wave == 0) seg_scan(sm, NW * nq, lane);
+            lds_barrier();
+            const int gtot = sm.scal[5];
+            emit_segments(sm, mn, K, K - gtot, out, lane, wave);
+            *n_gt_out = gtot;
+            return mn;
+        }
+        // the K-th key lies in [mn, mx]; the listed keys above mx are those above the bin
+        const uint32_t kth = refine_kth(sm, mn, mx, above_b, K, tid);
+        emit_from_lists(sm, kth, K, out, tid, n_gt_out);
+        return kth;
+    }
     if (wave == 0) {
         // Lane l takes the l-th copied candidate (any order).
         const bool v = lane < cnt_b;
         const uint4 mine = v ? small[lane] : make_uint4(0u, 0u, 0u, 0u);
         // T* is the need-th largest of them: the key of a lane with fewer
-        // than `need` keys above it and at least `need` at or above it
-        // (every lane compares its key with each candidate's).
+        // than `need` keys above it and at least `need` at or above it. Every
+        // lane compares its key with each candidate's, four keys per LDS
+        // read (one address for the whole wave: a broadcast).
         const int need = K - above_b;   // rank of T* inside the bin, from the top
+        const uint4* sk4 = reinterpret_cast<const uint4*>(skey);
         int gt = 0, ge = 0;
+#pragma unroll 4
         for (int j0 = 0; j0 < cnt_b; j0 += 4) {
+            const uint4 kk = sk4[j0 >> 2];   // past cnt_b: masked below
+            const uint32_t a[4] = {kk.x, kk.y, kk.z, kk.w};
 #pragma unroll
             for (int jj = 0; jj < 4; ++jj) {
-                const int j = min(j0 + jj, cnt_b - 1);
-                const uint32_t kj = __builtin_amdgcn_readlane(mine.x, j);
                 const bool in = j0 + jj < cnt_b;
-                gt += in && kj > mine.x;
-                ge += in && kj >= mine.x;
+                gt += in && a[jj] > mine.x;
+                ge += in && a[jj] >= mine.x;
             }
         }
         const uint64_t hitk = __ballot(v && gt < need && ge >= need);
@@ -1419,12 +1483,25 @@ DEV void topk_body(const Params& p) {
                 overflow = true;   // lists unusable: the fallback reads the whole row
                 f_spec = -1;
             } else {
-                // Round trip 1: every part's count and threshold (lane q of
-                // every wave: part q) and the length of list segment `wave`
-                // of every part.
+                // One round trip: every part's count and threshold and its
+                // per-wave list lengths (lane q: part q).
                 const int c_tot = lane < S ? ld_agent(p.part_count + slot0 + lane) : 0;
                 const uint32_t tp = lane < S ? (uint32_t)ld_agent((const int32_t*)p.part_thresh + slot0 + lane) : 0u;
-                const int c_w = lane < S ? ld_agent(p.part_wcnt + (slot0 + lane) * kSlotWaves + wave) : 0;
+                const auto rwc = row_rsrc(p.part_wcnt + slot0 * kSlotWaves, S * kSlotWaves * 4);
+                int4 wc[kSlotWaves / 4];
+#pragma unroll
+                for (int i = 0; i < kSlotWaves / 4; ++i) wc[i] = ld_agent16(rwc, lane * kSlotWaves * 4 + 16 * i);
+                // Lane q: part q's segment `wave` (c_w entries), the entries
+                // of its segments before it, and its total.
+                int c_w = 0, before_w = 0, tot_q = 0;
+#pragma unroll
+                for (int i = 0; i < kSlotWaves; ++i) {
+                    const int4 v4 = wc[i / 4];
+                    const int v = (i & 3) == 0 ? v4.x : (i & 3) == 1 ? v4.y : (i & 3) == 2 ? v4.z : v4.w;
+                    tot_q += v;
+                    before_w += i < wave ? v : 0;
+                    c_w = i == wave ? v : c_w;
+                }
                 // Totals of the row. Every part computes the same T_spec from
                 // the same data; a part that kept another threshold (or
                 // overflowed) sends the row to the fallback.
@@ -1432,53 +1509,54 @@ DEV void topk_body(const Params& p) {
                 const uint32_t trow = wave_max_u(tp);
                 const bool mixed = wave_min_u(lane < S ? tp : 0xFFFFFFFFu) != trow;
                 f_spec = wave_sum(c_tot & 0x7FFFFFFF);
-                overflow = ovf || mixed;
+                const int incl_t = wave_incl_scan(tot_q, lane);
+                overflow = ovf || mixed || __builtin_amdgcn_readlane(incl_t, kWave - 1) != f_spec;
                 tthr = trow;
                 if (!overflow && f_spec >= K && f_spec <= cap) {
                     // The merged list: every part's segments (the own part's
                     // too, from the workspace) packed in (part, wave) order,
                     // which is index order, then cut into one even segment
                     // per wave, so that the refine walks NW segments whatever
-                    // the number of parts. Segment (q, w) starts at the sum
-                    // of the segments before it.
-                    if (lane < S) {
-                        sm.sga[lane * NW + wave] = c_w;
-                        sm.sgb[lane * NW + wave] = 0;
-                    }
-                    lds_barrier();
-                    if (wave == 0) seg_scan(sm, S * NW, lane);
-                    lds_barrier();
-                    const int base_q = lane < S ? sm.sga[lane * NW + wave] : 0;   // lane q: start of segment (q, wave)
-                    // Round trip 2: wave w copies segments (q, w) of every
-                    // part q, entry t of their concatenation per lane (part
-                    // q holds t in [excl_q, incl_q)), four loads per lane in
-                    // flight. The other parts' keys join the refine's first
-                    // level, which holds the own part's already.
-                    const int incl = wave_incl_scan(c_w, lane);
-                    const int excl = incl - c_w;
-                    const int tot_w = __builtin_amdgcn_readlane(incl, kWave - 1);
+                    // the number of parts. Wave w copies segments (q, w),
+                    // four parts' first 64 entries in flight at a time; the
+                    // other parts' keys join the refine's first level, which
+                    // holds the own part's already.
+                    const int base_q = incl_t - tot_q + before_w;   // lane q: start of segment (q, wave)
                     const uint32_t msh = ref_shift(trow, max(gmax, trow));
                     const uint64_t* src_w = p.part_list + slot0 * kPartCap + wave * W::kCapW;
-                    for (int t0 = 0; t0 < tot_w; t0 += 4 * kWave) {
+                    auto put = [&](int P, uint64_t e, bool other) {
+                        sm.list[P] = make_uint2((uint32_t)e, (uint32_t)(e >> 32));
+                        if (other && !all_mode) ref_hist_add(sm, (uint32_t)e, trow, msh);
+                    };
+                    for (int q0 = 0; q0 < S; q0 += 4) {
                         uint64_t e[4];
-                        int dst[4], qs[4];
+                        int cq[4], bq[4];
 #pragma unroll
                         for (int c = 0; c < 4; ++c) {
-                            const int t = t0 + c * kWave + lane;
-                            int q = 0;
-#pragma unroll
-                            for (int r = 0; r < kMaxParts; ++r) q += (r < S && __builtin_amdgcn_readlane(incl, r) <= t);
-                            q = min(q, S - 1);
-                            const int i = t - __shfl(excl, q);
-                            dst[c] = __shfl(base_q, q) + i;
-                            qs[c] = q;
-                            e[c] = t < tot_w ? ld_agent(src_w + (int64_t)q * kPartCap + i) : 0ull;
+                            const int q = min(q0 + c, S - 1);
+                            cq[c] = q0 + c < S ? __builtin_amdgcn_readlane(c_w, q) : 0;
+                            bq[c] = __builtin_amdgcn_readlane(base_q, q);
+                            e[c] = lane < cq[c] ? ld_agent(src_w + (int64_t)q * kPartCap + lane) : 0ull;
                         }
 #pragma unroll
+                        for (int c = 0; c < 4; ++c)
+                            if (lane < cq[c]) put(bq[c] + lane, e[c], q0 + c != part);
+                        // entries past the first 64 (long segments), four per lane in flight
+#pragma unroll
                         for (int c = 0; c < 4; ++c) {
-                            if (t0 + c * kWave + lane < tot_w) {
-                                sm.list[dst[c]] = make_uint2((uint32_t)e[c], (uint32_t)(e[c] >> 32));
-                                if (!all_mode && qs[c] != part) ref_hist_add(sm, (uint32_t)e[c], trow, msh);
+                            const uint64_t* src = src_w + (int64_t)min(q0 + c, S - 1) * kPartCap;
+                            for (int i0 = kWave; i0 < cq[c]; i0 += 4 * kWave) {
+                                uint64_t t[4];
+#pragma unroll
+                                for (int u = 0; u < 4; ++u) {
+                                    const int i = i0 + u * kWave + lane;
+                                    t[u] = i < cq[c] ? ld_agent(src + i) : 0ull;
+                                }
+#pragma unroll
+                                for (int u = 0; u < 4; ++u) {
+                                    const int i = i0 + u * kWave + lane;
+                                    if (i < cq[c]) put(bq[c] + i, t[u], q0 + c != part);
+                                }
                             }
                         }
                     }

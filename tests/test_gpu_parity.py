@@ -388,6 +388,51 @@ def test_special_rows_with_guess_and_parts(ld, K, parts):
                           % (name, ld, K, parts))
 
 
+def _crowded_rows(ld, K, rng):
+    """Rows whose K-th key sits in a crowd of ~1.5 K candidates packed into a
+    few ulps (far narrower than a first-level refine bin): all one value, two
+    alternating values, consecutive floats, and consecutive floats with ties."""
+    rows = []
+    n_top = K - K // 4                          # the crowd holds the K-th largest
+    crowd = K + K // 2
+    one = np.float32(1.0).view(np.uint32)
+    kinds = [np.full(crowd, one, np.uint32),
+             one + (np.arange(crowd) % 2).astype(np.uint32),
+             one + np.arange(crowd, dtype=np.uint32),
+             one + (np.arange(crowd) // 3).astype(np.uint32)]
+    for bits in kinds:
+        x = rng.uniform(0.0, 0.5, ld).astype(np.float32)
+        pos = rng.permutation(ld)
+        x[pos[:n_top]] = rng.uniform(10.0, 20.0, n_top).astype(np.float32)
+        x[pos[n_top:n_top + crowd]] = rng.permutation(bits).view(np.float32)
+        rows.append(x)
+    rows = np.stack(rows)
+    return rows, np.full(rows.shape[0], ld, np.int32)
+
+
+@pytest.mark.parametrize("parts", [1, 4])
+@pytest.mark.parametrize("ld,K", [(100003, 2048), (60001, 300)])
+def test_crowded_kth_bin(ld, K, parts):
+    """The refine's K-th bin holds more candidates than one wave ranks:
+    resolved from the bin's min / max (one key) or by narrowing between
+    them; with the oracle's previous answer and a random guess, split or not,
+    and the radix path on the same rows."""
+    import paper_2604_22312_amd as g
+    rng = np.random.default_rng(ld + K + parts)
+    rows, lens = _crowded_rows(ld, K, rng)
+    exp, _, _ = oracle.topk(rows, K, row_len=lens)
+    S = torch.from_numpy(rows).to(DEV)
+    RL = torch.from_numpy(lens).to(DEV)
+    guesses = {"exact": exp, "random": rng.integers(0, ld, size=exp.shape).astype(np.int32)}
+    for name, pv in guesses.items():
+        note("crowded rows guess=%s ld=%d K=%d parts=%d" % (name, ld, K, parts))
+        out = _gvr_parts(S, RL, torch.from_numpy(np.ascontiguousarray(pv)).to(DEV), K, parts)
+        assert_rows_equal(out.cpu().numpy(), exp, "crowded rows guess=%s ld=%d K=%d parts=%d"
+                          % (name, ld, K, parts))
+    out = g.radix_topk(S, RL, None, K)
+    assert_rows_equal(out.cpu().numpy(), exp, "crowded rows radix ld=%d K=%d" % (ld, K))
+
+
 @pytest.mark.parametrize("parts", [1, 3])
 def test_misaligned_rows_with_guess(parts):
     rng = np.random.default_rng(19)
