@@ -195,7 +195,7 @@ gvr_status gvr_topk_ex(const float* scores, int64_t B, int64_t ld, const int32_t
  * static device array of the library instead of a library allocation. It
  * calls no hipMalloc, hipFree or other allocating routine, so it may be
  * captured into a HIP graph as any call's first, on any stream.
- *   - The array holds GVR_NOALLOC_SLOTS (row, part) slots: 32 MiB per device
+ *   - The array holds GVR_NOALLOC_SLOTS (row, part) slots: 34 MiB per device
  *     the library runs on, held until the process ends. An automatic split
  *     (options->parts == 0) is lowered to fit; a forced split with
  *     B * parts > GVR_NOALLOC_SLOTS returns GVR_ERR_WORKSPACE before

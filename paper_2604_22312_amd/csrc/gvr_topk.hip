@@ -113,6 +113,7 @@ constexpr int kGuessSamples = 256;             // guessed indices gathered: a st
 constexpr int kGuessBins = 1024;               // bins of the gathered-key histogram (16 per lane of wave 0)
 static_assert(kRefBins1 + kGuessBins <= kRefBins, "guess histogram above the first refine level");
 constexpr int kSpecQuantile = 65;              // T_spec: gathered key of rank ceil(65 / 2048 * sample size)
+static_assert(kRefBins1 == gvr_host::kSlotHistBins, "a workspace slot holds one part's first refine level");
 constexpr int kSmall = 64;                     // refine: K-th key's bin resolved by one wave up to this size
 constexpr int kMaxPasses = 8;                  // 2 + at most 4 narrowing passes + 1 final pass suffice
 constexpr int kMaxSecant = 8;                  // probes of the secant search after T0 (I_max)
@@ -141,6 +142,7 @@ struct Params {
     int32_t* part_count; // [rows][S] f(threshold) of each part, bit 31 = a wave list overflowed
     uint32_t* part_thresh; // [rows][S] threshold of each part's list (T_spec, the same in every part)
     int32_t* part_wcnt;  // [rows][S][kSlotWaves] list length of each wave of each part
+    int32_t* part_hist;  // [rows][S][kRefBins1] each part's first refine level over [T_spec, pmax]
     uint64_t* part_list; // [rows][S][kPartCap] (fp32 bits | index << 32) of each part
 };
 
@@ -796,6 +798,39 @@ DEV void keys_in_place(Smem<NW>& sm, uint2* seg, int cnt, bool hist, uint32_t rl
     }
 }
 
+// Wave 0: the bin b of a first refine level hb[0, kRefBins1) holding the
+// need0-th key from the top (need0 >= 1, at most the histogram's total), with
+// two wave scans; scal[0] = b, scal[2] = base + the keys in the bins above b,
+// scal[3] = b's count.
+template <int NW>
+DEV void kth_bin_wave0(Smem<NW>& sm, const int* hb, int need0, int base, int lane) {
+    // lane l owns bins [32 l, 32 l + 32)
+    const int4* h4 = reinterpret_cast<const int4*>(hb) + lane * 8;
+    int s = 0;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const int4 v = h4[j];
+        s += v.x + v.y + v.z + v.w;
+    }
+    const int incl = wave_incl_scan(s, lane);
+    const int total = __builtin_amdgcn_readlane(incl, 63);
+    const int abv = total - incl;   // keys in the bins of higher lanes
+    const uint64_t hit = __ballot(abv < need0 && abv + s >= need0);
+    const int L = hit ? (int)__builtin_ctzll(hit) : 0;
+    const int abv_l = __builtin_amdgcn_readlane(abv, L);
+    const int hj = lane < 32 ? hb[L * 32 + lane] : 0;
+    const int ij = wave_incl_scan(hj, lane);
+    const int s_l = __builtin_amdgcn_readlane(ij, 63);
+    const int abj = abv_l + s_l - ij;
+    const uint64_t hit2 = __ballot(lane < 32 && abj < need0 && abj + hj >= need0);
+    const int J = hit2 ? (int)__builtin_ctzll(hit2) : 0;
+    if (lane == 0) {
+        sm.scal[0] = L * 32 + J;
+        sm.scal[2] = base + __builtin_amdgcn_readlane(abj, J);
+        sm.scal[3] = __builtin_amdgcn_readlane(hj, J);
+    }
+}
+
 // Exact K-th key T* among the listed candidates and the emission. The K-th
 // key lies in [rlo, rhi]; `above` listed keys lie above rhi. One histogram
 // level of kRefBins1 bins over [rlo, bin_hi] (keys in (bin_hi, rhi] count in
@@ -827,33 +862,7 @@ DEV uint32_t refine_emit(Smem<NW>& sm, uint32_t rlo, uint32_t rhi, uint32_t bin_
     }
     // (a ready histogram is complete behind the caller's last barrier)
     const int need0 = K - above;   // >= 1: rank of T* among the keys in [rlo, rhi], from the top
-    if (wave == 0) {
-        // lane l owns bins [32 l, 32 l + 32)
-        const int4* h4 = reinterpret_cast<const int4*>(hb) + lane * 8;
-        int s = 0;
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const int4 v = h4[j];
-            s += v.x + v.y + v.z + v.w;
-        }
-        const int incl = wave_incl_scan(s, lane);
-        const int total = __builtin_amdgcn_readlane(incl, 63);
-        const int abv = total - incl;   // keys in the bins of higher lanes
-        const uint64_t hit = __ballot(abv < need0 && abv + s >= need0);
-        const int L = hit ? (int)__builtin_ctzll(hit) : 0;
-        const int abv_l = __builtin_amdgcn_readlane(abv, L);
-        const int hj = lane < 32 ? hb[L * 32 + lane] : 0;
-        const int ij = wave_incl_scan(hj, lane);
-        const int s_l = __builtin_amdgcn_readlane(ij, 63);
-        const int abj = abv_l + s_l - ij;
-        const uint64_t hit2 = __ballot(lane < 32 && abj < need0 && abj + hj >= need0);
-        const int J = hit2 ? (int)__builtin_ctzll(hit2) : 0;
-        if (lane == 0) {
-            sm.scal[0] = L * 32 + J;
-            sm.scal[2] = above + __builtin_amdgcn_readlane(abj, J);
-            sm.scal[3] = __builtin_amdgcn_readlane(hj, J);
-        }
-    }
+    if (wave == 0) kth_bin_wave0(sm, hb, need0, above, lane);
     lds_barrier();
     const int b = sm.scal[0];
     const int above_b = sm.scal[2];   // listed keys above bin b
@@ -1114,6 +1123,7 @@ DEV void topk_body(const Params& p) {
     int passes = 0;
     int f_spec = 0;          // f(tthr), or -1 if unknown
     bool hist_ready = false; // the refine's first histogram level is built (lists at tthr)
+    bool hist_full = false;  // rhist counts every key >= tthr of the row (first-level bins)
     uint32_t tthr = 0u;      // threshold of the speculative lists
     bool overflow = false;
     if (tid < NW) sm.seg_off[tid] = tid * W::kCapW;
@@ -1245,6 +1255,7 @@ DEV void topk_body(const Params& p) {
         // every list stays in index order; one capacity check per slab
         // (wave-uniform), and a wave whose list would overflow keeps counting.
         int cnt_w = 0;
+        int stored_w = 0;   // entries listed when the list filled up
         uint2* lw = sm.list + wave * W::kCapW;
         // The streaming waves wait for T_spec here, with their first slabs in
         // flight (polling an LDS flag, not a barrier: issuing those loads may
@@ -1262,6 +1273,9 @@ DEV void topk_body(const Params& p) {
         t1 = tstamp();
         tspec = max(tspec, 1u);
         const SpecTest test = make_spec_test(tspec);
+        // the refine's first level over [T_spec, max(pmax, T_spec)]
+        const bool own_hist = !all_mode;
+        const uint32_t hsh = ref_shift(tspec, max(gmax, tspec));
         // Slab s of this wave is the row's slab sg = sqb / 64 + s; slabs
         // [in_lo, in_hi) hold no element outside [0, n).
         const int in_lo = aoff > 0 ? 1 : 0, in_hi = (n + aoff) >> 8;
@@ -1305,6 +1319,16 @@ DEV void topk_body(const Params& p) {
                             if (f[c]) lds_store_pair(lw_addr + 8 * q, k[c], (uint32_t)(e0 + c));
                             q = add_lane_bit(q, m[c]);
                         }
+                    } else {
+                        // The list is full: the kept keys go to the refine's
+                        // first level only, so that it still counts every key
+                        // >= T_spec (the entries already listed join it below).
+                        if (cnt_w <= W::kCapW) stored_w = cnt_w;
+                        if (own_hist) {
+#pragma unroll
+                            for (int c = 0; c < 4; ++c)
+                                if (f[c]) ref_hist_add(sm, key_of_bits(k[c]), tspec, hsh);
+                        }
                     }
                     cnt_w += total;   // counted past capacity: the overflow is detected below
                 }
@@ -1343,8 +1367,7 @@ DEV void topk_body(const Params& p) {
         // do this while the others still stream. A part of a split row also
         // publishes the wave's list and its length right away (no wait): the
         // row's last part may merge it.
-        const bool own_hist = !all_mode;
-        if (cnt_w <= W::kCapW) keys_in_place(sm, lw, cnt_w, own_hist, tspec, ref_shift(tspec, max(gmax, tspec)), lane);
+        keys_in_place(sm, lw, cnt_w <= W::kCapW ? cnt_w : stored_w, own_hist, tspec, hsh, lane);
         if (S > 1) {
             const int64_t slot = row * S + part;
             if (cnt_w <= W::kCapW) {
@@ -1363,6 +1386,7 @@ DEV void topk_body(const Params& p) {
         overflow = wave_max_u(lane < NW ? (uint32_t)sm.wa[lane] : 0u) > (uint32_t)W::kCapW;
         f_spec = overflow ? -1 : sum_over_waves<NW>(sm.wa, lane);
         hist_ready = own_hist && !overflow;
+        hist_full = own_hist && S == 1;   // full lists or not, every kept key is in it
         tthr = tspec;
 
         if (overflow && S == 1) {
@@ -1441,7 +1465,7 @@ DEV void topk_body(const Params& p) {
                 lds_barrier();
                 overflow = false;
                 f_spec = f_all;
-                hist_ready = false;
+                hist_ready = own_hist;
             }
         }
 
@@ -1464,6 +1488,10 @@ DEV void topk_body(const Params& p) {
             if (tid == 0) {
                 p.part_count[slot0 + part] = (int32_t)((uint32_t)f_part | (overflow ? 0x80000000u : 0u));
                 p.part_thresh[slot0 + part] = tthr;
+            }
+            if (own_hist) {   // this part's first refine level, as bin pairs (summed after an overflow)
+                uint64_t* ph = reinterpret_cast<uint64_t*>(p.part_hist + (slot0 + part) * kRefBins1);
+                for (int i = tid; i < kRefBins1 / 2; i += W::kBlock) ph[i] = reinterpret_cast<const uint64_t*>(sm.u.rhist)[i];
             }
             __builtin_amdgcn_s_waitcnt(0);   // this wave's stores have completed (reached L2)
             __syncthreads();
@@ -1508,10 +1536,30 @@ DEV void topk_body(const Params& p) {
                 const bool ovf = wave_max_u(lane < S && c_tot < 0 ? 1u : 0u) != 0u;
                 const uint32_t trow = wave_max_u(tp);
                 const bool mixed = wave_min_u(lane < S ? tp : 0xFFFFFFFFu) != trow;
-                f_spec = wave_sum(c_tot & 0x7FFFFFFF);
+                f_spec = mixed ? -1 : wave_sum(c_tot & 0x7FFFFFFF);
                 const int incl_t = wave_incl_scan(tot_q, lane);
                 overflow = ovf || mixed || __builtin_amdgcn_readlane(incl_t, kWave - 1) != f_spec;
                 tthr = trow;
+                if (!mixed && own_hist && f_spec > cap) {
+                    // The row's first refine level: the sum of the parts'
+                    // (bin pair tid of every part in one round trip), which
+                    // counts every key >= T_spec of the row.
+                    for (int i = tid; i < kRefBins1 / 2; i += W::kBlock) {
+                        uint64_t hv[kMaxParts];
+#pragma unroll
+                        for (int k = 0; k < kMaxParts; ++k)
+                            hv[k] = k < S ? ld_agent(reinterpret_cast<const uint64_t*>(p.part_hist + (slot0 + k) * kRefBins1) + i)
+                                          : 0ull;
+                        int sx = 0, sy = 0;
+#pragma unroll
+                        for (int k = 0; k < kMaxParts; ++k) {
+                            sx += (int)(uint32_t)hv[k];
+                            sy += (int)(uint32_t)(hv[k] >> 32);
+                        }
+                        reinterpret_cast<int2*>(sm.u.rhist)[i] = make_int2(sx, sy);
+                    }
+                    hist_full = true;   // complete behind the fallback's first barrier
+                }
                 if (!overflow && f_spec >= K && f_spec <= cap) {
                     // The merged list: every part's segments (the own part's
                     // too, from the workspace) packed in (part, wave) order,
@@ -1701,6 +1749,85 @@ DEV void topk_body(const Params& p) {
         const uint32_t kmin = wave_min_u(lane < NW ? (uint32_t)sm.red[2][lane] : 0xFFFFFFFFu);
         const uint32_t kmax = wave_max_u(lane < NW ? (uint32_t)sm.red[3][lane] : 0u);
         win = make_window(kmin, max(kmin, kmax));
+    };
+    // Collect pass at threshold tc: every wave lists the keys >= tc of its
+    // full-row share in its own list (up to kCapW entries, counted past
+    // capacity: a share holds a few of them when f(tc) <= C is spread over
+    // the row). A wave that overflowed sends the row through one more pass
+    // at exact per-wave offsets. Returns f(tc); the lists hold every key >=
+    // tc if it is at most C.
+    auto collect_lists = [&](uint32_t tc) -> int {
+        __syncthreads();   // the previous lists and histogram are dead
+        uint2* lc = sm.list + wave * W::kCapW;
+        int c = 0;
+        stream_wave(xa, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
+            uint32_t k[4];
+            block_keys(v, k);
+            const int e0 = 4 * q - aoff;
+            const bool edge = (4 * qs - aoff < 0 || 4 * qs + 255 - aoff >= n);
+            bool f[4];
+            uint64_t m[4];
+#pragma unroll
+            for (int cc = 0; cc < 4; ++cc) {
+                f[cc] = k[cc] >= tc && (!edge || (e0 + cc >= 0 && e0 + cc < n));
+                m[cc] = __ballot(f[cc]);
+            }
+            int pos = c + (int)lanes_below(m[3], lanes_below(m[2], lanes_below(m[1], lanes_below(m[0], 0))));
+#pragma unroll
+            for (int cc = 0; cc < 4; ++cc) {
+                if (f[cc]) {
+                    if (pos < W::kCapW) lc[pos] = make_uint2(k[cc], (uint32_t)(e0 + cc));
+                    ++pos;
+                }
+            }
+            c += __popcll(m[0]) + __popcll(m[1]) + __popcll(m[2]) + __popcll(m[3]);
+        });
+        ++passes;
+        if (lane == 0) sm.wa[wave] = c;
+        __syncthreads();
+        const int f = sum_over_waves<NW>(sm.wa, lane);
+        const bool full = wave_max_u(lane < NW ? (uint32_t)sm.wa[lane] : 0u) > (uint32_t)W::kCapW;
+        if (!full) {
+            if (lane == 0) {
+                sm.seg_off[wave] = wave * W::kCapW;
+                sm.seg_cnt[wave] = c;
+            }
+        } else if (f <= cap) {
+            const int off = sum_over_waves_below(sm.wa, lane, wave);
+            __syncthreads();
+            if (lane == 0) {
+                sm.seg_off[wave] = off;
+                sm.seg_cnt[wave] = c;
+            }
+            uint2* lp = sm.list + off;
+            int run = 0;
+            stream_wave(xa, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
+                uint32_t k[4];
+                block_keys(v, k);
+                const int e0 = 4 * q - aoff;
+                const bool edge = (4 * qs - aoff < 0 || 4 * qs + 255 - aoff >= n);
+                bool ff[4];
+                uint64_t m[4];
+#pragma unroll
+                for (int cc = 0; cc < 4; ++cc) {
+                    ff[cc] = k[cc] >= tc && (!edge || (e0 + cc >= 0 && e0 + cc < n));
+                    m[cc] = __ballot(ff[cc]);
+                }
+                int pos = run + (int)lanes_below(m[3], lanes_below(m[2], lanes_below(m[1], lanes_below(m[0], 0))));
+#pragma unroll
+                for (int cc = 0; cc < 4; ++cc) {
+                    if (ff[cc]) {
+                        if (pos < c) lp[pos] = make_uint2(k[cc], (uint32_t)(e0 + cc));
+                        ++pos;
+                    }
+                }
+                run += __popcll(m[0]) + __popcll(m[1]) + __popcll(m[2]) + __popcll(m[3]);
+            });
+            ++passes;
+        }
+        if (tid == 0) sm.nq = 1;
+        __syncthreads();
+        return f;
     };
 
     int path = all_mode ? GVR_PATH_ALL : (have_prev ? GVR_PATH_GUESS : GVR_PATH_NO_GUESS);
@@ -1943,6 +2070,56 @@ DEV void topk_body(const Params& p) {
                 whole_range = false;
             }
         }
+        // What the speculative pass counted may name a threshold with
+        // K <= f <= C right away: T_spec itself when its lists are
+        // incomplete (a part's list overflowed), or, when f(T_spec) > C, the
+        // lower edge of the first refine level's bin holding the K-th key
+        // (the level counts every key >= T_spec). One collect pass then
+        // lists the candidates; a crowded bin is narrowed by count passes.
+        int coll = -1;   // f at the collect threshold tc (-1: none)
+        uint32_t tc = 0u;
+        if (spec && !secant && f_spec >= K && f_spec <= cap) {
+            tc = tthr;
+            coll = f_spec;
+            rlo = tthr;
+            rhi = 0xFFFFFFFFu;
+            bin_hi = max(gmax, tthr);
+            above = 0;
+        } else if (spec && !secant && f_spec > cap && hist_full) {
+            __syncthreads();   // the level is complete
+            if (wave == 0) kth_bin_wave0(sm, sm.u.rhist, K, 0, lane);
+            __syncthreads();
+            const int b = sm.scal[0], above_b = sm.scal[2], cnt_b = sm.scal[3];
+            __syncthreads();
+            const uint32_t hsh = ref_shift(tthr, max(gmax, tthr));
+            const uint64_t lo64 = (uint64_t)tthr + ((uint64_t)b << hsh);
+            const uint64_t end64 = std::min<uint64_t>(lo64 + ((uint64_t)1 << hsh) - 1, 0xFFFFFFFFu);
+            const uint32_t lo_b = (uint32_t)lo64;
+            const uint32_t hi_b = b == kRefBins1 - 1 ? 0xFFFFFFFFu : (uint32_t)end64;   // the top bin is open
+            if (above_b + cnt_b <= cap) {
+                tc = lo_b;
+                coll = above_b + cnt_b;
+                rlo = lo_b;
+                rhi = hi_b;
+                bin_hi = (uint32_t)end64;
+                above = b == kRefBins1 - 1 ? 0 : above_b;
+            } else {
+                win = make_window(lo_b, hi_b);
+                whole_range = false;
+            }
+        }
+        if (coll >= 0) {
+            const int f = collect_lists(tc);
+            if (f == coll) {
+                T = tc;
+                cands = f;
+                done_lists = true;
+            } else {   // not what was counted (cannot happen): count from the whole key range
+                win = make_window(0u, 0xFFFFFFFFu);
+                whole_range = true;
+            }
+        }
+        if (!done_lists) {
         if (whole_range) minmax_pass();   // the first window spans the row's [min, max]
         count_pass();
         for (;;) {
@@ -2069,6 +2246,7 @@ DEV void topk_body(const Params& p) {
             win = nw;
             count_pass();
         }
+        }
         t2 = tstamp();
     }
 
@@ -2174,7 +2352,7 @@ gvr_host::WorkspaceCache<HipDev> g_workspaces;
 
 // Scratch of the allocation-free entry point: the split-row workspace of up
 // to kStaticSlots (row, part) slots (arrival words, counts, thresholds,
-// per-wave counts, 128 KB of lists per slot: 32 MiB) as one device array.
+// per-wave counts, histograms, 128 KB of lists per slot: 34 MiB) as one device array.
 // Each device that runs the library holds its own copy until the process
 // ends. Its arrival words are zero when the library is loaded, and every
 // launch leaves the words it used at zero again (the last part of a row
@@ -2254,6 +2432,7 @@ gvr_status run(const float* scores, int64_t B, int64_t ld, const int32_t* row_le
         q.part_count = ws.part_count;
         q.part_thresh = ws.part_thresh;
         q.part_wcnt = ws.part_wcnt;
+        q.part_hist = ws.part_hist;
         q.part_list = ws.part_list;
         const dim3 grid((unsigned)(rows_pad * parts));
         const hipStream_t hs = (hipStream_t)stream;

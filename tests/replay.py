@@ -14,6 +14,14 @@ Methodology"). The steps follow the method:
   bottom (m valid samples), and at least key 1.
 * One pass counts f(T_spec) = #{key >= T_spec} (Sec. 4.1) per streaming wave
   (a wave's list holds 1024 entries); K <= f <= C accepts it (Lemma 1).
+* Otherwise, if K <= f <= C (a list overflowed), one collect pass at T_spec
+  (a part of one row) or again at exact per-wave offsets (one part). If
+  f > C, the first refine level (2048 bins of 2^s keys from T_spec, s the
+  smallest shift whose bins span [T_spec, max(pmax, T_spec)], higher keys in
+  the top bin) counts every key >= T_spec: the bin holding the K-th key gives
+  T' = its lower edge, and if f(T') <= C one collect pass lists the keys >= T'
+  (each of the 16 waves its full-row share, up to 1024 entries; a share
+  past that costs one more pass at exact offsets).
 * Otherwise count passes narrow a window of 256 bins around the K-th key
   (each evaluates f at 257 thresholds) until a threshold with K <= f <= C is
   found (one collect pass) or the K-th key is isolated (one emit pass).
@@ -31,6 +39,7 @@ WAVES = 16             # waves per workgroup; wave 0 computes the guess
 WAVE_CAP = 1024        # list entries per wave
 GUESS_SAMPLES = 256
 GUESS_BINS_LG = 10     # 1024 bins
+REF_BINS_LG = 11       # first refine level: 2048 bins
 SPEC_QUANTILE = 65
 WINDOW_BINS_LG = 8     # 256 bins per counting window
 MAX_PARTS = 16
@@ -68,16 +77,17 @@ def choose_parts(rows: int, ld: int, cus: int = 256) -> int:
     return s if stream_us * (1.0 - 1.0 / s) > 8.0 else 1
 
 
-def spec_threshold(xk: np.ndarray, n: int, prev: np.ndarray | None, K: int):
-    """(T_spec, valid samples) of Phase 1 on the sampled guess; T_spec None without a valid sample."""
+def spec_threshold(xk: np.ndarray, n: int, prev: np.ndarray | None, K: int, with_max: bool = False):
+    """(T_spec, valid samples) of Phase 1 on the sampled guess; T_spec None
+    without a valid sample. With `with_max`, also pmax (largest sampled key)."""
     st = -(-K // GUESS_SAMPLES)
     m = -(-K // st)
     if prev is None:
-        return None, 0
+        return (None, 0, 0) if with_max else (None, 0)
     idx = np.asarray(prev[: m * st: st][:m], dtype=np.int64)
     ok = (idx >= 0) & (idx < n)
     if not ok.any():
-        return None, 0
+        return (None, 0, 0) if with_max else (None, 0)
     gk = xk[idx[ok]]
     mn, mx = int(gk.min()), int(gk.max())
     sh = bin_shift(mx - mn + 1, GUESS_BINS_LG)
@@ -85,7 +95,8 @@ def spec_threshold(xk: np.ndarray, n: int, prev: np.ndarray | None, K: int):
     cnt = int(ok.sum())
     target = max(1, -(-SPEC_QUANTILE * cnt // K_MAX))
     b = int(np.argmax(np.cumsum(h) >= target))
-    return max(mn + (b << sh), 1), cnt
+    t = max(mn + (b << sh), 1)
+    return (t, cnt, mx) if with_max else (t, cnt)
 
 
 def wave_ranges(n: int, aoff: int, parts: int, part: int):
@@ -106,6 +117,36 @@ def wave_ranges(n: int, aoff: int, parts: int, part: int):
 
 def count_ge(xk: np.ndarray, t: int) -> int:
     return int((xk >= t).sum())
+
+
+def row_share_overflow(xk: np.ndarray, n: int, aoff: int, t: int) -> bool:
+    """Some wave's full-row share (16 waves, whole slabs each) holds more
+    than a list's 1024 keys >= t."""
+    nq = (n + aoff + 3) >> 2
+    nslab = (nq + 63) >> 6
+    per = -(-nslab // WAVES) * 64
+    for w in range(WAVES):
+        qb = min(w * per, nq)
+        qe = min(qb + per, nq)
+        lo, hi = max(0, 4 * qb - aoff), max(0, min(n, 4 * qe - aoff))
+        if hi > lo and count_ge(xk[lo:hi], t) > WAVE_CAP:
+            return True
+    return False
+
+
+def kth_level_bin(xk: np.ndarray, K: int, t: int, gmax: int):
+    """The first refine level over [t, max(gmax, t)]: (lower edge, upper edge
+    (0xFFFFFFFF for the open top bin), keys in the bins above, the bin's count)
+    of the bin holding the K-th key."""
+    sh = bin_shift(max(gmax, t) - t + 1, REF_BINS_LG)
+    kk = xk[xk >= t]
+    b = np.minimum((kk - t) >> sh, (1 << REF_BINS_LG) - 1).astype(np.int64)
+    h = np.bincount(b, minlength=1 << REF_BINS_LG)
+    above = np.concatenate([np.cumsum(h[::-1])[::-1][1:], [0]])   # keys in the bins above each bin
+    j = int(np.nonzero((above < K) & (above + h >= K))[0][0])
+    lo = t + (j << sh)
+    hi = 0xFFFFFFFF if j == (1 << REF_BINS_LG) - 1 else min(lo + (1 << sh) - 1, 0xFFFFFFFF)
+    return lo, hi, int(above[j]), int(h[j])
 
 
 def narrow(xk: np.ndarray, K: int, cap: int, lo: int, hi: int, passes: int):
@@ -162,7 +203,7 @@ def replay_row(x: np.ndarray, n: int, prev: np.ndarray | None, K: int, parts: in
         outcome, passes, thr, cands = narrow(xk, K, cap, 0, 0xFFFFFFFF, 0)
         return {"path": PATH["ties" if outcome == "ties" else "no_guess"], "passes": passes, "threshold": thr,
                 "candidates": cands}
-    tspec, gvalid = spec_threshold(xk, n, prev, K)
+    tspec, gvalid, gmax = spec_threshold(xk, n, prev, K, with_max=True)
     have_prev = prev is not None and gvalid > 0
     t = tspec if tspec is not None else 0xFFFFFFFF
     res["spec_threshold"] = t
@@ -184,10 +225,19 @@ def replay_row(x: np.ndarray, n: int, prev: np.ndarray | None, K: int, parts: in
     if overflow and parts == 1 and K <= f <= cap:      # collected again at packed offsets
         res.update(path=PATH[path], passes=2, threshold=t, candidates=f)
         return res
+    p = "narrowed" if path == "guess" else "no_guess"
+    if K <= f <= cap:                                  # a part's list overflowed: collect at T_spec
+        extra = 1 if row_share_overflow(xk, n, aoff, t) else 0
+        res.update(path=PATH[p], passes=2 + extra, threshold=t, candidates=f)
+        return res
     if f < K:
         lo, hi = 0, t - 1
-    else:
-        lo, hi = t, 0xFFFFFFFF
+    else:                                              # f > C: the K-th key's bin of the first refine level
+        lo, hi, above, cnt = kth_level_bin(xk, K, t, gmax)
+        if above + cnt <= cap:
+            extra = 1 if row_share_overflow(xk, n, aoff, lo) else 0
+            res.update(path=PATH[p], passes=2 + extra, threshold=lo, candidates=above + cnt)
+            return res
     outcome, passes, thr, cands = narrow(xk, K, cap, lo, hi, 1)
     p = "ties" if outcome == "ties" else ("narrowed" if path == "guess" else "no_guess")
     res.update(path=PATH[p], passes=passes, threshold=thr, candidates=cands)
