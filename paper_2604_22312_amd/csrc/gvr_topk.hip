@@ -32,20 +32,28 @@
 //   answer: the row was read once.
 //
 //   Refine (Sec. 4.2.4, Phase 4). One LDS histogram level over the listed
-//   keys, a two-scan bin search by one wave, then that wave ranks the few
-//   keys of the K-th key's bin to get T* and the per-wave emission offsets;
-//   every key > T* and the first K - #{key > T*} keys equal to T* (lower
-//   index first) are written out in ascending index order.
+//   keys (built while the lists are turned into keys), a two-scan bin search
+//   by one wave, then that wave ranks the few keys of the K-th key's bin to
+//   get T* and the per-segment emission offsets (a crowded bin is resolved
+//   from its min / max or narrowed); every key > T* and the first
+//   K - #{key > T*} keys equal to T* (lower index first) are written out in
+//   ascending index order.
 //
-//   When the guess does not deliver (no valid prev_topk, f(T_spec) outside
-//   [K, C], or a wave's list overflows) the last part reads the whole row
-//   again: count passes narrow a 256-bin window of key space around the K-th
-//   key (each pass evaluates f at 257 thresholds: the count cache of Phase 2
-//   generalised), then one collect pass gathers the <= C candidates at the
-//   accepted threshold with exact per-wave offsets, or, when ties straddle
-//   [K, C], an emit pass writes the selection directly. radix_topk runs only
-//   this schedule (one workgroup per row), starting from the whole key
-//   range: a distribution-agnostic radix select (Sec. 2.2).
+//   When the guess does not deliver, what the speculative pass counted is
+//   used first: its histogram level counts every key >= T_spec even where a
+//   list overflowed, so if f(T_spec) > C the bin holding the K-th key gives
+//   a threshold T' with K <= f(T') <= C, and one collect pass over the row
+//   lists the keys >= T' (if K <= f(T_spec) <= C but a list overflowed, the
+//   collect is at T_spec). Otherwise (f(T_spec) < K, no valid prev_topk, or
+//   a crowded bin) count passes narrow a 256-bin window of key space around
+//   the K-th key (each pass evaluates f at 257 thresholds: the count cache
+//   of Phase 2 generalised), then one collect pass gathers the <= C
+//   candidates at the accepted threshold with exact per-wave offsets, or,
+//   when ties straddle [K, C], an emit pass writes the selection directly.
+//   radix_topk (one workgroup per row) is a distribution-agnostic radix
+//   select (Sec. 2.2): a digit pass counts the top 11 key bits of the row,
+//   the bin holding the K-th key is collected in one more pass (or narrowed
+//   by count passes when it holds more than C keys).
 //
 //   On request (option flag 4) the paper's own Phase 2 schedule runs instead
 //   of the speculative pass: T0 = pmean of all guessed scores, one threshold
@@ -109,6 +117,7 @@ static_assert(Shape<kNWLong>::kCap == GVR_MAX_CANDIDATES, "the long-row shape ho
 static_assert(kSlotWaves == kNWLong && kPartCap == Shape<kNWLong>::kCap, "a workspace slot holds one part's lists");
 constexpr int kRefBins = 4096;                 // bins of a narrowing refine level (12 bits of key)
 constexpr int kRefBins1 = 2048;                // bins of the first refine level (32 per lane of one wave)
+constexpr int kDigitShift = 21;                // radix digit: the top 11 key bits, one first-level bin each
 constexpr int kGuessSamples = 256;             // guessed indices gathered: a strided sample of prev_topk
 constexpr int kGuessBins = 1024;               // bins of the gathered-key histogram (16 per lane of wave 0)
 static_assert(kRefBins1 + kGuessBins <= kRefBins, "guess histogram above the first refine level");
@@ -268,6 +277,12 @@ constexpr int kBufWord3 = 0x00020000;   // 32-bit data format, no swizzle
 DEV __amdgpu_buffer_rsrc_t row_rsrc(const void* base, int bytes) {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, kBufWord3);
 }
+// 16-byte buffer load (full-row passes: a row read twice, as by the radix
+// schedule, finds its second read in the caches).
+DEV float4 buf_load16(__amdgpu_buffer_rsrc_t r, int off) {
+    const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+    return make_float4(__uint_as_float(v.x), __uint_as_float(v.y), __uint_as_float(v.z), __uint_as_float(v.w));
+}
 // 16-byte buffer load with the non-temporal hint: a streamed row is read
 // once, and the hint keeps it from displacing reused lines.
 constexpr int kCpolNT = 2;
@@ -358,8 +373,9 @@ DEV int block_excl_scan(int& a, Smem<NW>& sm, int tid) {
 }
 
 // ------------------------------------------------------------------ streaming
-// One wave streams float4 blocks [qb, qe) of the row in slabs of 64 blocks
-// with kU slabs in flight; `body(v, q, qs)` gets each lane's block q, its data
+// One wave streams float4 blocks [qb, qe) of the row (buffer resource xr)
+// in slabs of 64 blocks with kU slabs in flight;
+// `body(v, q, qs)` gets each lane's block q, its data
 // and the slab's first block qs. Every block index is clamped to qlast, so no
 // load leaves the 16-byte blocks that hold the row (refills past the wave's
 // last slab re-read the row's last block and are never used); bodies mask
@@ -368,12 +384,11 @@ DEV int block_excl_scan(int& a, Smem<NW>& sm, int tid) {
 // consumed and unconditionally, so each slot keeps one register set and a
 // slab waits only for its own load (vmcnt(kU - 1)), not for all of them.
 template <typename Pro, typename Body>
-DEV void stream_wave(const float4* __restrict__ xa, int qb, int qe, int qlast, int lane, Pro&& prologue,
-                     Body&& body) {
+DEV void stream_wave(__amdgpu_buffer_rsrc_t xr, int qb, int qe, int qlast, int lane, Pro&& prologue, Body&& body) {
     const int nslab = qe > qb ? (qe - qb + 63) >> 6 : 0;
     float4 buf[kU];
 #pragma unroll
-    for (int u = 0; u < kU; ++u) buf[u] = xa[min(qb + u * 64 + lane, qlast)];
+    for (int u = 0; u < kU; ++u) buf[u] = buf_load16(xr, min(qb + u * 64 + lane, qlast) * 16);
     prologue();
     int s0 = 0;
     for (; s0 + kU <= nslab; s0 += kU) {
@@ -381,7 +396,7 @@ DEV void stream_wave(const float4* __restrict__ xa, int qb, int qe, int qlast, i
         for (int u = 0; u < kU; ++u) {
             const int s = s0 + u;
             body(buf[u], qb + s * 64 + lane, qb + s * 64);
-            buf[u] = xa[min(qb + (s + kU) * 64 + lane, qlast)];
+            buf[u] = buf_load16(xr, min(qb + (s + kU) * 64 + lane, qlast) * 16);
         }
     }
 #pragma unroll
@@ -1092,6 +1107,7 @@ DEV void topk_body(const Params& p) {
     const int aoff = (int)(((uintptr_t)x >> 2) & 31);   // slabs start on 128-byte lines
     const float4* xa = reinterpret_cast<const float4*>(x - aoff);
     const int nq = (n + aoff + 3) >> 2;
+    const __amdgpu_buffer_rsrc_t xr = row_rsrc(xa, nq * 16);   // the row's blocks, for full-row passes
     const int qlast = nq - 1;
     const int nslab_row = (nq + 63) >> 6;
     const int per = ((nslab_row + NW - 1) / NW) * 64;   // whole slabs per wave
@@ -1704,7 +1720,7 @@ DEV void topk_body(const Params& p) {
         for (int i = tid; i < NW * kBinsX; i += W::kBlock) (&sm.u.hist[0][0])[i] = 0;
         __syncthreads();
         const uint32_t lo = win.lo, sh = win.shift;
-        stream_wave(xa, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
+        stream_wave(xr, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
             uint32_t k[4];
             block_keys(v, k);
             const int e0 = 4 * q - aoff;
@@ -1725,7 +1741,7 @@ DEV void topk_body(const Params& p) {
     // first window spans [min, max] instead.
     auto minmax_pass = [&]() {
         uint32_t mn = 0xFFFFFFFFu, mx = 0u;
-        stream_wave(xa, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
+        stream_wave(xr, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
             uint32_t k[4];
             block_keys(v, k);
             const int e0 = 4 * q - aoff;
@@ -1750,6 +1766,27 @@ DEV void topk_body(const Params& p) {
         const uint32_t kmax = wave_max_u(lane < NW ? (uint32_t)sm.red[3][lane] : 0u);
         win = make_window(kmin, max(kmin, kmax));
     };
+    // Radix digit pass: a histogram of the top 11 key bits (sign, exponent
+    // and two mantissa bits: quarter-binade bins) of every element of the
+    // row, in the first refine level's 2048 bins.
+    auto digit_pass = [&]() {
+        __syncthreads();
+        for (int i = tid; i < kRefBins1; i += W::kBlock) sm.u.rhist[i] = 0;
+        __syncthreads();
+        stream_wave(xr, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
+            uint32_t k[4];
+            block_keys(v, k);
+            const int e0 = 4 * q - aoff;
+            const bool edge = (4 * qs - aoff < 0 || 4 * qs + 255 - aoff >= n);
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+                if (!edge || (e0 + c >= 0 && e0 + c < n))
+                    __hip_atomic_fetch_add(&sm.u.rhist[k[c] >> kDigitShift], 1, __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_WORKGROUP);
+        });
+        ++passes;
+        __syncthreads();
+    };
     // Collect pass at threshold tc: every wave lists the keys >= tc of its
     // full-row share in its own list (up to kCapW entries, counted past
     // capacity: a share holds a few of them when f(tc) <= C is spread over
@@ -1760,7 +1797,7 @@ DEV void topk_body(const Params& p) {
         __syncthreads();   // the previous lists and histogram are dead
         uint2* lc = sm.list + wave * W::kCapW;
         int c = 0;
-        stream_wave(xa, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
+        stream_wave(xr, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
             uint32_t k[4];
             block_keys(v, k);
             const int e0 = 4 * q - aoff;
@@ -1801,7 +1838,7 @@ DEV void topk_body(const Params& p) {
             }
             uint2* lp = sm.list + off;
             int run = 0;
-            stream_wave(xa, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
+            stream_wave(xr, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
                 uint32_t k[4];
                 block_keys(v, k);
                 const int e0 = 4 * q - aoff;
@@ -1891,7 +1928,7 @@ DEV void topk_body(const Params& p) {
         auto count_ge = [&](uint32_t tk, bool minmax) {
             int c = 0;
             uint32_t lo = 0xFFFFFFFFu, hi = 0u;
-            stream_wave(xa, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
+            stream_wave(xr, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
                 uint32_t k[4];
                 block_keys(v, k);
                 const int e0 = 4 * q - aoff;
@@ -1990,7 +2027,7 @@ DEV void topk_body(const Params& p) {
             }
             uint2* lc = sm.list + off;
             int run = 0;
-            stream_wave(xa, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
+            stream_wave(xr, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
                 uint32_t k[4];
                 block_keys(v, k);
                 const int e0 = 4 * q - aoff;
@@ -2108,19 +2145,38 @@ DEV void topk_body(const Params& p) {
                 whole_range = false;
             }
         }
+        if (whole_range && coll < 0) {
+            // Nothing bounds the K-th key: a digit pass, then the same choice
+            // over its bins (a bin of more than C keys is narrowed).
+            digit_pass();
+            if (wave == 0) kth_bin_wave0(sm, sm.u.rhist, K, 0, lane);
+            __syncthreads();
+            const int b = sm.scal[0], above_b = sm.scal[2], cnt_b = sm.scal[3];
+            __syncthreads();
+            const uint32_t lo_b = (uint32_t)b << kDigitShift;
+            const uint32_t hi_b = lo_b + ((1u << kDigitShift) - 1u);
+            if (above_b + cnt_b <= cap) {
+                tc = lo_b;
+                coll = above_b + cnt_b;
+                rlo = lo_b;
+                rhi = bin_hi = hi_b;
+                above = above_b;
+            } else {
+                win = make_window(lo_b, hi_b);
+            }
+            whole_range = false;
+        }
         if (coll >= 0) {
             const int f = collect_lists(tc);
             if (f == coll) {
                 T = tc;
                 cands = f;
                 done_lists = true;
-            } else {   // not what was counted (cannot happen): count from the whole key range
-                win = make_window(0u, 0xFFFFFFFFu);
-                whole_range = true;
+            } else {   // not what was counted (cannot happen): count from the row's [min, max]
+                minmax_pass();
             }
         }
         if (!done_lists) {
-        if (whole_range) minmax_pass();   // the first window spans the row's [min, max]
         count_pass();
         for (;;) {
             const int j = crossing();
@@ -2164,7 +2220,7 @@ DEV void topk_body(const Params& p) {
                 __syncthreads();
                 uint2* lc = sm.list + off;
                 int run = 0;
-                stream_wave(xa, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
+                stream_wave(xr, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
                     uint32_t k[4];
                     block_keys(v, k);
                     const int e0 = 4 * q - aoff;
@@ -2207,7 +2263,7 @@ DEV void topk_body(const Params& p) {
                 __syncthreads();
                 int gb = sum_over_waves_below(sm.wa, lane, wave);
                 int eb = sum_over_waves_below(sm.wb, lane, wave);
-                stream_wave(xa, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
+                stream_wave(xr, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
                     uint32_t k[4];
                     block_keys(v, k);
                     const int e0 = 4 * q - aoff;

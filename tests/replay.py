@@ -25,6 +25,9 @@ Methodology"). The steps follow the method:
 * Otherwise count passes narrow a window of 256 bins around the K-th key
   (each evaluates f at 257 thresholds) until a threshold with K <= f <= C is
   found (one collect pass) or the K-th key is isolated (one emit pass).
+* Without a guess (the radix schedule) nothing bounds the K-th key: a digit
+  pass counts the top 11 key bits of every element (2048 bins); the bin
+  holding the K-th key is collected (as above) or narrowed.
 
 The row split (parts, workgroup slabs) mirrors the launch the library plans
 for the 16-wave shape: rows of a call up to the number of compute units.
@@ -42,6 +45,7 @@ GUESS_BINS_LG = 10     # 1024 bins
 REF_BINS_LG = 11       # first refine level: 2048 bins
 SPEC_QUANTILE = 65
 WINDOW_BINS_LG = 8     # 256 bins per counting window
+DIGIT_SHIFT = 21       # radix digit: key >> 21
 MAX_PARTS = 16
 MIN_PART_ELEMS = 16384
 PATH = {"trivial": 0, "all": 1, "guess": 2, "narrowed": 3, "ties": 4, "no_guess": 5}
@@ -149,6 +153,19 @@ def kth_level_bin(xk: np.ndarray, K: int, t: int, gmax: int):
     return lo, hi, int(above[j]), int(h[j])
 
 
+def digit_then(xk: np.ndarray, n: int, aoff: int, K: int, cap: int, passes: int):
+    """The digit pass and what follows it: (outcome, passes, threshold, candidates)."""
+    h = np.bincount((xk >> DIGIT_SHIFT).astype(np.int64), minlength=1 << (32 - DIGIT_SHIFT))
+    above = np.concatenate([np.cumsum(h[::-1])[::-1][1:], [0]])
+    j = int(np.nonzero((above < K) & (above + h >= K))[0][0])
+    lo = j << DIGIT_SHIFT
+    hi = lo + (1 << DIGIT_SHIFT) - 1
+    if above[j] + h[j] <= cap:
+        extra = 1 if row_share_overflow(xk, n, aoff, lo) else 0
+        return "collect", passes + 2 + extra, lo, int(above[j] + h[j])
+    return narrow(xk, K, cap, lo, hi, passes + 1)
+
+
 def narrow(xk: np.ndarray, K: int, cap: int, lo: int, hi: int, passes: int):
     """Count passes over 256-bin windows starting from [lo, hi] (from the
     row's [min, max] after one min/max pass when nothing bounds the K-th key,
@@ -199,8 +216,8 @@ def replay_row(x: np.ndarray, n: int, prev: np.ndarray | None, K: int, parts: in
     all_mode = (prev is None or n <= 2 * K) and n <= cap and ws_all * 256 <= WAVE_CAP
     if all_mode:
         return {"path": PATH["all"], "passes": 1, "candidates": n}
-    if prev is None:   # the guess-free kernel: count passes from the whole key range
-        outcome, passes, thr, cands = narrow(xk, K, cap, 0, 0xFFFFFFFF, 0)
+    if prev is None:   # the guess-free kernel: a digit pass, then collect or narrow
+        outcome, passes, thr, cands = digit_then(xk, n, aoff, K, cap, 0)
         return {"path": PATH["ties" if outcome == "ties" else "no_guess"], "passes": passes, "threshold": thr,
                 "candidates": cands}
     tspec, gvalid, gmax = spec_threshold(xk, n, prev, K, with_max=True)
