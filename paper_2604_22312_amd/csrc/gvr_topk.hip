@@ -1768,11 +1768,20 @@ DEV void topk_body(const Params& p) {
     };
     // Radix digit pass: a histogram of the top 11 key bits (sign, exponent
     // and two mantissa bits: quarter-binade bins) of every element of the
-    // row, in the first refine level's 2048 bins.
+    // row, in the first refine level's 2048 bins. Most elements of a row
+    // fall in a few such bins, and same-address LDS atomics of one
+    // instruction serialise, so the pass counts into kDigitCopies copies
+    // (lane l adds to copy l % kDigitCopies; bin-major, so the copies of a
+    // bin sit in different banks) in the lists' space, summed afterwards.
+    constexpr int kDigitCopies = W::kCap * 2 >= kRefBins1 * 8 ? 8 : 4;
+    static_assert(W::kCap * 2 >= kRefBins1 * kDigitCopies, "the digit histogram copies fit the lists' space");
     auto digit_pass = [&]() {
+        int* dh = reinterpret_cast<int*>(sm.list);   // [kRefBins1][kDigitCopies]
         __syncthreads();
-        for (int i = tid; i < kRefBins1; i += W::kBlock) sm.u.rhist[i] = 0;
+        for (int i = tid; i < kRefBins1 * kDigitCopies / 4; i += W::kBlock)
+            reinterpret_cast<int4*>(dh)[i] = make_int4(0, 0, 0, 0);
         __syncthreads();
+        int* dl = dh + (lane & (kDigitCopies - 1));
         stream_wave(xr, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
             uint32_t k[4];
             block_keys(v, k);
@@ -1781,10 +1790,21 @@ DEV void topk_body(const Params& p) {
 #pragma unroll
             for (int c = 0; c < 4; ++c)
                 if (!edge || (e0 + c >= 0 && e0 + c < n))
-                    __hip_atomic_fetch_add(&sm.u.rhist[k[c] >> kDigitShift], 1, __ATOMIC_RELAXED,
+                    __hip_atomic_fetch_add(&dl[(k[c] >> kDigitShift) * kDigitCopies], 1, __ATOMIC_RELAXED,
                                            __HIP_MEMORY_SCOPE_WORKGROUP);
         });
         ++passes;
+        __syncthreads();
+        for (int i = tid; i < kRefBins1; i += W::kBlock) {
+            const int4* c4 = reinterpret_cast<const int4*>(dh + i * kDigitCopies);
+            int t = 0;
+#pragma unroll
+            for (int j = 0; j < kDigitCopies / 4; ++j) {
+                const int4 v = c4[j];
+                t += v.x + v.y + v.z + v.w;
+            }
+            sm.u.rhist[i] = t;
+        }
         __syncthreads();
     };
     // Collect pass at threshold tc: every wave lists the keys >= tc of its
@@ -1795,29 +1815,35 @@ DEV void topk_body(const Params& p) {
     // tc if it is at most C.
     auto collect_lists = [&](uint32_t tc) -> int {
         __syncthreads();   // the previous lists and histogram are dead
-        uint2* lc = sm.list + wave * W::kCapW;
+        // As in the speculative pass: the test on raw fp32 bits, every lane
+        // stores each element (kept ones at their rank, the others to a
+        // dummy slot in the histogram's space) while the slab fits the list.
+        const uint32_t lc_addr = lds_addr(sm.list + wave * W::kCapW);
+        const uint32_t dummy = lds_addr(sm.u.rhist) + 8 * lane;
+        const bool every = tc == 0u;   // key 0 passes too: no compare
+        const SpecTest test = make_spec_test(max(tc, 1u));
         int c = 0;
         stream_wave(xr, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
-            uint32_t k[4];
-            block_keys(v, k);
+            const uint32_t k[4] = {__float_as_uint(v.x), __float_as_uint(v.y), __float_as_uint(v.z), __float_as_uint(v.w)};
             const int e0 = 4 * q - aoff;
-            const bool edge = (4 * qs - aoff < 0 || 4 * qs + 255 - aoff >= n);
             bool f[4];
-            uint64_t m[4];
 #pragma unroll
-            for (int cc = 0; cc < 4; ++cc) {
-                f[cc] = k[cc] >= tc && (!edge || (e0 + cc >= 0 && e0 + cc < n));
-                m[cc] = __ballot(f[cc]);
+            for (int cc = 0; cc < 4; ++cc) f[cc] = every || (int32_t)(k[cc] ^ test.flip) >= test.bound;
+            if (4 * qs - aoff < 0 || 4 * qs + 255 - aoff >= n) {   // an edge slab (wave-uniform)
+#pragma unroll
+                for (int cc = 0; cc < 4; ++cc) f[cc] = f[cc] && e0 + cc >= 0 && e0 + cc < n;
             }
-            int pos = c + (int)lanes_below(m[3], lanes_below(m[2], lanes_below(m[1], lanes_below(m[0], 0))));
+            const uint64_t m[4] = {__ballot(f[0]), __ballot(f[1]), __ballot(f[2]), __ballot(f[3])};
+            const int total = __popcll(m[0]) + __popcll(m[1]) + __popcll(m[2]) + __popcll(m[3]);
+            if (c + total <= W::kCapW) {
+                int qq = (int)lanes_below(m[3], lanes_below(m[2], lanes_below(m[1], lanes_below(m[0], (uint32_t)c))));
 #pragma unroll
-            for (int cc = 0; cc < 4; ++cc) {
-                if (f[cc]) {
-                    if (pos < W::kCapW) lc[pos] = make_uint2(k[cc], (uint32_t)(e0 + cc));
-                    ++pos;
+                for (int cc = 0; cc < 4; ++cc) {
+                    lds_store_pair(f[cc] ? lc_addr + 8 * qq : dummy, key_of_bits(k[cc]), (uint32_t)(e0 + cc));
+                    qq = add_lane_bit(qq, m[cc]);
                 }
             }
-            c += __popcll(m[0]) + __popcll(m[1]) + __popcll(m[2]) + __popcll(m[3]);
+            c += total;   // counted past capacity
         });
         ++passes;
         if (lane == 0) sm.wa[wave] = c;
