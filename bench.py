@@ -594,8 +594,12 @@ def run_indexer(args, dev):
     synthetic FP8 inputs, workloads/indexer.py), then the Top-K. Lines: the
     indexer alone (HBM roofline: key cache + scales read once per request,
     scores written), the indexer followed by gvr_topk guided by the previous
-    step, and gvr_topk alone on the same scores. GPU time per call from a
-    replayed HIP graph; the 0.87 GB key cache exceeds the Infinity Cache."""
+    step (the indexer also scores each row's guess sample, the Top-K reads
+    the guess statistics), and gvr_topk / radix_topk alone on the same
+    scores; the Top-K's Phase 1 time with and without the fused guess. GPU
+    time per call from replayed HIP graphs; the 0.87 GB key cache exceeds
+    the Infinity Cache."""
+    import numpy as np
     import torch
     import paper_2604_22312_amd as g
     from workloads import indexer as WI
@@ -616,7 +620,23 @@ def run_indexer(args, dev):
     if not torch.equal(out, g.radix_topk(scores, rl1, None, K_TOPK)):
         raise SystemExit("bench: gvr_indexer_topk differs from radix_topk on its own scores")
 
-    def graph_us(fn, reps):
+    # Phase 1 of the Top-K (t_guess - t_start of the row stats, 100 MHz
+    # stamps): with the guess statistics the indexer computed (the fused
+    # call), and gathering the sample from the scores (gvr_topk_ex alone).
+    def p1_us(st):
+        d = g.decode_stats(st)
+        return round(float(np.median((d["t_guess"] - d["t_start"]).numpy())) / 100.0, 3)
+    st_f = g.new_stats(rows, dev)
+    g.gvr_indexer_topk(x.q[1], x.w, x.k, x.k_scale, rl1, prev, K_TOPK, scores=scores, out_idx=out, stats=st_f)
+    st_g = g.new_stats(rows, dev)
+    g.gvr_topk_ex(scores, rl1, prev, K_TOPK, out_idx=out, stats=st_g)
+    torch.cuda.synchronize()
+    p1 = {"fused_guess_us": p1_us(st_f), "gathered_guess_us": p1_us(st_g)}
+
+    # GPU time per call: one replayed graph of 4 calls per variant, timed in
+    # 7 interleaved rounds (the key cache streams from HBM, whose rate drifts
+    # over a run; interleaving keeps the variants comparable), medians.
+    def make_graph(fn):
         stream = torch.cuda.Stream()
         with torch.cuda.stream(stream):
             fn(stream)
@@ -627,20 +647,28 @@ def run_indexer(args, dev):
                 fn(stream)
         graph.replay()
         torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for _ in range(reps):
-            graph.replay()
-        e1.record()
-        torch.cuda.synchronize()
-        return e0.elapsed_time(e1) * 1e3 / (reps * 4)
+        return graph
 
-    reps = max(2, args.steps // 20)
-    t_idx = graph_us(lambda s: g.gvr_indexer_scores(x.q[1], x.w, x.k, x.k_scale, rl1, scores=scores, stream=s), reps)
-    t_both = graph_us(lambda s: g.gvr_indexer_topk(x.q[1], x.w, x.k, x.k_scale, rl1, prev, K_TOPK, scores=scores,
-                                                   out_idx=out, stream=s), reps)
-    t_topk = graph_us(lambda s: g.gvr_topk(scores, rl1, prev, K_TOPK, out_idx=out, stream=s), reps)
-    t_radix = graph_us(lambda s: g.radix_topk(scores, rl1, None, K_TOPK, out_idx=out, stream=s), reps)
+    variants = {
+        "idx": lambda s: g.gvr_indexer_scores(x.q[1], x.w, x.k, x.k_scale, rl1, scores=scores, stream=s),
+        "both": lambda s: g.gvr_indexer_topk(x.q[1], x.w, x.k, x.k_scale, rl1, prev, K_TOPK, scores=scores,
+                                             out_idx=out, stream=s),
+        "topk": lambda s: g.gvr_topk(scores, rl1, prev, K_TOPK, out_idx=out, stream=s),
+        "radix": lambda s: g.radix_topk(scores, rl1, None, K_TOPK, out_idx=out, stream=s),
+    }
+    graphs = {k: make_graph(f) for k, f in variants.items()}
+    reps = max(2, args.steps // 40)
+    times = {k: [] for k in graphs}
+    for _ in range(7):
+        for k, graph in graphs.items():
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(reps):
+                graph.replay()
+            e1.record()
+            torch.cuda.synchronize()
+            times[k].append(e0.elapsed_time(e1) * 1e3 / (reps * 4))
+    t_idx, t_both, t_topk, t_radix = (float(np.median(times[k])) for k in ("idx", "both", "topk", "radix"))
     n_cache = int(rl1.view(requests, group).max(dim=1).values.to(torch.int64).sum())
     n_rows = int(rl1.to(torch.int64).sum())
     idx_bytes = n_cache * (D + 4) + n_rows * 4 + rows * H * (D + 4)
@@ -649,6 +677,8 @@ def run_indexer(args, dev):
             "H": H, "D": D, "group": group,
             "indexer_us": round(t_idx, 3), "indexer_plus_gvr_topk_us": round(t_both, 3),
             "gvr_topk_alone_us": round(t_topk, 3), "radix_topk_alone_us": round(t_radix, 3),
+            "timing": "median of 7 interleaved rounds of replayed 4-call graphs",
+            "topk_phase1_median": p1,
             "indexer_roofline": {"bound": "hbm", "achieved": round(idx_bytes / t_idx / 1e3, 1), "peak": PEAK_HBM_GBS,
                                  "unit": "GB/s", "frac": round(idx_bytes / t_idx / 1e3 / PEAK_HBM_GBS, 4),
                                  "algorithmic_bytes_per_launch": idx_bytes,

@@ -63,7 +63,20 @@ gvr_status gvr_indexer_scores(const uint8_t* q, const float* w, const uint8_t* k
 /* The indexer, then gvr_topk_ex on its scores (same stream, back to back):
  * out_idx [B][K] receives the exact Top-K of every row of I (see
  * gvr_topk.h for the result definition, prev_topk, options and stats).
- * `scores` [B][ld] f32 is the caller's buffer for I and keeps it. */
+ * `scores` [B][ld] f32 is the caller's buffer for I and keeps it.
+ *
+ * Fused guess (Sec. 4.2.1, Phase 1): with a prev_topk, K >= 8 and the
+ * default schedule (not option flag 4, not flag 1), the indexer kernel also
+ * scores the keys at each row's strided sample of prev_topk (every
+ * ceil(K / 256)-th entry) with the same matrix steps as the row's scores, so
+ * the sampled scores equal the ones written, and reduces them to the row's
+ * guess statistics (T_spec, valid samples, pmin, pmax, sample sum). It
+ * leaves them in the last 8 words of the row's out_idx, where the Top-K
+ * reads them instead of gathering the sample's scores after the indexer;
+ * the Top-K then overwrites out_idx with the result. The answer, the row
+ * stats and the path are those of gvr_topk_ex on the same scores and guess
+ * (prev_topk may alias out_idx: each row's sample is read before its
+ * statistics are written). */
 gvr_status gvr_indexer_topk(const uint8_t* q, const float* w, const uint8_t* k, const float* k_scale,
                             int64_t B, int32_t H, int32_t D, int32_t group, int64_t ld,
                             const int32_t* row_len, float* scores, const int32_t* prev_topk, int32_t K,

@@ -73,6 +73,9 @@
 
 #include "gvr_topk.h"
 #include "host_plan.h"
+#include "wave_ops.h"
+#include "guess.h"
+#include "topk_internal.h"
 
 #define DEV __device__ __forceinline__
 
@@ -86,8 +89,8 @@ using gvr_host::kNWShort;
 using gvr_host::kPartCap;
 using gvr_host::kSlotWaves;
 using gvr_host::kXcds;
+using namespace gvr_dev;
 
-constexpr int kWave = 64;
 constexpr int kU = 8;                          // slabs in flight per wave (count / collect passes)
 constexpr int kSU = 8;                         // slabs in flight per wave (speculative pass)
 constexpr int kBins = 256;                     // bins of a counting window
@@ -118,10 +121,8 @@ static_assert(kSlotWaves == kNWLong && kPartCap == Shape<kNWLong>::kCap, "a work
 constexpr int kRefBins = 4096;                 // bins of a narrowing refine level (12 bits of key)
 constexpr int kRefBins1 = 2048;                // bins of the first refine level (32 per lane of one wave)
 constexpr int kDigitShift = 21;                // radix digit: the top 11 key bits, one first-level bin each
-constexpr int kGuessSamples = 256;             // guessed indices gathered: a strided sample of prev_topk
-constexpr int kGuessBins = 1024;               // bins of the gathered-key histogram (16 per lane of wave 0)
 static_assert(kRefBins1 + kGuessBins <= kRefBins, "guess histogram above the first refine level");
-constexpr int kSpecQuantile = 65;              // T_spec: gathered key of rank ceil(65 / 2048 * sample size)
+static_assert(kGuessMaxK == GVR_MAX_K, "the T_spec quantile is taken over the largest K");
 static_assert(kRefBins1 == gvr_host::kSlotHistBins, "a workspace slot holds one part's first refine level");
 constexpr int kSmall = 64;                     // refine: K-th key's bin resolved by one wave up to this size
 constexpr int kMaxPasses = 8;                  // 2 + at most 4 narrowing passes + 1 final pass suffice
@@ -152,85 +153,12 @@ struct Params {
     uint32_t* part_thresh; // [rows][S] threshold of each part's list (T_spec, the same in every part)
     int32_t* part_wcnt;  // [rows][S][kSlotWaves] list length of each wave of each part
     int32_t* part_hist;  // [rows][S][kRefBins1] each part's first refine level over [T_spec, pmax]
+    const int32_t* gstats; // or NULL: GuessStats words of every row (row stride K), from the indexer
     uint64_t* part_list; // [rows][S][kPartCap] (fp32 bits | index << 32) of each part
 };
 
 // ------------------------------------------------------------------ helpers
 
-DEV uint32_t key_of_bits(uint32_t u) { return u ^ ((uint32_t)((int32_t)u >> 31) | 0x80000000u); }
-DEV uint32_t key_of(float v) { return key_of_bits(__float_as_uint(v)); }
-DEV float float_of_key(uint32_t k) { return __uint_as_float((k & 0x80000000u) ? (k ^ 0x80000000u) : ~k); }
-
-// Number of set bits of m below this lane, plus acc.
-// Mask of lanes [0, r) for any r (wave-uniform): scalar instructions only.
-DEV uint64_t first_lanes(int r) { return r >= kWave ? ~0ull : (r <= 0 ? 0ull : (1ull << r) - 1ull); }
-
-DEV uint32_t lanes_below(uint64_t m, uint32_t acc) {
-    return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, acc));
-}
-
-// Wave-wide reductions and scans with DPP (VALU lane moves, no LDS round
-// trip): quad_perm / row_half_mirror / row_mirror combine the 16 lanes of a
-// row, readlane combines the four rows; every lane gets the result.
-template <int CTRL, int ROW_MASK = 0xF>
-DEV int dpp_i(int old, int x) {
-    return __builtin_amdgcn_update_dpp(old, x, CTRL, ROW_MASK, 0xF, false);
-}
-constexpr int kQuadSwap1 = 0xB1;   // quad_perm [1,0,3,2]
-constexpr int kQuadSwap2 = 0x4E;   // quad_perm [2,3,0,1]
-constexpr int kRowHalfMirror = 0x141;
-constexpr int kRowMirror = 0x140;
-constexpr int kRowShr1 = 0x111;
-constexpr int kRowBcast15 = 0x142;
-constexpr int kRowBcast31 = 0x143;
-
-DEV int wave_sum(int v) {
-    v += dpp_i<kQuadSwap1>(0, v);
-    v += dpp_i<kQuadSwap2>(0, v);
-    v += dpp_i<kRowHalfMirror>(0, v);
-    v += dpp_i<kRowMirror>(0, v);
-    return __builtin_amdgcn_readlane(v, 0) + __builtin_amdgcn_readlane(v, 16) + __builtin_amdgcn_readlane(v, 32) +
-           __builtin_amdgcn_readlane(v, 48);
-}
-DEV float wave_sum_f(float v) {
-    // fixed combination order: pairs, quads, halves, rows, then rows 0..3
-    v += __int_as_float(dpp_i<kQuadSwap1>(0, __float_as_int(v)));
-    v += __int_as_float(dpp_i<kQuadSwap2>(0, __float_as_int(v)));
-    v += __int_as_float(dpp_i<kRowHalfMirror>(0, __float_as_int(v)));
-    v += __int_as_float(dpp_i<kRowMirror>(0, __float_as_int(v)));
-    return ((__int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0)) +
-             __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16))) +
-            __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32))) +
-           __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
-}
-DEV uint32_t wave_min_u(uint32_t v) {
-    v = min(v, (uint32_t)dpp_i<kQuadSwap1>(0, (int)v));
-    v = min(v, (uint32_t)dpp_i<kQuadSwap2>(0, (int)v));
-    v = min(v, (uint32_t)dpp_i<kRowHalfMirror>(0, (int)v));
-    v = min(v, (uint32_t)dpp_i<kRowMirror>(0, (int)v));
-    return min(min((uint32_t)__builtin_amdgcn_readlane((int)v, 0), (uint32_t)__builtin_amdgcn_readlane((int)v, 16)),
-               min((uint32_t)__builtin_amdgcn_readlane((int)v, 32), (uint32_t)__builtin_amdgcn_readlane((int)v, 48)));
-}
-DEV uint32_t wave_max_u(uint32_t v) {
-    v = max(v, (uint32_t)dpp_i<kQuadSwap1>(0, (int)v));
-    v = max(v, (uint32_t)dpp_i<kQuadSwap2>(0, (int)v));
-    v = max(v, (uint32_t)dpp_i<kRowHalfMirror>(0, (int)v));
-    v = max(v, (uint32_t)dpp_i<kRowMirror>(0, (int)v));
-    return max(max((uint32_t)__builtin_amdgcn_readlane((int)v, 0), (uint32_t)__builtin_amdgcn_readlane((int)v, 16)),
-               max((uint32_t)__builtin_amdgcn_readlane((int)v, 32), (uint32_t)__builtin_amdgcn_readlane((int)v, 48)));
-}
-// Inclusive prefix sum over the 64 lanes: Hillis-Steele shifts inside each
-// 16-lane row (lanes without a source add 0), then row_bcast:15 / :31 carry
-// the row totals into the rows above.
-DEV int wave_incl_scan(int v, int /*lane*/) {
-    v += dpp_i<kRowShr1>(0, v);
-    v += dpp_i<kRowShr1 + 1>(0, v);
-    v += dpp_i<kRowShr1 + 3>(0, v);
-    v += dpp_i<kRowShr1 + 7>(0, v);
-    v += dpp_i<kRowBcast15, 0xA>(0, v);
-    v += dpp_i<kRowBcast31, 0xC>(0, v);
-    return v;
-}
 // Lane v of every wave reads wave v's value: one LDS read + one wave
 // reduction per cross-wave sum.
 template <int NW>
@@ -250,13 +178,6 @@ DEV void lds_barrier() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
-// Smallest s with (2^lg_bins << s) >= width, for 1 <= width <= 2^32: bins of
-// 2^s keys from the window's low edge cover `width` keys.
-DEV uint32_t bin_shift(uint64_t width, int lg_bins) {
-    const int bits = 64 - __builtin_clzll(width - 1 | 1);   // bit length of width - 1 (>= 1)
-    return (uint32_t)max(0, (width <= 1 ? 0 : bits) - lg_bins);
-}
-constexpr int log2i(int v) { return v <= 1 ? 0 : 1 + log2i(v / 2); }
 
 // A window of key space: bins j < kBins cover [lo + j<<shift, lo + (j+1)<<shift);
 // bin kBins holds every key >= lo + kBins<<shift; keys below lo are not counted.
@@ -1060,15 +981,22 @@ DEV void topk_body(const Params& p) {
     // kGuessSamples of them). The sample indices go out with the row length;
     // the gathers that depend on them are the only serial memory latency
     // before T_spec, and the part's first slabs are in flight meanwhile.
-    const int st_g = (p.K + kGuessSamples - 1) / kGuessSamples;
-    const int m_g = (p.K + st_g - 1) / st_g;
+    const int st_g = guess_stride(p.K);
+    const int m_g = guess_count(p.K);
     int pq[4] = {-1, -1, -1, -1};
+    int gw[5] = {-1, 0, -1, 0, 0};   // the indexer's GuessStats words of this row (gvr_indexer_topk)
     if (GUESS && p.prev && wave == 0) {
-        const int32_t* pv = p.prev + row * (int64_t)p.K;
+        if (p.gstats) {
+            const int32_t* g = p.gstats + row * (int64_t)p.K;
 #pragma unroll
-        for (int c = 0; c < 4; ++c) {
-            const int i = lane + 64 * c;
-            if (i < m_g) pq[c] = pv[i * st_g];
+            for (int c = 0; c < 5; ++c) gw[c] = g[c];
+        } else {
+            const int32_t* pv = p.prev + row * (int64_t)p.K;
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const int i = lane + 64 * c;
+                if (i < m_g) pq[c] = pv[i * st_g];
+            }
         }
     }
     // Row length through the scalar cache (row is wave-uniform): it does not
@@ -1176,70 +1104,24 @@ DEV void topk_body(const Params& p) {
                 // sampled guessed scores: pmin, pmax, pmean, and T_spec = lower
                 // edge of the histogram bin (over [pmin, pmax]) holding the
                 // gathered key of rank ceil(65 * m / 2048) from the bottom.
-                bool ok[4];
-                float gv[4];
-                uint32_t gk[4];
+                // From the indexer, when it scored the sample (one load).
+                GuessStats gs;
+                if (p.gstats) {
+                    gs = GuessStats{(uint32_t)gw[0], gw[1], (uint32_t)gw[2], (uint32_t)gw[3], __int_as_float(gw[4])};
+                } else {
+                    bool ok[4];
+                    float gv[4];
 #pragma unroll
-                for (int c = 0; c < 4; ++c) {
-                    ok[c] = pq[c] >= 0 && pq[c] < n;
-                    gv[c] = ok[c] ? x[pq[c]] : 0.f;
-                }
-                int cnt = 0;
-                uint32_t mn = 0xFFFFFFFFu, mx = 0u;
-                float sum = 0.f;
-#pragma unroll
-                for (int c = 0; c < 4; ++c) {
-                    gk[c] = key_of(gv[c]);
-                    if (ok[c]) {
-                        mn = min(mn, gk[c]);
-                        mx = max(mx, gk[c]);
-                        sum += gv[c];
-                        ++cnt;
+                    for (int c = 0; c < 4; ++c) {
+                        ok[c] = pq[c] >= 0 && pq[c] < n;
+                        gv[c] = ok[c] ? x[pq[c]] : 0.f;
                     }
-                }
-                cnt = wave_sum(cnt);
-                mn = wave_min_u(mn);
-                mx = wave_max_u(mx);
-                if (p.stats) sum = wave_sum_f(sum);   // pmean is only reported
-                uint32_t ts = 0xFFFFFFFFu;
-                if (cnt > 0) {
-                    const uint64_t width = (uint64_t)mx - mn + 1;
-                    const uint32_t sh = bin_shift(width, log2i(kGuessBins));
                     // (above the refine's first level, which stays free)
-                    int* gh = sm.u.rhist + kRefBins1;
-                    int4* h4 = reinterpret_cast<int4*>(gh) + lane * 4;   // lane owns 16 bins
-#pragma unroll
-                    for (int j = 0; j < 4; ++j) h4[j] = make_int4(0, 0, 0, 0);
-#pragma unroll
-                    for (int c = 0; c < 4; ++c)
-                        if (ok[c])
-                            __hip_atomic_fetch_add(&gh[(gk[c] - mn) >> sh], 1, __ATOMIC_RELAXED,
-                                                   __HIP_MEMORY_SCOPE_WORKGROUP);
-                    int h[16];
-                    int s16 = 0;
-#pragma unroll
-                    for (int j = 0; j < 4; ++j) {
-                        const int4 v = h4[j];
-                        h[4 * j] = v.x;
-                        h[4 * j + 1] = v.y;
-                        h[4 * j + 2] = v.z;
-                        h[4 * j + 3] = v.w;
-                        s16 += v.x + v.y + v.z + v.w;
-                    }
-                    const int target = max(1, (kSpecQuantile * cnt + GVR_MAX_K - 1) / GVR_MAX_K);
-                    const int incl = wave_incl_scan(s16, lane);
-                    const int excl = incl - s16;
-                    const uint64_t hit = __ballot(excl < target && incl >= target);
-                    const int L = hit ? (int)__builtin_ctzll(hit) : 0;
-                    int jsel = 0, run = excl;
-#pragma unroll
-                    for (int j = 0; j < 16; ++j) {
-                        if (run < target && run + h[j] >= target) jsel = j;
-                        run += h[j];
-                    }
-                    jsel = __builtin_amdgcn_readlane(jsel, L);
-                    ts = mn + ((uint32_t)(L * 16 + jsel) << sh);
+                    gs = guess_from_samples(gv, ok, sm.u.rhist + kRefBins1);
                 }
+                const uint32_t ts = gs.ts, mn = gs.mn, mx = gs.mx;
+                const int cnt = gs.cnt;
+                const float sum = gs.sum;
                 {   // the refine's first level, filled after the pass
                     int4* r4 = reinterpret_cast<int4*>(sm.u.rhist) + lane * (kRefBins1 / 4 / kWave);
 #pragma unroll
@@ -2463,7 +2345,7 @@ enum WsSource { kWsLibrary = 0, kWsStatic = 1 };
 
 gvr_status run(const float* scores, int64_t B, int64_t ld, const int32_t* row_len, const int32_t* prev,
                int32_t K, int32_t* out, void* stream, const gvr_options* opt, gvr_row_stats* stats,
-               int use_guess, WsSource ws_source) {
+               int use_guess, WsSource ws_source, const int32_t* gstats = nullptr) {
     gvr_host::CallOptions o;
     gvr_status st = gvr_host::validate(scores, B, ld, K, out, opt, use_guess, &o);
     if (st != GVR_OK) return st;
@@ -2516,6 +2398,7 @@ gvr_status run(const float* scores, int64_t B, int64_t ld, const int32_t* row_le
         q.part_wcnt = ws.part_wcnt;
         q.part_hist = ws.part_hist;
         q.part_list = ws.part_list;
+        q.gstats = (guess && gstats) ? gstats + r0 * K : nullptr;
         const dim3 grid((unsigned)(rows_pad * parts));
         const hipStream_t hs = (hipStream_t)stream;
         if (plan.shape == kNWMid) {
@@ -2543,6 +2426,18 @@ gvr_status run(const float* scores, int64_t B, int64_t ld, const int32_t* row_le
 }
 
 }  // namespace
+
+namespace gvr_internal {
+
+gvr_status topk_with_guess_stats(const float* scores, int64_t B, int64_t ld, const int32_t* row_len,
+                                 const int32_t* prev_topk, int32_t K, int32_t* out_idx, void* stream,
+                                 const gvr_options* options, gvr_row_stats* stats) {
+    if (K < kGuessWords || !out_idx) return GVR_ERR_INVALID_ARG;
+    return run(scores, B, ld, row_len, prev_topk, K, out_idx, stream, options, stats, 1, kWsLibrary,
+               out_idx + (K - kGuessWords));
+}
+
+}  // namespace gvr_internal
 
 extern "C" {
 

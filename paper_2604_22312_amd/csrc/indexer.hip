@@ -31,10 +31,14 @@
 #include <algorithm>
 
 #include "gvr_indexer.h"
+#include "guess.h"
+#include "host_plan.h"
+#include "topk_internal.h"
 
 namespace {
 
-constexpr int kWave = 64;
+using namespace gvr_dev;
+
 constexpr int kWaves = 4;                // waves per workgroup
 constexpr int kTile = 32;                // keys per ring slot (two 16-key matrix tiles)
 constexpr int kTilesPerWave = 32;        // ring slots of one wave's run (1024 keys)
@@ -59,6 +63,13 @@ struct IdxParams {
     int32_t chunks;       // workgroups per cache (key chunks)
     int32_t chunk_keys;   // keys per workgroup chunk
     int32_t run_keys;     // keys per wave run (a multiple of kTile)
+    // Fused guess (gvr_indexer_topk): workgroups [sample_base, + rows) score
+    // the keys at row b's strided sample of prev [rows][K] and write the
+    // sample's GuessStats words to gstats + b * K. prev NULL: none.
+    const int32_t* prev;
+    int32_t* gstats;
+    int32_t K;
+    int32_t sample_base;
 };
 
 // 32 bytes at p (16-byte aligned) as one matrix operand.
@@ -68,9 +79,120 @@ __device__ __forceinline__ v8i load32(const uint8_t* p) {
     return v8i{(int)a.x, (int)a.y, (int)a.z, (int)a.w, (int)b.x, (int)b.y, (int)b.z, (int)b.w};
 }
 
+// Score of the key in this lane's column of a 16-key tile for one row:
+// the H / 16 matrix steps (16 heads x 16 keys, the whole head dimension per
+// step), the key's scale, ReLU, the head weights wv (LDS, float4 per lane
+// quarter) and the sum over heads; every lane of the key's column ends with
+// it. The main loop and the fused guess both score keys here, so a sampled
+// key's score equals the one written for it.
+template <int H>
+__device__ __forceinline__ float tile_score(const v8i (&qa)[H / 16], const v8i& kb, float ks, const float4* wv,
+                                            int quarter) {
+    constexpr int MT = H / 16;
+    v4f acc[MT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+        acc[mt] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(qa[mt], kb, v4f{0.f, 0.f, 0.f, 0.f}, 0, 0, 0,
+                                                                   kUnitScales, 0, kUnitScales);
+    float sum = 0.f;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+        const float4 wq = wv[4 * mt + quarter];   // heads 16 mt + 4 quarter + (0..3)
+        sum += wq.x * fmaxf(acc[mt][0] * ks, 0.f);
+        sum += wq.y * fmaxf(acc[mt][1] * ks, 0.f);
+        sum += wq.z * fmaxf(acc[mt][2] * ks, 0.f);
+        sum += wq.w * fmaxf(acc[mt][3] * ks, 0.f);
+    }
+    sum += __shfl_xor(sum, 16, kWave);
+    sum += __shfl_xor(sum, 32, kWave);   // the four lanes of the key now hold its score
+    return sum;
+}
+
+// The fused guess of row b = blockIdx.x - sample_base: wave w scores samples
+// [64 w, 64 w + 64) (four 16-key tiles; sample i is key prev[b][i * st],
+// valid if inside [0, n_b)), then wave 0 reduces the 256 samples as the
+// Top-K's Phase 1 does and writes the row's GuessStats words.
+template <int H, int D>
+__device__ void sample_guess(const IdxParams& p, int b, float* wl) {
+    constexpr int MT = H / 16;
+    __shared__ float sc[kGuessSamples];
+    __shared__ int sv[kGuessSamples];
+    __shared__ int gh[kGuessBins];
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int g = b / p.group;
+    int64_t n64 = p.row_len ? (int64_t)p.row_len[b] : p.ld;
+    n64 = n64 < 0 ? 0 : (n64 > p.ld ? p.ld : n64);
+    const int col = lane & 15, quarter = lane >> 4;
+    const int qoff = 32 * (quarter % (D / 32));
+    const bool qlive = 32 * quarter < D;
+    for (int j = lane; j < H; j += kWave) wl[j] = p.w[(int64_t)b * H + j];
+    v8i qa[MT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+        const v8i v = load32(p.q + (((int64_t)b * H + 16 * mt + col) * D + qoff));
+        qa[mt] = qlive ? v : v8i{0, 0, 0, 0, 0, 0, 0, 0};
+    }
+    __builtin_amdgcn_wave_barrier();
+    const float4* wv = reinterpret_cast<const float4*>(wl);
+    const int st = guess_stride(p.K), m = guess_count(p.K);
+    const int32_t* pv = p.prev + (int64_t)b * p.K;
+    const uint8_t* kg = p.k + (int64_t)g * p.ld * D + qoff;
+    const float* sg = p.k_scale + (int64_t)g * p.ld;
+    int64_t key[4];
+    bool ok[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+        const int i = 64 * wave + 16 * t + col;
+        const int64_t s = i < m ? (int64_t)pv[(int64_t)i * st] : -1;
+        ok[t] = s >= 0 && s < n64;
+        key[t] = ok[t] ? s : 0;   // an invalid sample scores key 0 (ld > 0), unused
+    }
+    v8i kb[4];
+    float ks[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+        kb[t] = load32(kg + key[t] * D);
+        ks[t] = sg[key[t]];
+    }
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+        const float v = tile_score<H>(qa, kb[t], ks[t], wv, quarter);
+        if (quarter == 0) {
+            sc[64 * wave + 16 * t + col] = v;
+            sv[64 * wave + 16 * t + col] = ok[t];
+        }
+    }
+    __syncthreads();
+    if (wave == 0) {
+        float gv[4];
+        bool gok[4];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            gok[c] = sv[lane + 64 * c] != 0;
+            gv[c] = gok[c] ? sc[lane + 64 * c] : 0.f;
+        }
+        const GuessStats gs = guess_from_samples(gv, gok, gh);
+        if (lane == 0) {
+            int32_t* o = p.gstats + (int64_t)b * p.K;
+            o[0] = (int32_t)gs.ts;
+            o[1] = gs.cnt;
+            o[2] = (int32_t)gs.mn;
+            o[3] = (int32_t)gs.mx;
+            o[4] = __float_as_int(gs.sum);
+        }
+    }
+}
+
 template <int H, int D, int RG>
 __global__ __launch_bounds__(kWaves * kWave) void indexer_kernel(IdxParams p) {
     constexpr int MT = H / 16;   // 16-head row tiles
+    __shared__ float wl[kWaves][RG * H];
+    if (p.prev && (int)blockIdx.x >= p.sample_base) {
+        const int b = (int)blockIdx.x - p.sample_base;
+        if (b < p.rows) sample_guess<H, D>(p, b, &wl[threadIdx.x >> 6][0]);
+        return;
+    }
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int G = p.group;
@@ -104,7 +226,6 @@ __global__ __launch_bounds__(kWaves * kWave) void indexer_kernel(IdxParams p) {
     const int qoff = 32 * (quarter % (D / 32));
     const bool qlive = 32 * quarter < D;
 
-    __shared__ float wl[kWaves][RG * H];
     for (int j = lane; j < RG * H; j += kWave) wl[wave][j] = p.w[row0 * H + j];
     v8i qa[RG][MT];
 #pragma unroll
@@ -126,7 +247,7 @@ __global__ __launch_bounds__(kWaves * kWave) void indexer_kernel(IdxParams p) {
     // the same value there, so loads, matrix steps and stores run without
     // branches and the loads stay in flight across iterations.
     const int tiles = (int)((s_end - s_begin + kTile - 1) / kTile);
-    auto key_of = [&](int u, int t) { return min(s_begin + (int64_t)u * kTile + 16 * t + col, s_end - 1); };
+    auto key_at = [&](int u, int t) { return min(s_begin + (int64_t)u * kTile + 16 * t + col, s_end - 1); };
     struct Slot {
         v8i kb[2];
         float ks[2];
@@ -135,7 +256,7 @@ __global__ __launch_bounds__(kWaves * kWave) void indexer_kernel(IdxParams p) {
         Slot r;
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
-            const int64_t key = key_of(u, t);
+            const int64_t key = key_at(u, t);
             r.kb[t] = load32(kg + key * D);
             r.ks[t] = sg[key];
         }
@@ -146,24 +267,9 @@ __global__ __launch_bounds__(kWaves * kWave) void indexer_kernel(IdxParams p) {
         for (int t = 0; t < 2; ++t) {
 #pragma unroll
             for (int rr = 0; rr < RG; ++rr) {
-                v4f acc[MT];
-#pragma unroll
-                for (int mt = 0; mt < MT; ++mt)
-                    acc[mt] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(
-                        qa[rr][mt], r.kb[t], v4f{0.f, 0.f, 0.f, 0.f}, 0, 0, 0, kUnitScales, 0, kUnitScales);
-                float sum = 0.f;
-#pragma unroll
-                for (int mt = 0; mt < MT; ++mt) {
-                    const float4 wq = wv[rr * (H / 4) + 4 * mt + quarter];   // heads 16 mt + 4 quarter + (0..3)
-                    sum += wq.x * fmaxf(acc[mt][0] * r.ks[t], 0.f);
-                    sum += wq.y * fmaxf(acc[mt][1] * r.ks[t], 0.f);
-                    sum += wq.z * fmaxf(acc[mt][2] * r.ks[t], 0.f);
-                    sum += wq.w * fmaxf(acc[mt][3] * r.ks[t], 0.f);
-                }
-                sum += __shfl_xor(sum, 16, kWave);
-                sum += __shfl_xor(sum, 32, kWave);   // the four lanes of the key now hold its score
+                const float sum = tile_score<H>(qa[rr], r.kb[t], r.ks[t], wv + rr * (H / 4), quarter);
                 // the run covers the longer row of the pair: store this row's own keys
-                const int64_t key = key_of(u, t);
+                const int64_t key = key_at(u, t);
                 if (key < nr[rr]) out[rr * p.ld + key] = sum;
             }
         }
@@ -231,7 +337,9 @@ gvr_status launch(IdxParams q, int64_t caches, void* stream) {
     const int64_t chunks = (q.ld + q.chunk_keys - 1) / q.chunk_keys;
     if (chunks * caches > 0x7FFFFFFF) return GVR_ERR_TOO_LONG;
     q.chunks = (int32_t)chunks;
-    const unsigned grid = (unsigned)(chunks * caches);
+    if (chunks * caches + (q.prev ? q.rows : 0) > 0x7FFFFFFF) return GVR_ERR_TOO_LONG;
+    q.sample_base = (int32_t)(chunks * caches);   // the fused guess's workgroups follow the key chunks
+    const unsigned grid = (unsigned)(chunks * caches + (q.prev ? q.rows : 0));
     hipLaunchKernelGGL((indexer_kernel<H, D, RG>), dim3(grid), dim3(kWaves * kWave), 0, (hipStream_t)stream, q);
     return hipGetLastError() == hipSuccess ? GVR_OK : GVR_ERR_HIP;
 }
@@ -248,13 +356,10 @@ gvr_status launch_rg(const IdxParams& q, int64_t caches, void* stream) {
     return launch<H, D, 1>(q, caches, stream);
 }
 
-}  // namespace
-
-extern "C" {
-
-gvr_status gvr_indexer_scores(const uint8_t* q, const float* w, const uint8_t* k, const float* k_scale,
-                              int64_t B, int32_t H, int32_t D, int32_t group, int64_t ld,
-                              const int32_t* row_len, float* scores, void* stream) {
+// The indexer launch; with prev (and gstats), also the fused guess.
+gvr_status indexer_launch(const uint8_t* q, const float* w, const uint8_t* k, const float* k_scale, int64_t B,
+                          int32_t H, int32_t D, int32_t group, int64_t ld, const int32_t* row_len, float* scores,
+                          const int32_t* prev, int32_t K, int32_t* gstats, void* stream) {
     if (B < 0 || ld < 0) return GVR_ERR_INVALID_ARG;
     if (!(H == 32 || H == 64 || H == 128) || !(D == 64 || D == 128)) return GVR_ERR_INVALID_ARG;
     if (group < 1 || group > kWaves || B % group != 0) return GVR_ERR_INVALID_ARG;
@@ -262,6 +367,7 @@ gvr_status gvr_indexer_scores(const uint8_t* q, const float* w, const uint8_t* k
     if (B == 0 || ld == 0) return GVR_OK;
     if (!q || !w || !k || !k_scale || !scores) return GVR_ERR_INVALID_ARG;
     if (((uintptr_t)q | (uintptr_t)k) & 15) return GVR_ERR_INVALID_ARG;   // 16-byte loads
+    if (B > 0x7FFFFFFF) return GVR_ERR_TOO_LONG;
     IdxParams p;
     p.q = q;
     p.w = w;
@@ -272,6 +378,10 @@ gvr_status gvr_indexer_scores(const uint8_t* q, const float* w, const uint8_t* k
     p.ld = ld;
     p.rows = (int32_t)B;
     p.group = group;
+    p.prev = gstats ? prev : nullptr;
+    p.gstats = gstats;
+    p.K = K;
+    p.sample_base = 0;
     const int rg = rows_per_wave(H, group);
     const int wpr = kWaves / (group / rg);
     p.chunk_keys = wpr * kTilesPerWave * kTile;
@@ -283,6 +393,16 @@ gvr_status gvr_indexer_scores(const uint8_t* q, const float* w, const uint8_t* k
     return D == 64 ? launch_rg<128, 64>(p, caches, stream) : launch_rg<128, 128>(p, caches, stream);
 }
 
+}  // namespace
+
+extern "C" {
+
+gvr_status gvr_indexer_scores(const uint8_t* q, const float* w, const uint8_t* k, const float* k_scale,
+                              int64_t B, int32_t H, int32_t D, int32_t group, int64_t ld,
+                              const int32_t* row_len, float* scores, void* stream) {
+    return indexer_launch(q, w, k, k_scale, B, H, D, group, ld, row_len, scores, nullptr, 0, nullptr, stream);
+}
+
 gvr_status gvr_indexer_topk(const uint8_t* q, const float* w, const uint8_t* k, const float* k_scale,
                             int64_t B, int32_t H, int32_t D, int32_t group, int64_t ld,
                             const int32_t* row_len, float* scores, const int32_t* prev_topk, int32_t K,
@@ -292,8 +412,22 @@ gvr_status gvr_indexer_topk(const uint8_t* q, const float* w, const uint8_t* k, 
     gvr_status st = gvr_topk_ex(scores, 0, ld, row_len, prev_topk, K, out_idx, stream, options, stats);
     if (st != GVR_OK) return st;
     if (B > 0 && !out_idx) return GVR_ERR_INVALID_ARG;
-    st = gvr_indexer_scores(q, w, k, k_scale, B, H, D, group, ld, row_len, scores, stream);
+    // The fused guess: the indexer scores each row's sample of prev_topk and
+    // leaves the row's guess statistics in the tail of its out_idx row, where
+    // the Top-K reads them (instead of gathering the sample's scores after
+    // the indexer). Not with the paper's Phase 2 schedule (which reads every
+    // guessed score) or without a guess.
+    gvr_host::CallOptions o;
+    int dummy = 0;
+    st = gvr_host::validate(&dummy, 1, 1, K, &dummy, options, 1, &o);
     if (st != GVR_OK) return st;
+    const bool fused = prev_topk && o.use_guess && !o.secant && K >= kGuessWords;
+    int32_t* gstats = fused && out_idx ? out_idx + (K - kGuessWords) : nullptr;
+    st = indexer_launch(q, w, k, k_scale, B, H, D, group, ld, row_len, scores, prev_topk, K, gstats, stream);
+    if (st != GVR_OK) return st;
+    if (fused)
+        return gvr_internal::topk_with_guess_stats(scores, B, ld, row_len, prev_topk, K, out_idx, stream, options,
+                                                   stats);
     return gvr_topk_ex(scores, B, ld, row_len, prev_topk, K, out_idx, stream, options, stats);
 }
 

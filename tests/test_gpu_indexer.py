@@ -136,6 +136,22 @@ def check_topk(got, exp_scores, mag, rl, K, H, D):
         assert not np.any(mask[s + tol < kth - tol.max()]), "row %d: a clearly smaller score was taken" % b
 
 
+def check_fused_guess(st, sc, rl, prev, K, what):
+    """gvr_indexer_topk's Top-K took each row's guess statistics from the
+    indexer (which scored the sampled keys itself): the same T_spec, valid
+    sample count, pmean, path and passes as gvr_topk_ex gathering the
+    sample from the same scores."""
+    import paper_2604_22312_amd as g
+    st2 = g.new_stats(sc.shape[0], DEV)
+    out2 = g.gvr_topk_ex(sc, rl, prev, K, stats=st2)
+    torch.cuda.synchronize()
+    a, b = g.decode_stats(st), g.decode_stats(st2)
+    for f in ("path", "passes", "spec_threshold", "spec_count", "guess_valid", "threshold", "candidates"):
+        assert torch.equal(a[f], b[f]), "%s: %s differs (fused guess)" % (what, f)
+    assert torch.equal(a["pmean"].view(torch.int32), b["pmean"].view(torch.int32)), "%s: pmean differs" % what
+    return out2
+
+
 @pytest.mark.parametrize("group", [1, 2])
 def test_indexer_topk_parity(group):
     """Two decode steps: the second is guided by the first step's Top-K."""
@@ -156,6 +172,9 @@ def test_indexer_topk_parity(group):
     check_topk_exact(out.cpu().numpy(), sc.cpu().numpy(), x.row_len[1].numpy(), K_TOPK,
                      "indexer + topk group=%d" % group)
     check_topk(out.cpu().numpy(), ex1, mag1, x.row_len[1].numpy(), K_TOPK, H, D)
+    out_u = check_fused_guess(st, sc, x.row_len[1].to(DEV), torch.from_numpy(prev).to(DEV), K_TOPK,
+                              "indexer + topk group=%d" % group)
+    assert torch.equal(out_u, out)
     # and without a guess (radix schedule inside gvr_topk)
     out2, _ = g.gvr_indexer_topk(x.q[1].to(DEV), x.w.to(DEV), x.k.to(DEV), x.k_scale.to(DEV), x.row_len[1].to(DEV),
                                  None, K_TOPK)
@@ -190,10 +209,43 @@ def test_indexer_topk_many_rows():
                      "indexer + topk, %d rows" % x.rows)
     check_topk(out.cpu().numpy(), ex1, mag1, x.row_len[1].numpy(), K_TOPK, H, D)
     assert "error" not in {g.PATH_NAMES[int(v)] for v in g.decode_stats(st)["path"].tolist()}
+    check_fused_guess(st, sc, x.row_len[1].to(DEV), torch.from_numpy(prev).to(DEV), K_TOPK,
+                      "indexer + topk, %d rows" % x.rows)
     out2, _ = g.gvr_indexer_topk(x.q[1].to(DEV), x.w.to(DEV), x.k.to(DEV), x.k_scale.to(DEV), x.row_len[1].to(DEV),
                                  None, K_TOPK)
     torch.cuda.synchronize()
     assert np.array_equal(out2.cpu().numpy(), out.cpu().numpy())
+
+
+@pytest.mark.parametrize("K,flags", [(2048, 4), (5, 0), (300, 0)], ids=["paper_schedule", "K5", "K300"])
+def test_indexer_topk_guess_variants(K, flags):
+    """gvr_indexer_topk with the paper's Phase 2 schedule (not fused: it
+    reads every guessed score), with a K below the fused guess's words (not
+    fused) and with K = 300 (fused, st = 2): exact Top-K of the call's own
+    scores, and the fused rows' statistics equal gvr_topk_ex's."""
+    import paper_2604_22312_amd as g
+    H, D, ld = 64, 128, 30000
+    x = inputs(3, 2, ld, [29000, 12000, 30000], H, D, seed=41 + K, steps=2)
+    ex0, _ = oracle_scores(x, 0)
+    prev = np.full((x.rows, K), -1, np.int32)
+    for b in range(x.rows):
+        n = int(x.row_len[0, b])
+        prev[b, :min(n, K)] = IX_argtopk(ex0[b, :n], K)
+    note("indexer + topk K=%d flags=%d" % (K, flags))
+    st = g.new_stats(x.rows, DEV)
+    pv = torch.from_numpy(prev).to(DEV)
+    out, sc = g.gvr_indexer_topk(x.q[1].to(DEV), x.w.to(DEV), x.k.to(DEV), x.k_scale.to(DEV), x.row_len[1].to(DEV),
+                                 pv, K, options={"flags": flags} if flags else None, stats=st)
+    torch.cuda.synchronize()
+    check_topk_exact(out.cpu().numpy(), sc.cpu().numpy(), x.row_len[1].numpy(), K, "indexer + topk K=%d" % K)
+    if flags == 0:
+        check_fused_guess(st, sc, x.row_len[1].to(DEV), pv, K, "indexer + topk K=%d" % K)
+        # the guess and the output in one buffer (the decode loop's in-place form)
+        inplace = pv.clone()
+        g.gvr_indexer_topk(x.q[1].to(DEV), x.w.to(DEV), x.k.to(DEV), x.k_scale.to(DEV), x.row_len[1].to(DEV),
+                           inplace, K, out_idx=inplace)
+        torch.cuda.synchronize()
+        assert torch.equal(inplace, out), "indexer + topk K=%d: prev_topk aliasing out_idx" % K
 
 
 def IX_argtopk(s, K):
