@@ -139,6 +139,15 @@ typedef struct gvr_options {
                               B <= 2 x the compute units (then 16); without
                               one, 4 waves for ld <= 4096, else 8. Two of
                               bits 4-6 together are an error.
+                              bit 7: the parts of a split row hand over
+                              through an agent-scope release / acquire on
+                              the arrival counter (the memory model's form:
+                              an L2 writeback and invalidate per part, 2 to
+                              16 % slower on split calls) instead of
+                              completed stores read through the XCD's shared
+                              L2 (the default: the parts of a row run on one
+                              XCD, and the last part of a row whose parts
+                              did not reads the row itself).
                               No bit changes the result. */
     int32_t parts;         /* workgroups per row, 1..16 (0 = chosen from B, ld
                               and the device's compute units; a forced value is

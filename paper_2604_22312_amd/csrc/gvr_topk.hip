@@ -154,6 +154,7 @@ struct Params {
     int32_t* part_wcnt;  // [rows][S][kSlotWaves] list length of each wave of each part
     int32_t* part_hist;  // [rows][S][kRefBins1] each part's first refine level over [T_spec, pmax]
     const int32_t* gstats; // or NULL: GuessStats words of every row (row stride K), from the indexer
+    int32_t ordered_merge; // arrival counter updated with agent-scope release / acquire
     uint64_t* part_list; // [rows][S][kPartCap] (fp32 bits | index << 32) of each part
 };
 
@@ -1378,7 +1379,10 @@ DEV void topk_body(const Params& p) {
             // updated by a device-scope atomic after the stores completed,
             // also counts the parts per XCD (5 bits per XCD above 16 bits of
             // arrivals): the last part uses the lists only if every part ran
-            // on its XCD, and otherwise reads the whole row itself.
+            // on its XCD, and otherwise reads the whole row itself. On request
+            // the atomic is an agent-scope release / acquire instead, the
+            // memory model's form of this handoff (it writes back and
+            // invalidates the XCD's L2 around the atomic).
             const int64_t slot0 = row * S;
             // The part's exact f(T_spec): every wave counted past its list's
             // capacity, so the sum is exact even after an overflow (bit 31).
@@ -1397,7 +1401,9 @@ DEV void topk_body(const Params& p) {
                 const uint32_t xcc = (uint32_t)__builtin_amdgcn_s_getreg((31 << 11) | 20) & 7u;   // HW_REG_XCC_ID
                 const uint64_t add = 1ull + (1ull << (16 + 5 * xcc));
                 const uint64_t old =
-                    __hip_atomic_fetch_add(p.arrivals + row, add, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    p.ordered_merge
+                        ? __hip_atomic_fetch_add(p.arrivals + row, add, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT)
+                        : __hip_atomic_fetch_add(p.arrivals + row, add, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 const uint64_t now = old + add;
                 sm.scal[3] = (int)(old & 0xFFFFu);
                 sm.scal[2] = (int)((now >> (16 + 5 * xcc)) & 31u) == S;   // all parts on this XCD
@@ -2399,6 +2405,7 @@ gvr_status run(const float* scores, int64_t B, int64_t ld, const int32_t* row_le
         q.part_hist = ws.part_hist;
         q.part_list = ws.part_list;
         q.gstats = (guess && gstats) ? gstats + r0 * K : nullptr;
+        q.ordered_merge = o.ordered_merge;
         const dim3 grid((unsigned)(rows_pad * parts));
         const hipStream_t hs = (hipStream_t)stream;
         if (plan.shape == kNWMid) {

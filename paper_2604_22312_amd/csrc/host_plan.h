@@ -48,6 +48,7 @@ struct CallOptions {
     int secant = 0;
     int paper_refine = 0;
     int shape = 0;          // 0: automatic
+    int ordered_merge = 0;  // agent-scope release / acquire at a split row's merge
 };
 
 inline gvr_status validate(const void* scores, int64_t B, int64_t ld, int32_t K, const void* out,
@@ -63,7 +64,7 @@ inline gvr_status validate(const void* scores, int64_t B, int64_t ld, int32_t K,
             if (opt->capacity < K || opt->capacity > GVR_MAX_CANDIDATES) return GVR_ERR_INVALID_ARG;
             o->capacity = opt->capacity;
         }
-        if ((opt->flags & ~127) || opt->reserved1) return GVR_ERR_INVALID_ARG;
+        if ((opt->flags & ~255) || opt->reserved1) return GVR_ERR_INVALID_ARG;
         const int forced = (opt->flags >> 4) & 7;
         if (forced & (forced - 1)) return GVR_ERR_INVALID_ARG;   // two shapes forced
         if (opt->parts < 0 || opt->parts > kMaxParts) return GVR_ERR_INVALID_ARG;
@@ -71,6 +72,7 @@ inline gvr_status validate(const void* scores, int64_t B, int64_t ld, int32_t K,
         o->scatter = (opt->flags >> 1) & 1;
         o->secant = (opt->flags >> 2) & 1;
         o->paper_refine = (opt->flags >> 3) & 1;
+        o->ordered_merge = (opt->flags >> 7) & 1;
         o->shape = forced == 1 ? kNWShort : forced == 2 ? kNWLong : forced == 4 ? kNWMid : 0;
         o->parts = opt->parts;
     }

@@ -62,12 +62,13 @@ static void check_validate() {
     CHECK(validate(nullptr, 4, 100, 16, &dummy, nullptr, 1, &o) == GVR_ERR_INVALID_ARG);
     CHECK(validate(nullptr, 0, 100, 16, nullptr, nullptr, 1, &o) == GVR_OK);
     CHECK(validate(&dummy, 1, (int64_t)1 << 40, 16, &dummy, nullptr, 1, &o) == GVR_ERR_TOO_LONG);
-    gvr_options bad[] = {{100, 0, 0, 0}, {0, 48, 0, 0}, {0, 128, 0, 0}, {0, 0, 17, 0}, {0, 0, -1, 0}, {0, 0, 0, 1},
+    gvr_options bad[] = {{100, 0, 0, 0}, {0, 48, 0, 0}, {0, 256, 0, 0}, {0, 0, 17, 0}, {0, 0, -1, 0}, {0, 0, 0, 1},
                          {20000, 0, 0, 0}};
     for (const auto& b : bad) CHECK(validate(&dummy, 2, 100, 128, &dummy, &b, 1, &o) == GVR_ERR_INVALID_ARG);
-    gvr_options good = {4096, 1 | 8 | 64, 3, 0};
+    gvr_options good = {4096, 1 | 8 | 64 | 128, 3, 0};
     CHECK(validate(&dummy, 2, 100, 128, &dummy, &good, 1, &o) == GVR_OK);
-    CHECK(o.capacity == 4096 && o.use_guess == 0 && o.paper_refine == 1 && o.shape == kNWMid && o.parts == 3);
+    CHECK(o.capacity == 4096 && o.use_guess == 0 && o.paper_refine == 1 && o.shape == kNWMid && o.parts == 3 &&
+          o.ordered_merge == 1);
 }
 
 static void check_plans() {

@@ -84,7 +84,7 @@ def test_options_validation(L):
            g.Options(capacity=0, flags=80, parts=0, reserved1=0),       # two workgroup shapes forced
            g.Options(capacity=0, flags=96, parts=0, reserved1=0),       # two workgroup shapes forced
            g.Options(capacity=0, flags=112, parts=0, reserved1=0),      # three workgroup shapes forced
-           g.Options(capacity=0, flags=128, parts=0, reserved1=0),      # unknown flag bit
+           g.Options(capacity=0, flags=256, parts=0, reserved1=0),      # unknown flag bit
            g.Options(capacity=0, flags=0, parts=0, reserved1=1),        # reserved field set
            g.Options(capacity=0, flags=0, parts=17, reserved1=0),       # too many parts
            g.Options(capacity=0, flags=0, parts=-1, reserved1=0),       # negative parts
@@ -160,7 +160,7 @@ def test_indexer_validation(L):
     assert L.gvr_indexer_topk(a, a, a, a, 4, 64, 128, 2, 100, None, a, None, 0, a, None, None, None) == -2
     assert L.gvr_indexer_topk(a, a, a, a, 4, 64, 128, 2, 100, None, a, None, 2049, a, None, None, None) == -2
     import paper_2604_22312_amd as g
-    bad = g.Options(capacity=0, flags=128, parts=0, reserved1=0)
+    bad = g.Options(capacity=0, flags=256, parts=0, reserved1=0)
     assert L.gvr_indexer_topk(a, a, a, a, 4, 64, 128, 2, 100, None, a, None, 16, a, None, ctypes.byref(bad),
                               None) == -1
     assert L.gvr_indexer_topk(a, a, a, a, 4, 64, 128, 2, 100, None, a, None, 16, None, None, None, None) == -1

@@ -351,6 +351,36 @@ def test_parts_do_not_change_the_answer():
                 assert int(d["candidates"][r]) == cnt
 
 
+@pytest.mark.parametrize("case", [(2, 2, 4, None, 3), (3, 2, 8, "a", 8), (3, 2, 8, "b", 8), (4, 2, 2, None, 5)],
+                         ids=["c2_p3", "c3a_p8", "c3b_p8", "c4_p5"])
+def test_ordered_merge(case):
+    """Option flag 128 (agent-scope release / acquire at the split-row
+    handoff): the oracle's answer on split rows, including rows whose guess
+    fails (random previous Top-K), and the same row stats as the default
+    handoff."""
+    import paper_2604_22312_amd as g
+    cfg, steps, queries, sub, parts = case
+    w = workload(cfg, steps, queries, sub)
+    K = w.K
+    S = w.scores[1].to(DEV)
+    RL = w.row_len[1].to(DEV)
+    exp, _, _ = oracle.topk(w.scores[1].numpy(), K, row_len=w.row_len[1].numpy())
+    if w.random_prev is not None:
+        pd = w.random_prev[1].to(DEV)
+    else:
+        prev, _, _ = oracle.topk(w.scores[0].numpy(), K, row_len=w.row_len[0].numpy())
+        pd = torch.from_numpy(prev).to(DEV)
+    note("ordered merge c%d%s parts=%d" % (cfg, sub or "", parts))
+    st1, st2 = g.new_stats(w.rows, DEV), g.new_stats(w.rows, DEV)
+    out = g.gvr_topk_ex(S, RL, pd, K, options={"parts": parts, "flags": 128}, stats=st1)
+    assert_rows_equal(out.cpu().numpy(), exp, "ordered merge c%d%s parts=%d" % (cfg, sub or "", parts))
+    g.gvr_topk_ex(S, RL, pd, K, options={"parts": parts}, stats=st2)
+    torch.cuda.synchronize()
+    a, b = g.decode_stats(st1), g.decode_stats(st2)
+    for f in ("path", "passes", "threshold", "candidates", "spec_count"):
+        assert torch.equal(a[f], b[f]), f
+
+
 def test_parts_on_different_xcds():
     """Parts of a row placed on different XCDs (flag bit 1): the last part
     cannot use the lists through a shared L2 and reads the row itself; the
