@@ -45,9 +45,17 @@ def log(msg):
     sys.stderr.flush()
 
 
+KERNEL_SOURCES = ("gvr_topk.hip", "host_plan.h", "wave_ops.h", "guess.h", "topk_internal.h")
+
+
 def kernel_source_hash() -> str:
-    with open(os.path.join(ROOT, "paper_2604_22312_amd", "csrc", "gvr_topk.hip"), "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    """sha256[:16] of the Top-K kernel's source and the headers it includes
+    (in this order): the key under which measured counters are kept."""
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2604_22312_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def build_inputs(dev, config=CONFIG, sub=None, steps=None):
