@@ -87,7 +87,6 @@ using gvr_host::kNWLong;
 using gvr_host::kNWMid;
 using gvr_host::kNWShort;
 using gvr_host::kPartCap;
-using gvr_host::kSlotWaves;
 using gvr_host::kXcds;
 using namespace gvr_dev;
 
@@ -117,7 +116,7 @@ static_assert(Shape<kNWLong>::kCap == gvr_host::kCapLong && Shape<kNWMid>::kCap 
                   Shape<kNWShort>::kCap == gvr_host::kCapShort,
               "shape capacities as the host plans them");
 static_assert(Shape<kNWLong>::kCap == GVR_MAX_CANDIDATES, "the long-row shape holds the largest capacity");
-static_assert(kSlotWaves == kNWLong && kPartCap == Shape<kNWLong>::kCap, "a workspace slot holds one part's lists");
+static_assert(kPartCap == Shape<kNWLong>::kCap, "a workspace slot holds one part's lists");
 constexpr int kRefBins = 4096;                 // bins of a narrowing refine level (12 bits of key)
 constexpr int kRefBins1 = 2048;                // bins of the first refine level (32 per lane of one wave)
 constexpr int kDigitShift = 21;                // radix digit: the top 11 key bits, one first-level bin each
@@ -151,7 +150,6 @@ struct Params {
                          // bit 16; 0 between calls
     int32_t* part_count; // [rows][S] f(threshold) of each part, bit 31 = a wave list overflowed
     uint32_t* part_thresh; // [rows][S] threshold of each part's list (T_spec, the same in every part)
-    int32_t* part_wcnt;  // [rows][S][kSlotWaves] list length of each wave of each part
     int32_t* part_hist;  // [rows][S][kRefBins1] each part's first refine level over [T_spec, pmax]
     const int32_t* gstats; // or NULL: GuessStats words of every row (row stride K), from the indexer
     int32_t ordered_merge; // arrival counter updated with agent-scope release / acquire
@@ -425,7 +423,9 @@ DEV void seg_scan(Smem<NW>& sm, int nseg, int lane) {
 }
 
 // Exact K-th key among the listed candidates. The K-th key lies in
-// [wlo, whi]; `above` listed candidates lie above whi.
+// [wlo, whi]; `above` listed candidates lie above whi. Histogram levels of
+// kRefBins bins narrow the window; the first also finds the window's
+// smallest and largest listed key, and if they are one key it is the K-th.
 template <int NW>
 DEV uint32_t refine_kth(Smem<NW>& sm, uint32_t wlo, uint32_t whi, int above, int K, int tid) {
     using W = Shape<NW>;
@@ -437,18 +437,36 @@ DEV uint32_t refine_kth(Smem<NW>& sm, uint32_t wlo, uint32_t whi, int above, int
         const uint32_t s = bin_shift(width, log2i(kRefBins));
         for (int i = tid; i < kRefBins; i += W::kBlock) sm.u.rhist[i] = 0;
         lds_barrier();
+        uint32_t kmn = 0xFFFFFFFFu, kmx = 0u;   // the first level also finds the window's smallest and largest key
         for (int q = 0; q < nq; ++q) {
             const int j = wave + NW * q;
             const uint2* seg = sm.list + sm.seg_off[j];
             const int cnt = sm.seg_cnt[j];
             for (int i = lane; i < cnt; i += kWave) {
                 const uint32_t kk = seg[i].x;
-                if (kk >= wlo && kk <= whi)
+                if (kk >= wlo && kk <= whi) {
                     __hip_atomic_fetch_add(&sm.u.rhist[(kk - wlo) >> s], 1, __ATOMIC_RELAXED,
                                            __HIP_MEMORY_SCOPE_WORKGROUP);
+                    kmn = min(kmn, kk);
+                    kmx = max(kmx, kk);
+                }
+            }
+        }
+        if (level == 0) {
+            kmn = wave_min_u(kmn);
+            kmx = wave_max_u(kmx);
+            if (lane == 0) {
+                sm.red[2][wave] = (int)kmn;
+                sm.red[3][wave] = (int)kmx;
             }
         }
         lds_barrier();
+        if (level == 0) {
+            // one key in the window (ties, as in rounded scores): it is T*
+            const uint32_t mn = wave_min_u(lane < NW ? (uint32_t)sm.red[2][lane] : 0xFFFFFFFFu);
+            const uint32_t mx = wave_max_u(lane < NW ? (uint32_t)sm.red[3][lane] : 0u);
+            if (mn == mx) return mn;
+        }
         constexpr int PER = kRefBins / W::kBlock;   // 4 bins per thread
         int loc[PER];
         int mine = 0;
@@ -772,14 +790,13 @@ DEV void kth_bin_wave0(Smem<NW>& sm, const int* hb, int need0, int base, int lan
 // key lies in [rlo, rhi]; `above` listed keys lie above rhi. One histogram
 // level of kRefBins1 bins over [rlo, bin_hi] (keys in (bin_hi, rhi] count in
 // the top bin; built here unless `hist_ready`), then wave 0 finds the
-// bin b holding the K-th key with two wave scans. One pass over the lists
-// counts each segment's keys above b. If b holds at most kSmall candidates,
-// the pass also copies them (with their segment) to a small LDS array; wave 0
-// takes one candidate per lane, selects T* among them and the per-segment
-// emission offsets, and every wave emits its segments. Otherwise the pass
-// finds b's smallest and largest candidate keys and its count per segment:
-// if they are one key, that key is T*; else histogram narrowing (refine_kth)
-// continues between them.
+// bin b holding the K-th key with two wave scans. If b holds at most kSmall
+// candidates, one pass over the lists copies them (with their segment) to a
+// small LDS array and counts each segment's keys above b; wave 0 takes one
+// candidate per lane, selects T* among them and the per-segment emission
+// offsets, and every wave emits its segments. Otherwise histogram narrowing
+// (refine_kth) continues inside b; a bin whose keys are all one value (ties)
+// is resolved by its first level.
 template <int NW>
 DEV uint32_t refine_emit(Smem<NW>& sm, uint32_t rlo, uint32_t rhi, uint32_t bin_hi, int above, int K, int32_t* out,
                          int tid, int* n_gt_out, bool hist_ready) {
@@ -812,23 +829,24 @@ DEV uint32_t refine_emit(Smem<NW>& sm, uint32_t rlo, uint32_t rhi, uint32_t bin_
         emit_from_lists(sm, lo_b, K, out, tid, n_gt_out);
         return lo_b;
     }
+    if (cnt_b > kSmall) {   // narrowing inside the bin (a bin of one key ends after its first level)
+        lds_barrier();
+        const uint32_t kth = refine_kth(sm, lo_b, hi_b, above_b, K, tid);
+        emit_from_lists(sm, kth, K, out, tid, n_gt_out);
+        return kth;
+    }
     // Copy bin b's candidates, with their segment, to one small LDS array over
-    // the histogram (no longer needed; up to kSmall of them): a chunk that
+    // the histogram (no longer needed; at most kSmall of them): a chunk that
     // holds some (rare) reserves room with one LDS atomic. Each wave counts
-    // its segments' keys above the bin. A bin of more than kSmall candidates
-    // also gets its smallest and largest key and its count per segment: a bin
-    // whose candidates are all one key (ties, as in rounded scores) is
-    // resolved by this pass alone.
+    // its segments' keys above the bin.
     uint4* const small = reinterpret_cast<uint4*>(sm.u.rhist);
     uint32_t* const skey = reinterpret_cast<uint32_t*>(small + kSmall);   // their keys alone, for the rank
     const uint32_t wid = hi_b - lo_b;
-    const bool big = cnt_b > kSmall;
-    uint32_t bmin = 0xFFFFFFFFu, bmax = 0u;
     for (int q = 0; q < nq; ++q) {
         const int j = wave + NW * q;
         const uint2* seg = sm.list + sm.seg_off[j];
         const int cnt = sm.seg_cnt[j];
-        int gtl = 0, inl = 0;
+        int gtl = 0;
         for (int i0 = 0; i0 < cnt; i0 += 4 * kWave) {
             const int rem = cnt - i0;
             uint2 en[4];
@@ -840,62 +858,26 @@ DEV uint32_t refine_emit(Smem<NW>& sm, uint32_t rlo, uint32_t rhi, uint32_t bin_
                 gtl = add_lane_bit(gtl, __ballot(en[c].x > hi_b) & vm);
                 const uint64_t m = __ballot(en[c].x - lo_b <= wid) & vm;
                 if (m) {   // rare (wave-uniform)
-                    const bool in = (m >> lane) & 1;
-                    if (big) {
-                        inl += in;
-                        bmin = in ? min(bmin, en[c].x) : bmin;
-                        bmax = in ? max(bmax, en[c].x) : bmax;
-                    } else {
-                        int base = 0;
-                        if (lane == 0)
-                            base = __hip_atomic_fetch_add(&sm.scal[1], (int)__popcll(m), __ATOMIC_RELAXED,
-                                                          __HIP_MEMORY_SCOPE_WORKGROUP);
-                        base = __builtin_amdgcn_readfirstlane(base);
-                        const int pos = base + (int)lanes_below(m, 0);
-                        if (in && pos < kSmall) {
-                            small[pos] = make_uint4(en[c].x, en[c].y, (uint32_t)j, 0u);
-                            skey[pos] = en[c].x;
-                        }
+                    int base = 0;
+                    if (lane == 0)
+                        base = __hip_atomic_fetch_add(&sm.scal[1], (int)__popcll(m), __ATOMIC_RELAXED,
+                                                      __HIP_MEMORY_SCOPE_WORKGROUP);
+                    base = __builtin_amdgcn_readfirstlane(base);
+                    const int pos = base + (int)lanes_below(m, 0);
+                    if (((m >> lane) & 1) && pos < kSmall) {
+                        small[pos] = make_uint4(en[c].x, en[c].y, (uint32_t)j, 0u);
+                        skey[pos] = en[c].x;
                     }
                 }
             }
         }
         const int gt_hi = wave_sum(gtl);
-        const int in_b = big ? wave_sum(inl) : 0;
         if (lane == 0) {
             sm.sga[j] = gt_hi;
-            sm.sgb[j] = in_b;
-        }
-    }
-    if (big) {
-        bmin = wave_min_u(bmin);
-        bmax = wave_max_u(bmax);
-        if (lane == 0) {
-            sm.wa[wave] = (int)bmin;
-            sm.wb[wave] = (int)bmax;
+            sm.sgb[j] = 0;
         }
     }
     lds_barrier();
-    if (big) {
-        uint32_t mn = 0xFFFFFFFFu, mx = 0u;
-#pragma unroll
-        for (int w = 0; w < NW; ++w) {
-            mn = min(mn, (uint32_t)sm.wa[w]);
-            mx = max(mx, (uint32_t)sm.wb[w]);
-        }
-        if (mn == mx) {   // every candidate of bin b is T* = mn: sga / sgb hold keys > T* / == T*
-            if (wave == 0) seg_scan(sm, NW * nq, lane);
-            lds_barrier();
-            const int gtot = sm.scal[5];
-            emit_segments(sm, mn, K, K - gtot, out, lane, wave);
-            *n_gt_out = gtot;
-            return mn;
-        }
-        // the K-th key lies in [mn, mx]; the listed keys above mx are those above the bin
-        const uint32_t kth = refine_kth(sm, mn, mx, above_b, K, tid);
-        emit_from_lists(sm, kth, K, out, tid, n_gt_out);
-        return kth;
-    }
     if (wave == 0) {
         // Lane l takes the l-th copied candidate (any order).
         const bool v = lane < cnt_b;
@@ -1089,7 +1071,7 @@ DEV void topk_body(const Params& p) {
         const int lane16 = lane * 16, qlast16 = qlast * 16;
         const int off_last = (sqb + max(nsl - 1, 0) * 64) * 16;   // the wave's last slab
         auto slab_load = [&](int s) {
-            return buf_load16_nt(rrow, min(lane16 + min((sqb + s * 64) * 16, off_last), qlast16));
+            return buf_load16(rrow, min(lane16 + min((sqb + s * 64) * 16, off_last), qlast16));
         };
         float4 buf[kSU];
         if (nsl > 0) {
@@ -1263,18 +1245,8 @@ DEV void topk_body(const Params& p) {
         // Every wave turns its list into keys in place and adds them to the
         // refine's first histogram level over [T_spec, max(pmax, T_spec)]
         // (cleared by wave 0 before its flag): waves done with their slabs
-        // do this while the others still stream. A part of a split row also
-        // publishes the wave's list and its length right away (no wait): the
-        // row's last part may merge it.
+        // do this while the others still stream.
         keys_in_place(sm, lw, cnt_w <= W::kCapW ? cnt_w : stored_w, own_hist, tspec, hsh, lane);
-        if (S > 1) {
-            const int64_t slot = row * S + part;
-            if (cnt_w <= W::kCapW) {
-                uint64_t* pl = p.part_list + slot * kPartCap + wave * W::kCapW;
-                for (int i = lane; i < cnt_w; i += kWave) pl[i] = pack_entry(lw[i].x, lw[i].y);
-            }
-            if (lane == 0) p.part_wcnt[slot * kSlotWaves + wave] = cnt_w;
-        }
         if (lane == 0) {
             sm.wa[wave] = cnt_w;
             sm.seg_cnt[wave] = min(cnt_w, W::kCapW);
@@ -1369,9 +1341,9 @@ DEV void topk_body(const Params& p) {
         }
 
         if (S > 1) {
-            // ---------------- the part's count; the last part of the row goes on.
-            // The waves published their lists and list lengths as they
-            // finished. The parts of a row are launched on one XCD (the grid
+            // ---------------- publish the part; the last part of the row goes on.
+            // Each wave writes its list at its offset in the part's packed,
+            // index-ordered list. The parts of a row are launched on one XCD (the grid
             // mapping), so they share its L2: a part's plain stores have
             // reached that L2 once they complete (the vector L1 writes
             // through), and the last part reads them back from it with
@@ -1387,11 +1359,18 @@ DEV void topk_body(const Params& p) {
             // The part's exact f(T_spec): every wave counted past its list's
             // capacity, so the sum is exact even after an overflow (bit 31).
             const int f_part = sum_over_waves<NW>(sm.wa, lane);
+            if (!overflow) {
+                const int off_w = sum_over_waves_below(sm.wa, lane, wave);
+                uint64_t* pl = p.part_list + (slot0 + part) * kPartCap + off_w;
+                const uint2* lw = sm.list + wave * W::kCapW;
+                const int cnt = sm.wa[wave];
+                for (int i = lane; i < cnt; i += kWave) pl[i] = pack_entry(lw[i].x, lw[i].y);
+            }
             if (tid == 0) {
                 p.part_count[slot0 + part] = (int32_t)((uint32_t)f_part | (overflow ? 0x80000000u : 0u));
                 p.part_thresh[slot0 + part] = tthr;
             }
-            if (own_hist) {   // this part's first refine level, as bin pairs (summed after an overflow)
+            if (own_hist && overflow) {   // this part's first refine level, as bin pairs (its list is incomplete)
                 uint64_t* ph = reinterpret_cast<uint64_t*>(p.part_hist + (slot0 + part) * kRefBins1);
                 for (int i = tid; i < kRefBins1 / 2; i += W::kBlock) ph[i] = reinterpret_cast<const uint64_t*>(sm.u.rhist)[i];
             }
@@ -1415,24 +1394,20 @@ DEV void topk_body(const Params& p) {
                 overflow = true;   // lists unusable: the fallback reads the whole row
                 f_spec = -1;
             } else {
-                // One round trip: every part's count and threshold and its
-                // per-wave list lengths (lane q: part q).
+                // One round trip: every part's count and threshold (lane q:
+                // part q) and, with at most four parts, the first entries of
+                // every part's packed list (thread t: entries t + j * block),
+                // loaded before it is known how many exist.
                 const int c_tot = lane < S ? ld_agent(p.part_count + slot0 + lane) : 0;
                 const uint32_t tp = lane < S ? (uint32_t)ld_agent((const int32_t*)p.part_thresh + slot0 + lane) : 0u;
-                const auto rwc = row_rsrc(p.part_wcnt + slot0 * kSlotWaves, S * kSlotWaves * 4);
-                int4 wc[kSlotWaves / 4];
+                const bool spec_ld = S <= 4;
+                const int spec_j = S <= 2 ? 2 : 1;   // chunks of one block per part
+                uint64_t ev[4];
 #pragma unroll
-                for (int i = 0; i < kSlotWaves / 4; ++i) wc[i] = ld_agent16(rwc, lane * kSlotWaves * 4 + 16 * i);
-                // Lane q: part q's segment `wave` (c_w entries), the entries
-                // of its segments before it, and its total.
-                int c_w = 0, before_w = 0, tot_q = 0;
-#pragma unroll
-                for (int i = 0; i < kSlotWaves; ++i) {
-                    const int4 v4 = wc[i / 4];
-                    const int v = (i & 3) == 0 ? v4.x : (i & 3) == 1 ? v4.y : (i & 3) == 2 ? v4.z : v4.w;
-                    tot_q += v;
-                    before_w += i < wave ? v : 0;
-                    c_w = i == wave ? v : c_w;
+                for (int k = 0; k < 4; ++k) {
+                    const int q = spec_j == 2 ? k >> 1 : k, j = spec_j == 2 ? k & 1 : 0;
+                    ev[k] = (spec_ld && q < S) ? ld_agent(p.part_list + (slot0 + q) * kPartCap + tid + j * W::kBlock)
+                                               : 0ull;
                 }
                 // Totals of the row. Every part computes the same T_spec from
                 // the same data; a part that kept another threshold (or
@@ -1440,75 +1415,115 @@ DEV void topk_body(const Params& p) {
                 const bool ovf = wave_max_u(lane < S && c_tot < 0 ? 1u : 0u) != 0u;
                 const uint32_t trow = wave_max_u(tp);
                 const bool mixed = wave_min_u(lane < S ? tp : 0xFFFFFFFFu) != trow;
-                f_spec = mixed ? -1 : wave_sum(c_tot & 0x7FFFFFFF);
-                const int incl_t = wave_incl_scan(tot_q, lane);
-                overflow = ovf || mixed || __builtin_amdgcn_readlane(incl_t, kWave - 1) != f_spec;
+                const int cc = c_tot & 0x7FFFFFFF;
+                f_spec = mixed ? -1 : wave_sum(cc);
+                overflow = ovf || mixed;
                 tthr = trow;
+                const int coff = wave_incl_scan(cc, lane) - cc;   // lane q: part q's offset in the merged list
                 if (!mixed && own_hist && f_spec > cap) {
-                    // The row's first refine level: the sum of the parts'
-                    // (bin pair tid of every part in one round trip), which
-                    // counts every key >= T_spec of the row.
+                    // The row's first refine level, which counts every key
+                    // >= T_spec of the row: this part's own, plus the
+                    // published level of every other part whose list
+                    // overflowed (bin pair tid of each in one round trip),
+                    // then the keys of the other parts' complete lists.
+                    const uint32_t ovf_parts = (uint32_t)__ballot(lane < S && lane != part && c_tot < 0);
                     for (int i = tid; i < kRefBins1 / 2; i += W::kBlock) {
                         uint64_t hv[kMaxParts];
 #pragma unroll
                         for (int k = 0; k < kMaxParts; ++k)
-                            hv[k] = k < S ? ld_agent(reinterpret_cast<const uint64_t*>(p.part_hist + (slot0 + k) * kRefBins1) + i)
-                                          : 0ull;
-                        int sx = 0, sy = 0;
+                            hv[k] = ((ovf_parts >> k) & 1u)
+                                        ? ld_agent(reinterpret_cast<const uint64_t*>(p.part_hist + (slot0 + k) * kRefBins1) + i)
+                                        : 0ull;
+                        int2 h = reinterpret_cast<const int2*>(sm.u.rhist)[i];
 #pragma unroll
                         for (int k = 0; k < kMaxParts; ++k) {
-                            sx += (int)(uint32_t)hv[k];
-                            sy += (int)(uint32_t)(hv[k] >> 32);
+                            h.x += (int)(uint32_t)hv[k];
+                            h.y += (int)(uint32_t)(hv[k] >> 32);
                         }
-                        reinterpret_cast<int2*>(sm.u.rhist)[i] = make_int2(sx, sy);
+                        reinterpret_cast<int2*>(sm.u.rhist)[i] = h;
+                    }
+                    lds_barrier();   // the sums are in before the list keys are added
+                    const uint32_t hsh2 = ref_shift(trow, max(gmax, trow));
+                    for (int q = 0; q < S; ++q) {
+                        const int cq = __builtin_amdgcn_readlane(c_tot, q);
+                        if (q == part || cq < 0) continue;   // (wave-uniform)
+                        const uint64_t* src = p.part_list + (slot0 + q) * kPartCap;
+                        for (int i0 = 0; i0 < cq; i0 += 4 * W::kBlock) {
+                            uint64_t e[4];
+#pragma unroll
+                            for (int u = 0; u < 4; ++u) {
+                                const int i = i0 + u * W::kBlock + tid;
+                                e[u] = i < cq ? ld_agent(src + i) : 0ull;
+                            }
+#pragma unroll
+                            for (int u = 0; u < 4; ++u)
+                                if (i0 + u * W::kBlock + tid < cq) ref_hist_add(sm, (uint32_t)e[u], trow, hsh2);
+                        }
                     }
                     hist_full = true;   // complete behind the fallback's first barrier
                 }
                 if (!overflow && f_spec >= K && f_spec <= cap) {
-                    // The merged list: every part's segments (the own part's
-                    // too, from the workspace) packed in (part, wave) order,
-                    // which is index order, then cut into one even segment
-                    // per wave, so that the refine walks NW segments whatever
-                    // the number of parts. Wave w copies segments (q, w),
-                    // four parts' first 64 entries in flight at a time; the
+                    // The merged list: the parts' packed lists one after the
+                    // other (index order), split evenly over the waves. The
                     // other parts' keys join the refine's first level, which
                     // holds the own part's already.
-                    const int base_q = incl_t - tot_q + before_w;   // lane q: start of segment (q, wave)
                     const uint32_t msh = ref_shift(trow, max(gmax, trow));
-                    const uint64_t* src_w = p.part_list + slot0 * kPartCap + wave * W::kCapW;
-                    auto put = [&](int P, uint64_t e, bool other) {
+                    auto put = [&](int P, uint64_t e, int q) {
                         sm.list[P] = make_uint2((uint32_t)e, (uint32_t)(e >> 32));
-                        if (other && !all_mode) ref_hist_add(sm, (uint32_t)e, trow, msh);
+                        if (q != part && !all_mode) ref_hist_add(sm, (uint32_t)e, trow, msh);
                     };
-                    for (int q0 = 0; q0 < S; q0 += 4) {
-                        uint64_t e[4];
-                        int cq[4], bq[4];
+                    if (spec_ld) {
 #pragma unroll
-                        for (int c = 0; c < 4; ++c) {
-                            const int q = min(q0 + c, S - 1);
-                            cq[c] = q0 + c < S ? __builtin_amdgcn_readlane(c_w, q) : 0;
-                            bq[c] = __builtin_amdgcn_readlane(base_q, q);
-                            e[c] = lane < cq[c] ? ld_agent(src_w + (int64_t)q * kPartCap + lane) : 0ull;
+                        for (int k = 0; k < 4; ++k) {
+                            const int q = spec_j == 2 ? k >> 1 : k, j = spec_j == 2 ? k & 1 : 0;
+                            const int qq = min(q, S - 1);
+                            const int cq = __builtin_amdgcn_readlane(cc, qq), oq = __builtin_amdgcn_readlane(coff, qq);
+                            const int i = tid + j * W::kBlock;
+                            if (q < S && i < cq) put(oq + i, ev[k], q);
                         }
-#pragma unroll
-                        for (int c = 0; c < 4; ++c)
-                            if (lane < cq[c]) put(bq[c] + lane, e[c], q0 + c != part);
-                        // entries past the first 64 (long segments), four per lane in flight
-#pragma unroll
-                        for (int c = 0; c < 4; ++c) {
-                            const uint64_t* src = src_w + (int64_t)min(q0 + c, S - 1) * kPartCap;
-                            for (int i0 = kWave; i0 < cq[c]; i0 += 4 * kWave) {
-                                uint64_t t[4];
+                        // entries past the first spec_j blocks of a part (long lists)
+                        for (int q = 0; q < S; ++q) {
+                            const int cq = __builtin_amdgcn_readlane(cc, q), oq = __builtin_amdgcn_readlane(coff, q);
+                            const uint64_t* src = p.part_list + (slot0 + q) * kPartCap;
+                            for (int i0 = spec_j * W::kBlock; i0 < cq; i0 += 4 * W::kBlock) {
+                                uint64_t e[4];
 #pragma unroll
                                 for (int u = 0; u < 4; ++u) {
-                                    const int i = i0 + u * kWave + lane;
-                                    t[u] = i < cq[c] ? ld_agent(src + i) : 0ull;
+                                    const int i = i0 + u * W::kBlock + tid;
+                                    e[u] = i < cq ? ld_agent(src + i) : 0ull;
                                 }
 #pragma unroll
                                 for (int u = 0; u < 4; ++u) {
-                                    const int i = i0 + u * kWave + lane;
-                                    if (i < cq[c]) put(bq[c] + i, t[u], q0 + c != part);
+                                    const int i = i0 + u * W::kBlock + tid;
+                                    if (i < cq) put(oq + i, e[u], q);
                                 }
+                            }
+                        }
+                    } else {
+                        // Thread t owns merged positions t + j * block and
+                        // loads four of them (from their parts' lists) before
+                        // it stores any.
+                        for (int j0 = 0; j0 * W::kBlock < f_spec; j0 += 4) {
+                            int qj[4] = {0, 0, 0, 0}, oj[4] = {0, 0, 0, 0};
+                            for (int q = 1; q < S; ++q) {
+                                const int bq = __builtin_amdgcn_readlane(coff, q);
+#pragma unroll
+                                for (int u = 0; u < 4; ++u) {
+                                    const bool past = tid + (j0 + u) * W::kBlock >= bq;
+                                    qj[u] += past;
+                                    oj[u] = past ? bq : oj[u];
+                                }
+                            }
+                            uint64_t e[4];
+#pragma unroll
+                            for (int u = 0; u < 4; ++u) {
+                                const int P = tid + (j0 + u) * W::kBlock;
+                                e[u] = P < f_spec ? ld_agent(p.part_list + (slot0 + qj[u]) * kPartCap + (P - oj[u])) : 0ull;
+                            }
+#pragma unroll
+                            for (int u = 0; u < 4; ++u) {
+                                const int P = tid + (j0 + u) * W::kBlock;
+                                if (P < f_spec) put(P, e[u], qj[u]);
                             }
                         }
                     }
@@ -2401,7 +2416,6 @@ gvr_status run(const float* scores, int64_t B, int64_t ld, const int32_t* row_le
         q.arrivals = ws.arrivals;
         q.part_count = ws.part_count;
         q.part_thresh = ws.part_thresh;
-        q.part_wcnt = ws.part_wcnt;
         q.part_hist = ws.part_hist;
         q.part_list = ws.part_list;
         q.gstats = (guess && gstats) ? gstats + r0 * K : nullptr;

@@ -36,7 +36,6 @@ constexpr int kXcds = 8;               // gfx950 XCDs; workgroup i runs on XCD i
 // schedule, whose passes index the row with 64-bit addresses.
 constexpr int64_t kMaxSpecLd = ((int64_t)1 << 29) - 4096;
 constexpr int kPartCap = GVR_MAX_CANDIDATES;   // list entries of one (row, part) slot
-constexpr int kSlotWaves = kNWLong;            // per-wave list counts of one slot
 constexpr int kSlotHistBins = 2048;            // bins of a part's first refine histogram level
 
 // Options of one call after validation.
@@ -166,13 +165,13 @@ inline gvr_status plan_call(int64_t B, int64_t ld, int32_t K, bool have_prev, co
 
 // ------------------------------------------------------------ split-row workspace
 // Layout for `slots` (row, part) slots: arrival words [rows <= slots] u64,
-// part counts [slots] i32, part thresholds [slots] u32, per-wave list counts
-// [slots][kSlotWaves] i32, part histograms [slots][kSlotHistBins] i32, part
-// lists [slots][kPartCap] u64; each array starts on a 256-byte boundary.
+// part counts [slots] i32, part thresholds [slots] u32, part histograms
+// [slots][kSlotHistBins] i32, part lists [slots][kPartCap] u64; each array
+// starts on a 256-byte boundary.
 constexpr size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 struct WsLayout {
-    size_t arrivals, counts, thresh, wcounts, hists, lists, total;
+    size_t arrivals, counts, thresh, hists, lists, total;
 };
 
 constexpr WsLayout ws_layout(int64_t slots) {
@@ -180,17 +179,15 @@ constexpr WsLayout ws_layout(int64_t slots) {
     const size_t a = 0;
     const size_t c = a + align_up(s * sizeof(uint64_t), 256);
     const size_t t = c + align_up(s * sizeof(int32_t), 256);
-    const size_t w = t + align_up(s * sizeof(uint32_t), 256);
-    const size_t h = w + align_up(s * kSlotWaves * sizeof(int32_t), 256);
+    const size_t h = t + align_up(s * sizeof(uint32_t), 256);
     const size_t l = h + align_up(s * kSlotHistBins * sizeof(int32_t), 256);
-    return WsLayout{a, c, t, w, h, l, l + s * (size_t)kPartCap * sizeof(uint64_t)};
+    return WsLayout{a, c, t, h, l, l + s * (size_t)kPartCap * sizeof(uint64_t)};
 }
 
 struct WsPtrs {
     uint64_t* arrivals = nullptr;
     int32_t* part_count = nullptr;
     uint32_t* part_thresh = nullptr;
-    int32_t* part_wcnt = nullptr;
     int32_t* part_hist = nullptr;
     uint64_t* part_list = nullptr;
 };
@@ -202,7 +199,6 @@ inline WsPtrs ws_carve(void* base, int64_t slots) {
     w.arrivals = reinterpret_cast<uint64_t*>(b + L.arrivals);
     w.part_count = reinterpret_cast<int32_t*>(b + L.counts);
     w.part_thresh = reinterpret_cast<uint32_t*>(b + L.thresh);
-    w.part_wcnt = reinterpret_cast<int32_t*>(b + L.wcounts);
     w.part_hist = reinterpret_cast<int32_t*>(b + L.hists);
     w.part_list = reinterpret_cast<uint64_t*>(b + L.lists);
     return w;

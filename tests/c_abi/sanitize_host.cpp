@@ -110,11 +110,10 @@ static void check_workspace() {
     // layout: every array 256-byte aligned, in order, sized for the slots
     for (int64_t slots : {1, 2, 7, 64, 256, 2048}) {
         const WsLayout L = ws_layout(slots);
-        CHECK(L.arrivals == 0 && L.counts % 256 == 0 && L.thresh % 256 == 0 && L.wcounts % 256 == 0 &&
-              L.hists % 256 == 0 && L.lists % 256 == 0);
+        CHECK(L.arrivals == 0 && L.counts % 256 == 0 && L.thresh % 256 == 0 && L.hists % 256 == 0 &&
+              L.lists % 256 == 0);
         CHECK(L.counts >= (size_t)slots * 8 && L.thresh - L.counts >= (size_t)slots * 4 &&
-              L.wcounts - L.thresh >= (size_t)slots * 4 && L.hists - L.wcounts >= (size_t)slots * kSlotWaves * 4 &&
-              L.lists - L.hists >= (size_t)slots * kSlotHistBins * 4);
+              L.hists - L.thresh >= (size_t)slots * 4 && L.lists - L.hists >= (size_t)slots * kSlotHistBins * 4);
         CHECK(L.total == L.lists + (size_t)slots * kPartCap * 8);
     }
     // the cache: reuse, growth with the outgrown buffer kept, refusal under capture
