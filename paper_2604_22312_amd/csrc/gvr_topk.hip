@@ -239,15 +239,10 @@ DEV int add_lane_bit(int q, uint64_t m) {
 }
 
 // ------------------------------------------------------------------ LDS
-// List segments: the candidate list is a sequence of segments in index order
-// (the waves of one part, then the next part's), segment j held at
-// list[seg_off[j] .. + seg_cnt[j]). Wave w handles segments w, w + NW, ...
-// (nq of them): one per wave for a row held by one workgroup, one per part
-// after a split row's merge.
-template <int NW>
-struct SegCount {
-    static constexpr int value = NW * (NW == kNWLong ? kMaxParts : 1);
-};
+// List segments: the candidate list is a sequence of NW segments in index
+// order, segment w held at list[seg_off[w] .. + seg_cnt[w]) and handled by
+// wave w (its own list after a pass, or its even share of a split row's
+// merged list).
 template <int NW>
 struct Smem {
     uint2 list[Shape<NW>::kCap];                   // candidates (key, index), in segments
@@ -256,16 +251,15 @@ struct Smem {
         int rhist[kRefBins];            // refine / guess histogram
     } u;
     int F[kBinsX + 1];                  // F[j] = f(edge j) over the row
-    int seg_off[SegCount<NW>::value];
-    int seg_cnt[SegCount<NW>::value];
-    int sga[SegCount<NW>::value];       // per-segment counts (keys > T, keys == T), then exclusive offsets
-    int sgb[SegCount<NW>::value];
+    int seg_off[NW];
+    int seg_cnt[NW];
+    int sga[NW];                        // per-segment counts (keys > T, keys == T), then exclusive offsets
+    int sgb[NW];
     int wa[NW];
     int wb[NW];
     int red[4][NW];
     float redf[NW];
     int scal[8];
-    int nq;                             // segments per wave
     int guess_ready;                    // set by wave 0 once T_spec is in scal[4..7]
 };
 // Passes over the lists read four 64-entry chunks at a time, up to 255
@@ -380,41 +374,12 @@ DEV void block_keys(const float4& v, uint32_t (&k)[4]) {
 // segments (in place), by wave 0; the totals go to scal[5] and scal[6].
 template <int NW>
 DEV void seg_scan(Smem<NW>& sm, int nseg, int lane) {
-    if (nseg <= kWave) {   // one segment per lane
-        const int a = lane < nseg ? sm.sga[lane] : 0, b = lane < nseg ? sm.sgb[lane] : 0;
-        const int ia = wave_incl_scan(a, lane), ib = wave_incl_scan(b, lane);
-        if (lane < nseg) {
-            sm.sga[lane] = ia - a;
-            sm.sgb[lane] = ib - b;
-        }
-        if (lane == kWave - 1) {
-            sm.scal[5] = ia;
-            sm.scal[6] = ib;
-        }
-        return;
-    }
-    constexpr int PER = (SegCount<NW>::value + kWave - 1) / kWave;
-    int a[PER], b[PER];
-    int sa = 0, sb = 0;
-#pragma unroll
-    for (int r = 0; r < PER; ++r) {
-        const int j = lane * PER + r;
-        a[r] = j < nseg ? sm.sga[j] : 0;
-        b[r] = j < nseg ? sm.sgb[j] : 0;
-        sa += a[r];
-        sb += b[r];
-    }
-    const int ia = wave_incl_scan(sa, lane), ib = wave_incl_scan(sb, lane);
-    int ra = ia - sa, rb = ib - sb;
-#pragma unroll
-    for (int r = 0; r < PER; ++r) {
-        const int j = lane * PER + r;
-        if (j < nseg) {
-            sm.sga[j] = ra;
-            sm.sgb[j] = rb;
-        }
-        ra += a[r];
-        rb += b[r];
+    static_assert(NW <= kWave, "one segment per lane");
+    const int a = lane < nseg ? sm.sga[lane] : 0, b = lane < nseg ? sm.sgb[lane] : 0;
+    const int ia = wave_incl_scan(a, lane), ib = wave_incl_scan(b, lane);
+    if (lane < nseg) {
+        sm.sga[lane] = ia - a;
+        sm.sgb[lane] = ib - b;
     }
     if (lane == kWave - 1) {
         sm.scal[5] = ia;
@@ -430,7 +395,6 @@ template <int NW>
 DEV uint32_t refine_kth(Smem<NW>& sm, uint32_t wlo, uint32_t whi, int above, int K, int tid) {
     using W = Shape<NW>;
     const int lane = tid & 63, wave = tid >> 6;
-    const int nq = sm.nq;
     int need = K - above;   // >= 1
     for (int level = 0; level < 4 && wlo != whi; ++level) {
         const uint64_t width = (uint64_t)whi - wlo + 1;
@@ -438,8 +402,8 @@ DEV uint32_t refine_kth(Smem<NW>& sm, uint32_t wlo, uint32_t whi, int above, int
         for (int i = tid; i < kRefBins; i += W::kBlock) sm.u.rhist[i] = 0;
         lds_barrier();
         uint32_t kmn = 0xFFFFFFFFu, kmx = 0u;   // the first level also finds the window's smallest and largest key
-        for (int q = 0; q < nq; ++q) {
-            const int j = wave + NW * q;
+        {
+            const int j = wave;
             const uint2* seg = sm.list + sm.seg_off[j];
             const int cnt = sm.seg_cnt[j];
             for (int i = lane; i < cnt; i += kWave) {
@@ -546,8 +510,8 @@ DEV void emit_segment(const Smem<NW>& sm, int j, uint32_t T, int K, int take, in
 // Every wave emits its segments at the offsets in sga / sgb (after seg_scan).
 template <int NW>
 DEV void emit_segments(const Smem<NW>& sm, uint32_t T, int K, int take, int32_t* out, int lane, int wave) {
-    for (int q = 0; q < sm.nq; ++q) {
-        const int j = wave + NW * q;
+    {
+        const int j = wave;
         emit_segment(sm, j, T, K, take, sm.sga[j], sm.sgb[j], out, lane);
     }
 }
@@ -557,9 +521,8 @@ DEV void emit_segments(const Smem<NW>& sm, uint32_t T, int K, int take, int32_t*
 template <int NW>
 DEV void emit_from_lists(Smem<NW>& sm, uint32_t T, int K, int32_t* out, int tid, int* n_gt_out) {
     const int lane = tid & 63, wave = tid >> 6;
-    const int nq = sm.nq;
-    for (int q = 0; q < nq; ++q) {
-        const int j = wave + NW * q;
+    {
+        const int j = wave;
         const uint2* seg = sm.list + sm.seg_off[j];
         const int cnt = sm.seg_cnt[j];
         int gt = 0, eq = 0;
@@ -576,7 +539,7 @@ DEV void emit_from_lists(Smem<NW>& sm, uint32_t T, int K, int32_t* out, int tid,
         }
     }
     lds_barrier();
-    if (wave == 0) seg_scan(sm, NW * nq, lane);
+    if (wave == 0) seg_scan(sm, NW, lane);
     lds_barrier();
     const int gtot = sm.scal[5];
     emit_segments(sm, T, K, K - gtot, out, lane, wave);
@@ -586,8 +549,8 @@ DEV void emit_from_lists(Smem<NW>& sm, uint32_t T, int K, int32_t* out, int tid,
 // f(key) for every listed entry of this wave's segments (lane-strided).
 template <int NW, typename F>
 DEV void for_my_keys(const Smem<NW>& sm, int wave, int lane, F&& f) {
-    for (int q = 0; q < sm.nq; ++q) {
-        const int j = wave + NW * q;
+    {
+        const int j = wave;
         const uint2* seg = sm.list + sm.seg_off[j];
         const int cnt = sm.seg_cnt[j];
         for (int i = lane; i < cnt; i += kWave) f(seg[i].x);
@@ -802,7 +765,6 @@ DEV uint32_t refine_emit(Smem<NW>& sm, uint32_t rlo, uint32_t rhi, uint32_t bin_
                          int tid, int* n_gt_out, bool hist_ready) {
     using W = Shape<NW>;
     const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int nq = sm.nq;
     const uint32_t sh = ref_shift(rlo, bin_hi);
     int* hb = sm.u.rhist;
     if (tid == 0) sm.scal[1] = 0;   // ordered before its atomics by the barrier after the bin search
@@ -842,8 +804,8 @@ DEV uint32_t refine_emit(Smem<NW>& sm, uint32_t rlo, uint32_t rhi, uint32_t bin_
     uint4* const small = reinterpret_cast<uint4*>(sm.u.rhist);
     uint32_t* const skey = reinterpret_cast<uint32_t*>(small + kSmall);   // their keys alone, for the rank
     const uint32_t wid = hi_b - lo_b;
-    for (int q = 0; q < nq; ++q) {
-        const int j = wave + NW * q;
+    {
+        const int j = wave;
         const uint2* seg = sm.list + sm.seg_off[j];
         const int cnt = sm.seg_cnt[j];
         int gtl = 0;
@@ -906,7 +868,7 @@ DEV uint32_t refine_emit(Smem<NW>& sm, uint32_t rlo, uint32_t rhi, uint32_t bin_
         // each candidate adds itself to its segment's counts.
         if (v && mine.x > kth) __hip_atomic_fetch_add(&sm.sga[mine.z], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
         if (v && mine.x == kth) __hip_atomic_fetch_add(&sm.sgb[mine.z], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-        seg_scan(sm, NW * nq, lane);
+        seg_scan(sm, NW, lane);
         if (lane == 0) sm.scal[0] = (int)kth;
     }
     lds_barrier();
@@ -1054,7 +1016,6 @@ DEV void topk_body(const Params& p) {
     uint32_t tthr = 0u;      // threshold of the speculative lists
     bool overflow = false;
     if (tid < NW) sm.seg_off[tid] = tid * W::kCapW;
-    if (tid == 0) sm.nq = 1;
 
     if (spec) {
         if (!all_mode) {
@@ -1534,8 +1495,7 @@ DEV void topk_body(const Params& p) {
                         sm.seg_off[tid] = o;
                         sm.seg_cnt[tid] = min(chunk, f_spec - o);
                     }
-                    if (tid == 0) sm.nq = 1;
-                    lds_barrier();   // every wave reads the merged list, its segment table and histogram after this
+                                    lds_barrier();   // every wave reads the merged list, its segment table and histogram after this
                 }
             }
             // Ready for the next call (issued after the loads above).
@@ -1791,8 +1751,7 @@ DEV void topk_body(const Params& p) {
             });
             ++passes;
         }
-        if (tid == 0) sm.nq = 1;
-        __syncthreads();
+            __syncthreads();
         return f;
     };
 
