@@ -197,8 +197,7 @@ constexpr int kBufWord3 = 0x00020000;   // 32-bit data format, no swizzle
 DEV __amdgpu_buffer_rsrc_t row_rsrc(const void* base, int bytes) {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, kBufWord3);
 }
-// 16-byte buffer load (full-row passes: a row read twice, as by the radix
-// schedule, finds its second read in the caches).
+// 16-byte buffer load (the speculative pass: rows within its 32-bit offsets).
 DEV float4 buf_load16(__amdgpu_buffer_rsrc_t r, int off) {
     const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
     return make_float4(__uint_as_float(v.x), __uint_as_float(v.y), __uint_as_float(v.z), __uint_as_float(v.w));
@@ -287,8 +286,9 @@ DEV int block_excl_scan(int& a, Smem<NW>& sm, int tid) {
 }
 
 // ------------------------------------------------------------------ streaming
-// One wave streams float4 blocks [qb, qe) of the row (buffer resource xr)
-// in slabs of 64 blocks with kU slabs in flight;
+// One wave streams float4 blocks [qb, qe) of the row (64-bit addresses: a
+// full-row pass serves rows of any length) in slabs of 64 blocks with kU
+// slabs in flight;
 // `body(v, q, qs)` gets each lane's block q, its data
 // and the slab's first block qs. Every block index is clamped to qlast, so no
 // load leaves the 16-byte blocks that hold the row (refills past the wave's
@@ -298,11 +298,12 @@ DEV int block_excl_scan(int& a, Smem<NW>& sm, int tid) {
 // consumed and unconditionally, so each slot keeps one register set and a
 // slab waits only for its own load (vmcnt(kU - 1)), not for all of them.
 template <typename Pro, typename Body>
-DEV void stream_wave(__amdgpu_buffer_rsrc_t xr, int qb, int qe, int qlast, int lane, Pro&& prologue, Body&& body) {
+DEV void stream_wave(const float4* __restrict__ xa, int qb, int qe, int qlast, int lane, Pro&& prologue,
+                     Body&& body) {
     const int nslab = qe > qb ? (qe - qb + 63) >> 6 : 0;
     float4 buf[kU];
 #pragma unroll
-    for (int u = 0; u < kU; ++u) buf[u] = buf_load16(xr, min(qb + u * 64 + lane, qlast) * 16);
+    for (int u = 0; u < kU; ++u) buf[u] = xa[min(qb + u * 64 + lane, qlast)];
     prologue();
     int s0 = 0;
     for (; s0 + kU <= nslab; s0 += kU) {
@@ -310,7 +311,7 @@ DEV void stream_wave(__amdgpu_buffer_rsrc_t xr, int qb, int qe, int qlast, int l
         for (int u = 0; u < kU; ++u) {
             const int s = s0 + u;
             body(buf[u], qb + s * 64 + lane, qb + s * 64);
-            buf[u] = buf_load16(xr, min(qb + (s + kU) * 64 + lane, qlast) * 16);
+            buf[u] = xa[min(qb + (s + kU) * 64 + lane, qlast)];
         }
     }
 #pragma unroll
@@ -980,7 +981,6 @@ DEV void topk_body(const Params& p) {
     const int aoff = (int)(((uintptr_t)x >> 2) & 31);   // slabs start on 128-byte lines
     const float4* xa = reinterpret_cast<const float4*>(x - aoff);
     const int nq = (n + aoff + 3) >> 2;
-    const __amdgpu_buffer_rsrc_t xr = row_rsrc(xa, nq * 16);   // the row's blocks, for full-row passes
     const int qlast = nq - 1;
     const int nslab_row = (nq + 63) >> 6;
     const int per = ((nslab_row + NW - 1) / NW) * 64;   // whole slabs per wave
@@ -1015,6 +1015,30 @@ DEV void topk_body(const Params& p) {
     bool hist_full = false;  // rhist counts every key >= tthr of the row (first-level bins)
     uint32_t tthr = 0u;      // threshold of the speculative lists
     bool overflow = false;
+    // A part of a split row arrives once its published stores have
+    // completed (reached the XCD's L2): one device-scope atomic on the row's
+    // arrival word, which also counts the parts per XCD (5 bits per XCD above
+    // 16 bits of arrivals; option flag 128: an agent-scope release /
+    // acquire). True for the row's last part; *same_xcd: every part ran on
+    // this part's XCD.
+    auto arrive_last = [&](bool* same_xcd) -> bool {
+        __builtin_amdgcn_s_waitcnt(0);   // this wave's stores have completed (reached L2)
+        __syncthreads();
+        if (tid == 0) {
+            const uint32_t xcc = (uint32_t)__builtin_amdgcn_s_getreg((31 << 11) | 20) & 7u;   // HW_REG_XCC_ID
+            const uint64_t add = 1ull + (1ull << (16 + 5 * xcc));
+            const uint64_t old =
+                p.ordered_merge
+                    ? __hip_atomic_fetch_add(p.arrivals + row, add, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT)
+                    : __hip_atomic_fetch_add(p.arrivals + row, add, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            const uint64_t now = old + add;
+            sm.scal[3] = (int)(old & 0xFFFFu);
+            sm.scal[2] = (int)((now >> (16 + 5 * xcc)) & 31u) == S;   // all parts on this XCD
+        }
+        __syncthreads();
+        *same_xcd = sm.scal[2] != 0;
+        return sm.scal[3] == S - 1;
+    };
     if (tid < NW) sm.seg_off[tid] = tid * W::kCapW;
 
     if (spec) {
@@ -1335,22 +1359,8 @@ DEV void topk_body(const Params& p) {
                 uint64_t* ph = reinterpret_cast<uint64_t*>(p.part_hist + (slot0 + part) * kRefBins1);
                 for (int i = tid; i < kRefBins1 / 2; i += W::kBlock) ph[i] = reinterpret_cast<const uint64_t*>(sm.u.rhist)[i];
             }
-            __builtin_amdgcn_s_waitcnt(0);   // this wave's stores have completed (reached L2)
-            __syncthreads();
-            if (tid == 0) {
-                const uint32_t xcc = (uint32_t)__builtin_amdgcn_s_getreg((31 << 11) | 20) & 7u;   // HW_REG_XCC_ID
-                const uint64_t add = 1ull + (1ull << (16 + 5 * xcc));
-                const uint64_t old =
-                    p.ordered_merge
-                        ? __hip_atomic_fetch_add(p.arrivals + row, add, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT)
-                        : __hip_atomic_fetch_add(p.arrivals + row, add, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                const uint64_t now = old + add;
-                sm.scal[3] = (int)(old & 0xFFFFu);
-                sm.scal[2] = (int)((now >> (16 + 5 * xcc)) & 31u) == S;   // all parts on this XCD
-            }
-            __syncthreads();
-            if (sm.scal[3] != S - 1) return;   // another part of this row finishes it
-            const bool same_xcd = sm.scal[2] != 0;
+            bool same_xcd = false;
+            if (!arrive_last(&same_xcd)) return;   // another part of this row finishes it
             if (!same_xcd) {
                 overflow = true;   // lists unusable: the fallback reads the whole row
                 f_spec = -1;
@@ -1583,7 +1593,7 @@ DEV void topk_body(const Params& p) {
         for (int i = tid; i < NW * kBinsX; i += W::kBlock) (&sm.u.hist[0][0])[i] = 0;
         __syncthreads();
         const uint32_t lo = win.lo, sh = win.shift;
-        stream_wave(xr, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
+        stream_wave(xa, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
             uint32_t k[4];
             block_keys(v, k);
             const int e0 = 4 * q - aoff;
@@ -1604,7 +1614,7 @@ DEV void topk_body(const Params& p) {
     // first window spans [min, max] instead.
     auto minmax_pass = [&]() {
         uint32_t mn = 0xFFFFFFFFu, mx = 0u;
-        stream_wave(xr, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
+        stream_wave(xa, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
             uint32_t k[4];
             block_keys(v, k);
             const int e0 = 4 * q - aoff;
@@ -1638,14 +1648,14 @@ DEV void topk_body(const Params& p) {
     // bin sit in different banks) in the lists' space, summed afterwards.
     constexpr int kDigitCopies = W::kCap * 2 >= kRefBins1 * 8 ? 8 : 4;
     static_assert(W::kCap * 2 >= kRefBins1 * kDigitCopies, "the digit histogram copies fit the lists' space");
-    auto digit_pass = [&]() {
+    auto digit_pass = [&](int dqb, int dqe) {   // this wave's float4 blocks [dqb, dqe)
         int* dh = reinterpret_cast<int*>(sm.list);   // [kRefBins1][kDigitCopies]
         __syncthreads();
         for (int i = tid; i < kRefBins1 * kDigitCopies / 4; i += W::kBlock)
             reinterpret_cast<int4*>(dh)[i] = make_int4(0, 0, 0, 0);
         __syncthreads();
         int* dl = dh + (lane & (kDigitCopies - 1));
-        stream_wave(xr, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
+        stream_wave(xa, dqb, dqe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
             uint32_t k[4];
             block_keys(v, k);
             const int e0 = 4 * q - aoff;
@@ -1686,7 +1696,7 @@ DEV void topk_body(const Params& p) {
         const bool every = tc == 0u;   // key 0 passes too: no compare
         const SpecTest test = make_spec_test(max(tc, 1u));
         int c = 0;
-        stream_wave(xr, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
+        stream_wave(xa, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
             const uint32_t k[4] = {__float_as_uint(v.x), __float_as_uint(v.y), __float_as_uint(v.z), __float_as_uint(v.w)};
             const int e0 = 4 * q - aoff;
             bool f[4];
@@ -1727,7 +1737,7 @@ DEV void topk_body(const Params& p) {
             }
             uint2* lp = sm.list + off;
             int run = 0;
-            stream_wave(xr, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
+            stream_wave(xa, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
                 uint32_t k[4];
                 block_keys(v, k);
                 const int e0 = 4 * q - aoff;
@@ -1816,7 +1826,7 @@ DEV void topk_body(const Params& p) {
         auto count_ge = [&](uint32_t tk, bool minmax) {
             int c = 0;
             uint32_t lo = 0xFFFFFFFFu, hi = 0u;
-            stream_wave(xr, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
+            stream_wave(xa, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
                 uint32_t k[4];
                 block_keys(v, k);
                 const int e0 = 4 * q - aoff;
@@ -1915,7 +1925,7 @@ DEV void topk_body(const Params& p) {
             }
             uint2* lc = sm.list + off;
             int run = 0;
-            stream_wave(xr, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
+            stream_wave(xa, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
                 uint32_t k[4];
                 block_keys(v, k);
                 const int e0 = 4 * q - aoff;
@@ -1980,6 +1990,44 @@ DEV void topk_body(const Params& p) {
         }
     } else {
         bool whole_range = true;   // nothing bounds the K-th key yet
+        bool digits_counted = false;   // rhist holds the row's digit histogram (split radix rows)
+        if (!GUESS && S > 1) {
+            // ---------------- a split radix row: each part counts the digits
+            // of its share of the row (its waves split the part's slabs),
+            // publishes the histogram, and the last part to arrive sums them
+            // and goes on with the whole row (the handoff of the speculative
+            // pass's merge). Parts that did not all run on one XCD leave the
+            // last part to count the whole row itself.
+            const int pw = (ps1 - ps0 + NW - 1) / NW;
+            digit_pass(min((ps0 + min(wave * pw, ps1 - ps0)) * 64, nq), min((ps0 + min((wave + 1) * pw, ps1 - ps0)) * 64, nq));
+            const int64_t slot0 = row * S;
+            {
+                uint64_t* ph = reinterpret_cast<uint64_t*>(p.part_hist + (slot0 + part) * kRefBins1);
+                for (int i = tid; i < kRefBins1 / 2; i += W::kBlock) ph[i] = reinterpret_cast<const uint64_t*>(sm.u.rhist)[i];
+            }
+            bool same_xcd = false;
+            if (!arrive_last(&same_xcd)) return;   // another part of this row finishes it
+            if (same_xcd) {
+                for (int i = tid; i < kRefBins1 / 2; i += W::kBlock) {
+                    uint64_t hv[kMaxParts];
+#pragma unroll
+                    for (int k = 0; k < kMaxParts; ++k)
+                        hv[k] = k < S ? ld_agent(reinterpret_cast<const uint64_t*>(p.part_hist + (slot0 + k) * kRefBins1) + i)
+                                      : 0ull;
+                    int sx = 0, sy = 0;
+#pragma unroll
+                    for (int k = 0; k < kMaxParts; ++k) {
+                        sx += (int)(uint32_t)hv[k];
+                        sy += (int)(uint32_t)(hv[k] >> 32);
+                    }
+                    reinterpret_cast<int2*>(sm.u.rhist)[i] = make_int2(sx, sy);
+                }
+                digits_counted = true;
+            }
+            // Ready for the next call (issued after the loads above).
+            if (tid == 0) __hip_atomic_store(p.arrivals + row, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __syncthreads();   // the summed histogram is complete
+        }
         if (secant) {
             // The secant search gave up: narrow inside its counted bracket.
             path = GVR_PATH_NARROWED;
@@ -2036,7 +2084,7 @@ DEV void topk_body(const Params& p) {
         if (whole_range && coll < 0) {
             // Nothing bounds the K-th key: a digit pass, then the same choice
             // over its bins (a bin of more than C keys is narrowed).
-            digit_pass();
+            if (!digits_counted) digit_pass(qb, qe);
             if (wave == 0) kth_bin_wave0(sm, sm.u.rhist, K, 0, lane);
             __syncthreads();
             const int b = sm.scal[0], above_b = sm.scal[2], cnt_b = sm.scal[3];
@@ -2108,7 +2156,7 @@ DEV void topk_body(const Params& p) {
                 __syncthreads();
                 uint2* lc = sm.list + off;
                 int run = 0;
-                stream_wave(xr, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
+                stream_wave(xa, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
                     uint32_t k[4];
                     block_keys(v, k);
                     const int e0 = 4 * q - aoff;
@@ -2151,7 +2199,7 @@ DEV void topk_body(const Params& p) {
                 __syncthreads();
                 int gb = sum_over_waves_below(sm.wa, lane, wave);
                 int eb = sum_over_waves_below(sm.wb, lane, wave);
-                stream_wave(xr, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
+                stream_wave(xa, qb, qe, qlast, lane, [] {}, [&](const float4& v, int q, int qs) {
                     uint32_t k[4];
                     block_keys(v, k);
                     const int e0 = 4 * q - aoff;

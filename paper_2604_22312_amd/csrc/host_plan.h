@@ -86,7 +86,7 @@ inline gvr_status validate(const void* scores, int64_t B, int64_t ld, int32_t K,
 // two rows leaves the chip nearly idle and its merges cost a few us: there
 // parts of 8K-16K elements pay from 32K elements on (8 parts below 192K,
 // then 16).
-inline int choose_parts(int64_t rows, int64_t ld, int cus) {
+inline int choose_parts(int64_t rows, int64_t ld, int cus, bool radix = false) {
     if (rows <= 0 || rows >= cus) return 1;
     if (rows <= 2 && ld >= 32768 && cus >= 32 * rows) {
         int s = 1;
@@ -97,9 +97,12 @@ inline int choose_parts(int64_t rows, int64_t ld, int cus) {
     s = std::min<int64_t>(s, std::max<int64_t>(1, ld / kMinPartElems));
     s = std::min<int64_t>(s, kMaxParts);
     if (s <= 1) return 1;
-    const double stream_us = (double)ld * 4.0 / 33.0e3;   // one workgroup, whole row
+    // One workgroup's time for the pass the parts share: the speculative
+    // pass (~33 GB/s), or the radix digit pass (~25 GB/s, and the parts'
+    // handoff is only the histograms).
+    const double stream_us = (double)ld * 4.0 / (radix ? 25.0e3 : 33.0e3);
     const double saved_us = stream_us * (1.0 - 1.0 / (double)s);
-    return saved_us > 8.0 ? (int)s : 1;
+    return saved_us > (radix ? 4.0 : 8.0) ? (int)s : 1;
 }
 
 // Workgroup shape of a call: waves per workgroup (16, 8 or 4). Up to one row
@@ -145,7 +148,8 @@ inline gvr_status plan_call(int64_t B, int64_t ld, int32_t K, bool have_prev, co
     if (p.shape == kNWShort) p.capacity = std::min(p.capacity, kCapShort);
     if (p.shape == kNWMid) p.capacity = std::min(p.capacity, kCapMid);
     int parts = 1;
-    if (p.guess && p.shape == kNWLong && !o.secant) {   // the secant search reads whole rows
+    const bool secant = p.guess && o.secant;   // the secant search reads whole rows
+    if (p.shape == kNWLong && !secant) {
         if (o.parts > 0) {
             parts = o.parts;
             if (parts > 1 && (int64_t)parts * B > max_slots) {
@@ -153,7 +157,7 @@ inline gvr_status plan_call(int64_t B, int64_t ld, int32_t K, bool have_prev, co
                 parts = (int)std::max<int64_t>(1, max_slots / std::max<int64_t>(B, 1));
             }
         } else {
-            parts = choose_parts(B, ld, cus);
+            parts = choose_parts(B, ld, cus, !p.guess);
             if (parts > 1 && (int64_t)parts * B > max_slots)
                 parts = (int)std::max<int64_t>(1, max_slots / std::max<int64_t>(B, 1));
         }

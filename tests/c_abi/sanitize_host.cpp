@@ -81,8 +81,15 @@ static void check_plans() {
     // 8 rows of 131K split into 8 parts; one row of 262K into 16
     CHECK(plan_call(8, 131079, 2048, true, o, 256, kMaxSlots, false, &p) == GVR_OK && p.parts == 8);
     CHECK(plan_call(1, 262144, 2048, true, o, 256, kMaxSlots, false, &p) == GVR_OK && p.parts == 16);
-    // no guess: no split; short rows: 4 waves; mid rows: 8 waves with their capacities
-    CHECK(plan_call(8, 131079, 2048, false, o, 256, kMaxSlots, false, &p) == GVR_OK && !p.guess && p.parts == 1);
+    // no guess: the radix schedule splits few long rows too (8 parts of 131K),
+    // not 100K rows at 128 per call and 32K rows at 32; short rows: 4 waves;
+    // mid rows: 8 waves with their capacities
+    CHECK(plan_call(8, 131079, 2048, false, o, 256, kMaxSlots, false, &p) == GVR_OK && !p.guess && p.parts == 8);
+    CHECK(plan_call(32, 32831, 2048, false, o, 256, kMaxSlots, false, &p) == GVR_OK && !p.guess && p.parts == 1);
+    // the secant search never splits; the radix schedule with the secant flag still may
+    o.secant = 1;
+    CHECK(plan_call(8, 131079, 2048, false, o, 256, kMaxSlots, false, &p) == GVR_OK && !p.guess && p.parts == 8);
+    o.secant = 0;
     CHECK(plan_call(2048, 4000, 2048, false, o, 256, kMaxSlots, false, &p) == GVR_OK && p.shape == kNWShort &&
           p.capacity == kCapShort);
     CHECK(plan_call(1024, 32768, 2048, true, o, 256, kMaxSlots, false, &p) == GVR_OK && p.shape == kNWMid &&

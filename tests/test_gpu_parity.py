@@ -755,10 +755,12 @@ def test_short_shape_forced_paths(opts):
     assert_rows_equal(out.cpu().numpy(), exp, "radix short shape %s" % opts)
 
 
-@pytest.mark.parametrize("ld", [(1 << 29) - 4096, (1 << 29) - 4095], ids=["guess_path_limit", "past_the_limit"])
+@pytest.mark.parametrize("ld", [(1 << 29) - 4096, (1 << 29) - 4095, (1 << 30) + 4099],
+                         ids=["guess_path_limit", "past_the_limit", "past_4GB"])
 def test_rows_at_the_offset_limit(ld):
-    """The longest stride the guess path takes (its byte offsets are 32-bit)
-    and one past it, which runs the guess-free schedule: 4096 planted values
+    """The longest stride the guess path takes (its byte offsets are 32-bit),
+    one past it, and a row of more than 4 GB (past 32-bit byte offsets of
+    any kind), which run the guess-free schedule: 4096 planted values
     (1, 2, ..., 4096 at random indices, the rest 0) in a 2 GB row, the guess
     the planted values of ranks 1025..3072. The answer is known by
     construction: the indices of the 2048 largest planted values."""
