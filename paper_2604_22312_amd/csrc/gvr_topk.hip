@@ -202,24 +202,10 @@ DEV float4 buf_load16(__amdgpu_buffer_rsrc_t r, int off) {
     const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
     return make_float4(__uint_as_float(v.x), __uint_as_float(v.y), __uint_as_float(v.z), __uint_as_float(v.w));
 }
-// 16-byte buffer load with the non-temporal hint: a streamed row is read
-// once, and the hint keeps it from displacing reused lines.
-constexpr int kCpolNT = 2;
-DEV float4 buf_load16_nt(__amdgpu_buffer_rsrc_t r, int off) {
-    const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kCpolNT);
-    return make_float4(__uint_as_float(v.x), __uint_as_float(v.y), __uint_as_float(v.z), __uint_as_float(v.w));
-}
 // Device-scope loads of what other workgroups published (they skip the
 // vector L1).
 DEV int ld_agent(const int32_t* p) { return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
 DEV uint64_t ld_agent(const uint64_t* p) { return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
-// 16 bytes with the cache policy of those loads (device scope: sc1), from a
-// buffer resource: lanes past its end read zeros.
-constexpr int kCpolSC1 = 16;
-DEV int4 ld_agent16(__amdgpu_buffer_rsrc_t r, int off) {
-    const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kCpolSC1);
-    return make_int4((int)v.x, (int)v.y, (int)v.z, (int)v.w);
-}
 // Byte offset of an LDS object (its address in the LDS aperture).
 DEV uint32_t lds_addr(const void* p) {
     return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)p;
@@ -320,47 +306,10 @@ DEV void stream_wave(const float4* __restrict__ xa, int qb, int qe, int qlast, i
 }
 
 // Count key k (if `in`) into bin min((k - lo) >> sh, kBins) of a wave-private
-// histogram. With AGG, lanes sharing the first active lane's bin add in one
-// atomic: wide (radix) windows map most keys of a wave to a few bins, and
-// same-address LDS atomics serialise.
-template <bool AGG>
+// histogram.
 DEV void hist_add(int* hw, uint32_t k, bool in, uint32_t lo, uint32_t sh) {
     const uint32_t b = min((k - lo) >> sh, (uint32_t)kBins);
-    if (!AGG) {
-        if (in) __hip_atomic_fetch_add(&hw[b], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-        return;
-    }
-    const uint64_t act = __ballot(in);
-    if (!act) return;
-    const uint32_t lead = __builtin_amdgcn_readlane(b, (int)__builtin_ctzll(act));
-    const uint64_t same = __ballot(in && b == lead);
-    if (in && b == lead) {
-        if (lanes_below(same, 0) == 0)
-            __hip_atomic_fetch_add(&hw[lead], (int)__popcll(same), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-    } else if (in) {
-        __hip_atomic_fetch_add(&hw[b], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-    }
-}
-
-// Count key k (if `in`) into bin min((k - lo) >> sh, kBins) of a wave-private
-// histogram, for counting passes: the lanes of the (at most) two most common
-// bins of this instruction add with one atomic per bin (a window the data
-// crowds into few bins, and ties, would otherwise serialise on one LDS
-// address); the remaining lanes, spread over other bins, add one each.
-DEV void hist_add_peel(int* hw, uint32_t k, bool in, uint32_t lo, uint32_t sh, int lane) {
-    const uint32_t b = min((k - lo) >> sh, (uint32_t)kBins);
-    uint64_t act = __ballot(in);
-#pragma unroll
-    for (int it = 0; it < 2; ++it) {
-        if (!act) return;
-        const int first = (int)__builtin_ctzll(act);
-        const uint32_t lead = __builtin_amdgcn_readlane(b, first);
-        const uint64_t same = __ballot(b == lead) & act;
-        if (lane == first)
-            __hip_atomic_fetch_add(&hw[lead], (int)__popcll(same), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-        act &= ~same;
-    }
-    if ((act >> lane) & 1) __hip_atomic_fetch_add(&hw[b], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    if (in) __hip_atomic_fetch_add(&hw[b], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 
 DEV void block_keys(const float4& v, uint32_t (&k)[4]) {
@@ -1601,7 +1550,7 @@ DEV void topk_body(const Params& p) {
 #pragma unroll
             for (int c = 0; c < 4; ++c) {
                 const bool okc = !edge || (e0 + c >= 0 && e0 + c < n);
-                hist_add<false>(hw, k[c], okc && k[c] >= lo, lo, sh);
+                hist_add(hw, k[c], okc && k[c] >= lo, lo, sh);
             }
         });
         ++passes;

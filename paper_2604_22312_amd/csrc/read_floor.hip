@@ -97,7 +97,7 @@ __global__ __launch_bounds__(kFloorWaves * 64) void read_floor_kernel(const floa
         for (int w = 0; w < kFloorWaves; ++w) t ^= wsum[w];
         out[(int64_t)row * kFloorMaxParts + part] = t;
     }
-    if (part == 0 && threadIdx.x >= parts && threadIdx.x < kFloorMaxParts) out[(int64_t)row * kFloorMaxParts + threadIdx.x] = 0u;
+    if (part == 0 && (int)threadIdx.x >= parts && (int)threadIdx.x < kFloorMaxParts) out[(int64_t)row * kFloorMaxParts + threadIdx.x] = 0u;
 }
 
 // Compute units of a device, queried once per device.
