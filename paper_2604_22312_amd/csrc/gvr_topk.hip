@@ -197,9 +197,11 @@ constexpr int kBufWord3 = 0x00020000;   // 32-bit data format, no swizzle
 DEV __amdgpu_buffer_rsrc_t row_rsrc(const void* base, int bytes) {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, kBufWord3);
 }
-// 16-byte buffer load (the speculative pass: rows within its 32-bit offsets).
+// 16-byte buffer load (the speculative pass: rows within its 32-bit offsets);
+// NT: with the non-temporal hint (a streamed row is read once).
+template <bool NT>
 DEV float4 buf_load16(__amdgpu_buffer_rsrc_t r, int off) {
-    const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+    const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, NT ? 2 : 0);
     return make_float4(__uint_as_float(v.x), __uint_as_float(v.y), __uint_as_float(v.z), __uint_as_float(v.w));
 }
 // Device-scope loads of what other workgroups published (they skip the
@@ -851,7 +853,7 @@ constexpr uint32_t kKeyZeroBits = 0xFFFFFFFFu;
 
 DEV uint64_t pack_entry(uint32_t bits, uint32_t idx) { return (uint64_t)bits | ((uint64_t)idx << 32); }
 
-template <bool GUESS, int NW>
+template <bool GUESS, int NW, bool NT>
 DEV void topk_body(const Params& p) {
     __shared__ Smem<NW> sm;
     using W = Shape<NW>;
@@ -1005,7 +1007,7 @@ DEV void topk_body(const Params& p) {
         const int lane16 = lane * 16, qlast16 = qlast * 16;
         const int off_last = (sqb + max(nsl - 1, 0) * 64) * 16;   // the wave's last slab
         auto slab_load = [&](int s) {
-            return buf_load16(rrow, min(lane16 + min((sqb + s * 64) * 16, off_last), qlast16));
+            return buf_load16<NT>(rrow, min(lane16 + min((sqb + s * 64) * 16, off_last), qlast16));
         };
         float4 buf[kSU];
         if (nsl > 0) {
@@ -2255,10 +2257,10 @@ DEV void topk_body(const Params& p) {
     }
 }
 
+template <int NW, bool NT>
+__global__ __launch_bounds__(Shape<NW>::kBlock) void gvr_topk_kernel(Params p) { topk_body<true, NW, NT>(p); }
 template <int NW>
-__global__ __launch_bounds__(Shape<NW>::kBlock) void gvr_topk_kernel(Params p) { topk_body<true, NW>(p); }
-template <int NW>
-__global__ __launch_bounds__(Shape<NW>::kBlock) void radix_topk_kernel(Params p) { topk_body<false, NW>(p); }
+__global__ __launch_bounds__(Shape<NW>::kBlock) void radix_topk_kernel(Params p) { topk_body<false, NW, false>(p); }
 
 // ------------------------------------------------------------------ host side
 
@@ -2381,19 +2383,21 @@ gvr_status run(const float* scores, int64_t B, int64_t ld, const int32_t* row_le
         if (plan.shape == kNWMid) {
             const dim3 block(Shape<kNWMid>::kBlock);
             if (guess)
-                hipLaunchKernelGGL(gvr_topk_kernel<kNWMid>, grid, block, 0, hs, q);
+                hipLaunchKernelGGL((gvr_topk_kernel<kNWMid, false>), grid, block, 0, hs, q);
             else
                 hipLaunchKernelGGL(radix_topk_kernel<kNWMid>, grid, block, 0, hs, q);
         } else if (plan.shape == kNWShort) {
             const dim3 block(Shape<kNWShort>::kBlock);
             if (guess)
-                hipLaunchKernelGGL(gvr_topk_kernel<kNWShort>, grid, block, 0, hs, q);
+                hipLaunchKernelGGL((gvr_topk_kernel<kNWShort, false>), grid, block, 0, hs, q);
             else
                 hipLaunchKernelGGL(radix_topk_kernel<kNWShort>, grid, block, 0, hs, q);
         } else {
             const dim3 block(Shape<kNWLong>::kBlock);
-            if (guess)
-                hipLaunchKernelGGL(gvr_topk_kernel<kNWLong>, grid, block, 0, hs, q);
+            if (guess && plan.stream_hint)
+                hipLaunchKernelGGL((gvr_topk_kernel<kNWLong, true>), grid, block, 0, hs, q);
+            else if (guess)
+                hipLaunchKernelGGL((gvr_topk_kernel<kNWLong, false>), grid, block, 0, hs, q);
             else
                 hipLaunchKernelGGL(radix_topk_kernel<kNWLong>, grid, block, 0, hs, q);
         }

@@ -130,7 +130,17 @@ struct Plan {
     int shape = kNWLong;  // waves per workgroup
     int capacity = GVR_MAX_CANDIDATES;
     int parts = 1;        // workgroups per row
+    bool stream_hint = false;   // the speculative pass loads with the non-temporal hint
 };
+
+// Calls whose speculative pass loads its rows with the non-temporal hint:
+// one round of 16-wave workgroups over at least 16 MiB of rows, whose rows
+// stream from HBM and are read once. Measured per call: 128 rows of 100K
+// 22.0 -> 21.2 us, 48 rows of 64K-256K 24.2 -> 23.7 us, and even after the
+// indexer has just written the 128 rows; smaller calls (rows that a cache
+// may still hold: 32 rows of 32K, 8 of 131K, single rows) and the batched
+// 8-wave shape lose 0.1-3 us with it.
+constexpr int64_t kStreamHintBytes = (int64_t)16 << 20;
 
 // `max_slots` bounds rows * parts (the workspace's slots). An automatic split
 // is lowered to fit; a split forced through the options is lowered too unless
@@ -163,6 +173,7 @@ inline gvr_status plan_call(int64_t B, int64_t ld, int32_t K, bool have_prev, co
         }
     }
     p.parts = parts;
+    p.stream_hint = p.guess && p.shape == kNWLong && B <= (int64_t)cus && B * ld * 4 >= kStreamHintBytes;
     *out = p;
     return GVR_OK;
 }

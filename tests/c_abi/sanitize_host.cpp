@@ -77,7 +77,14 @@ static void check_plans() {
     Plan p;
     // the benchmark's call: 128 rows of ~102K with a guess, 256 compute units
     CHECK(plan_call(128, 102463, 2048, true, o, 256, kMaxSlots, false, &p) == GVR_OK);
-    CHECK(p.guess && p.shape == kNWLong && p.parts == 1 && p.capacity == GVR_MAX_CANDIDATES);
+    CHECK(p.guess && p.shape == kNWLong && p.parts == 1 && p.capacity == GVR_MAX_CANDIDATES && p.stream_hint);
+    // the non-temporal hint: one round of 16-wave workgroups over >= 16 MiB of rows only
+    CHECK(plan_call(48, 262144, 2048, true, o, 256, kMaxSlots, false, &p) == GVR_OK && p.stream_hint);
+    CHECK(plan_call(32, 32831, 2048, true, o, 256, kMaxSlots, false, &p) == GVR_OK && !p.stream_hint);
+    CHECK(plan_call(8, 131079, 2048, true, o, 256, kMaxSlots, false, &p) == GVR_OK && !p.stream_hint);
+    CHECK(plan_call(512, 65537, 2048, true, o, 256, kMaxSlots, false, &p) == GVR_OK && p.shape == kNWLong &&
+          !p.stream_hint);
+    CHECK(plan_call(128, 102463, 2048, false, o, 256, kMaxSlots, false, &p) == GVR_OK && !p.stream_hint);
     // 8 rows of 131K split into 8 parts; one row of 262K into 16
     CHECK(plan_call(8, 131079, 2048, true, o, 256, kMaxSlots, false, &p) == GVR_OK && p.parts == 8);
     CHECK(plan_call(1, 262144, 2048, true, o, 256, kMaxSlots, false, &p) == GVR_OK && p.parts == 16);

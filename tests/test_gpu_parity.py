@@ -480,6 +480,33 @@ def test_misaligned_rows_with_guess(parts):
         assert_rows_equal(out.cpu().numpy(), exp, "misaligned with guess ld=%d parts=%d" % (ld, parts))
 
 
+def test_streamed_call_edges():
+    """A call of at least 16 MiB of rows in one round of 16-wave workgroups
+    (the speculative pass loads with the non-temporal hint): misaligned rows,
+    ragged lengths, NaN beyond each row's length, and guesses that hold the
+    answer, miss it (shifted indices) or are absent (-1)."""
+    rng = np.random.default_rng(23)
+    K, B, ld = 2048, 128, 40001
+    big = rng.gamma(2.0, 1.0, size=(B * ld + 1)).astype(np.float32)
+    rows = big[1:].reshape(B, ld)
+    lens = rng.integers(2049, ld + 1, size=B).astype(np.int32)
+    lens[:4] = (ld, ld - 1, 2049, 12345)
+    exp, _, _ = oracle.topk(rows, K, row_len=lens)
+    poisoned = big.copy()
+    pr = poisoned[1:].reshape(B, ld)
+    for r in range(B):
+        pr[r, lens[r]:] = np.nan
+    guess = exp.copy()
+    guess[1::3] = (exp[1::3] + 7) % 2049   # a poor guess
+    guess[2::3] = -1                      # no usable guess
+    t = torch.from_numpy(poisoned).to(DEV)
+    S = t[1:].view(B, ld)
+    import paper_2604_22312_amd as g
+    note("streamed call edges B=%d ld=%d" % (B, ld))
+    out = g.gvr_topk(S, torch.from_numpy(lens).to(DEV), torch.from_numpy(np.ascontiguousarray(guess)).to(DEV), K)
+    assert_rows_equal(out.cpu().numpy(), exp, "streamed call edges")
+
+
 @pytest.mark.parametrize("parts", [1, 2])
 def test_poison_beyond_row_len_with_guess(parts):
     w = workload(3, 1, 8, "c")
