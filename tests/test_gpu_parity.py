@@ -754,6 +754,54 @@ def test_graph_survives_workspace_growth():
         assert_rows_equal(out2.cpu().numpy(), exp[:2], "replay %d after the workspace grew" % rep)
 
 
+def test_concurrent_streams_and_threads():
+    """Split-row calls from two host threads, each on its own stream and with
+    no synchronisation between the streams: every (device, stream) pair has
+    its own workspace, so the calls overlap on the device without sharing
+    arrival words or part lists, and every result equals the oracle."""
+    import threading
+    import paper_2604_22312_amd as g
+    rng = np.random.default_rng(41)
+    K, ld, B = 2048, 131072, 3
+    cases = []
+    for _ in range(2):
+        x = rng.standard_normal((B, ld)).astype(np.float32)
+        prevx = x + 0.05 * rng.standard_normal((B, ld)).astype(np.float32)
+        exp, _, _ = oracle.topk(x, K)
+        pexp, _, _ = oracle.topk(prevx, K)
+        cases.append((torch.from_numpy(x).to(DEV), torch.from_numpy(pexp).to(DEV), exp))
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    reps = 12
+    outs = [[torch.empty((B, K), dtype=torch.int32, device=DEV) for _ in range(reps)] for _ in range(2)]
+    errors = []
+
+    def worker(i):
+        try:
+            S, P, _ = cases[i]
+            with torch.cuda.stream(streams[i]):
+                for r in range(reps):
+                    opts = {"parts": 4 if r % 2 == 0 else 8}
+                    if r % 3 == 2:   # the guess-free schedule splits too
+                        g.radix_topk_ex(S, None, K, out_idx=outs[i][r], stream=streams[i], options=opts)
+                    else:
+                        g.gvr_topk_ex(S, None, P, K, out_idx=outs[i][r], stream=streams[i], options=opts)
+        except Exception as e:   # reported by the main thread
+            errors.append(e)
+
+    note("two host threads, two streams, split calls")
+    torch.cuda.synchronize()
+    threads = [threading.Thread(target=worker, args=(i,)) for i in range(2)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    torch.cuda.synchronize()
+    assert not errors, errors
+    for i in range(2):
+        for r in range(reps):
+            assert_rows_equal(outs[i][r].cpu().numpy(), cases[i][2], "thread %d call %d" % (i, r))
+
+
 @pytest.mark.parametrize("opts", [{"flags": 16, "capacity": 2048}, {"flags": 16, "capacity": 2500},
                                   {"flags": 16 | 1}, {"flags": 16 | 8, "capacity": 3000},
                                   {"flags": 64, "capacity": 2048}, {"flags": 64, "capacity": 2500},
