@@ -14,6 +14,8 @@ Functions mirror the C entry points:
 * ``gvr_topk_ex`` / ``radix_topk_ex`` (options, per-row stats)
 * ``gvr_topk_ex_noalloc`` -- ``gvr_topk_ex`` with no allocation inside the
   call (split-row workspace in a static device array)
+* ``prepare_gvr_topk`` / ``prepare_radix_topk`` -- a call checked and
+  marshalled once, re-enqueued by calling it (loops over fixed buffers)
 * ``gvr_rope_g(n, params=None, device=...)`` -- g(Delta) of the RoPE/YaRN prior
 * ``gvr_rope_prior(n, K, params=None, device=...)`` -- its static index set
   (``include/gvr_rope_prior.h``)
@@ -27,6 +29,7 @@ from .binding import (  # noqa: F401
     PATH_NAMES,
     GvrError,
     Options,
+    PreparedCall,
     RopeParams,
     decode_stats,
     gvr_indexer_scores,
@@ -41,6 +44,8 @@ from .binding import (  # noqa: F401
     lib,
     library_path,
     new_stats,
+    prepare_gvr_topk,
+    prepare_radix_topk,
     radix_topk,
     radix_topk_ex,
     status_string,

@@ -185,6 +185,62 @@ def radix_topk_ex(scores, row_len, K, out_idx=None, stream=None, options=None, s
     return _call_ex(True, scores, row_len, None, K, out_idx, stream, options, stats)
 
 
+class PreparedCall:
+    """One Top-K call whose tensors were checked and whose pointers were
+    marshalled once: calling the object enqueues the same call again, on the
+    same stream, and returns its ``out_idx``. The tensors must stay alive and
+    keep their shapes; their contents may change between calls. For loops over
+    fixed buffers, where the per-call checks would take more host time than
+    the kernel takes on the device."""
+    __slots__ = ("_f", "_args", "_name", "_dev", "out_idx", "_keep")
+
+    def __call__(self):
+        if torch.cuda.current_device() != self._dev:
+            with torch.cuda.device(self._dev):
+                st = self._f(*self._args)
+        else:
+            st = self._f(*self._args)
+        if st != 0:
+            raise GvrError(self._name, st)
+        return self.out_idx
+
+
+def _prepare(radix, scores, row_len, prev_topk, K, out_idx, stream, options):
+    B, ld, K, out_idx = _check(scores, row_len, None if radix else prev_topk, K, out_idx)
+    L = lib()
+    opt = None
+    if options is not None:
+        opt = Options(**options) if isinstance(options, dict) else options
+    pc = PreparedCall()
+    pc._dev = scores.device.index if scores.device.index is not None else torch.cuda.current_device()
+    sp = _stream(stream, scores.device)
+    if opt is None and not radix:
+        pc._name, pc._f = "gvr_topk", L.gvr_topk
+        pc._args = (_ptr(scores), B, ld, _ptr(row_len), _ptr(prev_topk), K, _ptr(out_idx), sp)
+    elif opt is None:
+        pc._name, pc._f = "radix_topk", L.radix_topk
+        pc._args = (_ptr(scores), B, ld, _ptr(row_len), None, K, _ptr(out_idx), sp)
+    elif radix:
+        pc._name, pc._f = "radix_topk_ex", L.radix_topk_ex
+        pc._args = (_ptr(scores), B, ld, _ptr(row_len), K, _ptr(out_idx), sp, ctypes.byref(opt), None)
+    else:
+        pc._name, pc._f = "gvr_topk_ex", L.gvr_topk_ex
+        pc._args = (_ptr(scores), B, ld, _ptr(row_len), _ptr(prev_topk), K, _ptr(out_idx), sp, ctypes.byref(opt), None)
+    pc.out_idx = out_idx
+    pc._keep = (scores, row_len, prev_topk, opt, stream)
+    return pc
+
+
+def prepare_gvr_topk(scores, row_len, prev_topk, K, out_idx=None, stream=None, options=None):
+    """A ``PreparedCall`` of ``gvr_topk`` (``gvr_topk_ex`` with options)."""
+    return _prepare(False, scores, row_len, prev_topk, K, out_idx, stream, options)
+
+
+def prepare_radix_topk(scores, row_len, K, out_idx=None, stream=None, options=None):
+    """A ``PreparedCall`` of ``radix_topk`` (``radix_topk_ex`` with options)."""
+    return _prepare(True, scores, row_len, None, K, out_idx, stream, options)
+
+
 def new_stats(B, device):
     """A zeroed stats tensor for ``*_ex`` calls."""
     return torch.zeros((B, STATS_INTS), dtype=torch.int32, device=device)

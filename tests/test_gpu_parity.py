@@ -754,6 +754,42 @@ def test_graph_survives_workspace_growth():
         assert_rows_equal(out2.cpu().numpy(), exp[:2], "replay %d after the workspace grew" % rep)
 
 
+def test_prepared_calls():
+    """The binding's prepared calls (arguments checked and marshalled once)
+    enqueue the same work as the plain calls: equal to the oracle on every
+    call, also after the input buffers were rewritten in place; an option the
+    library refuses raises on the call."""
+    import paper_2604_22312_amd as g
+    rng = np.random.default_rng(43)
+    K, B, ld = 2048, 4, 70001
+    x = rng.standard_normal((B, ld)).astype(np.float32)
+    lens = np.array([ld, ld - 5, 50000, 4096], np.int32)
+    S = torch.from_numpy(x).to(DEV)
+    RL = torch.from_numpy(lens).to(DEV)
+    exp, _, _ = oracle.topk(x, K, row_len=lens)
+    P = torch.from_numpy(np.ascontiguousarray(exp)).to(DEV)
+    stream = torch.cuda.Stream()
+    preps = {"gvr": g.prepare_gvr_topk(S, RL, P, K, stream=stream),
+             "gvr_ex": g.prepare_gvr_topk(S, RL, P, K, stream=stream, options={"parts": 3}),
+             "radix": g.prepare_radix_topk(S, RL, K, stream=stream),
+             "radix_ex": g.prepare_radix_topk(S, RL, K, stream=stream, options={"parts": 2})}
+    note("prepared calls")
+    for rep in range(2):
+        for name, pc in preps.items():
+            pc.out_idx.fill_(-7)
+            out = pc()
+            torch.cuda.synchronize()
+            assert out is pc.out_idx
+            assert_rows_equal(out.cpu().numpy(), exp, "prepared %s call %d" % (name, rep))
+        # new contents in the same buffers (the guess stays the old answer)
+        x = rng.standard_normal((B, ld)).astype(np.float32)
+        S.copy_(torch.from_numpy(x))
+        exp, _, _ = oracle.topk(x, K, row_len=lens)
+    bad = g.prepare_gvr_topk(S, RL, P, K, stream=stream, options={"flags": 256})
+    with pytest.raises(g.GvrError):
+        bad()
+
+
 def test_concurrent_streams_and_threads():
     """Split-row calls from two host threads, each on its own stream and with
     no synchronisation between the streams: every (device, stream) pair has
