@@ -101,6 +101,26 @@ def _stream(stream, device):
     return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
 
 
+def _on_device(dev):
+    """The tensors' device made current for the call (a no-op context when it
+    already is, which skips the device switch and restore)."""
+    idx = dev.index if isinstance(dev, torch.device) else int(dev)
+    if idx is None or torch.cuda.current_device() == idx:
+        return _NO_SWITCH
+    return torch.cuda.device(idx)
+
+
+class _NoSwitch:
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        return False
+
+
+_NO_SWITCH = _NoSwitch()
+
+
 def _check(scores, row_len, prev_topk, K, out_idx):
     if not isinstance(scores, torch.Tensor) or scores.dtype != torch.float32 or scores.dim() != 2:
         raise ValueError("scores must be a float32 tensor [B][ld]")
@@ -128,7 +148,7 @@ def _check(scores, row_len, prev_topk, K, out_idx):
 
 def _call(fn_name, scores, row_len, prev_topk, K, out_idx, stream):
     B, ld, K, out_idx = _check(scores, row_len, prev_topk, K, out_idx)
-    with torch.cuda.device(scores.device):
+    with _on_device(scores.device):
         st = getattr(lib(), fn_name)(_ptr(scores), B, ld, _ptr(row_len), _ptr(prev_topk), K,
                                      _ptr(out_idx), _stream(stream, scores.device))
     if st != 0:
@@ -155,7 +175,7 @@ def _call_ex(radix, scores, row_len, prev_topk, K, out_idx, stream, options, sta
     if options is not None:
         opt = Options(**options) if isinstance(options, dict) else options
     optp = ctypes.byref(opt) if opt is not None else None
-    with torch.cuda.device(scores.device):
+    with _on_device(scores.device):
         L = lib()
         if radix:
             st = L.radix_topk_ex(_ptr(scores), B, ld, _ptr(row_len), K, _ptr(out_idx),
@@ -300,7 +320,7 @@ def gvr_rope_g(n, params=None, device="cuda", g=None, theta=None, stream=None):
         if t is not None and (t.dtype != torch.float64 or t.numel() != size or t.device != dev
                               or not t.is_contiguous()):
             raise ValueError("g / theta must be contiguous float64 tensors of n / d/2 elements on the device")
-    with torch.cuda.device(dev):
+    with _on_device(dev):
         st = lib().gvr_rope_g(n, ctypes.byref(params), _ptr(g), _ptr(theta), _stream(stream, dev))
     if st != 0:
         raise GvrError("gvr_rope_g", st)
@@ -320,7 +340,7 @@ def gvr_rope_prior(n, K, params=None, device="cuda", out=None, g=None, stream=No
         out = torch.empty(max(K, 0), dtype=torch.int32, device=dev)
     elif out.dtype != torch.int32 or out.numel() != K or out.device != dev or not out.is_contiguous():
         raise ValueError("out must be a contiguous int32 tensor of K elements on the device")
-    with torch.cuda.device(dev):
+    with _on_device(dev):
         st = lib().gvr_rope_prior(n, K, ctypes.byref(params), _ptr(g), _ptr(out), _stream(stream, dev))
     if st != 0:
         raise GvrError("gvr_rope_prior", st)
@@ -359,7 +379,7 @@ def gvr_indexer_scores(q, w, k, k_scale, row_len=None, scores=None, stream=None)
     from FP8 E4M3 bytes q [B][H][D], key cache k [C][ld][D] shared by B / C
     consecutive rows, k_scale [C][ld] and head weights w [B][H]."""
     B, H, D, group, ld, scores = _check_indexer(q, w, k, k_scale, row_len, scores)
-    with torch.cuda.device(q.device):
+    with _on_device(q.device):
         st = lib().gvr_indexer_scores(_ptr(q), _ptr(w), _ptr(k), _ptr(k_scale), B, H, D, group, ld,
                                       _ptr(row_len), _ptr(scores), _stream(stream, q.device))
     if st != 0:
@@ -375,7 +395,7 @@ def gvr_indexer_topk(q, w, k, k_scale, row_len, prev_topk, K, scores=None, out_i
     opt = None
     if options is not None:
         opt = Options(**options) if isinstance(options, dict) else options
-    with torch.cuda.device(q.device):
+    with _on_device(q.device):
         st = lib().gvr_indexer_topk(_ptr(q), _ptr(w), _ptr(k), _ptr(k_scale), B, H, D, group, ld,
                                     _ptr(row_len), _ptr(scores), _ptr(prev_topk), K, _ptr(out_idx),
                                     _stream(stream, q.device), ctypes.byref(opt) if opt is not None else None,
@@ -402,7 +422,7 @@ def gvr_read_floor(scores, row_len=None, out_words=None, stream=None):
     elif (out_words.dtype != torch.int32 or out_words.shape != (B, 16) or out_words.device != scores.device
           or not out_words.is_contiguous()):
         raise ValueError("out_words must be a contiguous int32 tensor [B][16] on the scores' device")
-    with torch.cuda.device(scores.device):
+    with _on_device(scores.device):
         st = lib().gvr_read_floor(_ptr(scores), B, ld, _ptr(row_len), _ptr(out_words), _stream(stream, scores.device))
     if st != 0:
         raise GvrError("gvr_read_floor", st)
