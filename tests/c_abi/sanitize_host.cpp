@@ -88,6 +88,9 @@ static void check_plans() {
     // 8 rows of 131K split into 8 parts; one row of 262K into 16
     CHECK(plan_call(8, 131079, 2048, true, o, 256, kMaxSlots, false, &p) == GVR_OK && p.parts == 8);
     CHECK(plan_call(1, 262144, 2048, true, o, 256, kMaxSlots, false, &p) == GVR_OK && p.parts == 16);
+    CHECK(plan_call(1, 32768, 2048, true, o, 256, kMaxSlots, false, &p) == GVR_OK && p.parts == 8);
+    CHECK(plan_call(2, 70690, 2048, true, o, 256, kMaxSlots, false, &p) == GVR_OK && p.parts == 8);
+    CHECK(plan_call(1, 16384, 2048, true, o, 256, kMaxSlots, false, &p) == GVR_OK && p.parts == 1);
     // no guess: the radix schedule splits few long rows too (8 parts of 131K),
     // not 100K rows at 128 per call and 32K rows at 32; short rows: 4 waves;
     // mid rows: 8 waves with their capacities

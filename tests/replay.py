@@ -69,10 +69,7 @@ def choose_parts(rows: int, ld: int, cus: int = 256) -> int:
     if rows <= 0 or rows >= cus:
         return 1
     if rows <= 2 and ld >= 32768 and cus >= 32 * rows:
-        s = 1
-        while 2 * s <= ld // 8192 and 2 * s <= MAX_PARTS:
-            s *= 2
-        return min(s, 8) if ld < 196608 else s
+        return 8 if ld < 196608 else MAX_PARTS
     s = cus // rows
     s = min(s, max(1, ld // MIN_PART_ELEMS), MAX_PARTS)
     if s <= 1:
