@@ -90,6 +90,13 @@ inline gvr_status validate(const void* scores, int64_t B, int64_t ld, int32_t K,
 inline int choose_parts(int64_t rows, int64_t ld, int cus, bool radix = false) {
     if (rows <= 0 || rows >= cus) return 1;
     if (rows <= 2 && ld >= 32768 && cus >= 32 * rows) return ld < 196608 ? 8 : kMaxParts;
+    // Up to a quarter as many rows as compute units, from 48K elements on:
+    // four to eight parts per row (measured with a guess: 16 rows of 64K
+    // 16.8 -> 14.9 us in 8 parts, 48 rows 17.0 -> 15.6 in 5, 32 rows of 57K
+    // 16.2 -> 15.3 in 8; at 40K splitting gains nothing, and two parts never
+    // pay for their merge).
+    if (!radix && ld >= 49152 && cus / rows >= 4)
+        return (int)std::min<int64_t>(std::min<int64_t>(cus / rows, kMaxParts), ld < 196608 ? 8 : kMaxParts);
     int64_t s = cus / rows;
     s = std::min<int64_t>(s, std::max<int64_t>(1, ld / kMinPartElems));
     s = std::min<int64_t>(s, kMaxParts);

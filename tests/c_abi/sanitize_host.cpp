@@ -91,6 +91,12 @@ static void check_plans() {
     CHECK(plan_call(1, 32768, 2048, true, o, 256, kMaxSlots, false, &p) == GVR_OK && p.parts == 8);
     CHECK(plan_call(2, 70690, 2048, true, o, 256, kMaxSlots, false, &p) == GVR_OK && p.parts == 8);
     CHECK(plan_call(1, 16384, 2048, true, o, 256, kMaxSlots, false, &p) == GVR_OK && p.parts == 1);
+    // few rows from 48K elements: four to eight parts (with a guess)
+    CHECK(plan_call(16, 65536, 2048, true, o, 256, kMaxSlots, false, &p) == GVR_OK && p.parts == 8);
+    CHECK(plan_call(48, 65536, 2048, true, o, 256, kMaxSlots, false, &p) == GVR_OK && p.parts == 5);
+    CHECK(plan_call(64, 102400, 2048, true, o, 256, kMaxSlots, false, &p) == GVR_OK && p.parts == 4);
+    CHECK(plan_call(32, 40000, 2048, true, o, 256, kMaxSlots, false, &p) == GVR_OK && p.parts == 1);
+    CHECK(plan_call(65, 65536, 2048, true, o, 256, kMaxSlots, false, &p) == GVR_OK && p.parts == 1);
     // no guess: the radix schedule splits few long rows too (8 parts of 131K),
     // not 100K rows at 128 per call and 32K rows at 32; short rows: 4 waves;
     // mid rows: 8 waves with their capacities

@@ -70,6 +70,8 @@ def choose_parts(rows: int, ld: int, cus: int = 256) -> int:
         return 1
     if rows <= 2 and ld >= 32768 and cus >= 32 * rows:
         return 8 if ld < 196608 else MAX_PARTS
+    if ld >= 49152 and cus // rows >= 4:
+        return min(cus // rows, MAX_PARTS, 8 if ld < 196608 else MAX_PARTS)
     s = cus // rows
     s = min(s, max(1, ld // MIN_PART_ELEMS), MAX_PARTS)
     if s <= 1:

@@ -185,11 +185,13 @@ def test_gvr_repacks_bunched_candidates():
     assert int(st["passes"].max()) <= 3
 
 
-@pytest.mark.parametrize("rows", [1, 2])
-@pytest.mark.parametrize("n", [32768, 65537, 131072, 262144])
+@pytest.mark.parametrize("rows,n", [(r, n) for r in (1, 2) for n in (32768, 65537, 131072, 262144)]
+                         + [(16, 49153), (48, 65536), (64, 60001)])
 def test_gvr_small_batch_split_rows(rows, n):
-    """Calls of one or two long rows split each row over several workgroups
-    (the chip is otherwise idle); the answer is exact whatever the split."""
+    """Calls of a few long rows split each row over several workgroups (one
+    or two rows: 8 or 16 parts; up to a quarter as many rows as compute
+    units from 48K elements: 4 to 8 parts); the answer is exact whatever the
+    split."""
     import paper_2604_22312_amd as g
     s = WR.batch_scores(n, rows)
     exp, _, _ = oracle.topk(s, K_TOPK)
