@@ -402,12 +402,14 @@ DEV uint32_t refine_kth(Smem<NW>& sm, uint32_t wlo, uint32_t whi, int above, int
             if (run < need && nr >= need) {
                 sm.scal[0] = tid * PER + q;
                 sm.scal[1] = run;
+                sm.scal[2] = loc[q];
             }
             run = nr;
         }
         lds_barrier();
         const int b = sm.scal[0];
         const int ab = sm.scal[1];
+        const int cb = sm.scal[2];
         lds_barrier();
         if (b < 0) break;   // cannot happen for consistent counts; keeps every path finite
         need -= ab;
@@ -416,6 +418,53 @@ DEV uint32_t refine_kth(Smem<NW>& sm, uint32_t wlo, uint32_t whi, int above, int
         if (nhi > whi) nhi = whi;
         wlo = (uint32_t)nlo;
         whi = (uint32_t)nhi;
+        if (wlo != whi && cb <= kSmall) {
+            // A few candidates left in the window: copy their keys to a
+            // small LDS array (over the histogram, no longer needed) and let
+            // wave 0 rank them, one candidate per lane, against LDS-broadcast
+            // keys: T* is the need-th largest of them.
+            uint32_t* const skey = reinterpret_cast<uint32_t*>(sm.u.rhist);
+            if (tid == 0) sm.scal[3] = 0;
+            lds_barrier();
+            {
+                const uint2* seg = sm.list + sm.seg_off[wave];
+                const int cnt = sm.seg_cnt[wave];
+                for (int i0 = 0; i0 < cnt; i0 += kWave) {   // wave-uniform bound: every lane runs each step
+                    const int i = i0 + lane;
+                    const uint32_t kk = i < cnt ? seg[i].x : 0u;
+                    const bool in = i < cnt && kk >= wlo && kk <= whi;
+                    const uint64_t m = __ballot(in);
+                    if (m) {   // wave-uniform
+                        int base = 0;
+                        if (lane == 0)
+                            base = __hip_atomic_fetch_add(&sm.scal[3], (int)__popcll(m), __ATOMIC_RELAXED,
+                                                          __HIP_MEMORY_SCOPE_WORKGROUP);
+                        base = __builtin_amdgcn_readfirstlane(base);
+                        const int pos = base + (int)lanes_below(m, 0);
+                        if (in && pos < kSmall) skey[pos] = kk;
+                    }
+                }
+            }
+            lds_barrier();
+            if (wave == 0) {
+                const int c = min(cb, kSmall);
+                const bool v = lane < c;
+                const uint32_t mine = v ? skey[lane] : 0u;
+                int gt = 0, ge = 0;
+                for (int j = 0; j < c; ++j) {
+                    const uint32_t o = skey[j];   // one address for the wave: a broadcast
+                    gt += o > mine;
+                    ge += o >= mine;
+                }
+                const uint64_t hit = __ballot(v && gt < need && ge >= need);
+                const uint32_t kth = hit ? __builtin_amdgcn_readlane(mine, (int)__builtin_ctzll(hit)) : wlo;
+                if (lane == 0) sm.scal[0] = (int)kth;
+            }
+            lds_barrier();
+            const uint32_t kth = (uint32_t)sm.scal[0];
+            lds_barrier();   // scal[0] is read before it is written again
+            return kth;
+        }
     }
     return wlo;
 }
@@ -1923,7 +1972,15 @@ DEV void topk_body(const Params& p) {
         rhi = 0xFFFFFFFFu;
         bin_hi = max(gmax, tthr);
         above = 0;
-        if (all_mode) {   // no guess range: bin [min, max] of the (few) listed keys
+        if (all_mode) {
+            // No guess range: bin [min, max] of the (few) listed keys. When
+            // they hold both signs the range is cut at the sign: the keys of
+            // one sign lie binades away from the other's, so a range over
+            // both would crowd each side into a few bins. With at least K
+            // keys >= +0 the K-th key is one of them (range [min, max] of
+            // those); otherwise it is negative, below all of them (range of
+            // the negative keys, the others counted above it).
+            constexpr uint32_t kPos = 0x80000000u;   // key of +0.0
             uint32_t mn = 0xFFFFFFFFu, mx = 0u;
             for_my_keys(sm, wave, lane, [&](uint32_t kk) {
                 mn = min(mn, kk);
@@ -1938,6 +1995,32 @@ DEV void topk_body(const Params& p) {
             __syncthreads();
             rlo = wave_min_u(lane < NW ? (uint32_t)sm.red[2][lane] : 0xFFFFFFFFu);
             rhi = bin_hi = wave_max_u(lane < NW ? (uint32_t)sm.red[3][lane] : 0u);
+            if (rlo < kPos && rhi >= kPos) {   // both signs (workgroup-uniform): one more pass
+                uint32_t mn_p = 0xFFFFFFFFu, mx_n = 0u;
+                int npos = 0;
+                for_my_keys(sm, wave, lane, [&](uint32_t kk) {
+                    const bool pos = kk >= kPos;
+                    mn_p = pos ? min(mn_p, kk) : mn_p;
+                    mx_n = pos ? mx_n : max(mx_n, kk);
+                    npos += pos;
+                });
+                mn_p = wave_min_u(mn_p);
+                mx_n = wave_max_u(mx_n);
+                npos = wave_sum(npos);
+                if (lane == 0) {
+                    sm.red[0][wave] = (int)mn_p;
+                    sm.red[1][wave] = (int)mx_n;
+                    sm.wb[wave] = npos;
+                }
+                __syncthreads();
+                const int np = sum_over_waves<NW>(sm.wb, lane);
+                if (np >= K) {
+                    rlo = wave_min_u(lane < NW ? (uint32_t)sm.red[0][lane] : 0xFFFFFFFFu);
+                } else {
+                    rhi = bin_hi = wave_max_u(lane < NW ? (uint32_t)sm.red[1][lane] : 0u);
+                    above = np;
+                }
+            }
         }
     } else {
         bool whole_range = true;   // nothing bounds the K-th key yet
