@@ -811,16 +811,23 @@ DEV uint32_t refine_emit(Smem<NW>& sm, uint32_t rlo, uint32_t rhi, uint32_t bin_
         const int cnt = sm.seg_cnt[j];
         int gtl = 0;
         for (int i0 = 0; i0 < cnt; i0 += 4 * kWave) {
-            const int rem = cnt - i0;
             uint2 en[4];
 #pragma unroll
             for (int c = 0; c < 4; ++c) en[c] = seg[i0 + c * kWave + lane];   // past the count: masked below
+            // per lane: keys above the bin counted, bin members flagged (one
+            // ballot for the four entries: members are rare)
+            bool hit[4];
 #pragma unroll
             for (int c = 0; c < 4; ++c) {
-                const uint64_t vm = first_lanes(rem - c * kWave);   // valid lanes
-                gtl = add_lane_bit(gtl, __ballot(en[c].x > hi_b) & vm);
-                const uint64_t m = __ballot(en[c].x - lo_b <= wid) & vm;
-                if (m) {   // rare (wave-uniform)
+                const bool valid = i0 + c * kWave + lane < cnt;
+                gtl += (valid && en[c].x > hi_b) ? 1 : 0;
+                hit[c] = valid && en[c].x - lo_b <= wid;
+            }
+            if (!__ballot(hit[0] || hit[1] || hit[2] || hit[3])) continue;   // (wave-uniform)
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const uint64_t m = __ballot(hit[c]);
+                if (m) {   // (wave-uniform)
                     int base = 0;
                     if (lane == 0)
                         base = __hip_atomic_fetch_add(&sm.scal[1], (int)__popcll(m), __ATOMIC_RELAXED,
