@@ -493,14 +493,12 @@ DEV void emit_segment(const Smem<NW>& sm, int j, uint32_t T, int K, int take, in
                 const int o = g + min(eb, take);
                 if (fg && o < K) out[o] = (int)en[c].y;
             } else {
+                // a key > T goes after the first min(ties before it, take)
+                // ties; a tie is taken while fewer than `take` precede it, at
+                // the same position formula (one predicated store)
                 const int e = eb + (int)lanes_below(me, 0);
-                if (fg) {
-                    const int o = g + min(e, take);
-                    if (o >= 0 && o < K) out[o] = (int)en[c].y;
-                } else if (fe && e < take) {
-                    const int o = g + e;
-                    if (o >= 0 && o < K) out[o] = (int)en[c].y;
-                }
+                const int o = g + min(e, take);
+                if ((fg || (fe && e < take)) && o < K) out[o] = (int)en[c].y;
             }
             gb += __popcll(mg);
             eb += __popcll(me);
