@@ -502,9 +502,15 @@ def test_streamed_call_edges():
     t = torch.from_numpy(poisoned).to(DEV)
     S = t[1:].view(B, ld)
     import paper_2604_22312_amd as g
+    RL = torch.from_numpy(lens).to(DEV)
+    GU = torch.from_numpy(np.ascontiguousarray(guess)).to(DEV)
     note("streamed call edges B=%d ld=%d" % (B, ld))
-    out = g.gvr_topk(S, torch.from_numpy(lens).to(DEV), torch.from_numpy(np.ascontiguousarray(guess)).to(DEV), K)
+    out = g.gvr_topk(S, RL, GU, K)
     assert_rows_equal(out.cpu().numpy(), exp, "streamed call edges")
+    # the same call split in two parts per row (the hinted kernel's merge)
+    note("streamed call edges B=%d ld=%d parts=2" % (B, ld))
+    out = g.gvr_topk_ex(S, RL, GU, K, options={"parts": 2})
+    assert_rows_equal(out.cpu().numpy(), exp, "streamed call edges, two parts")
 
 
 @pytest.mark.parametrize("parts", [1, 2])
