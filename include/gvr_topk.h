@@ -48,8 +48,8 @@
  *     not synchronise.
  *
  * Workspace:
- *   - gvr_topk may split a long row over several workgroups (few rows, long
- *     rows: see gvr_options.parts). The parts exchange their candidate lists
+ *   - gvr_topk and radix_topk may split a long row over several workgroups
+ *     (few rows, long rows: see gvr_options.parts). The parts exchange their candidate lists
  *     through a device workspace that the library allocates on the first
  *     such call for each (device, stream) pair (hipMalloc; arrival counters
  *     + 128 KB per row part) and reuses for every later call on that stream.
@@ -66,7 +66,9 @@
  *     another stream, it must not overlap split calls on the capture stream
  *     (eager calls or replays of other graphs captured there): overlapping
  *     calls that share a workspace corrupt each other's merge.
- *   - radix_topk and unsplit gvr_topk calls use no workspace.
+ *   - Calls that do not split their rows use no workspace.
+ *   - gvr_topk_ex_ws / radix_topk_ex_ws take the workspace from the caller
+ *     instead (sized by gvr_workspace_size) and allocate nothing.
  */
 #ifndef GVR_TOPK_H
 #define GVR_TOPK_H
@@ -82,8 +84,9 @@ typedef enum {
     GVR_OK = 0,
     GVR_ERR_INVALID_ARG = -1,    /* B < 0, ld < 0, NULL required pointer, bad option */
     GVR_ERR_UNSUPPORTED_K = -2,  /* K < 1 or K > GVR_MAX_K */
-    GVR_ERR_WORKSPACE = -3,      /* gvr_topk_ex_noalloc: a forced split needs more
-                                    than GVR_NOALLOC_SLOTS (row, part) slots */
+    GVR_ERR_WORKSPACE = -3,      /* gvr_topk_ex_noalloc, *_ex_ws: a forced split
+                                    needs more (row, part) slots than the
+                                    call's workspace holds */
     GVR_ERR_HIP = -4,            /* the kernel launch failed */
     GVR_ERR_TOO_LONG = -5        /* ld > 2^31 - 16 */
 } gvr_status;
@@ -151,8 +154,9 @@ typedef struct gvr_options {
                               No bit changes the result. */
     int32_t parts;         /* workgroups per row, 1..16 (0 = chosen from B, ld
                               and the device's compute units; a forced value is
-                              lowered so that B * parts <= 2048); never changes
-                              the result */
+                              lowered so that B * parts <= 2048, or refused by
+                              the calls whose workspace is too small for it);
+                              never changes the result */
     int32_t reserved1;     /* must be 0 */
 } gvr_options;
 
@@ -222,6 +226,50 @@ gvr_status gvr_topk_ex_noalloc(const float* scores, int64_t B, int64_t ld, const
 gvr_status radix_topk_ex(const float* scores, int64_t B, int64_t ld, const int32_t* row_len,
                          int32_t K, int32_t* out_idx, void* stream, const gvr_options* options,
                          gvr_row_stats* stats);
+
+/* Caller-owned workspace: the graph-capture-safe form of the split
+ * schedule (the parts of a split row exchange their counts, thresholds,
+ * first refine histograms and candidate lists through it; Sec. 4).
+ *
+ * gvr_workspace_size writes to *bytes the workspace that a gvr_topk_ex_ws
+ * call (use_guess != 0, prev_topk non-NULL) or a radix_topk_ex_ws call
+ * (use_guess == 0) of this B, ld, K and options needs on the CURRENT device
+ * to split its rows as gvr_topk_ex / radix_topk_ex would (0 when it does not
+ * split them). It enqueues nothing. Errors: those of the call's own size and
+ * option checks (GVR_ERR_INVALID_ARG also for bytes == NULL);
+ * GVR_ERR_WORKSPACE for a forced split of more than 2^24 (row, part) slots;
+ * GVR_ERR_HIP if the current device cannot be read. */
+gvr_status gvr_workspace_size(int64_t B, int64_t ld, int32_t K, int use_guess, const gvr_options* options,
+                              size_t* bytes);
+
+/* gvr_topk_ex / radix_topk_ex with the split-row workspace supplied by the
+ * caller: `workspace` is a device buffer of ws_bytes bytes on the current
+ * device (8-byte aligned, 256 recommended; NULL only with ws_bytes == 0).
+ * The call allocates nothing, clears nothing and does not synchronise, so it
+ * may be captured into a HIP graph as any call's first, on any stream.
+ *   - Ownership: the caller's. The library keeps no reference once the call
+ *     returns; the enqueued kernel uses the buffer until it completes.
+ *   - Contents: zero-filled by the caller before its first use (hipMemset,
+ *     or a fill kernel inside a graph). Every call leaves it ready for the
+ *     next, so reuse needs no clearing as long as every call on the buffer
+ *     passes the same ws_bytes (the layout inside depends on it): clear it
+ *     again after changing ws_bytes.
+ *   - Size: with ws_bytes >= gvr_workspace_size's answer the call splits as
+ *     gvr_topk_ex / radix_topk_ex would. With less, an automatic split
+ *     (options->parts == 0) is lowered to what fits (down to one workgroup
+ *     per row, which uses no workspace), and a forced split that does not
+ *     fit returns GVR_ERR_WORKSPACE before anything is enqueued.
+ *   - Concurrency: calls that share one buffer must not overlap (one stream
+ *     orders them); calls on different buffers may.
+ *   - Errors: as gvr_topk_ex / radix_topk_ex, plus GVR_ERR_INVALID_ARG for a
+ *     NULL or misaligned workspace with ws_bytes > 0. The result is theirs
+ *     whatever the workspace size. */
+gvr_status gvr_topk_ex_ws(const float* scores, int64_t B, int64_t ld, const int32_t* row_len,
+                          const int32_t* prev_topk, int32_t K, int32_t* out_idx, void* stream,
+                          const gvr_options* options, gvr_row_stats* stats, void* workspace, size_t ws_bytes);
+gvr_status radix_topk_ex_ws(const float* scores, int64_t B, int64_t ld, const int32_t* row_len, int32_t K,
+                            int32_t* out_idx, void* stream, const gvr_options* options, gvr_row_stats* stats,
+                            void* workspace, size_t ws_bytes);
 
 /* Measurement helper, not a step of the Top-K: reads every element of
  * scores[b][0, n_b) once (n_b = clamp(row_len[b], 0, ld), row_len NULL = ld)

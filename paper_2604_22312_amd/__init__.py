@@ -14,6 +14,9 @@ Functions mirror the C entry points:
 * ``gvr_topk_ex`` / ``radix_topk_ex`` (options, per-row stats)
 * ``gvr_topk_ex_noalloc`` -- ``gvr_topk_ex`` with no allocation inside the
   call (split-row workspace in a static device array)
+* ``gvr_workspace_size`` / ``gvr_topk_ex_ws`` / ``radix_topk_ex_ws`` /
+  ``new_workspace`` -- the split-row workspace owned by the caller (nothing
+  allocated inside the call)
 * ``prepare_gvr_topk`` / ``prepare_radix_topk`` -- a call checked and
   marshalled once, re-enqueued by calling it (loops over fixed buffers)
 * ``gvr_rope_g(n, params=None, device=...)`` -- g(Delta) of the RoPE/YaRN prior
@@ -41,13 +44,17 @@ from .binding import (  # noqa: F401
     gvr_topk,
     gvr_topk_ex,
     gvr_topk_ex_noalloc,
+    gvr_topk_ex_ws,
+    gvr_workspace_size,
     lib,
     library_path,
     new_stats,
+    new_workspace,
     prepare_gvr_topk,
     prepare_radix_topk,
     radix_topk,
     radix_topk_ex,
+    radix_topk_ex_ws,
     status_string,
     version,
 )

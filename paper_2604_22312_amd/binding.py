@@ -62,6 +62,15 @@ def lib():
             f.argtypes = [vp, i64, i64, vp, vp, i32, vp, vp, ctypes.POINTER(Options), vp]
         L.radix_topk_ex.restype = ctypes.c_int
         L.radix_topk_ex.argtypes = [vp, i64, i64, vp, i32, vp, vp, ctypes.POINTER(Options), vp]
+        L.gvr_workspace_size.restype = ctypes.c_int
+        L.gvr_workspace_size.argtypes = [i64, i64, i32, ctypes.c_int, ctypes.POINTER(Options),
+                                         ctypes.POINTER(ctypes.c_size_t)]
+        L.gvr_topk_ex_ws.restype = ctypes.c_int
+        L.gvr_topk_ex_ws.argtypes = [vp, i64, i64, vp, vp, i32, vp, vp, ctypes.POINTER(Options), vp, vp,
+                                     ctypes.c_size_t]
+        L.radix_topk_ex_ws.restype = ctypes.c_int
+        L.radix_topk_ex_ws.argtypes = [vp, i64, i64, vp, i32, vp, vp, ctypes.POINTER(Options), vp, vp,
+                                       ctypes.c_size_t]
         L.gvr_rope_params_default.restype = None
         L.gvr_rope_params_default.argtypes = [ctypes.POINTER(RopeParams)]
         L.gvr_rope_g.restype = ctypes.c_int
@@ -203,6 +212,73 @@ def gvr_topk_ex_noalloc(scores, row_len, prev_topk, K, out_idx=None, stream=None
 
 def radix_topk_ex(scores, row_len, K, out_idx=None, stream=None, options=None, stats=None):
     return _call_ex(True, scores, row_len, None, K, out_idx, stream, options, stats)
+
+
+def _options(options):
+    if options is None:
+        return None
+    return Options(**options) if isinstance(options, dict) else options
+
+
+def gvr_workspace_size(B, ld, K, use_guess=True, options=None, device=None) -> int:
+    """Bytes of caller workspace a ``gvr_topk_ex_ws`` (``use_guess``, with a
+    guess) or ``radix_topk_ex_ws`` call of this shape and these options needs
+    on ``device`` (default: the current device); 0 when it does not split."""
+    opt = _options(options)
+    n = ctypes.c_size_t(0)
+    dev = torch.device(device) if device is not None else torch.device("cuda", torch.cuda.current_device())
+    with _on_device(dev):
+        st = lib().gvr_workspace_size(int(B), int(ld), int(K), 1 if use_guess else 0,
+                                      ctypes.byref(opt) if opt is not None else None, ctypes.byref(n))
+    if st != 0:
+        raise GvrError("gvr_workspace_size", st)
+    return int(n.value)
+
+
+def new_workspace(B, ld, K, use_guess=True, options=None, device=None):
+    """A zero-filled uint8 device tensor of ``gvr_workspace_size`` bytes (at
+    least one byte, so that its pointer is never NULL)."""
+    n = gvr_workspace_size(B, ld, K, use_guess, options, device)
+    dev = torch.device(device) if device is not None else torch.device("cuda", torch.cuda.current_device())
+    return torch.zeros(max(n, 1), dtype=torch.uint8, device=dev)
+
+
+def _call_ws(radix, scores, row_len, prev_topk, K, workspace, out_idx, stream, options, stats):
+    B, ld, K, out_idx = _check(scores, row_len, None if radix else prev_topk, K, out_idx)
+    if stats is not None and (stats.dtype != torch.int32 or stats.shape != (B, STATS_INTS)
+                              or stats.device != scores.device or not stats.is_contiguous()):
+        raise ValueError("stats must be a contiguous int32 tensor [B][%d] on the scores' device" % STATS_INTS)
+    if workspace is not None and (workspace.device != scores.device or not workspace.is_contiguous()):
+        raise ValueError("workspace must be a contiguous tensor on the scores' device")
+    nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    opt = _options(options)
+    optp = ctypes.byref(opt) if opt is not None else None
+    with _on_device(scores.device):
+        L = lib()
+        if radix:
+            st = L.radix_topk_ex_ws(_ptr(scores), B, ld, _ptr(row_len), K, _ptr(out_idx),
+                                    _stream(stream, scores.device), optp, _ptr(stats), _ptr(workspace), nbytes)
+        else:
+            st = L.gvr_topk_ex_ws(_ptr(scores), B, ld, _ptr(row_len), _ptr(prev_topk), K, _ptr(out_idx),
+                                  _stream(stream, scores.device), optp, _ptr(stats), _ptr(workspace), nbytes)
+    if st != 0:
+        raise GvrError("radix_topk_ex_ws" if radix else "gvr_topk_ex_ws", st)
+    return out_idx
+
+
+def gvr_topk_ex_ws(scores, row_len, prev_topk, K, workspace, out_idx=None, stream=None, options=None,
+                   stats=None):
+    """``gvr_topk_ex`` with the split-row workspace supplied by the caller
+    (``workspace``: a contiguous device tensor, zero-filled before its first
+    use, e.g. from ``new_workspace``; its size in bytes is passed as
+    ws_bytes; None = no workspace). ``out_idx`` is allocated here when it is
+    None, before the call."""
+    return _call_ws(False, scores, row_len, prev_topk, K, workspace, out_idx, stream, options, stats)
+
+
+def radix_topk_ex_ws(scores, row_len, K, workspace, out_idx=None, stream=None, options=None, stats=None):
+    """``radix_topk_ex`` with a caller workspace (as ``gvr_topk_ex_ws``)."""
+    return _call_ws(True, scores, row_len, None, K, workspace, out_idx, stream, options, stats)
 
 
 class PreparedCall:

@@ -2408,32 +2408,48 @@ gvr_status static_scratch(int device, void** out) {
     return GVR_OK;
 }
 
-enum WsSource { kWsLibrary = 0, kWsStatic = 1 };
+// Where a split call's workspace comes from: the library's per-stream cache,
+// the static array, or a buffer the caller passes in.
+enum WsSource { kWsLibrary = 0, kWsStatic = 1, kWsCaller = 2 };
+
+struct Workspace {
+    WsSource source = kWsLibrary;
+    void* base = nullptr;   // kWsCaller only
+    size_t bytes = 0;
+};
 
 gvr_status run(const float* scores, int64_t B, int64_t ld, const int32_t* row_len, const int32_t* prev,
                int32_t K, int32_t* out, void* stream, const gvr_options* opt, gvr_row_stats* stats,
-               int use_guess, WsSource ws_source, const int32_t* gstats = nullptr) {
+               int use_guess, Workspace wsrc, const int32_t* gstats = nullptr) {
     gvr_host::CallOptions o;
     gvr_status st = gvr_host::validate(scores, B, ld, K, out, opt, use_guess, &o);
     if (st != GVR_OK) return st;
+    int64_t caller_slots = 0;
+    if (wsrc.source == kWsCaller) {
+        if (wsrc.bytes > 0 && (!wsrc.base || (reinterpret_cast<uintptr_t>(wsrc.base) & 7))) return GVR_ERR_INVALID_ARG;
+        caller_slots = gvr_host::ws_slots_fitting(wsrc.bytes);
+    }
     if (B == 0) return GVR_OK;
     int device = 0;
     if (hipGetDevice(&device) != hipSuccess) return GVR_ERR_HIP;
     const int cus = cu_count(device);
     gvr_host::Plan plan;
-    const bool is_static = ws_source == kWsStatic;
-    st = gvr_host::plan_call(B, ld, K, prev != nullptr, o, cus,
-                             is_static ? gvr_host::kStaticSlots : gvr_host::kMaxSlots, is_static, &plan);
+    const int64_t max_slots = wsrc.source == kWsStatic   ? gvr_host::kStaticSlots
+                              : wsrc.source == kWsCaller ? caller_slots
+                                                         : gvr_host::kMaxSlots;
+    st = gvr_host::plan_call(B, ld, K, prev != nullptr, o, cus, max_slots, wsrc.source != kWsLibrary, &plan);
     if (st != GVR_OK) return st;
     const bool guess = plan.guess;
     const int parts = plan.parts;
     gvr_host::WsPtrs ws;
     if (parts > 1) {
-        if (is_static) {
+        if (wsrc.source == kWsStatic) {
             void* base = nullptr;
             st = static_scratch(device, &base);
             if (st != GVR_OK) return st;
             ws = gvr_host::ws_carve(base, gvr_host::kStaticSlots);
+        } else if (wsrc.source == kWsCaller) {
+            ws = gvr_host::ws_carve(wsrc.base, caller_slots);
         } else {
             st = g_workspaces.get(device, stream, B * (int64_t)parts, &ws);
             if (st != GVR_OK) return st;
@@ -2502,7 +2518,7 @@ gvr_status topk_with_guess_stats(const float* scores, int64_t B, int64_t ld, con
                                  const int32_t* prev_topk, int32_t K, int32_t* out_idx, void* stream,
                                  const gvr_options* options, gvr_row_stats* stats) {
     if (K < kGuessWords || !out_idx) return GVR_ERR_INVALID_ARG;
-    return run(scores, B, ld, row_len, prev_topk, K, out_idx, stream, options, stats, 1, kWsLibrary,
+    return run(scores, B, ld, row_len, prev_topk, K, out_idx, stream, options, stats, 1, Workspace(),
                out_idx + (K - kGuessWords));
 }
 
@@ -2512,30 +2528,61 @@ extern "C" {
 
 gvr_status gvr_topk(const float* scores, int64_t B, int64_t ld, const int32_t* row_len, const int32_t* prev_topk,
                     int32_t K, int32_t* out_idx, void* stream) {
-    return run(scores, B, ld, row_len, prev_topk, K, out_idx, stream, nullptr, nullptr, 1, kWsLibrary);
+    return run(scores, B, ld, row_len, prev_topk, K, out_idx, stream, nullptr, nullptr, 1, Workspace());
 }
 
 gvr_status radix_topk(const float* scores, int64_t B, int64_t ld, const int32_t* row_len, const int32_t* prev_topk,
                       int32_t K, int32_t* out_idx, void* stream) {
     (void)prev_topk;
-    return run(scores, B, ld, row_len, nullptr, K, out_idx, stream, nullptr, nullptr, 0, kWsLibrary);
+    return run(scores, B, ld, row_len, nullptr, K, out_idx, stream, nullptr, nullptr, 0, Workspace());
 }
 
 gvr_status gvr_topk_ex(const float* scores, int64_t B, int64_t ld, const int32_t* row_len, const int32_t* prev_topk,
                        int32_t K, int32_t* out_idx, void* stream, const gvr_options* options,
                        gvr_row_stats* stats) {
-    return run(scores, B, ld, row_len, prev_topk, K, out_idx, stream, options, stats, 1, kWsLibrary);
+    return run(scores, B, ld, row_len, prev_topk, K, out_idx, stream, options, stats, 1, Workspace());
 }
 
 gvr_status gvr_topk_ex_noalloc(const float* scores, int64_t B, int64_t ld, const int32_t* row_len,
                                const int32_t* prev_topk, int32_t K, int32_t* out_idx, void* stream,
                                const gvr_options* options, gvr_row_stats* stats) {
-    return run(scores, B, ld, row_len, prev_topk, K, out_idx, stream, options, stats, 1, kWsStatic);
+    return run(scores, B, ld, row_len, prev_topk, K, out_idx, stream, options, stats, 1, Workspace{kWsStatic, nullptr, 0});
 }
 
 gvr_status radix_topk_ex(const float* scores, int64_t B, int64_t ld, const int32_t* row_len, int32_t K,
                          int32_t* out_idx, void* stream, const gvr_options* options, gvr_row_stats* stats) {
-    return run(scores, B, ld, row_len, nullptr, K, out_idx, stream, options, stats, 0, kWsLibrary);
+    return run(scores, B, ld, row_len, nullptr, K, out_idx, stream, options, stats, 0, Workspace());
+}
+
+gvr_status gvr_workspace_size(int64_t B, int64_t ld, int32_t K, int use_guess, const gvr_options* options,
+                              size_t* bytes) {
+    if (!bytes) return GVR_ERR_INVALID_ARG;
+    *bytes = 0;
+    gvr_host::CallOptions o;
+    gvr_status st = gvr_host::validate_sizes(B, ld, K, options, use_guess ? 1 : 0, &o);
+    if (st != GVR_OK) return st;
+    if (B == 0) return GVR_OK;
+    int device = 0;
+    if (hipGetDevice(&device) != hipSuccess) return GVR_ERR_HIP;
+    gvr_host::Plan plan;
+    st = gvr_host::plan_call(B, ld, K, use_guess != 0, o, cu_count(device), gvr_host::kMaxCallerSlots, true, &plan);
+    if (st != GVR_OK) return st;
+    if (plan.parts > 1) *bytes = gvr_host::ws_layout(B * (int64_t)plan.parts).total;
+    return GVR_OK;
+}
+
+gvr_status gvr_topk_ex_ws(const float* scores, int64_t B, int64_t ld, const int32_t* row_len,
+                          const int32_t* prev_topk, int32_t K, int32_t* out_idx, void* stream,
+                          const gvr_options* options, gvr_row_stats* stats, void* workspace, size_t ws_bytes) {
+    return run(scores, B, ld, row_len, prev_topk, K, out_idx, stream, options, stats, 1,
+               Workspace{kWsCaller, workspace, ws_bytes});
+}
+
+gvr_status radix_topk_ex_ws(const float* scores, int64_t B, int64_t ld, const int32_t* row_len, int32_t K,
+                            int32_t* out_idx, void* stream, const gvr_options* options, gvr_row_stats* stats,
+                            void* workspace, size_t ws_bytes) {
+    return run(scores, B, ld, row_len, nullptr, K, out_idx, stream, options, stats, 0,
+               Workspace{kWsCaller, workspace, ws_bytes});
 }
 
 const char* gvr_status_string(gvr_status s) {
@@ -2543,7 +2590,7 @@ const char* gvr_status_string(gvr_status s) {
         case GVR_OK: return "ok";
         case GVR_ERR_INVALID_ARG: return "invalid argument";
         case GVR_ERR_UNSUPPORTED_K: return "unsupported K (1 <= K <= 2048)";
-        case GVR_ERR_WORKSPACE: return "the call needs more scratch than the allocation-free entry point holds";
+        case GVR_ERR_WORKSPACE: return "a forced split needs more workspace than the call was given";
         case GVR_ERR_HIP: return "HIP runtime error";
         case GVR_ERR_TOO_LONG: return "row stride too long";
     }

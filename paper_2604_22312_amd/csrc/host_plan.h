@@ -50,13 +50,14 @@ struct CallOptions {
     int ordered_merge = 0;  // agent-scope release / acquire at a split row's merge
 };
 
-inline gvr_status validate(const void* scores, int64_t B, int64_t ld, int32_t K, const void* out,
-                           const gvr_options* opt, int use_guess, CallOptions* o) {
+// Sizes and options of a call, without its pointers (the workspace query
+// takes no arrays).
+inline gvr_status validate_sizes(int64_t B, int64_t ld, int32_t K, const gvr_options* opt, int use_guess,
+                                 CallOptions* o) {
     *o = CallOptions();
     o->use_guess = use_guess;
     if (K < 1 || K > GVR_MAX_K) return GVR_ERR_UNSUPPORTED_K;
     if (B < 0 || ld < 0) return GVR_ERR_INVALID_ARG;
-    if (B > 0 && (!scores || !out)) return GVR_ERR_INVALID_ARG;
     if (ld > (int64_t)0x7FFFFFF0) return GVR_ERR_TOO_LONG;
     if (opt) {
         if (opt->capacity != 0) {
@@ -75,6 +76,14 @@ inline gvr_status validate(const void* scores, int64_t B, int64_t ld, int32_t K,
         o->shape = forced == 1 ? kNWShort : forced == 2 ? kNWLong : forced == 4 ? kNWMid : 0;
         o->parts = opt->parts;
     }
+    return GVR_OK;
+}
+
+inline gvr_status validate(const void* scores, int64_t B, int64_t ld, int32_t K, const void* out,
+                           const gvr_options* opt, int use_guess, CallOptions* o) {
+    const gvr_status st = validate_sizes(B, ld, K, opt, use_guess, o);
+    if (st != GVR_OK) return st;
+    if (B > 0 && (!scores || !out)) return GVR_ERR_INVALID_ARG;
     return GVR_OK;
 }
 
@@ -151,7 +160,7 @@ constexpr int64_t kStreamHintBytes = (int64_t)16 << 20;
 // `reject_forced` is set, in which case a forced split that does not fit is
 // GVR_ERR_WORKSPACE.
 inline gvr_status plan_call(int64_t B, int64_t ld, int32_t K, bool have_prev, const CallOptions& o, int cus,
-                            int max_slots, bool reject_forced, Plan* out) {
+                            int64_t max_slots, bool reject_forced, Plan* out) {
     Plan p;
     // Rows of at most 2K elements list every element (the guess would cut
     // few candidates): when no row is longer, the guess-free kernel runs.
@@ -210,6 +219,17 @@ struct WsPtrs {
     int32_t* part_hist = nullptr;
     uint64_t* part_list = nullptr;
 };
+
+// Most (row, part) slots whose layout fits in `bytes` (0 if not even one),
+// capped at kMaxCallerSlots.
+constexpr int64_t kMaxCallerSlots = (int64_t)1 << 24;
+inline int64_t ws_slots_fitting(size_t bytes) {
+    const size_t per_slot = sizeof(uint64_t) + sizeof(int32_t) + sizeof(uint32_t) +
+                            kSlotHistBins * sizeof(int32_t) + (size_t)kPartCap * sizeof(uint64_t);
+    int64_t s = (int64_t)std::min<size_t>(bytes / per_slot, (size_t)kMaxCallerSlots);
+    while (s > 0 && ws_layout(s).total > bytes) --s;
+    return s;
+}
 
 inline WsPtrs ws_carve(void* base, int64_t slots) {
     const WsLayout L = ws_layout(slots);

@@ -139,6 +139,27 @@ static void check_workspace() {
               L.hists - L.thresh >= (size_t)slots * 4 && L.lists - L.hists >= (size_t)slots * kSlotHistBins * 4);
         CHECK(L.total == L.lists + (size_t)slots * kPartCap * 8);
     }
+    // a caller's buffer of ws_layout(n).total bytes holds n slots, and one byte fewer does not
+    CHECK(ws_slots_fitting(0) == 0 && ws_slots_fitting(ws_layout(1).total - 1) == 0);
+    for (int64_t slots : {1, 2, 7, 64, 255, 256, 2048, 5000}) {
+        CHECK(ws_slots_fitting(ws_layout(slots).total) == slots);
+        CHECK(ws_slots_fitting(ws_layout(slots).total - 1) == slots - 1);
+        CHECK(ws_slots_fitting(ws_layout(slots + 1).total - 1) == slots);
+    }
+    CHECK(ws_slots_fitting((size_t)1 << 62) == kMaxCallerSlots);
+    // a caller's workspace plans: automatic splits lowered to the slots that fit, forced ones refused
+    {
+        CallOptions o;
+        Plan p;
+        CHECK(plan_call(8, 131079, 2048, true, o, 256, 64, true, &p) == GVR_OK && p.parts == 8);
+        CHECK(plan_call(8, 131079, 2048, true, o, 256, 40, true, &p) == GVR_OK && p.parts == 5);
+        CHECK(plan_call(8, 131079, 2048, true, o, 256, 0, true, &p) == GVR_OK && p.parts == 1);
+        o.parts = 4;
+        CHECK(plan_call(8, 131079, 2048, true, o, 256, 31, true, &p) == GVR_ERR_WORKSPACE);
+        CHECK(plan_call(8, 131079, 2048, true, o, 256, 32, true, &p) == GVR_OK && p.parts == 4);
+        o.parts = 1;
+        CHECK(plan_call(8, 131079, 2048, true, o, 256, 0, true, &p) == GVR_OK && p.parts == 1);
+    }
     // the cache: reuse, growth with the outgrown buffer kept, refusal under capture
     WorkspaceCache<FakeDev> cache;
     int s1 = 0, s2 = 0;

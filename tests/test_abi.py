@@ -35,7 +35,7 @@ def L():
 def test_header_declares_the_boundary():
     names = declared_functions()
     for n in ("gvr_topk", "radix_topk", "gvr_topk_ex", "radix_topk_ex", "gvr_topk_ex_noalloc",
-              "gvr_status_string", "gvr_version", "gvr_rope_params_default", "gvr_rope_g",
+              "gvr_workspace_size", "gvr_topk_ex_ws", "radix_topk_ex_ws", "gvr_status_string", "gvr_version", "gvr_rope_params_default", "gvr_rope_g",
               "gvr_rope_prior", "gvr_indexer_scores", "gvr_indexer_topk"):
         assert n in names, n
 
@@ -97,6 +97,30 @@ def test_options_validation(L):
     assert L.gvr_topk_ex_noalloc(vp(1), 2, 100, None, None, 0, vp(1), None, None, None) == -2
     assert L.gvr_topk_ex_noalloc(None, 2, 100, None, None, 16, vp(1), None, None, None) == -1
     assert L.gvr_topk_ex_noalloc(None, 0, 100, None, None, 16, None, None, None, None) == 0
+
+
+def test_caller_workspace_validation(L):
+    """The caller-workspace calls check sizes and options like gvr_topk_ex,
+    then the workspace pointer, all before touching the device."""
+    import paper_2604_22312_amd as g
+    vp, sz = ctypes.c_void_p, ctypes.c_size_t
+    ok = g.Options(capacity=0, flags=0, parts=0, reserved1=0)
+    bad = g.Options(capacity=0, flags=0, parts=17, reserved1=0)
+    for f in (lambda *a: L.gvr_topk_ex_ws(vp(1), 2, 100, None, None, *a),
+              lambda *a: L.radix_topk_ex_ws(vp(1), 2, 100, None, *a)):
+        assert f(0, vp(1), None, None, None, None, 0) == -2                     # K out of range
+        assert f(16, vp(1), None, ctypes.byref(bad), None, None, 0) == -1      # bad option
+        assert f(16, vp(1), None, ctypes.byref(ok), None, None, 4096) == -1    # NULL workspace, bytes > 0
+        assert f(16, vp(1), None, ctypes.byref(ok), None, vp(4100), 4096) == -1   # misaligned workspace
+    assert L.gvr_topk_ex_ws(None, 2, 100, None, None, 16, vp(1), None, None, None, None, 0) == -1
+    assert L.gvr_topk_ex_ws(None, 0, 100, None, None, 16, None, None, None, None, None, 0) == 0
+    n = sz(123)
+    assert L.gvr_workspace_size(0, 100, 16, 1, None, ctypes.byref(n)) == 0 and n.value == 0
+    assert L.gvr_workspace_size(2, 100, 16, 1, None, None) == -1
+    assert L.gvr_workspace_size(2, 100, 0, 1, None, ctypes.byref(n)) == -2
+    assert L.gvr_workspace_size(-1, 100, 16, 1, None, ctypes.byref(n)) == -1
+    assert L.gvr_workspace_size(2, 1 << 40, 16, 0, None, ctypes.byref(n)) == -5
+    assert L.gvr_workspace_size(2, 100, 16, 1, ctypes.byref(bad), ctypes.byref(n)) == -1
 
 
 def test_read_floor_validation(L):
