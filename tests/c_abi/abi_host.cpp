@@ -1,6 +1,7 @@
 // A host program that uses the library through its C ABI alone (no Python,
 // no torch): device buffers from the HIP runtime, gvr_topk / radix_topk /
-// gvr_topk_ex on one stream, each result compared with the C oracle
+// gvr_topk_ex and the caller-workspace calls on one stream, each result
+// compared with the C oracle
 // (oracle/oracle_topk.c, linked in as a test dependency).
 //
 // Inputs: B rows of stride ld from a 64-bit linear congruential generator
@@ -88,6 +89,25 @@ int main() {
         std::snprintf(name, sizeof name, "gvr_topk_ex flags %d", (int)f);
         failures += check(name, gvr_topk_ex(dx, B, ld, dlen, dprev, K, dout, stream, &opt, nullptr));
     }
+    // The caller-owned workspace: sized by gvr_workspace_size for a forced
+    // two-part split, zero-filled once, used by two calls in a row.
+    opt.flags = 0;
+    opt.parts = 2;
+    size_t ws_bytes = 0;
+    if (gvr_workspace_size(B, ld, K, 1, &opt, &ws_bytes) != GVR_OK || ws_bytes == 0) return 6;
+    void* ws = nullptr;
+    HIP_OK(hipMalloc(&ws, ws_bytes));
+    HIP_OK(hipMemset(ws, 0, ws_bytes));
+    failures += check("gvr_topk_ex_ws 2 parts", gvr_topk_ex_ws(dx, B, ld, dlen, dprev, K, dout, stream, &opt, nullptr,
+                                                                ws, ws_bytes));
+    failures += check("gvr_topk_ex_ws 2 parts again", gvr_topk_ex_ws(dx, B, ld, dlen, dprev, K, dout, stream, &opt,
+                                                                      nullptr, ws, ws_bytes));
+    failures += check("radix_topk_ex_ws 2 parts", radix_topk_ex_ws(dx, B, ld, dlen, K, dout, stream, &opt, nullptr,
+                                                                    ws, ws_bytes));
+    // a forced split that does not fit is refused before anything is enqueued
+    if (gvr_topk_ex_ws(dx, B, ld, dlen, dprev, K, dout, stream, &opt, nullptr, ws, ws_bytes / 2) != GVR_ERR_WORKSPACE)
+        ++failures;
+    HIP_OK(hipFree(ws));
     HIP_OK(hipFree(dx));
     HIP_OK(hipFree(dlen));
     HIP_OK(hipFree(dprev));
