@@ -56,15 +56,22 @@ def test_caller_workspace_matches_oracle(B, ld, radix):
     ws = g.new_workspace(B, ld, K_TOPK, use_guess=not radix)
     assert ws.numel() == nbytes
     note("caller workspace B=%d ld=%d radix=%d bytes=%d" % (B, ld, radix, nbytes))
+    st_ws, st_ref = g.new_stats(B, DEV), g.new_stats(B, DEV)
     if radix:
-        got = g.radix_topk_ex_ws(S, None, K_TOPK, ws)
-        ref = g.radix_topk_ex(S, None, K_TOPK)
+        got = g.radix_topk_ex_ws(S, None, K_TOPK, ws, stats=st_ws)
+        ref = g.radix_topk_ex(S, None, K_TOPK, stats=st_ref)
     else:
-        got = g.gvr_topk_ex_ws(S, None, P, K_TOPK, ws)
-        ref = g.gvr_topk_ex(S, None, P, K_TOPK)
+        got = g.gvr_topk_ex_ws(S, None, P, K_TOPK, ws, stats=st_ws)
+        ref = g.gvr_topk_ex(S, None, P, K_TOPK, stats=st_ref)
     torch.cuda.synchronize()
     assert_rows_equal(got.cpu().numpy(), exp, "caller workspace, first call")
     assert np.array_equal(got.cpu().numpy(), ref.cpu().numpy())
+    # the same schedule as the library-workspace call: every per-row statistic
+    # but the clock stamps agrees
+    a_st, r_st = g.decode_stats(st_ws), g.decode_stats(st_ref)
+    for key in ("n", "path", "passes", "candidates", "threshold", "kth_key", "n_gt", "guess_valid",
+                "spec_threshold", "spec_count"):
+        assert torch.equal(a_st[key], r_st[key]), key
     # second call on the same buffer: fewer rows, ragged lengths
     B2 = max(1, B // 2)
     lens = np.array([ld - 1 - 977 * i for i in range(B2)], np.int32)
