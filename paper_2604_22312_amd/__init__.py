@@ -18,7 +18,8 @@ Functions mirror the C entry points:
   ``new_workspace`` -- the split-row workspace owned by the caller (nothing
   allocated inside the call)
 * ``prepare_gvr_topk`` / ``prepare_radix_topk`` -- a call checked and
-  marshalled once, re-enqueued by calling it (loops over fixed buffers)
+  marshalled once, re-enqueued by calling it (loops over fixed buffers; with
+  ``workspace=``, on a caller workspace)
 * ``gvr_rope_g(n, params=None, device=...)`` -- g(Delta) of the RoPE/YaRN prior
 * ``gvr_rope_prior(n, K, params=None, device=...)`` -- its static index set
   (``include/gvr_rope_prior.h``)

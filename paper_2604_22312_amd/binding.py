@@ -301,7 +301,7 @@ class PreparedCall:
         return self.out_idx
 
 
-def _prepare(radix, scores, row_len, prev_topk, K, out_idx, stream, options):
+def _prepare(radix, scores, row_len, prev_topk, K, out_idx, stream, options, workspace=None):
     B, ld, K, out_idx = _check(scores, row_len, None if radix else prev_topk, K, out_idx)
     L = lib()
     opt = None
@@ -310,7 +310,19 @@ def _prepare(radix, scores, row_len, prev_topk, K, out_idx, stream, options):
     pc = PreparedCall()
     pc._dev = scores.device.index if scores.device.index is not None else torch.cuda.current_device()
     sp = _stream(stream, scores.device)
-    if opt is None and not radix:
+    if workspace is not None:
+        if workspace.device != scores.device or not workspace.is_contiguous():
+            raise ValueError("workspace must be a contiguous tensor on the scores' device")
+        nbytes = workspace.numel() * workspace.element_size()
+        optp = ctypes.byref(opt) if opt is not None else None
+        if radix:
+            pc._name, pc._f = "radix_topk_ex_ws", L.radix_topk_ex_ws
+            pc._args = (_ptr(scores), B, ld, _ptr(row_len), K, _ptr(out_idx), sp, optp, None, _ptr(workspace), nbytes)
+        else:
+            pc._name, pc._f = "gvr_topk_ex_ws", L.gvr_topk_ex_ws
+            pc._args = (_ptr(scores), B, ld, _ptr(row_len), _ptr(prev_topk), K, _ptr(out_idx), sp, optp, None,
+                        _ptr(workspace), nbytes)
+    elif opt is None and not radix:
         pc._name, pc._f = "gvr_topk", L.gvr_topk
         pc._args = (_ptr(scores), B, ld, _ptr(row_len), _ptr(prev_topk), K, _ptr(out_idx), sp)
     elif opt is None:
@@ -323,18 +335,20 @@ def _prepare(radix, scores, row_len, prev_topk, K, out_idx, stream, options):
         pc._name, pc._f = "gvr_topk_ex", L.gvr_topk_ex
         pc._args = (_ptr(scores), B, ld, _ptr(row_len), _ptr(prev_topk), K, _ptr(out_idx), sp, ctypes.byref(opt), None)
     pc.out_idx = out_idx
-    pc._keep = (scores, row_len, prev_topk, opt, stream)
+    pc._keep = (scores, row_len, prev_topk, opt, stream, workspace)
     return pc
 
 
-def prepare_gvr_topk(scores, row_len, prev_topk, K, out_idx=None, stream=None, options=None):
-    """A ``PreparedCall`` of ``gvr_topk`` (``gvr_topk_ex`` with options)."""
-    return _prepare(False, scores, row_len, prev_topk, K, out_idx, stream, options)
+def prepare_gvr_topk(scores, row_len, prev_topk, K, out_idx=None, stream=None, options=None, workspace=None):
+    """A ``PreparedCall`` of ``gvr_topk`` (``gvr_topk_ex`` with options;
+    ``gvr_topk_ex_ws`` with a caller ``workspace``, see ``new_workspace``)."""
+    return _prepare(False, scores, row_len, prev_topk, K, out_idx, stream, options, workspace)
 
 
-def prepare_radix_topk(scores, row_len, K, out_idx=None, stream=None, options=None):
-    """A ``PreparedCall`` of ``radix_topk`` (``radix_topk_ex`` with options)."""
-    return _prepare(True, scores, row_len, None, K, out_idx, stream, options)
+def prepare_radix_topk(scores, row_len, K, out_idx=None, stream=None, options=None, workspace=None):
+    """A ``PreparedCall`` of ``radix_topk`` (``radix_topk_ex`` with options;
+    ``radix_topk_ex_ws`` with a caller ``workspace``)."""
+    return _prepare(True, scores, row_len, None, K, out_idx, stream, options, workspace)
 
 
 def new_stats(B, device):

@@ -132,6 +132,47 @@ def test_caller_workspace_unsplit_shapes_need_none():
     assert_rows_equal(got.cpu().numpy(), exp, "unsplit call without a workspace")
 
 
+def test_prepared_calls_with_a_caller_workspace():
+    """Prepared calls (checked and marshalled once) on a caller workspace,
+    repeated with the rows rewritten in place, and captured into a HIP graph
+    replayed several times: every result equals the oracle."""
+    import paper_2604_22312_amd as g
+    B, ld = 2, 131072
+    rng = np.random.default_rng(61)
+    S = torch.empty((B, ld), dtype=torch.float32, device=DEV)
+    P = torch.empty((B, K_TOPK), dtype=torch.int32, device=DEV)
+    ws = g.new_workspace(B, ld, K_TOPK)
+    wsr = g.new_workspace(B, ld, K_TOPK, use_guess=False)
+    assert ws.numel() > 1 and wsr.numel() > 1
+    stream = torch.cuda.Stream()
+    pg = g.prepare_gvr_topk(S, None, P, K_TOPK, stream=stream, workspace=ws)
+    pr = g.prepare_radix_topk(S, None, K_TOPK, stream=stream, workspace=wsr)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=stream):
+        pg()
+        pr()
+    for rep in range(3):
+        x = rng.standard_normal((B, ld)).astype(np.float32)
+        exp, _, _ = oracle.topk(x, K_TOPK)
+        pexp, _, _ = oracle.topk(x + 0.05 * rng.standard_normal((B, ld)).astype(np.float32), K_TOPK)
+        S.copy_(torch.from_numpy(x))
+        P.copy_(torch.from_numpy(pexp))
+        note("prepared caller-workspace calls, round %d" % rep)
+        for pc in (pg, pr):
+            pc.out_idx.fill_(-7)
+            torch.cuda.synchronize()
+            out = pc()
+            torch.cuda.synchronize()
+            assert_rows_equal(out.cpu().numpy(), exp, "prepared %s, round %d" % (pc._name, rep))
+        pg.out_idx.fill_(-7)
+        pr.out_idx.fill_(-7)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert_rows_equal(pg.out_idx.cpu().numpy(), exp, "graph replay (gvr), round %d" % rep)
+        assert_rows_equal(pr.out_idx.cpu().numpy(), exp, "graph replay (radix), round %d" % rep)
+
+
 CAPTURE_FIRST_SPLIT = r"""
 import sys, numpy as np, torch
 sys.path.insert(0, sys.argv[1])
